@@ -1,0 +1,9 @@
+"""CPU float64 oracle for the Hydra-PPO hot path (test infrastructure only; see hydra_oracle)."""
+from .hydra_oracle import (  # noqa: F401
+    bf16_to_f64,
+    lora_linear_ref,
+    log_softmax_gather_ref,
+    score_logits_ref,
+    reward_ref,
+    score_head_ref,
+)

@@ -1,0 +1,344 @@
+"""Pins of the float64 oracle against what the mathematics fixes (CPU only).
+
+The paper prints no worked example for any quantity on this path, so each
+oracle function is pinned by exact brute force on tiny inputs, closed forms,
+invariants and independent library routines.  The mutation tests at the end
+plant plausible mistakes in copies of the oracle and check that these pins
+catch them.
+"""
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import hydra_oracle as O
+from workloads import f32_to_bf16, gen_linear, gen_logits, gen_score_head
+
+
+# ---------------------------------------------------------------- helpers
+
+def _int_bf16(rng, shape, lo=-8, hi=8):
+    """Small integers: exactly representable in bf16 and in every partial sum."""
+    v = rng.integers(lo, hi + 1, size=shape).astype(np.float32)
+    return f32_to_bf16(v), v.astype(np.int64)
+
+
+def _frac_lora(xi, Wi, Ai, Bi, s):
+    """Exact LoRA linear with Fractions and plain loops: y_off[m][n], y_on[m][n]."""
+    M, K = xi.shape
+    N, r = Bi.shape
+    s = Fraction(s)
+    y_off = [[Fraction(0)] * N for _ in range(M)]
+    y_on = [[Fraction(0)] * N for _ in range(M)]
+    for m in range(M):
+        T = [sum(Fraction(int(xi[m, k])) * int(Ai[j, k]) for k in range(K)) for j in range(r)]
+        for n in range(N):
+            base = sum(Fraction(int(xi[m, k])) * int(Wi[n, k]) for k in range(K))
+            y_off[m][n] = base
+            y_on[m][n] = base + s * sum(T[j] * int(Bi[n, j]) for j in range(r))
+    return y_off, y_on
+
+
+# ---------------------------------------------------------------- LoRA linear
+
+@pytest.mark.parametrize("M,K,N,r,s", [(3, 8, 5, 2, 2.0), (1, 16, 3, 1, -0.5), (4, 8, 7, 3, 0.25), (2, 8, 4, 0, 2.0)])
+def test_lora_linear_exact_bruteforce(M, K, N, r, s):
+    rng = np.random.default_rng(100 + M * 7 + K + N + r)
+    x, xi = _int_bf16(rng, (M, K))
+    W, Wi = _int_bf16(rng, (N, K))
+    A, Ai = _int_bf16(rng, (r, K))
+    B, Bi = _int_bf16(rng, (N, r))
+    y_off, y_on = O.lora_linear_ref(x, W, A, B, s)
+    e_off, e_on = _frac_lora(xi, Wi, Ai, Bi, s)
+    for m in range(M):
+        for n in range(N):
+            assert Fraction(y_off[m, n]) == e_off[m][n]
+            assert Fraction(y_on[m, n]) == e_on[m][n]
+
+
+def test_lora_linear_float_bruteforce_loops():
+    """Non-integer bf16 inputs: float64 triple loop (math.fsum, exact sums) vs the oracle."""
+    c = gen_linear(7, M=5, K=24, N=6, r=3, s=2.0)
+    X, W, A, B = (O.bf16_to_f64(t) for t in (c.x, c.W, c.A, c.B))
+    y_off, y_on = O.lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+    for m in range(5):
+        T = [math.fsum(X[m, k] * A[j, k] for k in range(24)) for j in range(3)]
+        for n in range(6):
+            base = math.fsum(X[m, k] * W[n, k] for k in range(24))
+            on = base + c.s * math.fsum(T[j] * B[n, j] for j in range(3))
+            assert abs(y_off[m, n] - base) <= 1e-13 * max(1.0, abs(base))
+            assert abs(y_on[m, n] - on) <= 1e-12 * max(1.0, abs(on))
+
+
+def test_lora_linear_merged_weight_invariant():
+    """y_on equals x (W + s B A)^T computed from the explicitly merged weight."""
+    c = gen_linear(11, M=33, K=128, N=96, r=8, s=2.0)
+    X, W, A, B = (O.bf16_to_f64(t) for t in (c.x, c.W, c.A, c.B))
+    W_merged = W + c.s * (B @ A)            # [N x K]
+    expect = X @ W_merged.T
+    _, y_on = O.lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+    assert np.max(np.abs(y_on - expect)) <= 1e-12 * np.max(np.abs(expect))
+
+
+def test_lora_linear_b_zero_and_s_zero_are_lora_off():
+    c = gen_linear(12, M=9, K=64, N=40, r=8, s=2.0)
+    y_off, y_on = O.lora_linear_ref(c.x, c.W, c.A, np.zeros_like(c.B), c.s)
+    assert np.array_equal(y_on, y_off)
+    y_off2, y_on2 = O.lora_linear_ref(c.x, c.W, c.A, c.B, 0.0)
+    assert np.array_equal(y_on2, y_off2)
+    assert np.array_equal(y_off, y_off2)
+
+
+def test_lora_linear_linear_in_scale_and_row_permutation():
+    c = gen_linear(13, M=12, K=64, N=32, r=4, s=1.0)
+    off1, on1 = O.lora_linear_ref(c.x, c.W, c.A, c.B, 1.0)
+    _, on3 = O.lora_linear_ref(c.x, c.W, c.A, c.B, 3.0)
+    d1 = on1 - off1
+    assert np.allclose(on3 - off1, 3.0 * d1, rtol=1e-12, atol=1e-12)
+    perm = np.random.default_rng(0).permutation(12)
+    offp, onp = O.lora_linear_ref(c.x[perm], c.W, c.A, c.B, 1.0)
+    assert np.array_equal(offp, off1[perm]) and np.array_equal(onp, on1[perm])
+
+
+def test_lora_linear_adapter_selection():
+    """Two adapter sets over one base (Hydra-PPO): each on-output uses only its own pair."""
+    a = gen_linear(14, M=6, K=32, N=16, r=4)
+    b = gen_linear(15, M=6, K=32, N=16, r=4)
+    off_a, on_a = O.lora_linear_ref(a.x, a.W, a.A, a.B, 2.0)
+    off_b, on_b = O.lora_linear_ref(a.x, a.W, b.A, b.B, 2.0)
+    assert np.array_equal(off_a, off_b)
+    assert not np.allclose(on_a, on_b)
+
+
+# ---------------------------------------------------------------- log-softmax / gather
+
+def test_log_softmax_rows_normalise():
+    z = np.random.default_rng(1).normal(0, 2, (7, 1000))
+    ids = np.arange(7, dtype=np.int32)
+    _, lse = O.log_softmax_gather_ref(z, ids)
+    for i in range(7):
+        assert abs(np.exp(z[i] - lse[i]).sum() - 1.0) < 1e-12
+
+
+def test_log_softmax_uniform_row_closed_form():
+    V = 32000
+    z = np.zeros((2, V))
+    z[1] += 3.5
+    lp, lse = O.log_softmax_gather_ref(z, np.array([5, V - 1], dtype=np.int32))
+    assert lp[0] == -math.log(V)
+    assert abs(lp[1] + 10.373491181781864) < 1e-12
+    assert abs(lse[1] - (3.5 + math.log(V))) < 1e-12
+
+
+def test_log_softmax_two_class_closed_form():
+    rng = np.random.default_rng(2)
+    z = rng.normal(0, 3, (50, 2))
+    lp0, _ = O.log_softmax_gather_ref(z, np.zeros(50, np.int32))
+    lp1, _ = O.log_softmax_gather_ref(z, np.ones(50, np.int32))
+    assert np.allclose(lp0, -np.log1p(np.exp(z[:, 1] - z[:, 0])), rtol=0, atol=1e-13)
+    assert np.allclose(lp1, -np.log1p(np.exp(z[:, 0] - z[:, 1])), rtol=0, atol=1e-13)
+
+
+def test_log_softmax_shift_invariance_and_overflow():
+    rng = np.random.default_rng(3)
+    z = rng.normal(0, 2, (4, 500))
+    ids = rng.integers(0, 500, 4).astype(np.int32)
+    lp, _ = O.log_softmax_gather_ref(z, ids)
+    lp2, _ = O.log_softmax_gather_ref(z + 1234.5, ids)
+    assert np.allclose(lp, lp2, rtol=0, atol=1e-9)
+    big = np.zeros((2, 100))
+    big[:, 7] = 1e4
+    lpb, _ = O.log_softmax_gather_ref(big, np.array([7, 8], np.int32))
+    assert lpb[0] == 0.0 and lpb[1] == -1e4
+
+
+def test_log_softmax_matches_torch_float64():
+    torch = pytest.importorskip("torch")
+    z = np.random.default_rng(4).normal(0, 2, (16, 32000))
+    ids = np.random.default_rng(5).integers(0, 32000, 16).astype(np.int32)
+    lp, _ = O.log_softmax_gather_ref(z, ids)
+    ref = torch.log_softmax(torch.from_numpy(z), dim=1)[torch.arange(16), torch.from_numpy(ids).long()].numpy()
+    assert np.max(np.abs(lp - ref)) < 1e-12
+
+
+def test_log_softmax_matches_scipy_logsumexp():
+    scipy_special = pytest.importorskip("scipy.special")
+    z = np.random.default_rng(6).normal(0, 2, (8, 4000))
+    _, lse = O.log_softmax_gather_ref(z, np.zeros(8, np.int32))
+    assert np.max(np.abs(lse - scipy_special.logsumexp(z, axis=1))) < 1e-12
+
+
+def test_log_softmax_out_of_range_token_is_nan():
+    z = np.zeros((3, 10))
+    lp, _ = O.log_softmax_gather_ref(z, np.array([-1, 10, 3], np.int32))
+    assert math.isnan(lp[0]) and math.isnan(lp[1]) and not math.isnan(lp[2])
+
+
+# ---------------------------------------------------------------- KL
+
+def test_kl_zero_when_lora_off_for_both():
+    on, off, ids = gen_logits(20, M=6, V=3000)
+    r = O.score_logits_ref(off, off, ids)
+    assert np.all(r["kl"] == 0.0)
+    c = gen_score_head(21, 2, 4, 64, 300, 4)
+    rr = O.score_head_ref(c.h, c.W_lm, c.A, np.zeros_like(c.B), c.s, c.ids)
+    assert np.all(rr["kl"] == 0.0)
+
+
+def test_kl_antisymmetric_and_shift_free():
+    on, off, ids = gen_logits(22, M=6, V=3000)
+    a = O.score_logits_ref(on, off, ids)
+    b = O.score_logits_ref(off, on, ids)
+    assert np.array_equal(a["kl"], -b["kl"])
+    shift = np.arange(6, dtype=np.float64)[:, None] * 3.25
+    c = O.score_logits_ref(on.astype(np.float64) + shift, on, ids)
+    assert np.max(np.abs(c["kl"])) < 1e-12
+
+
+def test_kl_sign_follows_sampled_token_logit():
+    """Raising only the sampled token's logit raises lp_on, so KL = lp_on - lp_off > 0."""
+    V = 50
+    off = np.zeros((3, V))
+    ids = np.array([1, 2, 3], np.int32)
+    on = off.copy()
+    on[np.arange(3), ids] += 1.0
+    r = O.score_logits_ref(on, off, ids)
+    expect = 1.0 - math.log((V - 1 + math.e) / V)
+    assert np.allclose(r["kl"], expect, rtol=0, atol=1e-13)
+
+
+# ---------------------------------------------------------------- reward head and composition
+
+def test_reward_exact_bruteforce():
+    rng = np.random.default_rng(30)
+    n_seq, seq_len, K = 3, 4, 16
+    h, hi = _int_bf16(rng, (n_seq * seq_len, K))
+    w, wi = _int_bf16(rng, (K,))
+    got = O.reward_ref(h, w, n_seq, seq_len)
+    for b in range(n_seq):
+        row = b * seq_len + seq_len - 1
+        assert Fraction(got[b]) == sum(Fraction(int(hi[row, k])) * int(wi[k]) for k in range(K))
+
+
+def test_reward_equals_lora_off_linear_with_one_output():
+    c = gen_score_head(31, 3, 5, 64, 100, 4)
+    rew = O.reward_ref(c.h, c.w_rm, 3, 5)
+    last = np.array([b * 5 + 4 for b in range(3)])
+    y_off, _ = O.lora_linear_ref(c.h[last], c.w_rm[None, :], np.zeros((0, 64), np.uint16),
+                                 np.zeros((1, 0), np.uint16), 0.0)
+    assert np.allclose(rew, y_off[:, 0], rtol=1e-14, atol=0)
+
+
+def test_score_head_is_linear_then_log_softmax():
+    c = gen_score_head(32, 2, 8, 64, 500, 8)
+    r = O.score_head_ref(c.h, c.W_lm, c.A, c.B, c.s, c.ids, c.w_rm, 2, 8)
+    z_off, z_on = O.lora_linear_ref(c.h, c.W_lm, c.A, c.B, c.s)
+    r2 = O.score_logits_ref(z_on, z_off, c.ids)
+    for k in ("lp_on", "lp_off", "kl", "lse_on", "lse_off"):
+        assert np.array_equal(r[k], r2[k])
+    assert r["reward"].shape == (2,)
+    sub = np.array([3, 7, 15])
+    rs = O.score_head_ref(c.h[sub], c.W_lm, c.A, c.B, c.s, c.ids[sub], c.w_rm, 2, 8, rows=sub)
+    assert np.allclose(rs["lp_on"], r["lp_on"][sub], rtol=0, atol=1e-12)
+    assert np.allclose(rs["reward"], r["reward"], rtol=0, atol=0)
+
+
+# ---------------------------------------------------------------- mutation checks
+
+def _pins_for_linear(fn):
+    """Run the linear pins against ``fn``; return True iff all pass."""
+    try:
+        rng = np.random.default_rng(5)
+        x, xi = _int_bf16(rng, (3, 8))
+        W, Wi = _int_bf16(rng, (5, 8))
+        A, Ai = _int_bf16(rng, (2, 8))
+        B, Bi = _int_bf16(rng, (5, 2))
+        y_off, y_on = fn(x, W, A, B, 2.0)
+        e_off, e_on = _frac_lora(xi, Wi, Ai, Bi, 2.0)
+        ok = all(Fraction(y_off[m, n]) == e_off[m][n] and Fraction(y_on[m, n]) == e_on[m][n]
+                 for m in range(3) for n in range(5))
+        c = gen_linear(11, M=9, K=32, N=12, r=4, s=2.0)
+        X, Wd, Ad, Bd = (O.bf16_to_f64(t) for t in (c.x, c.W, c.A, c.B))
+        _, on = fn(c.x, c.W, c.A, c.B, c.s)
+        ok = ok and np.allclose(on, X @ (Wd + c.s * Bd @ Ad).T, rtol=1e-12, atol=1e-12)
+        return bool(ok)
+    except Exception:
+        return False
+
+
+def _pins_for_logsoftmax(fn):
+    try:
+        V = 32000
+        lp, _ = fn(np.zeros((1, V)), np.array([0], np.int32))
+        ok = abs(lp[0] + math.log(V)) < 1e-12
+        z = np.random.default_rng(2).normal(0, 3, (20, 2))
+        lp0, _ = fn(z, np.zeros(20, np.int32))
+        ok = ok and np.allclose(lp0, -np.log1p(np.exp(z[:, 1] - z[:, 0])), atol=1e-12, rtol=0)
+        big = np.zeros((1, 10))
+        big[0, 3] = 1e4
+        lpb, _ = fn(big, np.array([3], np.int32))
+        ok = ok and lpb[0] == 0.0
+        return bool(ok)
+    except Exception:
+        return False
+
+
+def test_pins_accept_the_oracle():
+    assert _pins_for_linear(O.lora_linear_ref)
+    assert _pins_for_logsoftmax(O.log_softmax_gather_ref)
+
+
+def _mut_no_scale(x, W, A, B, s):
+    X, Wd, Ad, Bd = (O.bf16_to_f64(t) for t in (x, W, A, B))
+    return X @ Wd.T, X @ Wd.T + (X @ Ad.T) @ Bd.T
+
+
+def _mut_transposed_b(x, W, A, B, s):
+    X, Wd, Ad, Bd = (O.bf16_to_f64(t) for t in (x, W, A, B))
+    Bt = Bd.reshape(Bd.shape[1], Bd.shape[0]).T          # wrong memory order for B
+    return X @ Wd.T, X @ Wd.T + s * (X @ Ad.T) @ Bt.T
+
+
+def _mut_dropped_base(x, W, A, B, s):
+    X, Wd, Ad, Bd = (O.bf16_to_f64(t) for t in (x, W, A, B))
+    return X @ Wd.T, s * (X @ Ad.T) @ Bd.T
+
+
+def _mut_w_reshaped(x, W, A, B, s):
+    X, Wd, Ad, Bd = (O.bf16_to_f64(t) for t in (x, W, A, B))
+    Wt = Wd.reshape(Wd.shape[1], Wd.shape[0]).T          # W read as [K x N]
+    return X @ Wt.T if Wt.shape[1] == X.shape[1] else X @ Wd.T * 0, None
+
+
+@pytest.mark.parametrize("mut", [_mut_no_scale, _mut_transposed_b, _mut_dropped_base, _mut_w_reshaped])
+def test_pins_catch_linear_mutations(mut):
+    assert not _pins_for_linear(mut)
+
+
+def _mut_lse_without_max(z, ids):
+    z = np.asarray(z, np.float64)
+    with np.errstate(over="ignore"):
+        lse = np.log(np.exp(z).sum(1))
+    return z[np.arange(len(ids)), ids] - lse, lse
+
+
+def _mut_lse_missing_max_term(z, ids):
+    z = np.asarray(z, np.float64)
+    m = z.max(1, keepdims=True)
+    lse = np.log(np.exp(z - m).sum(1))                   # forgot "+ m"
+    return z[np.arange(len(ids)), ids] - lse, lse
+
+
+def _mut_wrong_sign(z, ids):
+    lp, lse = O.log_softmax_gather_ref(z, ids)
+    return -lp, lse
+
+
+def _mut_off_by_one_token(z, ids):
+    return O.log_softmax_gather_ref(z, (np.asarray(ids) + 1) % np.asarray(z).shape[1])
+
+
+@pytest.mark.parametrize("mut", [_mut_lse_without_max, _mut_lse_missing_max_term, _mut_wrong_sign, _mut_off_by_one_token])
+def test_pins_catch_log_softmax_mutations(mut):
+    assert not _pins_for_logsoftmax(mut)
