@@ -1,0 +1,152 @@
+/*
+ * hydra.h -- C ABI of the Hydra-PPO hot path on MI355X (gfx950).
+ *
+ * The operations follow "Efficient RLHF: Reducing the Memory Usage of PPO"
+ * (arXiv 2309.00754):
+ *   - LoRA on every linear layer of the actor and critic (Sec. 2, Stage 3);
+ *   - Dynamic LoRA: the reference / reward model is the same network with the
+ *     LoRA parameters ignored, LO(.) (Sec. 3, "Dynamic LoRA");
+ *   - Hydra-PPO: one frozen base and two adapter sets, actor and critic; the
+ *     active set is the one whose (A, B) pair is passed (Sec. 3, "Stage 2");
+ *   - pi^hydra's two heads: a causal-LM head and a scalar reward head on the
+ *     same input (Sec. 3, opening paragraph);
+ *   - reward and reference log-probabilities from the LoRA-off model
+ *     (App. A, Alg. 1 and Alg. 2).
+ *
+ * Conventions shared by every entry point
+ *   - All tensor arguments are DEVICE pointers (hipMalloc'd or equivalent),
+ *     row-major and contiguous.  bf16 values are passed as uint16_t bit
+ *     patterns.  Operands read with 16-byte vector loads (x, W, A, h, W_lm,
+ *     the fp32 logits and the workspace) must be 16-byte aligned; fp32 and
+ *     int32 arrays 4-byte aligned; B and w_rm 2-byte aligned.
+ *   - A linear layer's frozen weight W is stored output-major [N x K] (the
+ *     nn.Linear.weight layout), LoRA-down A is [r x K], LoRA-up B is [N x r]:
+ *         y_off = x W^T                     (LoRA off)
+ *         y_on  = x W^T + s (x A^T) B^T     (LoRA on)
+ *     Products are bf16 x bf16 with fp32 accumulation; outputs are fp32.
+ *   - Ownership: the caller owns every buffer.  The library allocates no
+ *     device memory and keeps no mutable global state; calls on different
+ *     streams are independent.
+ *   - Asynchrony: each call validates its arguments on the host, enqueues its
+ *     kernels on `stream` (a hipStream_t; NULL = the default stream) and
+ *     returns.  Inputs must stay valid until the stream reaches that point.
+ *   - Errors: argument errors are detected on the host before any HIP call and
+ *     returned as a negative status with nothing enqueued.  A failed launch
+ *     returns HYDRA_ERR_HIP.  Data errors found on the device (a token id
+ *     outside [0, V)) produce NaN in that token's outputs and OR 1 into
+ *     *err_flag when err_flag is non-NULL.  NaN / Inf inputs propagate.
+ *   - Results are deterministic: no floating-point atomics; every reduction
+ *     runs in a fixed order, and the LoRA-on and LoRA-off log-softmax use
+ *     identical reduction trees, so KL is exactly 0 wherever the two logit
+ *     rows are equal (e.g. r = 0, s = 0 or B = 0).
+ */
+#ifndef HYDRA_H_
+#define HYDRA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HYDRA_OK = 0,
+  HYDRA_ERR_NULL = -1,        /* a required pointer is NULL                         */
+  HYDRA_ERR_SHAPE = -2,       /* a size is out of range or inconsistent             */
+  HYDRA_ERR_ALIGN = -3,       /* a pointer is not aligned as required               */
+  HYDRA_ERR_UNSUPPORTED = -4, /* a valid request this build does not handle         */
+  HYDRA_ERR_WORKSPACE = -5,   /* the workspace is missing or too small              */
+  HYDRA_ERR_HIP = -6          /* the HIP runtime reported an error at launch        */
+} hydra_status;
+
+/* Largest LoRA rank accepted. */
+#define HYDRA_MAX_RANK 64
+
+/*
+ * hydra_lora_linear -- the LoRA-switchable linear layer.
+ * Defined by: Sec. 2 Stage 3 (LoRA on all linears), Sec. 3 "Dynamic LoRA"
+ * (LO(.) = LoRA off on the same W) and "Stage 2: Hydra-PPO" (the adapter set
+ * in use is the (A, B) passed).
+ *
+ *   x     [M x K] bf16   input rows (tokens)
+ *   W     [N x K] bf16   frozen base weight, read once for both outputs
+ *   A     [r x K] bf16   LoRA down projection (may be NULL iff r == 0)
+ *   B     [N x r] bf16   LoRA up projection   (may be NULL iff r == 0)
+ *   s     fp32           LoRA scale
+ *   y_off [M x N] fp32   out: x W^T                  (NULL: not written)
+ *   y_on  [M x N] fp32   out: x W^T + s (x A^T) B^T  (NULL: not written)
+ * At least one output must be non-NULL.  Requires M, N, K >= 1, K % 8 == 0,
+ * K <= 2^21, 0 <= r <= HYDRA_MAX_RANK, and M, N below 2^31.  With r == 0, y_on equals
+ * y_off.  M <= 16 selects the bandwidth-bound (decode) kernel, larger M the
+ * MFMA GEMM; both compute the same function.
+ */
+hydra_status hydra_lora_linear(const uint16_t* x, const uint16_t* W, const uint16_t* A, const uint16_t* B,
+                               float s, int64_t M, int64_t N, int64_t K, int64_t r,
+                               float* y_off, float* y_on, void* stream);
+
+/*
+ * hydra_score_workspace_bytes -- device workspace that hydra_score needs for
+ * M = n_seq * seq_len token rows and a vocabulary of V.  Writes *bytes.
+ * Returns HYDRA_ERR_NULL for a NULL `bytes`, HYDRA_ERR_SHAPE for M or V < 1.
+ */
+hydra_status hydra_score_workspace_bytes(int64_t M, int64_t V, size_t* bytes);
+
+/*
+ * hydra_score -- fused two-head PPO scoring pass.
+ * Defined by: Sec. 3 (pi^hydra's CLM head and reward head on the same input),
+ * App. A Alg. 1 / Alg. 2 ("turn LoRA off ... compute reward and reference log
+ * probabilities"; the actor log-probability is the LoRA-on pass), App. B
+ * (the KL penalty weight beta is applied by the caller, not here).
+ *
+ *   h        [M x K] bf16   final hidden states, M = n_seq * seq_len, sequence-major
+ *   W_lm     [V x K] bf16   CLM head weight (output-major)
+ *   A, B     [r x K], [V x r] bf16   LoRA of the CLM head (NULL iff r == 0)
+ *   s        fp32           LoRA scale
+ *   tokens   [M] int32      sampled token scored at each row (the caller applies
+ *                           the usual next-token shift)
+ *   w_rm     [K] bf16       reward head weight (no bias); NULL: reward not computed
+ *   lp_on    [M] fp32       out: log softmax(z_on)[token],  z_on  = h W^T + s (h A^T) B^T
+ *   lp_off   [M] fp32       out: log softmax(z_off)[token], z_off = h W^T
+ *   kl       [M] fp32       out: lp_on - lp_off (per-token sampled KL estimate)
+ *   reward   [n_seq] fp32   out: <h[b*seq_len + seq_len - 1], w_rm> (NULL: skipped)
+ *   lse_on, lse_off [M] fp32  out, optional: log-sum-exp of each logit row
+ *   workspace, workspace_bytes  device scratch of at least
+ *                           hydra_score_workspace_bytes(M, V) bytes, 16-byte aligned
+ *   err_flag [1] int32      optional device flag; 1 is OR-ed in for an out-of-range token
+ * The [M x V] logits are never written to memory.  Requires K % 8 == 0,
+ * K <= 2^21, 0 <= r <= HYDRA_MAX_RANK, V >= 1, M and V below 2^31.
+ */
+hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t* A, const uint16_t* B, float s,
+                         const int32_t* tokens, const uint16_t* w_rm,
+                         int64_t n_seq, int64_t seq_len, int64_t K, int64_t V, int64_t r,
+                         float* lp_on, float* lp_off, float* kl, float* reward, float* lse_on, float* lse_off,
+                         void* workspace, size_t workspace_bytes, int32_t* err_flag, void* stream);
+
+/*
+ * hydra_score_logits -- the scoring epilogue alone, from materialised logits.
+ * Defined by: App. A Alg. 2 (reference log-probabilities), Sec. 2 Stage 3
+ * (the PPO policy ratio uses the same sampled-token log-probabilities).
+ *
+ *   logits_on, logits_off [M x V] fp32   logits of the LoRA-on and LoRA-off passes
+ *   tokens   [M] int32                   sampled token per row
+ *   lp_on, lp_off, kl [M] fp32           out (as in hydra_score)
+ *   lse_on, lse_off [M] fp32             out, optional (NULL: not written)
+ *   err_flag [1] int32                   optional, as in hydra_score
+ * Requires M, V >= 1.
+ */
+hydra_status hydra_score_logits(const float* logits_on, const float* logits_off, const int32_t* tokens,
+                                int64_t M, int64_t V, float* lp_on, float* lp_off, float* kl,
+                                float* lse_on, float* lse_off, int32_t* err_flag, void* stream);
+
+/* A static, human-readable name for a status code. */
+const char* hydra_status_string(hydra_status status);
+
+/* ABI version of this header (incremented on any incompatible change). */
+int hydra_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HYDRA_H_ */

@@ -1,0 +1,25 @@
+"""MI355X-native Hydra-PPO hot path: LoRA-switchable linear and PPO scoring epilogue.
+
+The compute runs in libhydra.so (hand-written HIP kernels for gfx950 behind the
+C ABI of include/hydra.h); this package only marshals PyTorch tensors into it.
+"""
+from ._binding import (  # noqa: F401
+    EXPORTED,
+    HYDRA_ERR_ALIGN,
+    HYDRA_ERR_HIP,
+    HYDRA_ERR_NULL,
+    HYDRA_ERR_SHAPE,
+    HYDRA_ERR_UNSUPPORTED,
+    HYDRA_ERR_WORKSPACE,
+    HYDRA_MAX_RANK,
+    HYDRA_OK,
+    HydraError,
+    HydraLibraryMissing,
+    LIB_PATH,
+    hydra_lora_linear,
+    hydra_score,
+    hydra_score_logits,
+    hydra_score_workspace_bytes,
+    lib,
+    status_string,
+)

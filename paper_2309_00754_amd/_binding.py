@@ -1,0 +1,204 @@
+"""ctypes binding of libhydra (the C ABI declared in include/hydra.h).
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+libhydra.  Tensors are PyTorch tensors on a ROCm device (PyTorch provides the
+device memory and the stream); they are checked for dtype, shape, device and
+contiguity, then their data pointers are passed through.  There is no CPU
+fallback: a missing library raises ``HydraLibraryMissing``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libhydra.so")
+
+HYDRA_OK = 0
+HYDRA_ERR_NULL = -1
+HYDRA_ERR_SHAPE = -2
+HYDRA_ERR_ALIGN = -3
+HYDRA_ERR_UNSUPPORTED = -4
+HYDRA_ERR_WORKSPACE = -5
+HYDRA_ERR_HIP = -6
+HYDRA_MAX_RANK = 64
+
+# Every symbol include/hydra.h declares.
+EXPORTED = (
+    "hydra_lora_linear",
+    "hydra_score_workspace_bytes",
+    "hydra_score",
+    "hydra_score_logits",
+    "hydra_status_string",
+    "hydra_abi_version",
+)
+
+
+class HydraLibraryMissing(ImportError):
+    pass
+
+
+class HydraError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = int(status)
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+_vp = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_f32 = ctypes.c_float
+
+
+def lib() -> ctypes.CDLL:
+    """Load libhydra.so (built in-tree by ``python -m paper_2309_00754_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise HydraLibraryMissing(
+            f"{LIB_PATH} is not built; run `python -m paper_2309_00754_amd.build` (no CPU fallback exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    L.hydra_lora_linear.argtypes = [_vp, _vp, _vp, _vp, _f32, _i64, _i64, _i64, _i64, _vp, _vp, _vp]
+    L.hydra_lora_linear.restype = ctypes.c_int
+    L.hydra_score_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(ctypes.c_size_t)]
+    L.hydra_score_workspace_bytes.restype = ctypes.c_int
+    L.hydra_score.argtypes = [_vp, _vp, _vp, _vp, _f32, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
+                              _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _vp]
+    L.hydra_score.restype = ctypes.c_int
+    L.hydra_score_logits.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+    L.hydra_score_logits.restype = ctypes.c_int
+    L.hydra_status_string.argtypes = [ctypes.c_int]
+    L.hydra_status_string.restype = ctypes.c_char_p
+    L.hydra_abi_version.argtypes = []
+    L.hydra_abi_version.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return lib().hydra_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != HYDRA_OK:
+        raise HydraError(status, where)
+
+
+# ------------------------------------------------------------------ tensor helpers
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else int(t.data_ptr())
+
+
+def _stream_handle(stream) -> Optional[int]:
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def _need(t, name, dtypes, shape=None):
+    torch = _torch()
+    if t is None:
+        return
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a ROCm device, got {t.device}")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def _bf16_types():
+    torch = _torch()
+    return (torch.bfloat16, torch.int16, torch.uint16)
+
+
+# ------------------------------------------------------------------ entry points
+
+def hydra_lora_linear(x, W, A, B, s: float, y_off=None, y_on=None, stream=None) -> None:
+    """y_off = x W^T and/or y_on = x W^T + s (x A^T) B^T (see include/hydra.h).
+
+    x [M,K], W [N,K], A [r,K], B [N,r]: bf16 (or 16-bit integer tensors holding
+    bf16 bits); y_off, y_on [M,N] float32 outputs (either may be None).
+    """
+    torch = _torch()
+    bf = _bf16_types()
+    M, K = x.shape
+    N = W.shape[0]
+    r = 0 if A is None else A.shape[0]
+    _need(x, "x", bf)
+    _need(W, "W", bf, (N, K))
+    _need(A, "A", bf, (r, K))
+    _need(B, "B", bf, (N, r))
+    _need(y_off, "y_off", (torch.float32,), (M, N))
+    _need(y_on, "y_on", (torch.float32,), (M, N))
+    st = lib().hydra_lora_linear(_ptr(x), _ptr(W), _ptr(A), _ptr(B), float(s), M, N, K, r,
+                                 _ptr(y_off), _ptr(y_on), _stream_handle(stream))
+    _check(st, "hydra_lora_linear")
+
+
+def hydra_score_workspace_bytes(M: int, V: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().hydra_score_workspace_bytes(int(M), int(V), ctypes.byref(out)), "hydra_score_workspace_bytes")
+    return int(out.value)
+
+
+def hydra_score(h, W_lm, A, B, s: float, tokens, w_rm, n_seq: int, seq_len: int,
+                lp_on, lp_off, kl, reward=None, lse_on=None, lse_off=None,
+                workspace=None, err_flag=None, stream=None) -> None:
+    """Fused CLM-head (LoRA on and off) log-prob / KL scoring plus the reward head."""
+    torch = _torch()
+    bf = _bf16_types()
+    M, K = h.shape
+    V = W_lm.shape[0]
+    r = 0 if A is None else A.shape[0]
+    if M != n_seq * seq_len:
+        raise ValueError("h rows must equal n_seq * seq_len")
+    _need(h, "h", bf)
+    _need(W_lm, "W_lm", bf, (V, K))
+    _need(A, "A", bf, (r, K))
+    _need(B, "B", bf, (V, r))
+    _need(tokens, "tokens", (torch.int32,), (M,))
+    _need(w_rm, "w_rm", bf, (K,))
+    for name, t in (("lp_on", lp_on), ("lp_off", lp_off), ("kl", kl), ("lse_on", lse_on), ("lse_off", lse_off)):
+        _need(t, name, (torch.float32,), (M,))
+    _need(reward, "reward", (torch.float32,), (n_seq,))
+    _need(err_flag, "err_flag", (torch.int32,), (1,))
+    need = hydra_score_workspace_bytes(M, V)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=h.device)
+    _need(workspace, "workspace", (torch.uint8,))
+    st = lib().hydra_score(_ptr(h), _ptr(W_lm), _ptr(A), _ptr(B), float(s), _ptr(tokens), _ptr(w_rm),
+                           int(n_seq), int(seq_len), K, V, r, _ptr(lp_on), _ptr(lp_off), _ptr(kl), _ptr(reward),
+                           _ptr(lse_on), _ptr(lse_off), _ptr(workspace), workspace.numel(), _ptr(err_flag),
+                           _stream_handle(stream))
+    _check(st, "hydra_score")
+
+
+def hydra_score_logits(logits_on, logits_off, tokens, lp_on, lp_off, kl,
+                       lse_on=None, lse_off=None, err_flag=None, stream=None) -> None:
+    """Sampled-token log-probabilities and KL from materialised fp32 logits."""
+    torch = _torch()
+    M, V = logits_on.shape
+    _need(logits_on, "logits_on", (torch.float32,))
+    _need(logits_off, "logits_off", (torch.float32,), (M, V))
+    _need(tokens, "tokens", (torch.int32,), (M,))
+    for name, t in (("lp_on", lp_on), ("lp_off", lp_off), ("kl", kl), ("lse_on", lse_on), ("lse_off", lse_off)):
+        _need(t, name, (torch.float32,), (M,))
+    _need(err_flag, "err_flag", (torch.int32,), (1,))
+    st = lib().hydra_score_logits(_ptr(logits_on), _ptr(logits_off), _ptr(tokens), M, V, _ptr(lp_on), _ptr(lp_off),
+                                  _ptr(kl), _ptr(lse_on), _ptr(lse_off), _ptr(err_flag), _stream_handle(stream))
+    _check(st, "hydra_score_logits")

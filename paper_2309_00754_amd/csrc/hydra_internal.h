@@ -1,0 +1,73 @@
+// Launchers shared between the C-ABI layer and the kernel translation units.
+// Every launcher assumes its arguments were validated by hydra_api.cpp.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hydra {
+
+struct LinearArgs {
+  const uint16_t* x;  // [M x K] bf16
+  const uint16_t* W;  // [N x K] bf16
+  const uint16_t* A;  // [r x K] bf16
+  const uint16_t* B;  // [N x r] bf16
+  float s;
+  int M, N, K, r;
+  float* y_off;  // [M x N] or nullptr
+  float* y_on;   // [M x N] or nullptr
+};
+
+// Per (row, column tile) partial log-sum-exp state written by the fused
+// CLM-head GEMM: (max_off, sumexp_off, max_on, sumexp_on).
+struct ScoreGemmArgs {
+  LinearArgs lin;          // N = V, y_off / y_on unused
+  const int32_t* tokens;   // [M]
+  float4* part;            // [M x ntn]
+  float* zt;               // [M x 2]: (z_off[token], z_on[token])
+  int ntn;                 // number of column tiles
+};
+
+struct CombineArgs {
+  const float4* part;      // [M x ntn]
+  const float* zt;         // [M x 2]
+  const int32_t* tokens;   // [M]
+  int M, V, ntn;
+  float* lp_on;
+  float* lp_off;
+  float* kl;
+  float* lse_on;           // optional
+  float* lse_off;          // optional
+  int32_t* err;            // optional
+  // reward head
+  const uint16_t* h;       // [M x K]
+  const uint16_t* w_rm;    // [K] or nullptr
+  float* reward;           // [n_seq] or nullptr
+  int n_seq, seq_len, K;
+};
+
+struct LogitsArgs {
+  const float* on;
+  const float* off;
+  const int32_t* tokens;
+  int M, V;
+  float* lp_on;
+  float* lp_off;
+  float* kl;
+  float* lse_on;
+  float* lse_off;
+  int32_t* err;
+};
+
+// Column-tile width of the fused scoring GEMM (number of vocabulary entries
+// one workgroup reduces).
+constexpr int kScoreTileN = 256;
+
+hipError_t launch_lora_gemm(const LinearArgs& a, hipStream_t stream);
+hipError_t launch_lora_gemv(const LinearArgs& a, hipStream_t stream);
+hipError_t launch_score_gemm(const ScoreGemmArgs& a, hipStream_t stream);
+hipError_t launch_score_combine(const CombineArgs& a, hipStream_t stream);
+hipError_t launch_score_logits(const LogitsArgs& a, hipStream_t stream);
+
+}  // namespace hydra

@@ -1,0 +1,119 @@
+"""GPU parity of hydra_lora_linear (both kernels) against the float64 oracle."""
+import numpy as np
+import pytest
+
+import paper_2309_00754_amd as H
+import workloads as WL
+from oracle import lora_linear_ref
+from gpu_helpers import assert_rel, dev_bf16, host, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(c, device, want_off=True, want_on=True, s=None, B=None):
+    import torch
+    s = c.s if s is None else s
+    B = c.B if B is None else B
+    x, W = dev_bf16(c.x, device), dev_bf16(c.W, device)
+    A = dev_bf16(c.A, device) if c.r > 0 else None
+    Bt = dev_bf16(B, device) if c.r > 0 else None
+    y_off = torch.full((c.M, c.N), float("nan"), device=device) if want_off else None
+    y_on = torch.full((c.M, c.N), float("nan"), device=device) if want_on else None
+    H.hydra_lora_linear(x, W, A, Bt, s, y_off, y_on)
+    torch.cuda.synchronize()
+    return (host(y_off) if want_off else None), (host(y_on) if want_on else None)
+
+
+SHAPES = [
+    # (M, K, N, r): decode kernel (M <= 16) and MFMA GEMM (M > 16), ragged
+    # rows / columns / K tails, every padded-rank class, rank 0.
+    (1, 64, 40, 8), (3, 520, 300, 16), (4, 4096, 256, 16), (16, 512, 512, 8), (16, 72, 1000, 64),
+    (5, 136, 33, 1), (7, 256, 20, 0), (2, 8, 17, 33),
+    (17, 64, 256, 8), (33, 520, 300, 16), (128, 512, 256, 16), (130, 72, 513, 1), (257, 1024, 700, 33),
+    (200, 64, 256, 0), (64, 128, 96, 64), (300, 2048, 1200, 17), (129, 8, 255, 16),
+]
+
+
+@pytest.mark.parametrize("M,K,N,r", SHAPES)
+def test_linear_matches_oracle(M, K, N, r, dev):
+    seed = 1000 + M + 7 * K + 13 * N + r
+    say("lora_linear", dict(M=M, K=K, N=N, r=r, seed=seed))
+    c = WL.gen_linear(seed, M, K, N, r, s=2.0)
+    y_off, y_on = _run(c, dev)
+    e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+    assert_rel(y_off, e_off, "y_off")
+    assert_rel(y_on, e_on, "y_on")
+
+
+@pytest.mark.parametrize("M", [4, 64])
+def test_linear_single_outputs(M, dev):
+    say("lora_linear single outputs", M)
+    c = WL.gen_linear(77, M, 256, 300, 16)
+    e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+    off_only, _ = _run(c, dev, want_on=False)
+    _, on_only = _run(c, dev, want_off=False)
+    assert_rel(off_only, e_off, "y_off only")
+    assert_rel(on_only, e_on, "y_on only")
+    both_off, both_on = _run(c, dev)
+    assert np.array_equal(off_only, both_off) and np.array_equal(on_only, both_on)
+
+
+@pytest.mark.parametrize("M", [4, 200])
+def test_lora_off_identities_are_bitwise(M, dev):
+    """B = 0 or s = 0 turns LoRA off: y_on must equal y_off bit for bit."""
+    say("lora_linear B=0 / s=0", M)
+    c = WL.gen_linear(78, M, 512, 384, 16)
+    off, on = _run(c, dev, B=np.zeros_like(c.B))
+    assert np.array_equal(off, on)
+    off2, on2 = _run(c, dev, s=0.0)
+    assert np.array_equal(off2, on2) and np.array_equal(off, off2)
+
+
+@pytest.mark.parametrize("M", [4, 300])
+def test_linear_deterministic(M, dev):
+    say("lora_linear determinism", M)
+    c = WL.gen_linear(79, M, 1024, 520, 16)
+    a = _run(c, dev)
+    b = _run(c, dev)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_adapter_selection_actor_vs_critic(dev):
+    """Hydra-PPO: two adapter sets over one W; each call uses only the pair passed."""
+    say("adapter selection")
+    act = WL.gen_linear(80, 96, 256, 128, 16)
+    crit = WL.gen_linear(81, 96, 256, 128, 16)
+    c2 = WL.LinearCase("critic", act.x, act.W, crit.A, crit.B, 2.0)
+    off_a, on_a = _run(act, dev)
+    off_c, on_c = _run(c2, dev)
+    assert np.array_equal(off_a, off_c)
+    assert_rel(on_c, lora_linear_ref(act.x, act.W, crit.A, crit.B, 2.0)[1], "critic y_on")
+
+
+def test_decode_qkvo_full(dev):
+    """Decode step, batch 4: the four 4096x4096 attention projections, r = 16 (full oracle)."""
+    cases = WL.make("decode_qkvo")
+    for c in cases:
+        say("decode", c.name, c.M, c.K, c.N, c.r)
+        y_off, y_on = _run(c, dev)
+        e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+        assert_rel(y_off, e_off, f"{c.name} y_off")
+        assert_rel(y_on, e_on, f"{c.name} y_on")
+
+
+def test_prefill_layer_full_size_sampled_rows(dev):
+    """Prefill, M = 2048: all seven linears of one Llama-7B layer, r = 16.
+
+    The GPU computes every row in the launch configuration the bench times;
+    the oracle checks 40 sampled rows (first, last, and random) of each.
+    """
+    cases = WL.make("prefill_layer")
+    rng = np.random.default_rng(3)
+    rows = np.unique(np.concatenate([[0, 1, 127, 128, 2047], rng.integers(0, 2048, 35)]))
+    for c in cases:
+        say("prefill", c.name, c.M, c.K, c.N, c.r)
+        y_off, y_on = _run(c, dev)
+        e_off, e_on = lora_linear_ref(c.x[rows], c.W, c.A, c.B, c.s)
+        assert_rel(y_off[rows], e_off, f"{c.name} y_off")
+        assert_rel(y_on[rows], e_on, f"{c.name} y_on")
+        assert np.all(np.isfinite(y_off)) and np.all(np.isfinite(y_on))
