@@ -85,7 +85,9 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   const int M = a.M, N = a.N, K = a.K;
   const int t = threadIdx.x;
   const int lane = t & 63;
-  const int wave = t >> 6;
+  // The wave index is made provably wave-uniform (an SGPR), so branches on it
+  // are scalar branches: MFMAs must never sit under exec-masked divergence.
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int wr = wave >> 1;  // wave row (0..1)
   const int wc = wave & 1;   // wave column (0..1)
   const int l16 = lane & 15;

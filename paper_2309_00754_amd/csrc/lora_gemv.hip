@@ -31,7 +31,7 @@ __global__ __launch_bounds__(WAVES * 64) void lora_gemv_kernel(LinearArgs a) {
 
   const int M = a.M, N = a.N, K = a.K;
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15;
   const int lg = lane >> 4;
   const int n0 = blockIdx.x * NB;
