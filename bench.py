@@ -1,0 +1,309 @@
+"""Benchmark of the Hydra-PPO hot path on one MI355X.
+
+One step is one pass of the whole path over one batch of 4 sequences x 512
+tokens at Llama-7B shapes (hidden 4096, MLP 11008, vocabulary 32000, LoRA
+rank 16, scale 2), i.e. the inference stage of one PPO iteration for one
+decoder layer plus the heads:
+
+  * decode: one generation step of the four attention projections, M = 4
+    (hydra_lora_linear, bandwidth-bound kernel), both LoRA-off and LoRA-on outputs;
+  * prefill: the seven LoRA linears of a layer over all 2048 tokens
+    (hydra_lora_linear, dual-output MFMA GEMM), both outputs;
+  * score: the CLM head with LoRA on and off, sampled-token log-probabilities,
+    per-token KL and the reward head over the 2048 tokens (hydra_score; the
+    logits are never materialised).
+
+Inputs are synthetic (seeded Gaussians, see workloads/) and already resident
+in HBM when the timed region starts.  Each kernel launch is bracketed by HIP
+events on the stream it runs on.  The standalone scoring epilogue over
+materialised logits (hydra_score_logits, 512 x 32000) is timed separately
+(rotating four input sets so that the 256 MB last-level cache does not serve
+it) and reported under "aux"; it is not part of the step.
+
+Prints one JSON line.  ``--gpus`` above 1 is refused: this path is built and
+measured on a single GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "dual-path LoRA GEMM TFLOP/s + scoring tokens/s, % of MFMA/HBM roofline"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+
+
+def lin_flops(M, K, N, r):
+    return 2.0 * M * K * N + 2.0 * M * K * r + 2.0 * M * r * N
+
+
+def lin_bytes(M, K, N, r):
+    return 2.0 * (M * K + N * K + r * K + N * r) + 2 * 4.0 * M * N
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--parts", default="decode,prefill,score",
+                   help="comma list of step parts to run (profiling aid; the metric needs all three)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-aux", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU oracle sample")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus > 1 or world > 1:
+        print(f"bench.py: --gpus {max(args.gpus, world)} refused: this build runs and measures the path on one "
+              f"GPU only (the data-parallel sharding is described, not launched)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2309_00754_amd as H
+    import workloads as WL
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a ROCm GPU", file=sys.stderr)
+        sys.exit(1)
+    H.lib()  # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    parts = [p for p in args.parts.split(",") if p]
+
+    def bf(u):
+        return torch.from_numpy(np.ascontiguousarray(u).view(np.int16)).to(dev)
+
+    t_gen = time.perf_counter()
+    launches = []   # (part, label, fn, flops, bytes)
+    host = {}
+
+    if "decode" in parts:
+        host["decode"] = WL.make("decode_qkvo")
+        for c in host["decode"]:
+            x, W, A, B = bf(c.x), bf(c.W), bf(c.A), bf(c.B)
+            yo = torch.empty(c.M, c.N, device=dev)
+            yn = torch.empty(c.M, c.N, device=dev)
+            fn = (lambda x=x, W=W, A=A, B=B, s=c.s, yo=yo, yn=yn: H.hydra_lora_linear(x, W, A, B, s, yo, yn))
+            launches.append(("decode", c.name, fn, lin_flops(c.M, c.K, c.N, c.r), lin_bytes(c.M, c.K, c.N, c.r)))
+    if "prefill" in parts:
+        xs = {}
+        host["prefill"] = WL.make("prefill_layer")
+        for c in host["prefill"]:
+            if id(c.x) not in xs:
+                xs[id(c.x)] = bf(c.x)
+            x = xs[id(c.x)]
+            W, A, B = bf(c.W), bf(c.A), bf(c.B)
+            yo = torch.empty(c.M, c.N, device=dev)
+            yn = torch.empty(c.M, c.N, device=dev)
+            fn = (lambda x=x, W=W, A=A, B=B, s=c.s, yo=yo, yn=yn: H.hydra_lora_linear(x, W, A, B, s, yo, yn))
+            launches.append(("prefill", c.name, fn, lin_flops(c.M, c.K, c.N, c.r), lin_bytes(c.M, c.K, c.N, c.r)))
+    sc = None
+    if "score" in parts:
+        sc = host["score"] = WL.make("two_head_score")
+        h, Wl, A, B, w_rm = bf(sc.h), bf(sc.W_lm), bf(sc.A), bf(sc.B), bf(sc.w_rm)
+        ids = torch.from_numpy(sc.ids).to(dev)
+        M = sc.M
+        lp_on, lp_off, kl = (torch.empty(M, device=dev) for _ in range(3))
+        reward = torch.empty(sc.n_seq, device=dev)
+        ws = torch.empty(H.hydra_score_workspace_bytes(M, sc.V), dtype=torch.uint8, device=dev)
+        fn = (lambda: H.hydra_score(h, Wl, A, B, sc.s, ids, w_rm, sc.n_seq, sc.seq_len, lp_on, lp_off, kl,
+                                    reward=reward, workspace=ws))
+        fl = lin_flops(M, sc.K, sc.V, sc.r) + 2.0 * sc.n_seq * sc.K
+        by = 2.0 * (M * sc.K + sc.V * sc.K + sc.r * sc.K + sc.V * sc.r + sc.K) + 4.0 * M + 3 * 4.0 * M + 4.0 * sc.n_seq
+        launches.append(("score", "clm_rm_head", fn, fl, by))
+    torch.cuda.synchronize()
+    t_gen = time.perf_counter() - t_gen
+
+    stream = torch.cuda.current_stream()
+
+    def step(evs=None):
+        for i, (_, _, fn, _, _) in enumerate(launches):
+            if evs is not None:
+                evs[i][0].record(stream)
+            fn()
+            if evs is not None:
+                evs[i][1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in launches]
+           for _ in range(K)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    start.record(stream)
+    for k in range(K):
+        step(evs[k])
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / K
+
+    # per-launch kernel durations (ms), averaged over the timed steps
+    dur = np.array([[evs[k][i][0].elapsed_time(evs[k][i][1]) for i in range(len(launches))] for k in range(K)])
+    avg = dur.mean(0)
+
+    comp = {}
+    for part in ("decode", "prefill", "score"):
+        idx = [i for i, l in enumerate(launches) if l[0] == part]
+        if not idx:
+            continue
+        t = float(sum(avg[i] for i in idx)) * 1e-3
+        fl = sum(launches[i][3] for i in idx)
+        by = sum(launches[i][4] for i in idx)
+        d = dict(launches=len(idx), us=round(t * 1e6, 2), tflops=round(fl / t / 1e12, 2),
+                 gbps=round(by / t / 1e9, 1))
+        if part == "decode":
+            d["bound"] = "hbm"
+            d["frac"] = round(by / t / 1e9 / PEAK_HBM_GBPS, 4)
+        else:
+            d["bound"] = "mfma"
+            d["frac"] = round(fl / t / 1e12 / PEAK_BF16_TFLOPS, 4)
+        if part == "score":
+            d["tokens_per_s"] = round(sc.M / t, 1)
+        d["per_launch_us"] = {launches[i][1]: round(float(avg[i]) * 1e3, 2) for i in idx}
+        comp[part] = d
+
+    total_flops = sum(l[3] for l in launches)
+    value = total_flops / (ms_per_step * 1e-3) / 1e12
+
+    # the dominant kernel: the part with the largest share of the step
+    dom = max(comp, key=lambda p: comp[p]["us"])
+    dcomp = comp[dom]
+    if dcomp["bound"] == "hbm":
+        roof = dict(bound="hbm", achieved=dcomp["gbps"], peak=PEAK_HBM_GBPS, unit="GB/s", frac=dcomp["frac"])
+    else:
+        roof = dict(bound="mfma", achieved=dcomp["tflops"], peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                    frac=dcomp["frac"])
+    roof["kernel"] = {"prefill": "lora_gemm_kernel<16,false>", "score": "lora_gemm_kernel<16,true>+combine",
+                      "decode": "lora_gemv_kernel<16,16,8>"}[dom]
+    roof["traffic"] = None
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "hydra_ppo_inference_pass_llama7b_b4x512",
+            "parts": parts,
+            "batch": 4, "seq_len": 512, "hidden": 4096, "mlp": 11008, "vocab": 32000,
+            "lora_rank": 16, "lora_scale": 2.0, "decode_rows": 4, "prefill_rows": 2048,
+            "parallelism": "single_gpu",
+        },
+        "scoring_tokens_per_s": comp.get("score", {}).get("tokens_per_s"),
+        "roofline": roof,
+        "components": comp,
+        "wall_s_timed": round(wall, 4),
+        "input_gen_s": round(t_gen, 2),
+    }
+
+    if not args.no_aux:
+        out["aux"] = {"score_logits": bench_score_logits(torch, H, WL, dev)}
+
+    if not args.no_cpu_baseline:
+        hi = None
+        if all(k in host for k in ("decode", "prefill", "score")):
+            hi = (host["decode"], host["prefill"], host["score"])
+        out["cpu_baseline"] = cpu_baseline(args.cpu_seconds, hi)
+
+    print(json.dumps(out), flush=True)
+
+
+def bench_score_logits(torch, H, WL, dev, iters=20):
+    """hydra_score_logits on 512 x 32000 fp32 logits (on and off), four rotating input sets."""
+    on, off, ids = WL.make("score_logits")
+    M, V = on.shape
+    sets = []
+    for i in range(4):
+        sets.append((torch.from_numpy(on).to(dev) + 0.0 * i, torch.from_numpy(off).to(dev),
+                     torch.from_numpy(ids).to(dev)))
+    outs = [torch.empty(M, device=dev) for _ in range(3)]
+    for i in range(3):
+        a, b, t = sets[i % 4]
+        H.hydra_score_logits(a, b, t, *outs)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
+    for i in range(iters):
+        a, b, t = sets[i % 4]
+        evs[i][0].record(stream)
+        H.hydra_score_logits(a, b, t, *outs)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    us = float(np.median([s.elapsed_time(e) for s, e in evs])) * 1e3
+    by = 2.0 * M * V * 4 + 4.0 * M + 3 * 4.0 * M
+    return dict(rows=M, vocab=V, us=round(us, 2), gbps=round(by / us / 1e3, 1),
+                frac_hbm=round(by / us / 1e3 / PEAK_HBM_GBPS, 4), tokens_per_s=round(M / us * 1e6, 1),
+                note="median of per-launch HIP events over 4 rotating input sets (1.05 GB > last-level cache)")
+
+
+def cpu_baseline(target_s: float, host_inputs=None):
+    """The float64 oracle, as it stands, on a row sample of the same step (host cores)."""
+    import oracle
+    import workloads as WL
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+
+    if host_inputs is None:
+        host_inputs = (WL.make("decode_qkvo"), WL.make("prefill_layer"), WL.make("two_head_score"))
+    dec, pre, sc = host_inputs
+
+    def run(rows):
+        fl = 0.0
+        t0 = time.perf_counter()
+        for c in dec:
+            oracle.lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+            fl += lin_flops(c.M, c.K, c.N, c.r)
+        for c in pre:
+            oracle.lora_linear_ref(c.x[:rows], c.W, c.A, c.B, c.s)
+            fl += lin_flops(rows, c.K, c.N, c.r)
+        oracle.score_head_ref(sc.h[:rows], sc.W_lm, sc.A, sc.B, sc.s, sc.ids[:rows])
+        oracle.reward_ref(sc.h, sc.w_rm, sc.n_seq, sc.seq_len)
+        fl += lin_flops(rows, sc.K, sc.V, sc.r) + 2.0 * sc.n_seq * sc.K
+        return fl, time.perf_counter() - t0
+
+    # time = a + b * rows: fit from two short runs, then size the sample
+    _, t1 = run(16)
+    _, t2 = run(64)
+    b = max((t2 - t1) / 48.0, 1e-6)
+    a = max(t1 - 16 * b, 0.0)
+    rows = int(min(2048, max(64, (target_s - a) / b)))
+    fl, t = run(rows)
+    return dict(value=round(fl / t / 1e12, 5), unit="TFLOP/s", cores=int(threads), kind="oracle",
+                seconds=round(t, 2),
+                sample=f"float64 oracle on one step with the 2048-token parts cut to their first {rows} rows "
+                       f"(decode 4 x M=4 in full; prefill 7 linears and two-head scoring on {rows} rows)",
+                host_cpus=len(os.sched_getaffinity(0)))
+
+
+if __name__ == "__main__":
+    main()

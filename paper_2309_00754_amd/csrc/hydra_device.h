@@ -32,6 +32,39 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, int byte_o
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
 }
 
+// Raw buffer descriptor as four dwords (base, base_hi | stride 0, bytes,
+// format), for use by inline assembly.  All fields must be wave-uniform.
+__device__ __forceinline__ i32x4_t make_rsrc_raw(const void* base, uint32_t bytes) {
+  const uint64_t p = (uint64_t)(uintptr_t)base;
+  return i32x4_t{(int)(uint32_t)p, (int)((uint32_t)(p >> 32) & 0xFFFFu), (int)bytes, 0x00020000};
+}
+
+// 16 bytes per lane copied from a buffer straight into LDS (no register
+// staging): lane i writes [lds_base + 16 i, lds_base + 16 i + 16).  lds_base
+// must be wave-uniform; an out-of-range offset writes zeros.  Issued through
+// inline assembly so that the compiler does not add its own (conservative)
+// waits for it: the callers wait explicitly with wait_vm_barrier before any
+// wave reads the copied data.  M0 is set here; nothing else in these kernels
+// uses M0.
+__device__ __forceinline__ void dma16(const i32x4_t& rsrc, const void* lds_base, int byte_off) {
+  const uint32_t lds_addr = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_base;
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(lds_addr), "v"(byte_off), "s"(rsrc) : "memory");
+}
+
+// Wait until at most N of this wave's vector-memory loads (including LDS
+// copies) are still in flight and all of its LDS operations are done, then
+// join the workgroup barrier.  The empty asm statements stop the compiler
+// from moving memory accesses across the barrier.
+template <int N>
+__device__ __forceinline__ void wait_vm_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit field");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | (((N >> 4) & 3) << 14));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint32_t u16) { return __uint_as_float(u16 << 16); }
 
 // float -> bf16 bits, round to nearest even (finite inputs).

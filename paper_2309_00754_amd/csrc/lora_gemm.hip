@@ -48,7 +48,10 @@ struct Layout {
   static constexpr int WOFF = BM * CPR;
   static constexpr int AOFF = (BM + BN) * CPR;
   static constexpr int STAGE = (BM + BN + RP) * CPR;  // uint4 per stage
-  static constexpr int A_ITERS = (RP * CPR + NT - 1) / NT;
+  // three stages when they fit in the 160 KB of LDS, else two
+  static constexpr int NSTAGES = 3 * STAGE * 16 <= 160 * 1024 ? 3 : 2;
+  static_assert(BM * 2 * RP * 2 <= STAGE * 16, "Ts must fit in one stage");
+  static_assert(BN * RP * 2 + (2 * BM * 4 + BM) * 4 <= STAGE * 16, "Bs, red and tok must fit in one stage");
 };
 
 struct GemmArgs {
@@ -79,7 +82,12 @@ __device__ __forceinline__ void tile_of(int bid, int ntm, int ntn, int& tm, int&
 template <int RP, bool SCORE>
 __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   using L = Layout<RP>;
-  __shared__ uint4 smem[2 * L::STAGE];
+  constexpr int NS = L::NSTAGES;
+  // One array per pipeline stage, always addressed with compile-time stage
+  // indices, so that the compiler's own waits for the LDS copies stay exact.
+  __shared__ uint4 sm0[L::STAGE];
+  __shared__ uint4 sm1[L::STAGE];
+  __shared__ uint4 sm2[NS == 3 ? L::STAGE : 1];
 
   const LinearArgs& a = g.lin;
   const int M = a.M, N = a.N, K = a.K;
@@ -98,42 +106,41 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   const int m0 = tmi * BM;
   const int n0 = tni * BN;
 
-  // ---- global -> register staging: thread t moves 16-byte chunk c of rows
-  // rb + 32 i.  Buffer resources cover exactly the tile's valid rows, so rows
-  // past M (or N, or r) read as zeros; a chunk past K gets an out-of-range
-  // offset and reads as zeros too.
-  const int c = t & 7;
-  const int rb = t >> 3;
-  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x + (size_t)m0 * K, (uint32_t)min(BM, M - m0) * K * 2u);
-  const __amdgpu_buffer_rsrc_t wrs = make_rsrc(a.W + (size_t)n0 * K, (uint32_t)min(BN, N - n0) * K * 2u);
-  const __amdgpu_buffer_rsrc_t arsrc = make_rsrc(a.A, (uint32_t)min(a.r, RP) * K * 2u);
+  // ---- global -> LDS copies.  One copy instruction moves 8 rows x 128 bytes
+  // (64 lanes x 16 bytes) into 1 KB of LDS; lane i fills LDS chunk i of it,
+  // so it fetches the global chunk that the swizzle maps there.  Buffer
+  // resources cover exactly the tile's valid rows (rows past M, N or r read
+  // as zeros); a chunk past K gets an out-of-range offset (zeros as well).
+  const i32x4_t xr = make_rsrc_raw(a.x + (size_t)m0 * K, (uint32_t)min(BM, M - m0) * K * 2u);
+  const i32x4_t wrs = make_rsrc_raw(a.W + (size_t)n0 * K, (uint32_t)min(BN, N - n0) * K * 2u);
+  const i32x4_t arsrc = make_rsrc_raw(a.A, (uint32_t)min(a.r, RP) * K * 2u);
   const int row_bytes = K * 2;
-  const int cofs = c * 16;
+  const int c = (lane & 7) ^ (lane >> 3);   // global chunk fetched by this lane
+  const int rl = lane >> 3;                 // row within the 8-row copy
+  constexpr int XI = BM / 8 / 4;            // copies per wave: x
+  constexpr int WI = BN / 8 / 4;            //                  W
+  constexpr int AI = RP / 8;                // copies in total: A
+  constexpr int AIW = (AI + 3) / 4;         // most A copies one wave issues
+  constexpr int DPW = XI + WI + AI / 4;     // fewest copies any wave issues per slab
 
-  uint4 rx[BM / 32], rw[BN / 32], ra[L::A_ITERS > 0 ? L::A_ITERS : 1];
-
-  auto load_stage = [&](int k0) __attribute__((always_inline)) {
-    const int kofs = (k0 + c * 8) < K ? k0 * 2 + cofs : kOutOfRange;
+  auto issue = [&](uint4* st, int kt) __attribute__((always_inline)) {
+    const int k0 = kt * BK;
+    const bool kv = k0 + c * 8 < K;
+    const int kb = k0 * 2 + c * 16;
 #pragma unroll
-    for (int i = 0; i < BM / 32; ++i)
-      rx[i] = buf_load16(xr, kofs == kOutOfRange ? kOutOfRange : (rb + 32 * i) * row_bytes + kofs);
+    for (int j = 0; j < XI; ++j) {
+      const int ci = wave * XI + j;
+      dma16(xr, st + L::XOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kb : kOutOfRange);
+    }
 #pragma unroll
-    for (int i = 0; i < BN / 32; ++i)
-      rw[i] = buf_load16(wrs, kofs == kOutOfRange ? kOutOfRange : (rb + 32 * i) * row_bytes + kofs);
+    for (int j = 0; j < WI; ++j) {
+      const int ci = wave * WI + j;
+      dma16(wrs, st + L::WOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kb : kOutOfRange);
+    }
 #pragma unroll
-    for (int i = 0; i < L::A_ITERS; ++i)
-      ra[i] = buf_load16(arsrc, kofs == kOutOfRange ? kOutOfRange : (rb + 32 * i) * row_bytes + kofs);
-  };
-  auto store_stage = [&](int buf) __attribute__((always_inline)) {
-    uint4* s = smem + buf * L::STAGE;
-#pragma unroll
-    for (int i = 0; i < BM / 32; ++i) s[L::XOFF + lds_idx(rb + 32 * i, c)] = rx[i];
-#pragma unroll
-    for (int i = 0; i < BN / 32; ++i) s[L::WOFF + lds_idx(rb + 32 * i, c)] = rw[i];
-#pragma unroll
-    for (int i = 0; i < L::A_ITERS; ++i) {
-      const int row = rb + 32 * i;
-      if (row < RP) s[L::AOFF + lds_idx(row, c)] = ra[i];
+    for (int j = 0; j < AIW; ++j) {
+      const int ci = wave + 4 * j;
+      if (ci < AI) dma16(arsrc, st + L::AOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kb : kOutOfRange);
     }
   };
 
@@ -149,15 +156,7 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < (TJ > 0 ? TJ : 1); ++j) accT[q][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int nkt = (K + BK - 1) / BK;
-  load_stage(0);
-  store_stage(0);
-  __syncthreads();
-
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nkt) load_stage((kt + 1) * BK);
-    const uint4* s = smem + buf * L::STAGE;
+  auto compute = [&](const uint4* s) __attribute__((always_inline)) {
 #pragma unroll
     for (int kk = 0; kk < BK / 32; ++kk) {
       const int cc = kk * 4 + lg;
@@ -184,17 +183,43 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
         }
       }
     }
-    if (kt + 1 < nkt) store_stage(buf ^ 1);
-    __syncthreads();
+  };
+
+  // ---- pipeline: slab kt lives in stage kt % NS; slabs kt+1 .. kt+NS-2 are
+  // in flight while slab kt is multiplied.  At the top of each step, the
+  // wait leaves only the later slabs' copies outstanding, and the barrier
+  // makes every wave's part of slab kt visible and retires the stage read in
+  // the previous step, which is then refilled with slab kt + NS - 1.
+  const int nkt = (K + BK - 1) / BK;
+  auto step = [&](const uint4* cur, uint4* nxt, int kt) __attribute__((always_inline)) {
+    if (kt + 1 < nkt) wait_vm_barrier<DPW * (NS - 2)>();
+    else wait_vm_barrier<0>();
+    if (kt + NS - 1 < nkt) issue(nxt, kt + NS - 1);
+    compute(cur);
+  };
+  issue(sm0, 0);
+  if constexpr (NS == 3) {
+    if (nkt > 1) issue(sm1, 1);
+    for (int kt = 0; kt < nkt; kt += 3) {
+      step(sm0, sm2, kt);
+      if (kt + 1 < nkt) step(sm1, sm0, kt + 1);
+      if (kt + 2 < nkt) step(sm2, sm1, kt + 2);
+    }
+  } else {
+    for (int kt = 0; kt < nkt; kt += 2) {
+      step(sm0, sm1, kt);
+      if (kt + 1 < nkt) step(sm1, sm0, kt + 1);
+    }
   }
+  wait_vm_barrier<0>();  // every wave is done with the stages before the epilogue reuses them
 
   // ---------------------------------------------------------------- epilogue
-  // LDS is free again (the loop ended with a barrier).  Layout:
-  //   Ts [BM][2 RP] bf16: s*T split into hi (columns 0..RP) and lo (RP..2RP)
-  //   Bs [BN][RP]   bf16: the tile's rows of B, zero padded to RP
-  //   SCORE only: red [2][BM][4] fp32 and tok [BM] int32 after them.
-  uint16_t* Ts = reinterpret_cast<uint16_t*>(smem);
-  uint16_t* Bs = Ts + BM * 2 * RP;
+  // The stages are free again.  Layout:
+  //   stage 0: Ts [BM][2 RP] bf16, s*T split into hi (columns 0..RP) and lo (RP..2RP)
+  //   stage 1: Bs [BN][RP] bf16, the tile's rows of B zero padded to RP;
+  //            SCORE only: red [2][BM][4] fp32 and tok [BM] int32 after it.
+  uint16_t* Ts = reinterpret_cast<uint16_t*>(sm0);
+  uint16_t* Bs = reinterpret_cast<uint16_t*>(sm1);
   float* red = reinterpret_cast<float*>(Bs + BN * RP);
   int* tok = reinterpret_cast<int*>(red + 2 * BM * 4);
 
