@@ -65,6 +65,17 @@ __device__ __forceinline__ void wait_vm_barrier() {
   asm volatile("" ::: "memory");
 }
 
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+
+// D = A * B + C on one 32x32 output tile with a K = 16 step, bf16 inputs,
+// fp32 accumulation.  Lane l supplies row (l % 32) of A and column (l % 32)
+// of B, each as eight consecutive k values of k-group (l / 32); element
+// 4 i + e of the result lane l holds is D[8 i + 4 (l / 32) + e][l % 32].
+__device__ __forceinline__ f32x16_t mfma32(const uint4& a, const uint4& b, const f32x16_t& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                 c, 0, 0, 0);
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint32_t u16) { return __uint_as_float(u16 << 16); }
 
 // float -> bf16 bits, round to nearest even (finite inputs).

@@ -3,14 +3,20 @@
 // x W^T + s (x A^T) B^T (Sec. 3, "Dynamic LoRA" and "Stage 2: Hydra-PPO":
 // the reference / reward roles are the same network with LoRA ignored).
 //
-// Structure (one 128 x 256 output tile per 256-thread workgroup):
-//  * main loop over K in 64-wide slabs: the x slab [128 x 64], the W slab
-//    [256 x 64] and the LoRA-down slab A [RP x 64] are staged through LDS
-//    (double buffered, XOR-swizzled 16-byte chunks) and consumed by
-//    v_mfma_f32_16x16x32_bf16; each of the 4 waves owns a 64 x 128 sub-tile;
+// Structure (one 128 x 256 output tile per 256-thread workgroup, one
+// workgroup per CU):
+//  * the x slab [128 x 64], the W slab [256 x 64] and the LoRA-down slab
+//    A [RP x 64] of each 64-wide K slab are copied straight from HBM/L2 into
+//    LDS (buffer_load ... lds, no register staging) two slabs ahead, through
+//    a three-stage ring of XOR-swizzled 16-byte chunks;
+//  * each of the 4 waves owns a 64 x 128 sub-tile and runs
+//    v_mfma_f32_32x32x16_bf16 with W as the A operand and x as the B operand,
+//    so that every lane ends up holding four consecutive output columns of
+//    one row (float4 stores in the epilogue); the LDS reads of the next
+//    k-step and the copies of a later slab are slotted between the MFMAs;
 //  * the rank-r product T = x A^T of the tile's 128 rows is accumulated in the
-//    same loop from the x fragments already in registers (each wave owns 32
-//    of the rows, so the work is balanced), and never leaves the chip;
+//    same loop (v_mfma_f32_16x16x32_bf16, 32 rows per wave, so the work is
+//    balanced) and never leaves the chip;
 //  * epilogue: the accumulators are the LoRA-off result.  s*T is split into
 //    bf16 hi + lo parts and multiplied against [B; B] by MFMA, adding the
 //    LoRA update to the same accumulators, which become the LoRA-on result.
@@ -31,15 +37,15 @@ constexpr int BK = 64;         // K slab
 constexpr int NT = 256;        // threads per workgroup (4 waves)
 constexpr int WM = 64;         // wave tile rows
 constexpr int WN = 128;        // wave tile columns
-constexpr int TM = WM / 16;    // MFMA tiles per wave, rows
-constexpr int TN = WN / 16;    // MFMA tiles per wave, columns
+constexpr int MT = WM / 32;    // 32-row x tiles per wave
+constexpr int NTL = WN / 32;   // 32-row W tiles per wave
 constexpr int CPR = BK / 8;    // 16-byte chunks per LDS row
 constexpr int GROUP_M = 8;     // row tiles walked together (L2 reuse of W)
 
 static_assert(kScoreTileN == BN, "score partials assume one partial per GEMM column tile");
 
 // LDS chunk index of (row, 16-byte chunk c): chunks are XOR-swizzled by the
-// row so that the 16 lanes reading one column of chunks hit distinct banks.
+// row so that the lanes reading one column of chunks hit distinct banks.
 __device__ __forceinline__ int lds_idx(int row, int c) { return row * CPR + (c ^ (row & 7)); }
 
 template <int RP>
@@ -60,6 +66,7 @@ struct GemmArgs {
   float4* part;
   float* zt;
   int ntm, ntn;
+  int vec4;  // outputs may be written with 16-byte stores (N % 4 == 0, 16-byte aligned)
 };
 
 // Workgroup id -> (row tile, column tile).  Consecutive workgroup ids are
@@ -84,7 +91,7 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   using L = Layout<RP>;
   constexpr int NS = L::NSTAGES;
   // One array per pipeline stage, always addressed with compile-time stage
-  // indices, so that the compiler's own waits for the LDS copies stay exact.
+  // indices.
   __shared__ uint4 sm0[L::STAGE];
   __shared__ uint4 sm1[L::STAGE];
   __shared__ uint4 sm2[NS == 3 ? L::STAGE : 1];
@@ -100,6 +107,8 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   const int wc = wave & 1;   // wave column (0..1)
   const int l16 = lane & 15;
   const int lg = lane >> 4;
+  const int l32 = lane & 31;
+  const int lh = lane >> 5;
 
   int tmi, tni;
   tile_of(blockIdx.x, g.ntm, g.ntn, tmi, tni);
@@ -122,93 +131,155 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   constexpr int AI = RP / 8;                // copies in total: A
   constexpr int AIW = (AI + 3) / 4;         // most A copies one wave issues
   constexpr int DPW = XI + WI + AI / 4;     // fewest copies any wave issues per slab
+  const int nkt = (K + BK - 1) / BK;
 
-  auto issue = [&](uint4* st, int kt) __attribute__((always_inline)) {
-    const int k0 = kt * BK;
-    const bool kv = k0 + c * 8 < K;
-    const int kb = k0 * 2 + c * 16;
+  f32x16_t acc[MT][NTL];
 #pragma unroll
-    for (int j = 0; j < XI; ++j) {
-      const int ci = wave * XI + j;
-      dma16(xr, st + L::XOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kb : kOutOfRange);
-    }
+  for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int j = 0; j < WI; ++j) {
-      const int ci = wave * WI + j;
-      dma16(wrs, st + L::WOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kb : kOutOfRange);
-    }
+    for (int j = 0; j < NTL; ++j)
 #pragma unroll
-    for (int j = 0; j < AIW; ++j) {
-      const int ci = wave + 4 * j;
-      if (ci < AI) dma16(arsrc, st + L::AOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kb : kOutOfRange);
-    }
-  };
-
-  f32x4_t acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
   constexpr int TJ = RP / 16;
-  f32x4_t accT[2][TJ > 0 ? TJ : 1];
+  constexpr int TJ1 = TJ > 0 ? TJ : 1;
+  f32x4_t accT[2][TJ1];
 #pragma unroll
   for (int q = 0; q < 2; ++q)
 #pragma unroll
-    for (int j = 0; j < (TJ > 0 ? TJ : 1); ++j) accT[q][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TJ1; ++j) accT[q][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  auto compute = [&](const uint4* s) __attribute__((always_inline)) {
-#pragma unroll
-    for (int kk = 0; kk < BK / 32; ++kk) {
-      const int cc = kk * 4 + lg;
-      uint4 af[TM], bfr[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) af[i] = s[L::XOFF + lds_idx(wr * WM + i * 16 + l16, cc)];
-#pragma unroll
-      for (int j = 0; j < TN; ++j) bfr[j] = s[L::WOFF + lds_idx(wc * WN + j * 16 + l16, cc)];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma16(af[i], bfr[j], acc[i][j]);
-      if constexpr (TJ > 0) {
-#pragma unroll
-        for (int j = 0; j < TJ; ++j) {
-          const uint4 alo = s[L::AOFF + lds_idx(j * 16 + l16, cc)];
-          if (wc == 0) {
-            accT[0][j] = mfma16(af[0], alo, accT[0][j]);
-            accT[1][j] = mfma16(af[1], alo, accT[1][j]);
-          } else {
-            accT[0][j] = mfma16(af[2], alo, accT[0][j]);
-            accT[1][j] = mfma16(af[3], alo, accT[1][j]);
-          }
-        }
-      }
+  // Register fragments of one 32-wide k-step: for each 16-wide half h, the W
+  // rows (A operand) and x rows (B operand) of the 32x32x16 MFMAs; the x rows
+  // of this wave's 32 T rows and the LoRA-down rows in the 16x16x32 layout.
+  // Two sets alternate so that the next k-step's LDS reads overlap the
+  // current k-step's MFMAs.
+  struct Frag {
+    uint4 w[2][NTL];
+    uint4 x[2][MT];
+    uint4 tx[2];
+    uint4 a[TJ1];
+  };
+  Frag F0, F1;
+  constexpr int NMAIN = 2 * MT * NTL;          // 32x32x16 MFMAs per k-step
+  constexpr int NR = 2 * NTL + 2 * MT + (TJ > 0 ? 2 + TJ : 0);  // LDS reads per k-step
+  constexpr int ND = XI + WI + AIW;           // copy instructions per wave per slab (at most)
+  static_assert(ND <= NMAIN, "one copy slot per MFMA");
+
+  auto read_one = [&](Frag& F, const uint4* s, int kk, int r) __attribute__((always_inline)) {
+    if (r < 2 * NTL) {
+      const int h = r / NTL, ni = r % NTL;
+      F.w[h][ni] = s[L::WOFF + lds_idx(wc * WN + ni * 32 + l32, kk * 4 + 2 * h + lh)];
+    } else if (r < 2 * NTL + 2 * MT) {
+      const int h = (r - 2 * NTL) / MT, mi = (r - 2 * NTL) % MT;
+      F.x[h][mi] = s[L::XOFF + lds_idx(wr * WM + mi * 32 + l32, kk * 4 + 2 * h + lh)];
+    } else if (r < 2 * NTL + 2 * MT + 2) {
+      const int q = r - 2 * NTL - 2 * MT;
+      F.tx[q] = s[L::XOFF + lds_idx(wr * WM + (wc * 2 + q) * 16 + l16, kk * 4 + lg)];
+    } else {
+      const int j = r - 2 * NTL - 2 * MT - 2;
+      F.a[j] = s[L::AOFF + lds_idx(j * 16 + l16, kk * 4 + lg)];
     }
   };
-
-  // ---- pipeline: slab kt lives in stage kt % NS; slabs kt+1 .. kt+NS-2 are
-  // in flight while slab kt is multiplied.  At the top of each step, the
-  // wait leaves only the later slabs' copies outstanding, and the barrier
-  // makes every wave's part of slab kt visible and retires the stage read in
-  // the previous step, which is then refilled with slab kt + NS - 1.
-  const int nkt = (K + BK - 1) / BK;
-  auto step = [&](const uint4* cur, uint4* nxt, int kt) __attribute__((always_inline)) {
-    if (kt + 1 < nkt) wait_vm_barrier<DPW * (NS - 2)>();
-    else wait_vm_barrier<0>();
-    if (kt + NS - 1 < nkt) issue(nxt, kt + NS - 1);
-    compute(cur);
+  auto dma_one = [&](uint4* st, int kofs, bool kv, int d) __attribute__((always_inline)) {
+    if (d < XI) {
+      const int ci = wave * XI + d;
+      dma16(xr, st + L::XOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kofs : kOutOfRange);
+    } else if (d < XI + WI) {
+      const int ci = wave * WI + (d - XI);
+      dma16(wrs, st + L::WOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kofs : kOutOfRange);
+    } else {
+      const int ci = wave + 4 * (d - XI - WI);
+      if (ci < AI) dma16(arsrc, st + L::AOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kofs : kOutOfRange);
+    }
   };
-  issue(sm0, 0);
+  auto issue_all = [&](uint4* st, int kt) __attribute__((always_inline)) {
+    const int k0 = kt * BK;
+#pragma unroll
+    for (int d = 0; d < ND; ++d) dma_one(st, k0 * 2 + c * 16, k0 + c * 8 < K, d);
+  };
+
+  // Copy instructions [d0, d1) of a slab go out in one k-step, the rest in
+  // the other, so that no k-step stalls on a burst of copies.
+  constexpr int DA = (ND + 1) / 2;  // copies issued in k-step 0
+
+  // One k-step: the NMAIN MFMAs of the wave tile on Fc (then the LoRA-down
+  // MFMAs), with one LDS read that fills Fn and one copy of a later slab
+  // slotted after each MFMA.  The scheduling barriers keep that order.
+  auto kstep = [&](const Frag& Fc, Frag& Fn, const uint4* rs, int rkk, uint4* dst, int dkt, int d0, int d1)
+      __attribute__((always_inline)) {
+    const bool do_dma = d1 > d0;
+    const int k0 = dkt * BK;
+    const bool kv = dkt < nkt && k0 + c * 8 < K;
+    const int kofs = k0 * 2 + c * 16;
+#pragma unroll
+    for (int m = 0; m < NMAIN; ++m) {
+      const int h = m / (MT * NTL), mi = (m / NTL) % MT, ni = m % NTL;
+      acc[mi][ni] = mfma32(Fc.w[h][ni], Fc.x[h][mi], acc[mi][ni]);
+      if (m < NR) read_one(Fn, rs, rkk, m);
+      if (do_dma && m >= d0 && m < d1) dma_one(dst, kofs, kv, m);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (TJ > 0) {
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) {
+        accT[0][j] = mfma16(Fc.tx[0], Fc.a[j], accT[0][j]);
+        accT[1][j] = mfma16(Fc.tx[1], Fc.a[j], accT[1][j]);
+      }
+    }
+#pragma unroll
+    for (int r = NMAIN; r < NR; ++r) read_one(Fn, rs, rkk, r);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // ---- pipeline.  Slab kt lives in stage kt % NS.  Each iteration:
+  //   k-step 0 of slab kt (MFMAs on F0) while F1 <- k-step 1 of slab kt and
+  //     the first copies of slab kt + NS - 1 go into the stage freed one
+  //     iteration ago;
+  //   wait for slab kt + 1, barrier (stage kt is retired, kt + 1 visible);
+  //   k-step 1 of slab kt (MFMAs on F1) while F0 <- k-step 0 of slab kt + 1
+  //     and the remaining copies go out.
+  // With NS = 3, at the barrier only the first part of slab kt + 2 (DAW per
+  // wave at least) may still be in flight; with NS = 2 all copies of slab
+  // kt + 1 go out in k-step 0 and are waited for at the barrier.  Past the
+  // last slab the copies get out-of-range offsets (they write zeros into a
+  // stage that is not read again) and the last iteration's reads fill
+  // registers that are not used, so every iteration is the same straight-line
+  // code.
+  constexpr int DAW = NS == 3 ? (DA < XI + WI ? DA : XI + WI) : 0;
+  auto iter = [&](const uint4* cur, uint4* dst, const uint4* nxt, int kt) __attribute__((always_inline)) {
+    if constexpr (NS == 3) {
+      kstep(F0, F1, cur, 1, dst, kt + 2, 0, DA);
+      wait_vm_barrier<DAW>();
+      kstep(F1, F0, nxt, 0, dst, kt + 2, DA, ND);
+    } else {
+      kstep(F0, F1, cur, 1, dst, kt + 1, 0, ND);
+      wait_vm_barrier<0>();
+      kstep(F1, F0, nxt, 0, nullptr, 0, 0, 0);
+    }
+  };
+  issue_all(sm0, 0);
   if constexpr (NS == 3) {
-    if (nkt > 1) issue(sm1, 1);
+    if (nkt > 1) {
+      issue_all(sm1, 1);
+      wait_vm_barrier<DPW>();
+    } else {
+      wait_vm_barrier<0>();
+    }
+  } else {
+    wait_vm_barrier<0>();
+  }
+#pragma unroll
+  for (int r = 0; r < NR; ++r) read_one(F0, sm0, 0, r);
+  if constexpr (NS == 3) {
     for (int kt = 0; kt < nkt; kt += 3) {
-      step(sm0, sm2, kt);
-      if (kt + 1 < nkt) step(sm1, sm0, kt + 1);
-      if (kt + 2 < nkt) step(sm2, sm1, kt + 2);
+      iter(sm0, sm2, sm1, kt);
+      if (kt + 1 < nkt) iter(sm1, sm0, sm2, kt + 1);
+      if (kt + 2 < nkt) iter(sm2, sm1, sm0, kt + 2);
     }
   } else {
     for (int kt = 0; kt < nkt; kt += 2) {
-      step(sm0, sm1, kt);
-      if (kt + 1 < nkt) step(sm1, sm0, kt + 1);
+      iter(sm0, sm1, sm1, kt);
+      if (kt + 1 < nkt) iter(sm1, sm0, sm0, kt + 1);
     }
   }
   wait_vm_barrier<0>();  // every wave is done with the stages before the epilogue reuses them
@@ -227,15 +298,16 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   if constexpr (TJ > 0) {
     if (want_on) {
       const float sc = a.s;
+      // accT[q][j] holds T[wr*64 + (wc*2+q)*16 + 4 lg + e][16 j + l16]
 #pragma unroll
       for (int q = 0; q < 2; ++q)
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int row = wr * WM + (wc * 2 + q) * 16 + lg * 4 + i;
+          for (int e = 0; e < 4; ++e) {
+            const int row = wr * WM + (wc * 2 + q) * 16 + lg * 4 + e;
             const int col = j * 16 + l16;
-            const float v = sc * accT[q][j][i];
+            const float v = sc * accT[q][j][e];
             const uint32_t hi = f32_to_bf16_rne(v);
             const uint32_t lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
             Ts[row * 2 * RP + col] = (uint16_t)hi;
@@ -259,42 +331,53 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   }
   __syncthreads();
 
-  // s*T*B^T added by MFMA: A operand = [hi | lo] rows of Ts, B operand = [B; B].
+  // s*T*B^T added by 32x32x16 MFMAs: A operand = rows of [B | B] (k < RP picks
+  // B against the hi part, k >= RP against the lo part), B operand = rows of
+  // Ts ([hi | lo] along k).
   auto apply_lora = [&]() __attribute__((always_inline)) {
     if constexpr (TJ > 0) {
 #pragma unroll
-      for (int ks = 0; ks < (2 * RP) / 32; ++ks) {
-        const int kofs = ks * 32 + lg * 8;   // k within [0, 2 RP)
+      for (int ks = 0; ks < (2 * RP) / 16; ++ks) {
+        const int kofs = ks * 16 + lh * 8;   // k within [0, 2 RP)
         const int kb = kofs % RP;            // matching column of B
-        uint4 tf[TM], bfr[TN];
+        uint4 bfr[NTL], tf[MT];
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
-          tf[i] = *reinterpret_cast<const uint4*>(Ts + (wr * WM + i * 16 + l16) * 2 * RP + kofs);
+        for (int ni = 0; ni < NTL; ++ni)
+          bfr[ni] = *reinterpret_cast<const uint4*>(Bs + (wc * WN + ni * 32 + l32) * RP + kb);
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          bfr[j] = *reinterpret_cast<const uint4*>(Bs + (wc * WN + j * 16 + l16) * RP + kb);
+        for (int mi = 0; mi < MT; ++mi)
+          tf[mi] = *reinterpret_cast<const uint4*>(Ts + (wr * WM + mi * 32 + l32) * 2 * RP + kofs);
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+        for (int mi = 0; mi < MT; ++mi)
 #pragma unroll
-          for (int j = 0; j < TN; ++j) acc[i][j] = mfma16(tf[i], bfr[j], acc[i][j]);
+          for (int ni = 0; ni < NTL; ++ni) acc[mi][ni] = mfma32(bfr[ni], tf[mi], acc[mi][ni]);
       }
     }
   };
 
+  // acc[mi][ni][4 i + e] holds y[wr*64 + mi*32 + l32][wc*128 + ni*32 + 8 i + 4 lh + e]
   if constexpr (!SCORE) {
     auto store = [&](float* y) __attribute__((always_inline)) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+      for (int mi = 0; mi < MT; ++mi) {
+        const int row = m0 + wr * WM + mi * 32 + l32;
+        if (row >= M) continue;
+        float* yr = y + (size_t)row * N;
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int col = n0 + wc * WN + j * 16 + l16;
-          if (col >= N) continue;
+        for (int ni = 0; ni < NTL; ++ni)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int row = m0 + wr * WM + i * 16 + lg * 4 + e;
-            if (row < M) y[(size_t)row * N + col] = acc[i][j][e];
+          for (int i = 0; i < 4; ++i) {
+            const int col = n0 + wc * WN + ni * 32 + 8 * i + 4 * lh;
+            const f32x16_t& v = acc[mi][ni];
+            if (g.vec4 && col + 3 < N) {
+              *reinterpret_cast<float4*>(yr + col) = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if (col + e < N) yr[col + e] = v[4 * i + e];
+            }
           }
-        }
+      }
     };
     if (a.y_off) store(a.y_off);
     if (a.y_on) {
@@ -302,42 +385,42 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
       store(a.y_on);
     }
   } else {
-    // Per-row (max, sum exp) over this wave's 128 columns, then over the two
-    // waves sharing the rows.  Identical code for the off and on passes.
+    // Per-row (max, sum exp) over this wave's 128 columns (64 per lane, then
+    // the lane pair l, l + 32), then over the two waves sharing the rows.
+    // Identical code for the off and on passes.
     auto row_stats = [&](int slot) __attribute__((always_inline)) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+      for (int mi = 0; mi < MT; ++mi) {
+        const int rlc = wr * WM + mi * 32 + l32;
+        const int tk = tok[rlc];
+        float mx = -INFINITY;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int rl = wr * WM + i * 16 + lg * 4 + e;
-          const int tk = tok[rl];
-          float mx = -INFINITY;
+        for (int ni = 0; ni < NTL; ++ni)
 #pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const int col = n0 + wc * WN + j * 16 + l16;
-            if (col < N) mx = fmaxf(mx, acc[i][j][e]);
+          for (int k = 0; k < 16; ++k) {
+            const int col = n0 + wc * WN + ni * 32 + 8 * (k >> 2) + 4 * lh + (k & 3);
+            if (col < N) mx = fmaxf(mx, acc[mi][ni][k]);
             // the lane holding the sampled token's column records its logit
-            if (col == tk) g.zt[(size_t)(m0 + rl) * 2 + (slot >> 1)] = acc[i][j][e];
+            if (col == tk) g.zt[(size_t)(m0 + rlc) * 2 + (slot >> 1)] = acc[mi][ni][k];
           }
-          float sm = 0.f;
-          if (mx != -INFINITY) {
+        float sm = 0.f;
+        if (mx != -INFINITY) {
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-              const int col = n0 + wc * WN + j * 16 + l16;
-              if (col < N) sm += exp_e(acc[i][j][e] - mx);
+          for (int ni = 0; ni < NTL; ++ni)
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+              const int col = n0 + wc * WN + ni * 32 + 8 * (k >> 2) + 4 * lh + (k & 3);
+              if (col < N) sm += exp_e(acc[mi][ni][k] - mx);
             }
-          }
-#pragma unroll
-          for (int off = 1; off < 16; off <<= 1) {
-            const float mo = __shfl_xor(mx, off);
-            const float so = __shfl_xor(sm, off);
-            lse_merge(mx, sm, mo, so);
-          }
-          if (l16 == 0) {
-            red[(wc * BM + rl) * 4 + slot] = mx;
-            red[(wc * BM + rl) * 4 + slot + 1] = sm;
-          }
         }
+        const float mo = __shfl_xor(mx, 32);
+        const float so = __shfl_xor(sm, 32);
+        lse_merge(mx, sm, mo, so);
+        if (lh == 0) {
+          red[(wc * BM + rlc) * 4 + slot] = mx;
+          red[(wc * BM + rlc) * 4 + slot + 1] = sm;
+        }
+      }
     };
     row_stats(0);     // LoRA off
     apply_lora();
@@ -370,6 +453,8 @@ hipError_t launch(const GemmArgs& g, int rp, hipStream_t stream) {
 
 int padded_rank(int r) { return r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : 64; }
 
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
 }  // namespace
 
 hipError_t launch_lora_gemm(const LinearArgs& a, hipStream_t stream) {
@@ -377,6 +462,7 @@ hipError_t launch_lora_gemm(const LinearArgs& a, hipStream_t stream) {
   g.lin = a;
   g.ntm = (a.M + BM - 1) / BM;
   g.ntn = (a.N + BN - 1) / BN;
+  g.vec4 = (a.N % 4 == 0) && (!a.y_off || aligned16(a.y_off)) && (!a.y_on || aligned16(a.y_on));
   const int rp = a.y_on ? padded_rank(a.r) : 0;
   return launch<false>(g, rp, stream);
 }
