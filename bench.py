@@ -60,6 +60,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-aux", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU oracle sample")
+    p.add_argument("--copy-bytes", type=int, default=0,
+                   help="run one plain device-to-device copy of this many bytes before the steps "
+                        "(calibrates FETCH_SIZE / WRITE_SIZE counters in a profiling run)")
     return p.parse_args()
 
 
@@ -125,6 +128,14 @@ def main():
         launches.append(("score", "clm_rm_head", fn, fl, by))
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
+
+    if args.copy_bytes > 0:
+        src = torch.full((args.copy_bytes,), 7, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     stream = torch.cuda.current_stream()
 
@@ -193,7 +204,10 @@ def main():
                     frac=dcomp["frac"])
     roof["kernel"] = {"prefill": "lora_gemm_kernel<16,false>", "score": "lora_gemm_kernel<16,true>+combine",
                       "decode": "lora_gemv_kernel<16,16,8>"}[dom]
-    roof["traffic"] = None
+    tr = committed_traffic(dom)
+    roof["traffic"] = None if tr is None else tr["bytes_per_launch"]
+    if tr is not None:
+        roof["traffic_detail"] = tr
 
     out = {
         "metric": METRIC,
@@ -232,6 +246,45 @@ def main():
         out["cpu_baseline"] = cpu_baseline(args.cpu_seconds, hi)
 
     print(json.dumps(out), flush=True)
+
+
+def kernel_source_digest() -> str:
+    """sha256 of the HIP sources the dominant kernels are built from."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2309_00754_amd", "csrc")
+    for name in ("lora_gemm.hip", "hydra_device.h"):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def committed_traffic(part: str):
+    """HBM bytes per launch of the dominant kernel, from the committed counter summary.
+
+    profiles/traffic_<part>.txt holds FETCH_SIZE / WRITE_SIZE readings scaled by a
+    plain copy of known size, and the digest of the kernel sources they were taken
+    on; when the sources have changed since, the figure is stale and None is returned.
+    """
+    path = os.path.join(ROOT, "profiles", f"traffic_{part}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.split("=", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256") != kernel_source_digest():
+        return None
+    try:
+        return {"bytes_per_launch": float(kv["hbm_bytes_per_launch"]),
+                "read_bytes_per_launch": float(kv["read_bytes_per_launch"]),
+                "write_bytes_per_launch": float(kv["write_bytes_per_launch"]),
+                "algorithmic_bytes_per_launch": float(kv["algorithmic_bytes_per_launch"]),
+                "source": os.path.relpath(path, ROOT)}
+    except (KeyError, ValueError):
+        return None
 
 
 def bench_score_logits(torch, H, WL, dev, iters=20):

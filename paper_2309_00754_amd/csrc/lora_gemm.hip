@@ -133,6 +133,31 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   constexpr int DPW = XI + WI + AI / 4;     // fewest copies any wave issues per slab
   const int nkt = (K + BK - 1) / BK;
 
+  // The epilogue's global inputs are fetched now, so that they have arrived
+  // long before the main loop ends: the tile's rows of B (thread t holds row
+  // n0 + t, zero padded to RP; rows past N read as zeros through the buffer
+  // resource) and, for SCORE, the sampled token of row m0 + t.
+  constexpr bool B_EARLY = RP > 0 && RP <= 32;
+  uint32_t breg[B_EARLY ? RP : 1];
+  const bool want_on = SCORE || a.y_on != nullptr;
+  if constexpr (B_EARLY) {
+    const __amdgpu_buffer_rsrc_t brs = make_rsrc(a.B + (size_t)n0 * a.r, (uint32_t)min(BN, N - n0) * a.r * 2u);
+#pragma unroll
+    for (int j = 0; j < RP; ++j) {
+      const bool ok = want_on && j < a.r;
+      const uint32_t v = __builtin_amdgcn_raw_buffer_load_b16(brs, ok ? (t * a.r + j) * 2 : kOutOfRange, 0, 0);
+      breg[j] = ok ? v : 0u;
+    }
+  }
+  int tok_early = -1;
+  if constexpr (SCORE) {
+    if (t < BM) {
+      const int row = m0 + t;
+      const int v = g.tokens[row < M ? row : 0];
+      tok_early = row < M ? v : -1;
+    }
+  }
+
   f32x16_t acc[MT][NTL];
 #pragma unroll
   for (int i = 0; i < MT; ++i)
@@ -294,7 +319,6 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   float* red = reinterpret_cast<float*>(Bs + BN * RP);
   int* tok = reinterpret_cast<int*>(red + 2 * BM * 4);
 
-  const bool want_on = SCORE || a.y_on != nullptr;
   if constexpr (TJ > 0) {
     if (want_on) {
       const float sc = a.s;
@@ -313,21 +337,28 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
             Ts[row * 2 * RP + col] = (uint16_t)hi;
             Ts[row * 2 * RP + RP + col] = (uint16_t)lo;
           }
-      for (int e = t; e < BN * RP; e += NT) {
-        const int n = e / RP, j = e - (e / RP) * RP;
-        const int gn = n0 + n;
-        const bool ok = gn < N && j < a.r;
-        const uint16_t v = a.B[ok ? (size_t)gn * a.r + j : 0];
-        Bs[e] = ok ? v : (uint16_t)0;
+      if constexpr (B_EARLY) {
+        static_assert(BN == NT, "one B row per thread");
+#pragma unroll
+        for (int j = 0; j < RP; j += 2) *reinterpret_cast<uint32_t*>(Bs + t * RP + j) = breg[j] | (breg[j + 1] << 16);
+      } else {
+        // large ranks: all loads of the thread are issued before any store
+        uint16_t v[RP];
+#pragma unroll
+        for (int i = 0; i < RP; ++i) {
+          const int e = t + i * NT;
+          const int n = e / RP, j = e % RP;
+          const bool ok = n0 + n < N && j < a.r;
+          const uint16_t u = a.B[ok ? (size_t)(n0 + n) * a.r + j : 0];
+          v[i] = ok ? u : (uint16_t)0;
+        }
+#pragma unroll
+        for (int i = 0; i < RP; ++i) Bs[t + i * NT] = v[i];
       }
     }
   }
   if constexpr (SCORE) {
-    for (int e = t; e < BM; e += NT) {
-      const int row = m0 + e;
-      const int v = g.tokens[row < M ? row : 0];
-      tok[e] = row < M ? v : -1;
-    }
+    if (t < BM) tok[t] = tok_early;
   }
   __syncthreads();
 
