@@ -93,13 +93,17 @@ def main():
     host = {}
 
     if "decode" in parts:
-        host["decode"] = WL.make("decode_qkvo")
-        for c in host["decode"]:
-            x, W, A, B = bf(c.x), bf(c.W), bf(c.A), bf(c.B)
-            yo = torch.empty(c.M, c.N, device=dev)
-            yn = torch.empty(c.M, c.N, device=dev)
-            fn = (lambda x=x, W=W, A=A, B=B, s=c.s, yo=yo, yn=yn: H.hydra_lora_linear(x, W, A, B, s, yo, yn))
-            launches.append(("decode", c.name, fn, lin_flops(c.M, c.K, c.N, c.r), lin_bytes(c.M, c.K, c.N, c.r)))
+        # the four attention projections of one decode step, one grouped launch
+        host["decode"] = dec = WL.make("decode_qkvo")
+        xd = bf(dec[0].x)
+        gW = [bf(c.W) for c in dec]
+        gA = [bf(c.A) for c in dec]
+        gB = [bf(c.B) for c in dec]
+        gyo = [torch.empty(c.M, c.N, device=dev) for c in dec]
+        gyn = [torch.empty(c.M, c.N, device=dev) for c in dec]
+        fn = (lambda: H.hydra_lora_linear_group([xd] * len(dec), gW, gA, gB, [c.s for c in dec], gyo, gyn))
+        launches.append(("decode", "qkvo", fn, sum(lin_flops(c.M, c.K, c.N, c.r) for c in dec),
+                         sum(lin_bytes(c.M, c.K, c.N, c.r) for c in dec)))
     if "prefill" in parts:
         xs = {}
         host["prefill"] = WL.make("prefill_layer")
@@ -203,7 +207,7 @@ def main():
         roof = dict(bound="mfma", achieved=dcomp["tflops"], peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
                     frac=dcomp["frac"])
     roof["kernel"] = {"prefill": "lora_gemm_kernel<16,false>", "score": "lora_gemm_kernel<16,true>+combine",
-                      "decode": "lora_gemv_kernel<16,16,8>"}[dom]
+                      "decode": "lora_gemv_kernel<16,32,16,8> (grouped q/k/v/o)"}[dom]
     tr = committed_traffic(dom)
     roof["traffic"] = None if tr is None else tr["bytes_per_launch"]
     if tr is not None:

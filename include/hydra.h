@@ -85,6 +85,32 @@ hydra_status hydra_lora_linear(const uint16_t* x, const uint16_t* W, const uint1
                                float s, int64_t M, int64_t N, int64_t K, int64_t r,
                                float* y_off, float* y_on, void* stream);
 
+/* Largest number of linears in one hydra_lora_linear_group call. */
+#define HYDRA_MAX_GROUP 8
+
+/*
+ * hydra_lora_linear_group -- G independent LoRA-switchable linears that share
+ * M, N, K and r, in one launch (for instance the q/k/v/o projections of one
+ * decode step, App. A Alg. 2 "generate"; each with its own adapter).
+ * Defined by: the same passages as hydra_lora_linear.
+ *
+ *   G                     1 <= G <= HYDRA_MAX_GROUP
+ *   x, W, A, B, y_off, y_on   HOST arrays of G device pointers with the meaning,
+ *                         layout and alignment of hydra_lora_linear's arguments;
+ *                         A, B, y_off, y_on may be NULL arrays (all members NULL)
+ *                         or hold NULL entries
+ *   s                     HOST array of G scales
+ * Member i computes exactly what hydra_lora_linear(x[i], W[i], A[i], B[i], s[i],
+ * M, N, K, r, y_off[i], y_on[i]) computes.  Each member needs at least one
+ * output.  M <= 16 runs one launch for the whole group; larger M runs the GEMM
+ * once per member.  Errors as in hydra_lora_linear; HYDRA_ERR_SHAPE for G out
+ * of range.
+ */
+hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const uint16_t* const* W,
+                                     const uint16_t* const* A, const uint16_t* const* B, const float* s,
+                                     int64_t M, int64_t N, int64_t K, int64_t r,
+                                     float* const* y_off, float* const* y_on, void* stream);
+
 /*
  * hydra_score_workspace_bytes -- device workspace that hydra_score needs for
  * M = n_seq * seq_len token rows and a vocabulary of V.  Writes *bytes.

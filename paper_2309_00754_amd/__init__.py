@@ -11,12 +11,14 @@ from ._binding import (  # noqa: F401
     HYDRA_ERR_SHAPE,
     HYDRA_ERR_UNSUPPORTED,
     HYDRA_ERR_WORKSPACE,
+    HYDRA_MAX_GROUP,
     HYDRA_MAX_RANK,
     HYDRA_OK,
     HydraError,
     HydraLibraryMissing,
     LIB_PATH,
     hydra_lora_linear,
+    hydra_lora_linear_group,
     hydra_score,
     hydra_score_logits,
     hydra_score_workspace_bytes,

@@ -23,10 +23,12 @@ HYDRA_ERR_UNSUPPORTED = -4
 HYDRA_ERR_WORKSPACE = -5
 HYDRA_ERR_HIP = -6
 HYDRA_MAX_RANK = 64
+HYDRA_MAX_GROUP = 8
 
 # Every symbol include/hydra.h declares.
 EXPORTED = (
     "hydra_lora_linear",
+    "hydra_lora_linear_group",
     "hydra_score_workspace_bytes",
     "hydra_score",
     "hydra_score_logits",
@@ -63,6 +65,10 @@ def lib() -> ctypes.CDLL:
     L = ctypes.CDLL(LIB_PATH)
     L.hydra_lora_linear.argtypes = [_vp, _vp, _vp, _vp, _f32, _i64, _i64, _i64, _i64, _vp, _vp, _vp]
     L.hydra_lora_linear.restype = ctypes.c_int
+    _pp = ctypes.POINTER(ctypes.c_void_p)
+    L.hydra_lora_linear_group.argtypes = [_i64, _pp, _pp, _pp, _pp, ctypes.POINTER(ctypes.c_float), _i64, _i64, _i64,
+                                          _i64, _pp, _pp, _vp]
+    L.hydra_lora_linear_group.restype = ctypes.c_int
     L.hydra_score_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(ctypes.c_size_t)]
     L.hydra_score_workspace_bytes.restype = ctypes.c_int
     L.hydra_score.argtypes = [_vp, _vp, _vp, _vp, _f32, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
@@ -148,6 +154,42 @@ def hydra_lora_linear(x, W, A, B, s: float, y_off=None, y_on=None, stream=None) 
     st = lib().hydra_lora_linear(_ptr(x), _ptr(W), _ptr(A), _ptr(B), float(s), M, N, K, r,
                                  _ptr(y_off), _ptr(y_on), _stream_handle(stream))
     _check(st, "hydra_lora_linear")
+
+
+def _ptr_array(ts):
+    arr = (ctypes.c_void_p * len(ts))()
+    for i, t in enumerate(ts):
+        arr[i] = _ptr(t)
+    return arr
+
+
+def hydra_lora_linear_group(xs, Ws, As, Bs, ss, y_offs=None, y_ons=None, stream=None) -> None:
+    """G linears with shared M, N, K, r in one call (see include/hydra.h).
+
+    xs, Ws, As, Bs, y_offs, y_ons: sequences of G tensors (entries may be None);
+    ss: G scales.
+    """
+    torch = _torch()
+    bf = _bf16_types()
+    G = len(Ws)
+    if not (len(xs) == len(As) == len(Bs) == len(ss) == G):
+        raise ValueError("all per-member sequences must have the same length")
+    y_offs = list(y_offs) if y_offs is not None else [None] * G
+    y_ons = list(y_ons) if y_ons is not None else [None] * G
+    M, K = xs[0].shape
+    N = Ws[0].shape[0]
+    r = next((a.shape[0] for a in As if a is not None), 0)
+    for i in range(G):
+        _need(xs[i], "x", bf, (M, K))
+        _need(Ws[i], "W", bf, (N, K))
+        _need(As[i], "A", bf, (r, K))
+        _need(Bs[i], "B", bf, (N, r))
+        _need(y_offs[i], "y_off", (torch.float32,), (M, N))
+        _need(y_ons[i], "y_on", (torch.float32,), (M, N))
+    svals = (ctypes.c_float * G)(*[float(v) for v in ss])
+    st = lib().hydra_lora_linear_group(G, _ptr_array(xs), _ptr_array(Ws), _ptr_array(As), _ptr_array(Bs), svals,
+                                       M, N, K, r, _ptr_array(y_offs), _ptr_array(y_ons), _stream_handle(stream))
+    _check(st, "hydra_lora_linear_group")
 
 
 def hydra_score_workspace_bytes(M: int, V: int) -> int:

@@ -31,32 +31,71 @@ extern "C" {
 hydra_status hydra_lora_linear(const uint16_t* x, const uint16_t* W, const uint16_t* A, const uint16_t* B, float s,
                                int64_t M, int64_t N, int64_t K, int64_t r, float* y_off, float* y_on,
                                void* stream) {
-  if (!x || !W) return HYDRA_ERR_NULL;
+  return hydra_lora_linear_group(1, &x, &W, &A, &B, &s, M, N, K, r, &y_off, &y_on, stream);
+}
+
+hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const uint16_t* const* W,
+                                     const uint16_t* const* A, const uint16_t* const* B, const float* s, int64_t M,
+                                     int64_t N, int64_t K, int64_t r, float* const* y_off, float* const* y_on,
+                                     void* stream) {
+  if (G < 1 || G > HYDRA_MAX_GROUP) return HYDRA_ERR_SHAPE;
+  if (!x || !W || !s) return HYDRA_ERR_NULL;
   if (!y_off && !y_on) return HYDRA_ERR_NULL;
   if (!dim_ok(M) || !dim_ok(N) || !dim_ok(K) || (K % 8) != 0 || K > kMaxK) return HYDRA_ERR_SHAPE;
   if (r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
-  if (y_off && y_off == y_on) return HYDRA_ERR_SHAPE;
-  const bool lora = y_on && r > 0;
-  if (lora && (!A || !B)) return HYDRA_ERR_NULL;
-  if (!aligned(x, 16) || !aligned(W, 16)) return HYDRA_ERR_ALIGN;
-  if (lora && (!aligned(A, 16) || !aligned(B, 2))) return HYDRA_ERR_ALIGN;
-  if ((y_off && !aligned(y_off, 4)) || (y_on && !aligned(y_on, 4))) return HYDRA_ERR_ALIGN;
-
-  hydra::LinearArgs a{};
-  a.x = x;
-  a.W = W;
-  a.A = lora ? A : nullptr;
-  a.B = lora ? B : nullptr;
-  a.s = s;
-  a.M = int(M);
-  a.N = int(N);
-  a.K = int(K);
-  a.r = lora ? int(r) : 0;
-  a.y_off = y_off;
-  a.y_on = y_on;
+  hydra::GroupArgs g{};
+  g.G = int(G);
+  g.M = int(M);
+  g.N = int(N);
+  g.K = int(K);
+  g.r = int(r);
+  bool any_on = false;
+  for (int64_t i = 0; i < G; ++i) {
+    float* yo = y_off ? y_off[i] : nullptr;
+    float* yn = y_on ? y_on[i] : nullptr;
+    if (!x[i] || !W[i]) return HYDRA_ERR_NULL;
+    if (!yo && !yn) return HYDRA_ERR_NULL;
+    if (yo && yo == yn) return HYDRA_ERR_SHAPE;
+    const bool lora = yn && r > 0;
+    const uint16_t* Ai = A ? A[i] : nullptr;
+    const uint16_t* Bi = B ? B[i] : nullptr;
+    if (lora && (!Ai || !Bi)) return HYDRA_ERR_NULL;
+    if (!aligned(x[i], 16) || !aligned(W[i], 16)) return HYDRA_ERR_ALIGN;
+    if (lora && (!aligned(Ai, 16) || !aligned(Bi, 2))) return HYDRA_ERR_ALIGN;
+    if ((yo && !aligned(yo, 4)) || (yn && !aligned(yn, 4))) return HYDRA_ERR_ALIGN;
+    g.x[i] = x[i];
+    g.W[i] = W[i];
+    g.A[i] = lora ? Ai : nullptr;
+    g.B[i] = lora ? Bi : nullptr;
+    g.y_off[i] = yo;
+    g.y_on[i] = yn;
+    g.s[i] = s[i];
+    any_on = any_on || lora;
+  }
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (M <= kDecodeMaxRows) return from_hip(hydra::launch_lora_gemv(a, st));
-  return from_hip(hydra::launch_lora_gemm(a, st));
+  if (M <= kDecodeMaxRows) {
+    // y_on of a member without an adapter equals its y_off: the kernel's
+    // update adds s * 0 there, because that member's A and B read as zeros.
+    if (!any_on) g.r = 0;
+    return from_hip(hydra::launch_lora_gemv_group(g, st));
+  }
+  for (int i = 0; i < g.G; ++i) {
+    hydra::LinearArgs a{};
+    a.x = g.x[i];
+    a.W = g.W[i];
+    a.A = g.A[i];
+    a.B = g.B[i];
+    a.s = g.s[i];
+    a.M = g.M;
+    a.N = g.N;
+    a.K = g.K;
+    a.r = g.A[i] ? g.r : 0;
+    a.y_off = g.y_off[i];
+    a.y_on = g.y_on[i];
+    const hipError_t e = hydra::launch_lora_gemm(a, st);
+    if (e != hipSuccess) return HYDRA_ERR_HIP;
+  }
+  return HYDRA_OK;
 }
 
 hydra_status hydra_score_workspace_bytes(int64_t M, int64_t V, size_t* bytes) {

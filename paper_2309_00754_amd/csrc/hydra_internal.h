@@ -19,6 +19,20 @@ struct LinearArgs {
   float* y_on;   // [M x N] or nullptr
 };
 
+// A group of G independent LoRA-switchable linears with the same M, N, K, r
+// (e.g. the attention projections of one decode step), for one launch.
+constexpr int kMaxGroup = 8;
+struct GroupArgs {
+  const uint16_t* x[kMaxGroup];
+  const uint16_t* W[kMaxGroup];
+  const uint16_t* A[kMaxGroup];
+  const uint16_t* B[kMaxGroup];
+  float* y_off[kMaxGroup];
+  float* y_on[kMaxGroup];
+  float s[kMaxGroup];
+  int G, M, N, K, r;
+};
+
 // Per (row, column tile) partial log-sum-exp state written by the fused
 // CLM-head GEMM: (max_off, sumexp_off, max_on, sumexp_on).
 struct ScoreGemmArgs {
@@ -65,7 +79,7 @@ struct LogitsArgs {
 constexpr int kScoreTileN = 256;
 
 hipError_t launch_lora_gemm(const LinearArgs& a, hipStream_t stream);
-hipError_t launch_lora_gemv(const LinearArgs& a, hipStream_t stream);
+hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream);
 hipError_t launch_score_gemm(const ScoreGemmArgs& a, hipStream_t stream);
 hipError_t launch_score_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_score_logits(const LogitsArgs& a, hipStream_t stream);

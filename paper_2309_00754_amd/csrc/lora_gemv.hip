@@ -1,18 +1,22 @@
-// Decode-shaped (M <= 16) LoRA-switchable linear for gfx950.
+// Decode-shaped (M <= 16) LoRA-switchable linear for gfx950, for one or a
+// group of linears in a single launch.
 //
 // At decode time (App. A, Alg. 1 / Alg. 2: "generate ... for T steps") each
 // linear sees one new token per sequence, so the work is a stream over W at
 // HBM rate with almost no arithmetic intensity.  Design:
-//  * one workgroup per 16 output columns; its WAVES waves split K.  Each lane
-//    loads 16 contiguous bytes of one W row straight from global memory into
-//    the B operand of v_mfma_f32_16x16x32_bf16 (W is output-major, so a row
-//    of W is a column of W^T); the x rows (<= 16) fill the A operand.  No LDS
-//    staging on the hot path; UNROLL k-steps of loads are issued before their
-//    MFMAs so that each CU keeps many W bytes in flight;
+//  * grid = (column blocks of NB outputs) x (linears of the group); the
+//    WAVES waves of a workgroup split K.  Each lane loads 16 contiguous bytes
+//    of a W row straight from global memory into the B operand of
+//    v_mfma_f32_16x16x32_bf16 (W is output-major, so a row of W is a column
+//    of W^T); the x rows (<= 16) fill the A operand.  No LDS on the hot path;
+//    UNROLL k-steps of loads are issued before their MFMAs;
 //  * the LoRA-down rows A (<= 64) are consumed the same way, giving
-//    T = x A^T in fp32 next to the base product (A is small and shared by all
-//    workgroups, so it is served from L2);
-//  * partial sums of the waves are combined in LDS in a fixed order; then
+//    T = x A^T in fp32 next to the base product; every workgroup reads A (it
+//    is small and L2-resident), and NB = 32 columns per workgroup halves that
+//    overhead relative to W;
+//  * the tile's rows of B are fetched into LDS at kernel start; the waves'
+//    partial sums are combined in LDS in a fixed order (wave w sums
+//    accumulator w), then one thread per output forms
 //    y_off = x W^T and y_on = y_off + s * sum_j T[m][j] B[n][j] in fp32.
 #include "hydra_device.h"
 #include "hydra_internal.h"
@@ -20,21 +24,48 @@
 namespace hydra {
 namespace {
 
-constexpr int NB = 16;  // output columns per workgroup
-
-template <int RP, int WAVES, int UNROLL>
-__global__ __launch_bounds__(WAVES * 64) void lora_gemv_kernel(LinearArgs a) {
-  constexpr int TJ = RP / 16;
-  constexpr int NACC = 1 + TJ;
+template <int RP, int NB, int WAVES, int UNROLL>
+__global__ __launch_bounds__(WAVES * 64) void lora_gemv_kernel(GroupArgs ga) {
+  constexpr int CT = NB / 16;        // 16-column MFMA tiles per workgroup
+  constexpr int TJ = RP / 16;        // 16-column tiles of T
+  constexpr int NACC = CT + TJ;
+  static_assert(NACC <= WAVES, "one wave per accumulator in the reduction");
   __shared__ f32x4_t red[WAVES][NACC][64];
-  __shared__ float Ts[16][RP > 0 ? RP : 1];
+  __shared__ f32x4_t fin[NACC][64];
+  __shared__ uint16_t Bs[NB][RP > 0 ? RP : 1];
 
-  const int M = a.M, N = a.N, K = a.K;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int gi = blockIdx.y;
+  const uint16_t* __restrict__ X = ga.x[gi];
+  const uint16_t* __restrict__ Wt = ga.W[gi];
+  const uint16_t* __restrict__ At = ga.A[gi];
+  const uint16_t* __restrict__ Bt = ga.B[gi];
+  float* __restrict__ y_off = ga.y_off[gi];
+  float* __restrict__ y_on = ga.y_on[gi];
+  const float s = ga.s[gi];
+  const int M = ga.M, N = ga.N, K = ga.K, r = ga.r;
+
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int l16 = lane & 15;
   const int lg = lane >> 4;
   const int n0 = blockIdx.x * NB;
+
+  // A member of the group without y_on has no adapter (A, B may be NULL):
+  // its A and B descriptors cover zero bytes, so every read of them is a zero.
+  const bool has_lora = y_on != nullptr && At != nullptr && Bt != nullptr;
+
+  // B rows of this column block, zero padded to RP (read once, early).
+  if constexpr (RP > 0) {
+    const __amdgpu_buffer_rsrc_t brs =
+        make_rsrc(has_lora ? Bt + (size_t)n0 * r : nullptr, has_lora ? (uint32_t)min(NB, N - n0) * r * 2u : 0u);
+    for (int e = t; e < NB * RP; e += WAVES * 64) {
+      const int n = e / RP, j = e % RP;
+      const bool ok = j < r;
+      const uint32_t v = __builtin_amdgcn_raw_buffer_load_b16(brs, ok ? (n * r + j) * 2 : kOutOfRange, 0, 0);
+      Bs[n][j] = ok ? (uint16_t)v : (uint16_t)0;
+    }
+  }
 
   const int ksteps = (K + 31) / 32;
   const int per_wave = (ksteps + WAVES - 1) / WAVES;
@@ -42,100 +73,100 @@ __global__ __launch_bounds__(WAVES * 64) void lora_gemv_kernel(LinearArgs a) {
   const int ks1 = min(ksteps, ks0 + per_wave);
 
   // Buffer resources cover exactly the valid rows of x (M), of this
-  // workgroup's W slab (<= 16 rows) and of A (r): other rows read as zeros,
-  // as does a k chunk past K (out-of-range offset).
-  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(a.x, (uint32_t)M * K * 2u);
-  const __amdgpu_buffer_rsrc_t wrs = make_rsrc(a.W + (size_t)n0 * K, (uint32_t)min(NB, N - n0) * K * 2u);
-  const __amdgpu_buffer_rsrc_t ars = make_rsrc(a.A, (uint32_t)min(a.r, RP) * K * 2u);
+  // workgroup's W rows and of A (r): other rows read as zeros, as does a k
+  // chunk past K (out-of-range offset).
+  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(X, (uint32_t)M * K * 2u);
+  const __amdgpu_buffer_rsrc_t wrs = make_rsrc(Wt + (size_t)n0 * K, (uint32_t)min(NB, N - n0) * K * 2u);
+  const __amdgpu_buffer_rsrc_t ars = make_rsrc(has_lora ? At : nullptr, has_lora ? (uint32_t)min(r, RP) * K * 2u : 0u);
   const int row_off = l16 * K * 2 + lg * 16;
+  const int tile_off = 16 * K * 2;
 
   f32x4_t acc[NACC];
 #pragma unroll
   for (int j = 0; j < NACC; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   for (int ks = ks0; ks < ks1; ks += UNROLL) {
-    uint4 xf[UNROLL], wf[UNROLL], af[UNROLL][TJ > 0 ? TJ : 1];
+    uint4 xf[UNROLL], wf[UNROLL][CT], af[UNROLL][TJ > 0 ? TJ : 1];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
       const bool kv = (ks + u) < ks1 && (ks + u) * 32 + lg * 8 < K;
       const int off = kv ? row_off + (ks + u) * 64 : kOutOfRange;
-      wf[u] = buf_load16(wrs, off);
+#pragma unroll
+      for (int c = 0; c < CT; ++c) wf[u][c] = buf_load16(wrs, kv ? off + c * tile_off : kOutOfRange);
       xf[u] = buf_load16(xrs, off);
 #pragma unroll
-      for (int j = 0; j < TJ; ++j) af[u][j] = buf_load16(ars, kv ? off + j * 16 * K * 2 : kOutOfRange);
+      for (int j = 0; j < TJ; ++j) af[u][j] = buf_load16(ars, kv ? off + j * tile_off : kOutOfRange);
     }
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      acc[0] = mfma16(xf[u], wf[u], acc[0]);
 #pragma unroll
-      for (int j = 0; j < TJ; ++j) acc[1 + j] = mfma16(xf[u], af[u][j], acc[1 + j]);
+      for (int c = 0; c < CT; ++c) acc[c] = mfma16(xf[u], wf[u][c], acc[c]);
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) acc[CT + j] = mfma16(xf[u], af[u][j], acc[CT + j]);
     }
   }
 
 #pragma unroll
   for (int j = 0; j < NACC; ++j) red[wave][j][lane] = acc[j];
   __syncthreads();
-
-  // Wave 0 sums the per-wave partials in wave order.  Its lane holds
-  // D[m = 4 lg + e][n0 + l16] of the base product and T[m = 4 lg + e][16 j + l16]
-  // of the LoRA-down product.
-  f32x4_t sum[NACC];
-  if (wave == 0) {
-#pragma unroll
-    for (int j = 0; j < NACC; ++j) {
-      sum[j] = red[0][j][lane];
-      for (int w = 1; w < WAVES; ++w) sum[j] += red[w][j][lane];
-    }
-    if constexpr (TJ > 0) {
-#pragma unroll
-      for (int j = 0; j < TJ; ++j)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) Ts[lg * 4 + e][j * 16 + l16] = sum[1 + j][e];
-    }
+  // Wave w sums accumulator w over the waves, in wave order.
+  if (wave < NACC) {
+    f32x4_t sum = red[0][wave][lane];
+    for (int w = 1; w < WAVES; ++w) sum += red[w][wave][lane];
+    fin[wave][lane] = sum;
   }
   __syncthreads();
-  if (wave != 0) return;
 
-  const int n = n0 + l16;
+  // fin[c][lane] holds D[m = 4 (lane / 16) + e][col 16 c + lane % 16] of the
+  // base product (c < CT) or of T (c >= CT).  One thread per output (m, n).
+  if (t >= M * NB) return;
+  const int m = t / NB, nl = t % NB;
+  const int n = n0 + nl;
   if (n >= N) return;
-  float bn[RP > 0 ? RP : 1];
+  const int src_lane = (m >> 2) * 16;
+  const float yo = fin[nl >> 4][src_lane + (nl & 15)][m & 3];
+  if (y_off) y_off[(size_t)m * N + n] = yo;
+  if (y_on) {
+    float d = 0.f;
+    if constexpr (RP > 0) {
 #pragma unroll
-  for (int j = 0; j < RP; ++j) {
-    const bool ok = j < a.r;
-    const uint16_t v = a.B[ok ? (size_t)n * a.r + j : 0];
-    bn[j] = ok ? bf16_to_f32(v) : 0.f;
-  }
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int m = lg * 4 + e;
-    if (m >= M) continue;
-    const float yo = sum[0][e];
-    if (a.y_off) a.y_off[(size_t)m * N + n] = yo;
-    if (a.y_on) {
-      float d = 0.f;
-#pragma unroll
-      for (int j = 0; j < RP; ++j) d = fmaf(Ts[m][j], bn[j], d);
-      a.y_on[(size_t)m * N + n] = yo + a.s * d;
+      for (int j = 0; j < RP; ++j)
+        d = fmaf(fin[CT + (j >> 4)][src_lane + (j & 15)][m & 3], bf16_to_f32(Bs[nl][j]), d);
     }
+    y_on[(size_t)m * N + n] = yo + s * d;
   }
 }
 
-template <int RP>
-hipError_t launch_rp(const LinearArgs& a, hipStream_t stream) {
+template <int RP, int NB>
+hipError_t launch_cfg(const GroupArgs& g, hipStream_t stream) {
   constexpr int WAVES = 16, UNROLL = 8;
-  const dim3 grid((a.N + NB - 1) / NB), block(WAVES * 64);
-  hipLaunchKernelGGL((lora_gemv_kernel<RP, WAVES, UNROLL>), grid, block, 0, stream, a);
+  const dim3 grid((g.N + NB - 1) / NB, g.G), block(WAVES * 64);
+  hipLaunchKernelGGL((lora_gemv_kernel<RP, NB, WAVES, UNROLL>), grid, block, 0, stream, g);
   return hipGetLastError();
+}
+
+template <int NB>
+hipError_t launch_nb(const GroupArgs& g, int rp, hipStream_t stream) {
+  switch (rp) {
+    case 0: return launch_cfg<0, NB>(g, stream);
+    case 16: return launch_cfg<16, NB>(g, stream);
+    case 32: return launch_cfg<32, NB>(g, stream);
+    default: return launch_cfg<64, NB>(g, stream);
+  }
 }
 
 }  // namespace
 
-hipError_t launch_lora_gemv(const LinearArgs& a, hipStream_t stream) {
-  const int r = a.y_on ? a.r : 0;
-  if (r == 0) return launch_rp<0>(a, stream);
-  if (r <= 16) return launch_rp<16>(a, stream);
-  if (r <= 32) return launch_rp<32>(a, stream);
-  return launch_rp<64>(a, stream);
+hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream) {
+  bool any_on = false;
+  for (int i = 0; i < g.G; ++i) any_on = any_on || g.y_on[i] != nullptr;
+  const int r = any_on ? g.r : 0;
+  const int rp = r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : 64;
+  // 32 columns per workgroup when that still gives at least two workgroups
+  // per CU, else 16 (more workgroups for a small N).
+  const long wg32 = (long)((g.N + 31) / 32) * g.G;
+  if (wg32 >= 512) return launch_nb<32>(g, rp, stream);
+  return launch_nb<16>(g, rp, stream);
 }
 
 }  // namespace hydra

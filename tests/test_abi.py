@@ -134,3 +134,34 @@ def test_binding_raises_typed_error():
     with pytest.raises(H.HydraError) as ei:
         Bd._check(H.HYDRA_ERR_SHAPE, "probe")
     assert ei.value.status == H.HYDRA_ERR_SHAPE
+
+
+def _grp(G=2, xs=(P, P), Ws=(P, P), As=(P, P), Bs=(P, P), ss=(2.0, 2.0), M=4, N=64, K=64, r=8,
+         yo=(P, P), yn=(P + 0x1000, P + 0x1000)):
+    def arr(v):
+        if v is None:
+            return None
+        a = (ctypes.c_void_p * len(v))()
+        for i, p in enumerate(v):
+            a[i] = p
+        return a
+    svals = None if ss is None else (ctypes.c_float * len(ss))(*ss)
+    return H.lib().hydra_lora_linear_group(G, arr(xs), arr(Ws), arr(As), arr(Bs), svals, M, N, K, r,
+                                           arr(yo), arr(yn), None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(G=0), H.HYDRA_ERR_SHAPE),
+    (dict(G=9), H.HYDRA_ERR_SHAPE),
+    (dict(xs=None), H.HYDRA_ERR_NULL),
+    (dict(ss=None), H.HYDRA_ERR_NULL),
+    (dict(yo=None, yn=None), H.HYDRA_ERR_NULL),
+    (dict(xs=(P, None)), H.HYDRA_ERR_NULL),
+    (dict(yo=(P, None), yn=(P + 0x1000, None)), H.HYDRA_ERR_NULL),
+    (dict(As=(P, None)), H.HYDRA_ERR_NULL),
+    (dict(K=20), H.HYDRA_ERR_SHAPE),
+    (dict(Ws=(P, P8)), H.HYDRA_ERR_ALIGN),
+    (dict(yo=(P, P), yn=(P + 0x1000, P)), H.HYDRA_ERR_SHAPE),
+])
+def test_lora_linear_group_rejects(kw, code):
+    assert _grp(**kw) == code
