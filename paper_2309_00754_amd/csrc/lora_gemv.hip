@@ -12,8 +12,8 @@
 //    UNROLL k-steps of loads are issued before their MFMAs;
 //  * the LoRA-down rows A (<= 64) are consumed the same way, giving
 //    T = x A^T in fp32 next to the base product; every workgroup reads A (it
-//    is small and L2-resident), and NB = 32 columns per workgroup halves that
-//    overhead relative to W;
+//    is small and L2-resident), so the widest column block that still fills
+//    the chip (NB = 64, 32 or 16) is used to amortise it over more of W;
 //  * the tile's rows of B are fetched into LDS at kernel start; the waves'
 //    partial sums are combined in LDS in a fixed order (wave w sums
 //    accumulator w), then one thread per output forms
@@ -139,7 +139,8 @@ __global__ __launch_bounds__(WAVES * 64) void lora_gemv_kernel(GroupArgs ga) {
 
 template <int RP, int NB>
 hipError_t launch_cfg(const GroupArgs& g, hipStream_t stream) {
-  constexpr int WAVES = 16, UNROLL = 8;
+  // 16 waves split K; every wave keeps 8 k-steps of W in flight (4 at NB = 64).
+  constexpr int WAVES = 16, UNROLL = NB >= 64 ? 4 : 8;
   const dim3 grid((g.N + NB - 1) / NB, g.G), block(WAVES * 64);
   hipLaunchKernelGGL((lora_gemv_kernel<RP, NB, WAVES, UNROLL>), grid, block, 0, stream, g);
   return hipGetLastError();
@@ -162,10 +163,12 @@ hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream) {
   for (int i = 0; i < g.G; ++i) any_on = any_on || g.y_on[i] != nullptr;
   const int r = any_on ? g.r : 0;
   const int rp = r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : 64;
-  // 32 columns per workgroup when that still gives at least two workgroups
-  // per CU, else 16 (more workgroups for a small N).
+  // The widest column block that still gives at least one workgroup per CU:
+  // wider blocks amortise the per-workgroup reads of A over more of W.
+  const long wg64 = (long)((g.N + 63) / 64) * g.G;
   const long wg32 = (long)((g.N + 31) / 32) * g.G;
-  if (wg32 >= 512) return launch_nb<32>(g, rp, stream);
+  if (wg64 >= 256) return launch_nb<64>(g, rp, stream);
+  if (wg32 >= 256) return launch_nb<32>(g, rp, stream);
   return launch_nb<16>(g, rp, stream);
 }
 

@@ -61,6 +61,18 @@ __global__ __launch_bounds__(THREADS) void score_logits_kernel(LogitsArgs o) {
   const float* zon = o.on + (size_t)row * V;
   const float* zoff = o.off + (size_t)row * V;
 
+  // The sampled token's two logits are fetched first, so that their latency
+  // overlaps the streaming pass instead of following the reduction.
+  int tk = 0;
+  float z_on = 0.f, z_off = 0.f;
+  if (t == 0) {
+    tk = o.tokens[row];
+    if (tk >= 0 && tk < V) {
+      z_on = zon[tk];
+      z_off = zoff[tk];
+    }
+  }
+
   float m_on = -INFINITY, s_on = 0.f, m_off = -INFINITY, s_off = 0.f;
   if constexpr (VEC) {
     const int nv4 = V >> 2;
@@ -138,10 +150,6 @@ __global__ __launch_bounds__(THREADS) void score_logits_kernel(LogitsArgs o) {
       lse_merge(mo, so, red[0][i], red[1][i]);
       lse_merge(mf, sf, red[2][i], red[3][i]);
     }
-    const int tk = o.tokens[row];
-    const bool ok = tk >= 0 && tk < V;
-    const float z_on = ok ? zon[tk] : 0.f;
-    const float z_off = ok ? zoff[tk] : 0.f;
     finish_row(row, tk, V, z_on, z_off, mo, so, mf, sf, o);
   }
 }
@@ -157,6 +165,14 @@ __global__ __launch_bounds__(CB_THREADS) void score_combine_kernel(CombineArgs c
     const int row = blockIdx.x * CB_ROWS + (t >> 6);
     if (row >= c.M) return;
     const int lane = t & 63;
+    // token and gathered logits first: their latency overlaps the merge
+    const int tk = c.tokens[row];
+    const bool ok = tk >= 0 && tk < c.V;
+    float z_off = 0.f, z_on = 0.f;
+    if (lane == 0 && ok) {
+      z_off = c.zt[(size_t)row * 2 + 0];
+      z_on = c.zt[(size_t)row * 2 + 1];
+    }
     const float4* p = c.part + (size_t)row * c.ntn;
     float mo = -INFINITY, so = 0.f, mn = -INFINITY, sn = 0.f;
     for (int j = lane; j < c.ntn; j += 64) {
@@ -174,10 +190,6 @@ __global__ __launch_bounds__(CB_THREADS) void score_combine_kernel(CombineArgs c
       o.lse_on = c.lse_on;
       o.lse_off = c.lse_off;
       o.err = c.err;
-      const int tk = c.tokens[row];
-      const bool ok = tk >= 0 && tk < c.V;
-      const float z_off = ok ? c.zt[(size_t)row * 2 + 0] : 0.f;
-      const float z_on = ok ? c.zt[(size_t)row * 2 + 1] : 0.f;
       finish_row(row, tk, c.V, z_on, z_off, mn, sn, mo, so, o);
     }
     return;
