@@ -3,28 +3,40 @@
 // x W^T + s (x A^T) B^T (Sec. 3, "Dynamic LoRA" and "Stage 2: Hydra-PPO":
 // the reference / reward roles are the same network with LoRA ignored).
 //
-// Structure (one 128 x 256 output tile per 256-thread workgroup, one
-// workgroup per CU):
-//  * the x slab [128 x 64], the W slab [256 x 64] and the LoRA-down slab
-//    A [RP x 64] of each 64-wide K slab are copied straight from HBM/L2 into
-//    LDS (buffer_load ... lds, no register staging) two slabs ahead, through
-//    a three-stage ring of XOR-swizzled 16-byte chunks;
-//  * each of the 4 waves owns a 64 x 128 sub-tile and runs
+// Structure (one 128 x 256 output tile per 512-thread workgroup, one
+// workgroup per CU, two waves per SIMD):
+//  * waves 4..7 are copy waves: they move the x slab [128 x 64], the W slab
+//    [256 x 64] and the LoRA-down slab A [RP x 64] of each 64-wide K slab
+//    straight from HBM/L2 into LDS (buffer_load ... lds, no register
+//    staging), up to two slabs ahead, through a three-stage ring of
+//    XOR-swizzled 16-byte chunks.  Vector-memory instructions issued by a
+//    wave that also feeds the matrix cores stall its MFMA stream; with the
+//    copies on their own waves the MFMA waves issue nothing but LDS reads
+//    and MFMAs in the main loop;
+//  * waves 0..3 each own a 64 x 128 sub-tile and run
 //    v_mfma_f32_32x32x16_bf16 with W as the A operand and x as the B operand,
 //    so that every lane ends up holding four consecutive output columns of
 //    one row (float4 stores in the epilogue); the LDS reads of the next
-//    k-step and the copies of a later slab are slotted between the MFMAs;
+//    16-wide k-step are slotted between the MFMAs of the current one;
+//  * one workgroup barrier per slab hands the ring over: before it the copy
+//    waves have waited for their copies of slab kt + 1 and the MFMA waves
+//    have finished reading slab kt, after it the stage of slab kt is refilled
+//    with slab kt + 3;
 //  * the rank-r product T = x A^T of the tile's 128 rows is accumulated in the
-//    same loop (v_mfma_f32_16x16x32_bf16, 32 rows per wave, so the work is
-//    balanced) and never leaves the chip;
+//    same loop (v_mfma_f32_16x16x32_bf16, 32 rows per MFMA wave) and never
+//    leaves the chip;
 //  * epilogue: the accumulators are the LoRA-off result.  s*T is split into
 //    bf16 hi + lo parts and multiplied against [B; B] by MFMA, adding the
 //    LoRA update to the same accumulators, which become the LoRA-on result.
-//    With B = 0 or s = 0 the update adds exact zeros, so y_on == y_off.
+//    With B = 0 or s = 0 the update adds exact zeros, so y_on == y_off.  The
+//    copy waves fetch the tile's rows of B (and, for SCORE, the sampled
+//    tokens) at kernel start and stage them in LDS for the epilogue;
 //  * SCORE variant (CLM head, N = V): instead of storing logits, each row's
 //    (max, sum exp) over the tile's 256 columns is reduced for both passes,
 //    the sampled token's logit is picked up by the lane that holds it, and a
 //    float4 partial per (row, column tile) is written for the combine kernel.
+#include <type_traits>
+
 #include "hydra_device.h"
 #include "hydra_internal.h"
 
@@ -34,7 +46,8 @@ namespace {
 constexpr int BM = 128;        // tile rows (tokens)
 constexpr int BN = 256;        // tile columns (outputs)
 constexpr int BK = 64;         // K slab
-constexpr int NT = 256;        // threads per workgroup (4 waves)
+constexpr int NTM = 256;       // MFMA threads (waves 0..3)
+constexpr int NT = 512;        // threads per workgroup (4 MFMA + 4 copy waves)
 constexpr int WM = 64;         // wave tile rows
 constexpr int WN = 128;        // wave tile columns
 constexpr int MT = WM / 32;    // 32-row x tiles per wave
@@ -86,6 +99,26 @@ __device__ __forceinline__ void tile_of(int bid, int ntm, int ntn, int& tm, int&
   tn = in / gsize;
 }
 
+// s_waitcnt with only the vector-memory counter (N outstanding at most).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit field");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0xF << 8) | (((N >> 4) & 3) << 14));
+  asm volatile("" ::: "memory");
+}
+
+// LDS operations of this wave complete, then the workgroup barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0), vmcnt / expcnt untouched
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int V>
+using IC = std::integral_constant<int, V>;
+
 template <int RP, bool SCORE>
 __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   using L = Layout<RP>;
@@ -103,8 +136,8 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   // The wave index is made provably wave-uniform (an SGPR), so branches on it
   // are scalar branches: MFMAs must never sit under exec-masked divergence.
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int wr = wave >> 1;  // wave row (0..1)
-  const int wc = wave & 1;   // wave column (0..1)
+  const int wr = (wave >> 1) & 1;  // MFMA wave row (0..1)
+  const int wc = wave & 1;         // MFMA wave column (0..1)
   const int l16 = lane & 15;
   const int lg = lane >> 4;
   const int l32 = lane & 31;
@@ -114,203 +147,14 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   tile_of(blockIdx.x, g.ntm, g.ntn, tmi, tni);
   const int m0 = tmi * BM;
   const int n0 = tni * BN;
-
-  // ---- global -> LDS copies.  One copy instruction moves 8 rows x 128 bytes
-  // (64 lanes x 16 bytes) into 1 KB of LDS; lane i fills LDS chunk i of it,
-  // so it fetches the global chunk that the swizzle maps there.  Buffer
-  // resources cover exactly the tile's valid rows (rows past M, N or r read
-  // as zeros); a chunk past K gets an out-of-range offset (zeros as well).
-  const i32x4_t xr = make_rsrc_raw(a.x + (size_t)m0 * K, (uint32_t)min(BM, M - m0) * K * 2u);
-  const i32x4_t wrs = make_rsrc_raw(a.W + (size_t)n0 * K, (uint32_t)min(BN, N - n0) * K * 2u);
-  const i32x4_t arsrc = make_rsrc_raw(a.A, (uint32_t)min(a.r, RP) * K * 2u);
-  const int row_bytes = K * 2;
-  const int c = (lane & 7) ^ (lane >> 3);   // global chunk fetched by this lane
-  const int rl = lane >> 3;                 // row within the 8-row copy
-  constexpr int XI = BM / 8 / 4;            // copies per wave: x
-  constexpr int WI = BN / 8 / 4;            //                  W
-  constexpr int AI = RP / 8;                // copies in total: A
-  constexpr int AIW = (AI + 3) / 4;         // most A copies one wave issues
-  constexpr int DPW = XI + WI + AI / 4;     // fewest copies any wave issues per slab
   const int nkt = (K + BK - 1) / BK;
-
-  // The epilogue's global inputs are fetched now, so that they have arrived
-  // long before the main loop ends: the tile's rows of B (thread t holds row
-  // n0 + t, zero padded to RP; rows past N read as zeros through the buffer
-  // resource) and, for SCORE, the sampled token of row m0 + t.
-  constexpr bool B_EARLY = RP > 0 && RP <= 32;
-  uint32_t breg[B_EARLY ? RP : 1];
   const bool want_on = SCORE || a.y_on != nullptr;
-  if constexpr (B_EARLY) {
-    const __amdgpu_buffer_rsrc_t brs = make_rsrc(a.B + (size_t)n0 * a.r, (uint32_t)min(BN, N - n0) * a.r * 2u);
-#pragma unroll
-    for (int j = 0; j < RP; ++j) {
-      const bool ok = want_on && j < a.r;
-      const uint32_t v = __builtin_amdgcn_raw_buffer_load_b16(brs, ok ? (t * a.r + j) * 2 : kOutOfRange, 0, 0);
-      breg[j] = ok ? v : 0u;
-    }
-  }
-  int tok_early = -1;
-  if constexpr (SCORE) {
-    if (t < BM) {
-      const int row = m0 + t;
-      const int v = g.tokens[row < M ? row : 0];
-      tok_early = row < M ? v : -1;
-    }
-  }
 
-  f32x16_t acc[MT][NTL];
-#pragma unroll
-  for (int i = 0; i < MT; ++i)
-#pragma unroll
-    for (int j = 0; j < NTL; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
   constexpr int TJ = RP / 16;
   constexpr int TJ1 = TJ > 0 ? TJ : 1;
-  f32x4_t accT[2][TJ1];
-#pragma unroll
-  for (int q = 0; q < 2; ++q)
-#pragma unroll
-    for (int j = 0; j < TJ1; ++j) accT[q][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  constexpr int RP2 = RP > 0 ? RP / 2 : 1;
 
-  // Register fragments of one 32-wide k-step: for each 16-wide half h, the W
-  // rows (A operand) and x rows (B operand) of the 32x32x16 MFMAs; the x rows
-  // of this wave's 32 T rows and the LoRA-down rows in the 16x16x32 layout.
-  // Two sets alternate so that the next k-step's LDS reads overlap the
-  // current k-step's MFMAs.
-  struct Frag {
-    uint4 w[2][NTL];
-    uint4 x[2][MT];
-    uint4 tx[2];
-    uint4 a[TJ1];
-  };
-  Frag F0, F1;
-  constexpr int NMAIN = 2 * MT * NTL;          // 32x32x16 MFMAs per k-step
-  constexpr int NR = 2 * NTL + 2 * MT + (TJ > 0 ? 2 + TJ : 0);  // LDS reads per k-step
-  constexpr int ND = XI + WI + AIW;           // copy instructions per wave per slab (at most)
-  static_assert(ND <= NMAIN, "one copy slot per MFMA");
-
-  auto read_one = [&](Frag& F, const uint4* s, int kk, int r) __attribute__((always_inline)) {
-    if (r < 2 * NTL) {
-      const int h = r / NTL, ni = r % NTL;
-      F.w[h][ni] = s[L::WOFF + lds_idx(wc * WN + ni * 32 + l32, kk * 4 + 2 * h + lh)];
-    } else if (r < 2 * NTL + 2 * MT) {
-      const int h = (r - 2 * NTL) / MT, mi = (r - 2 * NTL) % MT;
-      F.x[h][mi] = s[L::XOFF + lds_idx(wr * WM + mi * 32 + l32, kk * 4 + 2 * h + lh)];
-    } else if (r < 2 * NTL + 2 * MT + 2) {
-      const int q = r - 2 * NTL - 2 * MT;
-      F.tx[q] = s[L::XOFF + lds_idx(wr * WM + (wc * 2 + q) * 16 + l16, kk * 4 + lg)];
-    } else {
-      const int j = r - 2 * NTL - 2 * MT - 2;
-      F.a[j] = s[L::AOFF + lds_idx(j * 16 + l16, kk * 4 + lg)];
-    }
-  };
-  auto dma_one = [&](uint4* st, int kofs, bool kv, int d) __attribute__((always_inline)) {
-    if (d < XI) {
-      const int ci = wave * XI + d;
-      dma16(xr, st + L::XOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kofs : kOutOfRange);
-    } else if (d < XI + WI) {
-      const int ci = wave * WI + (d - XI);
-      dma16(wrs, st + L::WOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kofs : kOutOfRange);
-    } else {
-      const int ci = wave + 4 * (d - XI - WI);
-      if (ci < AI) dma16(arsrc, st + L::AOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kofs : kOutOfRange);
-    }
-  };
-  auto issue_all = [&](uint4* st, int kt) __attribute__((always_inline)) {
-    const int k0 = kt * BK;
-#pragma unroll
-    for (int d = 0; d < ND; ++d) dma_one(st, k0 * 2 + c * 16, k0 + c * 8 < K, d);
-  };
-
-  // Copy instructions [d0, d1) of a slab go out in one k-step, the rest in
-  // the other, so that no k-step stalls on a burst of copies.
-  constexpr int DA = (ND + 1) / 2;  // copies issued in k-step 0
-
-  // One k-step: the NMAIN MFMAs of the wave tile on Fc (then the LoRA-down
-  // MFMAs), with one LDS read that fills Fn and one copy of a later slab
-  // slotted after each MFMA.  The scheduling barriers keep that order.
-  auto kstep = [&](const Frag& Fc, Frag& Fn, const uint4* rs, int rkk, uint4* dst, int dkt, int d0, int d1)
-      __attribute__((always_inline)) {
-    const bool do_dma = d1 > d0;
-    const int k0 = dkt * BK;
-    const bool kv = dkt < nkt && k0 + c * 8 < K;
-    const int kofs = k0 * 2 + c * 16;
-#pragma unroll
-    for (int m = 0; m < NMAIN; ++m) {
-      const int h = m / (MT * NTL), mi = (m / NTL) % MT, ni = m % NTL;
-      acc[mi][ni] = mfma32(Fc.w[h][ni], Fc.x[h][mi], acc[mi][ni]);
-      if (m < NR) read_one(Fn, rs, rkk, m);
-      if (do_dma && m >= d0 && m < d1) dma_one(dst, kofs, kv, m);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if constexpr (TJ > 0) {
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) {
-        accT[0][j] = mfma16(Fc.tx[0], Fc.a[j], accT[0][j]);
-        accT[1][j] = mfma16(Fc.tx[1], Fc.a[j], accT[1][j]);
-      }
-    }
-#pragma unroll
-    for (int r = NMAIN; r < NR; ++r) read_one(Fn, rs, rkk, r);
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
-  // ---- pipeline.  Slab kt lives in stage kt % NS.  Each iteration:
-  //   k-step 0 of slab kt (MFMAs on F0) while F1 <- k-step 1 of slab kt and
-  //     the first copies of slab kt + NS - 1 go into the stage freed one
-  //     iteration ago;
-  //   wait for slab kt + 1, barrier (stage kt is retired, kt + 1 visible);
-  //   k-step 1 of slab kt (MFMAs on F1) while F0 <- k-step 0 of slab kt + 1
-  //     and the remaining copies go out.
-  // With NS = 3, at the barrier only the first part of slab kt + 2 (DAW per
-  // wave at least) may still be in flight; with NS = 2 all copies of slab
-  // kt + 1 go out in k-step 0 and are waited for at the barrier.  Past the
-  // last slab the copies get out-of-range offsets (they write zeros into a
-  // stage that is not read again) and the last iteration's reads fill
-  // registers that are not used, so every iteration is the same straight-line
-  // code.
-  constexpr int DAW = NS == 3 ? (DA < XI + WI ? DA : XI + WI) : 0;
-  auto iter = [&](const uint4* cur, uint4* dst, const uint4* nxt, int kt) __attribute__((always_inline)) {
-    if constexpr (NS == 3) {
-      kstep(F0, F1, cur, 1, dst, kt + 2, 0, DA);
-      wait_vm_barrier<DAW>();
-      kstep(F1, F0, nxt, 0, dst, kt + 2, DA, ND);
-    } else {
-      kstep(F0, F1, cur, 1, dst, kt + 1, 0, ND);
-      wait_vm_barrier<0>();
-      kstep(F1, F0, nxt, 0, nullptr, 0, 0, 0);
-    }
-  };
-  issue_all(sm0, 0);
-  if constexpr (NS == 3) {
-    if (nkt > 1) {
-      issue_all(sm1, 1);
-      wait_vm_barrier<DPW>();
-    } else {
-      wait_vm_barrier<0>();
-    }
-  } else {
-    wait_vm_barrier<0>();
-  }
-#pragma unroll
-  for (int r = 0; r < NR; ++r) read_one(F0, sm0, 0, r);
-  if constexpr (NS == 3) {
-    for (int kt = 0; kt < nkt; kt += 3) {
-      iter(sm0, sm2, sm1, kt);
-      if (kt + 1 < nkt) iter(sm1, sm0, sm2, kt + 1);
-      if (kt + 2 < nkt) iter(sm2, sm1, sm0, kt + 2);
-    }
-  } else {
-    for (int kt = 0; kt < nkt; kt += 2) {
-      iter(sm0, sm1, sm1, kt);
-      if (kt + 1 < nkt) iter(sm1, sm0, sm0, kt + 1);
-    }
-  }
-  wait_vm_barrier<0>();  // every wave is done with the stages before the epilogue reuses them
-
-  // ---------------------------------------------------------------- epilogue
-  // The stages are free again.  Layout:
+  // Epilogue layout (the stages are free again by then):
   //   stage 0: Ts [BM][2 RP] bf16, s*T split into hi (columns 0..RP) and lo (RP..2RP)
   //   stage 1: Bs [BN][RP] bf16, the tile's rows of B zero padded to RP;
   //            SCORE only: red [2][BM][4] fp32 and tok [BM] int32 after it.
@@ -319,48 +163,265 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   float* red = reinterpret_cast<float*>(Bs + BN * RP);
   int* tok = reinterpret_cast<int*>(red + 2 * BM * 4);
 
-  if constexpr (TJ > 0) {
-    if (want_on) {
-      const float sc = a.s;
-      // accT[q][j] holds T[wr*64 + (wc*2+q)*16 + 4 lg + e][16 j + l16]
+  if (wave >= 4) {
+    // ------------------------------------------------------------ copy waves
+    const int cw = wave - 4;  // copy wave index (0..3), wave-uniform
+    const int tl = t - NTM;   // copy thread index (0..255)
+    // Values the copy waves fetch early and stage in LDS for the epilogue: the
+    // tile's rows of B (copy thread tl holds row n0 + tl, zero padded to RP,
+    // two bf16 per register) and, for SCORE, the sampled token of row m0 + tl.
+    uint32_t breg[RP2];
+    int tok_early = -1;
+
+    if constexpr (RP > 0) {
+      static_assert(BN == NT - NTM, "one B row per copy thread");
+      const __amdgpu_buffer_rsrc_t brs = make_rsrc(a.B + (size_t)n0 * a.r, (uint32_t)min(BN, N - n0) * a.r * 2u);
+      uint32_t v[RP];
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
+      for (int j = 0; j < RP; ++j) {
+        const bool ok = want_on && j < a.r;
+        v[j] = __builtin_amdgcn_raw_buffer_load_b16(brs, ok ? (tl * a.r + j) * 2 : kOutOfRange, 0, 0);
+      }
 #pragma unroll
-        for (int j = 0; j < TJ; ++j)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int row = wr * WM + (wc * 2 + q) * 16 + lg * 4 + e;
-            const int col = j * 16 + l16;
-            const float v = sc * accT[q][j][e];
-            const uint32_t hi = f32_to_bf16_rne(v);
-            const uint32_t lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
-            Ts[row * 2 * RP + col] = (uint16_t)hi;
-            Ts[row * 2 * RP + RP + col] = (uint16_t)lo;
-          }
-      if constexpr (B_EARLY) {
-        static_assert(BN == NT, "one B row per thread");
-#pragma unroll
-        for (int j = 0; j < RP; j += 2) *reinterpret_cast<uint32_t*>(Bs + t * RP + j) = breg[j] | (breg[j + 1] << 16);
-      } else {
-        // large ranks: all loads of the thread are issued before any store
-        uint16_t v[RP];
-#pragma unroll
-        for (int i = 0; i < RP; ++i) {
-          const int e = t + i * NT;
-          const int n = e / RP, j = e % RP;
-          const bool ok = n0 + n < N && j < a.r;
-          const uint16_t u = a.B[ok ? (size_t)(n0 + n) * a.r + j : 0];
-          v[i] = ok ? u : (uint16_t)0;
-        }
-#pragma unroll
-        for (int i = 0; i < RP; ++i) Bs[t + i * NT] = v[i];
+      for (int j = 0; j < RP; j += 2) breg[j / 2] = (v[j] & 0xFFFFu) | (v[j + 1] << 16);
+    }
+    if constexpr (SCORE) {
+      if (tl < BM) {
+        const int row = m0 + tl;
+        const int v = g.tokens[row < M ? row : 0];
+        tok_early = row < M ? v : -1;
       }
     }
+
+    // One copy instruction moves 8 rows x 128 bytes (64 lanes x 16 bytes)
+    // into 1 KB of LDS; lane i fills LDS chunk i of it, so it fetches the
+    // global chunk that the swizzle maps there.  Buffer resources cover
+    // exactly the tile's valid rows (rows past M, N or r read as zeros); a
+    // chunk past K gets an out-of-range offset (zeros as well).  The copies
+    // of a slab are dealt round-robin to the copy waves: x blocks 0..15, W
+    // blocks 16..47, A blocks 48.., copy wave cw takes blocks cw, cw + 4, ...
+    const i32x4_t xr = make_rsrc_raw(a.x + (size_t)m0 * K, (uint32_t)min(BM, M - m0) * K * 2u);
+    const i32x4_t wrs = make_rsrc_raw(a.W + (size_t)n0 * K, (uint32_t)min(BN, N - n0) * K * 2u);
+    const i32x4_t arsrc = make_rsrc_raw(a.A, (uint32_t)min(a.r, RP) * K * 2u);
+    const int row_bytes = K * 2;
+    const int c = (lane & 7) ^ (lane >> 3);  // global chunk fetched by this lane
+    const int rl = lane >> 3;                // row within the 8-row copy
+    constexpr int XD = BM / 8, WD = BN / 8, AD = RP / 8;
+    static_assert(XD % 4 == 0 && WD % 4 == 0, "x and W blocks split evenly over the copy waves");
+    constexpr int XJ = XD / 4, WJ = WD / 4;
+    constexpr int DMAX = XJ + WJ + (AD + 3) / 4;  // copies per slab of copy wave 0
+    const int dn = XJ + WJ + (AD - cw + 3) / 4;   // copies per slab of this wave
+
+    auto issue = [&](uint4* st, int kt) __attribute__((always_inline)) {
+      const int k0 = kt * BK;
+      const bool kv = k0 + c * 8 < K;
+      const int kofs = k0 * 2 + c * 16;
+#pragma unroll
+      for (int j = 0; j < DMAX; ++j) {
+        if (j < XJ) {
+          const int ci = cw + 4 * j;
+          dma16(xr, st + L::XOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kofs : kOutOfRange);
+        } else if (j < XJ + WJ) {
+          const int ci = cw + 4 * (j - XJ);
+          dma16(wrs, st + L::WOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kofs : kOutOfRange);
+        } else {
+          const int ci = cw + 4 * (j - XJ - WJ);
+          if (ci < AD) dma16(arsrc, st + L::AOFF + ci * 64, kv ? (ci * 8 + rl) * row_bytes + kofs : kOutOfRange);
+        }
+      }
+    };
+    // Wait until only the copies of the `later` most recent slabs may still
+    // be in flight.
+    auto wait_slabs = [&](int later) __attribute__((always_inline)) {
+      if (later <= 0) {
+        wait_vm<0>();
+      } else if (later == 1) {
+        if (dn == DMAX) wait_vm<DMAX>(); else wait_vm<(DMAX > 0 ? DMAX - 1 : 0)>();
+      } else {
+        if (dn == DMAX) wait_vm<2 * DMAX>(); else wait_vm<(DMAX > 0 ? 2 * DMAX - 2 : 0)>();
+      }
+    };
+
+    issue(sm0, 0);
+    if (nkt > 1) issue(sm1, 1);
+    if constexpr (NS == 3) {
+      if (nkt > 2) issue(sm2, 2);
+    }
+    wait_slabs(min(NS - 1, nkt - 1));
+    lds_barrier();  // slab 0 is in LDS
+    // Before barrier kt: slab kt + 1 has landed.  After it: stage kt % NS is
+    // no longer read and receives slab kt + NS.
+    auto step_copy = [&](uint4* st, int kt) __attribute__((always_inline)) {
+      wait_slabs(min(kt + NS - 1, nkt - 1) - (kt + 1));
+      lds_barrier();
+      if (kt + NS < nkt) issue(st, kt + NS);
+    };
+    if constexpr (NS == 3) {
+      for (int kt = 0; kt < nkt; kt += 3) {
+        step_copy(sm0, kt);
+        if (kt + 1 < nkt) step_copy(sm1, kt + 1);
+        if (kt + 2 < nkt) step_copy(sm2, kt + 2);
+      }
+    } else {
+      for (int kt = 0; kt < nkt; kt += 2) {
+        step_copy(sm0, kt);
+        if (kt + 1 < nkt) step_copy(sm1, kt + 1);
+      }
+    }
+    wait_vm<0>();
+    lds_barrier();  // every wave is done with the stages
+    if constexpr (RP > 0) {
+#pragma unroll
+      for (int j = 0; j < RP; j += 2) *reinterpret_cast<uint32_t*>(Bs + tl * RP + j) = breg[j / 2];
+    }
+    if constexpr (SCORE) {
+      if (tl < BM) tok[tl] = tok_early;
+    }
+    __syncthreads();  // Ts, Bs and tok staged
+    if constexpr (SCORE) __syncthreads();  // row statistics in red
+    return;
   }
-  if constexpr (SCORE) {
-    if (t < BM) tok[t] = tok_early;
+
+  // -------------------------------------------------------------- MFMA waves
+  f32x16_t acc[MT][NTL];
+  f32x4_t accT[2][TJ1];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NTL; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int j = 0; j < TJ1; ++j) accT[q][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // Register fragments of one 16-wide k-step (W rows as the A operand, x
+  // rows as the B operand of the 32x32x16 MFMAs), double buffered so that
+  // the next k-step's LDS reads overlap the current k-step's MFMAs, and the
+  // T fragments of one 32-wide half slab (this wave's 32 x rows and the
+  // LoRA-down rows, 16x16x32 layout), read in the even k-step and consumed
+  // in the odd one.
+  struct Frag {
+    uint4 w[NTL];
+    uint4 x[MT];
+  };
+  struct TFrag {
+    uint4 tx[2];
+    uint4 a[TJ1];
+  };
+  Frag F0, F1;
+  TFrag TF;
+  constexpr int NMAIN = MT * NTL;      // MFMAs per k-step
+  constexpr int NRM = NTL + MT;        // main-fragment reads per k-step
+  constexpr int NRT = TJ > 0 ? 2 + TJ : 0;  // T-fragment reads (even k-steps)
+
+  // chunk (16 bytes = 8 k values) read by this lane in k-step s: lanes
+  // 0..31 take k 16 s .. 16 s + 7, lanes 32..63 the next 8.
+  auto read_main = [&](Frag& F, const uint4* s, int step, int r) __attribute__((always_inline)) {
+    const int ch = 2 * step + lh;
+    if (r < NTL) {
+      F.w[r] = s[L::WOFF + lds_idx(wc * WN + r * 32 + l32, ch)];
+    } else {
+      const int mi = r - NTL;
+      F.x[mi] = s[L::XOFF + lds_idx(wr * WM + mi * 32 + l32, ch)];
+    }
+  };
+  auto read_t = [&](const uint4* s, int half, int r) __attribute__((always_inline)) {
+    const int ch = 4 * half + lg;
+    if (r < 2) {
+      TF.tx[r] = s[L::XOFF + lds_idx(wr * WM + (wc * 2 + r) * 16 + l16, ch)];
+    } else {
+      TF.a[r - 2] = s[L::AOFF + lds_idx((r - 2) * 16 + l16, ch)];
+    }
+  };
+
+  // k-step S of the current slab: MFMAs on Fc; reads of k-step S + 1 (of
+  // `nxt` when S == 3) into Fn and, in even k-steps, of this half slab's T
+  // fragments; in odd k-steps the T MFMAs of the half slab.
+  auto kstep = [&](auto S, const Frag& Fc, Frag& Fn, const uint4* cur, const uint4* nxt)
+      __attribute__((always_inline)) {
+    constexpr int s = decltype(S)::value;
+    constexpr bool even = (s & 1) == 0;
+    constexpr int NR = NRM + (even ? NRT : 0);
+    const uint4* rs = s == 3 ? nxt : cur;
+    constexpr int snext = (s + 1) & 3;
+#pragma unroll
+    for (int m = 0; m < NMAIN; ++m) {
+      const int mi = m / NTL, ni = m % NTL;
+      acc[mi][ni] = mfma32(Fc.w[ni], Fc.x[mi], acc[mi][ni]);
+      if (m < NR) {
+        if (m < NRM) read_main(Fn, rs, snext, m);
+        else read_t(cur, s / 2, m - NRM);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int m = NMAIN; m < NR; ++m) {
+      if (m < NRM) read_main(Fn, rs, snext, m);
+      else read_t(cur, s / 2, m - NRM);
+    }
+    if constexpr (!even && TJ > 0) {
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) {
+        accT[0][j] = mfma16(TF.tx[0], TF.a[j], accT[0][j]);
+        accT[1][j] = mfma16(TF.tx[1], TF.a[j], accT[1][j]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // Slab kt: k-steps 0..2 on `cur`; barrier (slab kt fully read, slab
+  // kt + 1 landed); k-step 3, whose reads already take slab kt + 1 from
+  // `nxt`.  Past the last slab those reads fill registers that are never
+  // used, so every slab is the same straight-line code.
+  auto slab = [&](const uint4* cur, const uint4* nxt) __attribute__((always_inline)) {
+    kstep(IC<0>{}, F0, F1, cur, nxt);
+    kstep(IC<1>{}, F1, F0, cur, nxt);
+    kstep(IC<2>{}, F0, F1, cur, nxt);
+    lds_barrier();
+    kstep(IC<3>{}, F1, F0, cur, nxt);
+  };
+
+  lds_barrier();  // slab 0 is in LDS
+#pragma unroll
+  for (int r = 0; r < NRM; ++r) read_main(F0, sm0, 0, r);
+  if constexpr (NS == 3) {
+    for (int kt = 0; kt < nkt; kt += 3) {
+      slab(sm0, sm1);
+      if (kt + 1 < nkt) slab(sm1, sm2);
+      if (kt + 2 < nkt) slab(sm2, sm0);
+    }
+  } else {
+    for (int kt = 0; kt < nkt; kt += 2) {
+      slab(sm0, sm1);
+      if (kt + 1 < nkt) slab(sm1, sm0);
+    }
   }
-  __syncthreads();
+  lds_barrier();  // every wave is done with the stages before the epilogue reuses them
+
+  // ---------------------------------------------------------------- epilogue
+  if constexpr (TJ > 0) {
+      if (want_on) {
+        const float sc = a.s;
+        // accT[q][j] holds T[wr*64 + (wc*2+q)*16 + 4 lg + e][16 j + l16]
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int j = 0; j < TJ; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int row = wr * WM + (wc * 2 + q) * 16 + lg * 4 + e;
+              const int col = j * 16 + l16;
+              const float v = sc * accT[q][j][e];
+              const uint32_t hi = f32_to_bf16_rne(v);
+              const uint32_t lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
+              Ts[row * 2 * RP + col] = (uint16_t)hi;
+              Ts[row * 2 * RP + RP + col] = (uint16_t)lo;
+            }
+      }
+    }
+  __syncthreads();  // Ts, Bs and tok staged
 
   // s*T*B^T added by 32x32x16 MFMAs: A operand = rows of [B | B] (k < RP picks
   // B against the hi part, k >= RP against the lo part), B operand = rows of
