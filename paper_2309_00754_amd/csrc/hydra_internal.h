@@ -40,7 +40,9 @@ struct ScoreGemmArgs {
   const int32_t* tokens;   // [M]
   float4* part;            // [M x ntn]
   float* zt;               // [M x 2]: (z_off[token], z_on[token])
+  uint16_t* ts;            // [M x 2 RP] bf16: hi and lo parts of s * h A^T (RP = padded rank)
   int ntn;                 // number of column tiles
+  int ntm;                 // number of row tiles (set by the launcher)
 };
 
 struct CombineArgs {

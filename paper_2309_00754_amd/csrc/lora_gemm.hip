@@ -29,12 +29,8 @@
 //    bf16 hi + lo parts and multiplied against [B; B] by MFMA, adding the
 //    LoRA update to the same accumulators, which become the LoRA-on result.
 //    With B = 0 or s = 0 the update adds exact zeros, so y_on == y_off.  The
-//    copy waves fetch the tile's rows of B (and, for SCORE, the sampled
-//    tokens) at kernel start and stage them in LDS for the epilogue;
-//  * SCORE variant (CLM head, N = V): instead of storing logits, each row's
-//    (max, sum exp) over the tile's 256 columns is reduced for both passes,
-//    the sampled token's logit is picked up by the lane that holds it, and a
-//    float4 partial per (row, column tile) is written for the combine kernel.
+//    copy waves fetch the tile's rows of B at kernel start and stage them in
+//    LDS for the epilogue.
 #include <type_traits>
 
 #include "hydra_device.h"
@@ -55,8 +51,6 @@ constexpr int NTL = WN / 32;   // 32-row W tiles per wave
 constexpr int CPR = BK / 8;    // 16-byte chunks per LDS row
 constexpr int GROUP_M = 8;     // row tiles walked together (L2 reuse of W)
 
-static_assert(kScoreTileN == BN, "score partials assume one partial per GEMM column tile");
-
 // LDS chunk index of (row, 16-byte chunk c): chunks are XOR-swizzled by the
 // row so that the lanes reading one column of chunks hit distinct banks.
 __device__ __forceinline__ int lds_idx(int row, int c) { return row * CPR + (c ^ (row & 7)); }
@@ -70,14 +64,11 @@ struct Layout {
   // three stages when they fit in the 160 KB of LDS, else two
   static constexpr int NSTAGES = 3 * STAGE * 16 <= 160 * 1024 ? 3 : 2;
   static_assert(BM * 2 * RP * 2 <= STAGE * 16, "Ts must fit in one stage");
-  static_assert(BN * RP * 2 + (2 * BM * 4 + BM) * 4 <= STAGE * 16, "Bs, red and tok must fit in one stage");
+  static_assert(BN * RP * 2 <= STAGE * 16, "Bs must fit in one stage");
 };
 
 struct GemmArgs {
   LinearArgs lin;
-  const int32_t* tokens;
-  float4* part;
-  float* zt;
   int ntm, ntn;
   int vec4;  // outputs may be written with 16-byte stores (N % 4 == 0, 16-byte aligned)
 };
@@ -119,7 +110,7 @@ __device__ __forceinline__ void lds_barrier() {
 template <int V>
 using IC = std::integral_constant<int, V>;
 
-template <int RP, bool SCORE>
+template <int RP>
 __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   using L = Layout<RP>;
   constexpr int NS = L::NSTAGES;
@@ -148,7 +139,7 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   const int m0 = tmi * BM;
   const int n0 = tni * BN;
   const int nkt = (K + BK - 1) / BK;
-  const bool want_on = SCORE || a.y_on != nullptr;
+  const bool want_on = a.y_on != nullptr;
 
   constexpr int TJ = RP / 16;
   constexpr int TJ1 = TJ > 0 ? TJ : 1;
@@ -156,22 +147,18 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
 
   // Epilogue layout (the stages are free again by then):
   //   stage 0: Ts [BM][2 RP] bf16, s*T split into hi (columns 0..RP) and lo (RP..2RP)
-  //   stage 1: Bs [BN][RP] bf16, the tile's rows of B zero padded to RP;
-  //            SCORE only: red [2][BM][4] fp32 and tok [BM] int32 after it.
+  //   stage 1: Bs [BN][RP] bf16, the tile's rows of B zero padded to RP.
   uint16_t* Ts = reinterpret_cast<uint16_t*>(sm0);
   uint16_t* Bs = reinterpret_cast<uint16_t*>(sm1);
-  float* red = reinterpret_cast<float*>(Bs + BN * RP);
-  int* tok = reinterpret_cast<int*>(red + 2 * BM * 4);
 
   if (wave >= 4) {
     // ------------------------------------------------------------ copy waves
     const int cw = wave - 4;  // copy wave index (0..3), wave-uniform
     const int tl = t - NTM;   // copy thread index (0..255)
-    // Values the copy waves fetch early and stage in LDS for the epilogue: the
-    // tile's rows of B (copy thread tl holds row n0 + tl, zero padded to RP,
-    // two bf16 per register) and, for SCORE, the sampled token of row m0 + tl.
+    // The tile's rows of B, fetched early and staged in LDS for the epilogue
+    // (copy thread tl holds row n0 + tl, zero padded to RP, two bf16 per
+    // register).
     uint32_t breg[RP2];
-    int tok_early = -1;
 
     if constexpr (RP > 0) {
       static_assert(BN == NT - NTM, "one B row per copy thread");
@@ -184,13 +171,6 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
       }
 #pragma unroll
       for (int j = 0; j < RP; j += 2) breg[j / 2] = (v[j] & 0xFFFFu) | (v[j + 1] << 16);
-    }
-    if constexpr (SCORE) {
-      if (tl < BM) {
-        const int row = m0 + tl;
-        const int v = g.tokens[row < M ? row : 0];
-        tok_early = row < M ? v : -1;
-      }
     }
 
     // One copy instruction moves 8 rows x 128 bytes (64 lanes x 16 bytes)
@@ -274,11 +254,7 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int j = 0; j < RP; j += 2) *reinterpret_cast<uint32_t*>(Bs + tl * RP + j) = breg[j / 2];
     }
-    if constexpr (SCORE) {
-      if (tl < BM) tok[tl] = tok_early;
-    }
-    __syncthreads();  // Ts, Bs and tok staged
-    if constexpr (SCORE) __syncthreads();  // row statistics in red
+    __syncthreads();  // Ts and Bs staged
     return;
   }
 
@@ -421,7 +397,7 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
             }
       }
     }
-  __syncthreads();  // Ts, Bs and tok staged
+  __syncthreads();  // Ts and Bs staged
 
   // s*T*B^T added by 32x32x16 MFMAs: A operand = rows of [B | B] (k < RP picks
   // B against the hi part, k >= RP against the lo part), B operand = rows of
@@ -448,96 +424,42 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   };
 
   // acc[mi][ni][4 i + e] holds y[wr*64 + mi*32 + l32][wc*128 + ni*32 + 8 i + 4 lh + e]
-  if constexpr (!SCORE) {
-    auto store = [&](float* y) __attribute__((always_inline)) {
+  auto store = [&](float* y) __attribute__((always_inline)) {
 #pragma unroll
-      for (int mi = 0; mi < MT; ++mi) {
-        const int row = m0 + wr * WM + mi * 32 + l32;
-        if (row >= M) continue;
-        float* yr = y + (size_t)row * N;
-#pragma unroll
-        for (int ni = 0; ni < NTL; ++ni)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int col = n0 + wc * WN + ni * 32 + 8 * i + 4 * lh;
-            const f32x16_t& v = acc[mi][ni];
-            if (g.vec4 && col + 3 < N) {
-              *reinterpret_cast<float4*>(yr + col) = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
-            } else {
-#pragma unroll
-              for (int e = 0; e < 4; ++e)
-                if (col + e < N) yr[col + e] = v[4 * i + e];
-            }
-          }
-      }
-    };
-    if (a.y_off) store(a.y_off);
-    if (a.y_on) {
-      apply_lora();
-      store(a.y_on);
-    }
-  } else {
-    // Per-row (max, sum exp) over this wave's 128 columns (64 per lane, then
-    // the lane pair l, l + 32), then over the two waves sharing the rows.
-    // Identical code for the off and on passes.
-    auto row_stats = [&](int slot) __attribute__((always_inline)) {
-#pragma unroll
-      for (int mi = 0; mi < MT; ++mi) {
-        const int rlc = wr * WM + mi * 32 + l32;
-        const int tk = tok[rlc];
-        float mx = -INFINITY;
-#pragma unroll
-        for (int ni = 0; ni < NTL; ++ni)
-#pragma unroll
-          for (int k = 0; k < 16; ++k) {
-            const int col = n0 + wc * WN + ni * 32 + 8 * (k >> 2) + 4 * lh + (k & 3);
-            if (col < N) mx = fmaxf(mx, acc[mi][ni][k]);
-            // the lane holding the sampled token's column records its logit
-            if (col == tk) g.zt[(size_t)(m0 + rlc) * 2 + (slot >> 1)] = acc[mi][ni][k];
-          }
-        float sm = 0.f;
-        if (mx != -INFINITY) {
-#pragma unroll
-          for (int ni = 0; ni < NTL; ++ni)
-#pragma unroll
-            for (int k = 0; k < 16; ++k) {
-              const int col = n0 + wc * WN + ni * 32 + 8 * (k >> 2) + 4 * lh + (k & 3);
-              if (col < N) sm += exp_e(acc[mi][ni][k] - mx);
-            }
-        }
-        const float mo = __shfl_xor(mx, 32);
-        const float so = __shfl_xor(sm, 32);
-        lse_merge(mx, sm, mo, so);
-        if (lh == 0) {
-          red[(wc * BM + rlc) * 4 + slot] = mx;
-          red[(wc * BM + rlc) * 4 + slot + 1] = sm;
-        }
-      }
-    };
-    row_stats(0);     // LoRA off
-    apply_lora();
-    row_stats(2);     // LoRA on
-    __syncthreads();
-    for (int e = t; e < BM; e += NT) {
-      const int row = m0 + e;
+    for (int mi = 0; mi < MT; ++mi) {
+      const int row = m0 + wr * WM + mi * 32 + l32;
       if (row >= M) continue;
-      float mo = red[e * 4 + 0], so = red[e * 4 + 1];
-      float mn = red[e * 4 + 2], sn = red[e * 4 + 3];
-      lse_merge(mo, so, red[(BM + e) * 4 + 0], red[(BM + e) * 4 + 1]);
-      lse_merge(mn, sn, red[(BM + e) * 4 + 2], red[(BM + e) * 4 + 3]);
-      g.part[(size_t)row * g.ntn + tni] = make_float4(mo, so, mn, sn);
+      float* yr = y + (size_t)row * N;
+#pragma unroll
+      for (int ni = 0; ni < NTL; ++ni)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int col = n0 + wc * WN + ni * 32 + 8 * i + 4 * lh;
+          const f32x16_t& v = acc[mi][ni];
+          if (g.vec4 && col + 3 < N) {
+            *reinterpret_cast<float4*>(yr + col) = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (col + e < N) yr[col + e] = v[4 * i + e];
+          }
+        }
     }
+  };
+  if (a.y_off) store(a.y_off);
+  if (a.y_on) {
+    apply_lora();
+    store(a.y_on);
   }
 }
 
-template <bool SCORE>
 hipError_t launch(const GemmArgs& g, int rp, hipStream_t stream) {
   const dim3 grid(g.ntm * g.ntn), block(NT);
   switch (rp) {
-    case 0: hipLaunchKernelGGL((lora_gemm_kernel<0, SCORE>), grid, block, 0, stream, g); break;
-    case 16: hipLaunchKernelGGL((lora_gemm_kernel<16, SCORE>), grid, block, 0, stream, g); break;
-    case 32: hipLaunchKernelGGL((lora_gemm_kernel<32, SCORE>), grid, block, 0, stream, g); break;
-    case 64: hipLaunchKernelGGL((lora_gemm_kernel<64, SCORE>), grid, block, 0, stream, g); break;
+    case 0: hipLaunchKernelGGL((lora_gemm_kernel<0>), grid, block, 0, stream, g); break;
+    case 16: hipLaunchKernelGGL((lora_gemm_kernel<16>), grid, block, 0, stream, g); break;
+    case 32: hipLaunchKernelGGL((lora_gemm_kernel<32>), grid, block, 0, stream, g); break;
+    case 64: hipLaunchKernelGGL((lora_gemm_kernel<64>), grid, block, 0, stream, g); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -556,20 +478,7 @@ hipError_t launch_lora_gemm(const LinearArgs& a, hipStream_t stream) {
   g.ntn = (a.N + BN - 1) / BN;
   g.vec4 = (a.N % 4 == 0) && (!a.y_off || aligned16(a.y_off)) && (!a.y_on || aligned16(a.y_on));
   const int rp = a.y_on ? padded_rank(a.r) : 0;
-  return launch<false>(g, rp, stream);
-}
-
-hipError_t launch_score_gemm(const ScoreGemmArgs& s, hipStream_t stream) {
-  GemmArgs g{};
-  g.lin = s.lin;
-  g.lin.y_off = nullptr;
-  g.lin.y_on = nullptr;
-  g.tokens = s.tokens;
-  g.part = s.part;
-  g.zt = s.zt;
-  g.ntm = (s.lin.M + BM - 1) / BM;
-  g.ntn = s.ntn;
-  return launch<true>(g, padded_rank(s.lin.r), stream);
+  return launch(g, rp, stream);
 }
 
 }  // namespace hydra

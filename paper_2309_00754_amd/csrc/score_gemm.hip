@@ -1,0 +1,430 @@
+// Fused CLM-head scoring GEMM for gfx950 (MI355X): the LoRA-off and LoRA-on
+// logits z_off = h W^T and z_on = z_off + s (h A^T) B^T of the CLM head are
+// reduced to per-row (max, sum exp) partials and the sampled token's logit
+// without ever being written to memory (Sec. 3, the CLM head of pi^hydra;
+// App. A, Alg. 1 / Alg. 2, reference and actor log-probabilities).
+//
+// The vocabulary dimension gives thousands of output tiles, so this GEMM uses
+// the largest tile the register file allows, which moves the least data per
+// MFMA through L2 and LDS (the matrix cores run power-limited, and data
+// movement costs power):
+//  * one 256 x 256 output tile per 256-thread workgroup (one wave per SIMD);
+//    each wave owns a 128 x 128 sub-tile = 4 x 4 v_mfma_f32_32x32x16_bf16
+//    tiles, 256 fp32 accumulators per lane (held in AGPRs);
+//  * K slabs of 32 go through a four-stage LDS ring (32 KB per stage, rows of
+//    64 bytes, 16-byte chunks XOR-swizzled by row / 4).  The copies
+//    (buffer_load ... lds) are issued by the MFMA waves themselves, four per
+//    16-wide k-step, three slabs ahead of use;
+//  * one barrier per slab: before it every wave has read the slab's last
+//    fragments and waited for its copies of the next slab, after it the freed
+//    stage is refilled;
+//  * the rank-r product T = h A^T is the same for every column tile of a row
+//    block, so it is computed once by score_t_kernel (bf16 hi + lo parts of
+//    s*T in the workspace) instead of in the main loop;
+//  * epilogue: per-row (max, sum exp) of the LoRA-off logits, then the LoRA
+//    update s*T*B^T added to the accumulators by MFMA (A operand = rows of
+//    [B | B], B operand = rows of [hi | lo]), then the same statistics of the
+//    LoRA-on logits; the lane holding the sampled token's column records its
+//    logit.  One float4 (max_off, sum_off, max_on, sum_on) per (row, column
+//    tile) goes to the workspace for score_combine_kernel.
+// With B = 0 or s = 0 the LoRA update adds exact zeros, so the on and off
+// statistics (computed by the same code) are bit-identical and KL == 0.
+#include "hydra_device.h"
+#include "hydra_internal.h"
+
+namespace hydra {
+namespace {
+
+constexpr int BM = 256;        // tile rows (tokens)
+constexpr int BN = 256;        // tile columns (vocabulary entries)
+constexpr int BK = 32;         // K slab
+constexpr int NT = 256;        // threads per workgroup (4 waves)
+constexpr int WM = 128;        // wave tile rows
+constexpr int WN = 128;        // wave tile columns
+constexpr int MT = WM / 32;    // 32-row x tiles per wave
+constexpr int NTL = WN / 32;   // 32-row W tiles per wave
+constexpr int CPR = BK / 8;    // 16-byte chunks per LDS row
+constexpr int NS = 4;          // ring stages
+constexpr int STAGE = (BM + BN) * CPR;  // uint4 per stage (32 KB)
+constexpr int XOFF = 0;
+constexpr int WOFF = BM * CPR;
+constexpr int GROUP_M = 8;     // row tiles walked together (L2 reuse of W)
+constexpr int DPW = (BM + BN) / 16 / 4;  // copies per wave per slab (16 rows of 64 bytes each)
+
+static_assert(kScoreTileN == BN, "one partial per GEMM column tile");
+static_assert(DPW == 8, "the k-step schedule issues four copies per k-step");
+static_assert(BM * 2 * 4 * 4 <= STAGE * 16, "the epilogue's row statistics fit in one stage");
+
+// LDS chunk index of (row, 16-byte chunk c) in a stage: rows of 64 bytes, the
+// chunk is XOR-ed with (row / 4) % 4 so that the 16 lanes of one read phase
+// (16 consecutive rows, one chunk) cover all banks.
+__device__ __forceinline__ int sidx(int row, int c) { return row * CPR + (c ^ ((row >> 2) & 3)); }
+
+// Workgroup id -> (row tile, column tile): as in the dual GEMM, each XCD gets a
+// contiguous range of the logical order when the tile count allows, and the
+// logical order walks GROUP_M row tiles per column tile.
+__device__ __forceinline__ void tile_of(int bid, int ntm, int ntn, int& tm, int& tn) {
+  const int total = ntm * ntn;
+  int lid = bid;
+  if ((total & 7) == 0) lid = (bid & 7) * (total >> 3) + (bid >> 3);
+  const int per_group = GROUP_M * ntn;
+  const int group = lid / per_group;
+  const int first_m = group * GROUP_M;
+  const int gsize = min(ntm - first_m, GROUP_M);
+  const int in = lid - group * per_group;
+  tm = first_m + in % gsize;
+  tn = in / gsize;
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm_lds_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit field");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | (((N >> 4) & 3) << 14));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int V>
+struct IC {
+  static constexpr int value = V;
+};
+
+// RAGGED: the vocabulary is not a multiple of the column tile, so the last
+// column tile masks the columns past N.
+template <int RP, bool RAGGED>
+__global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
+  __shared__ uint4 sm[NS][STAGE];
+
+  const LinearArgs& a = g.lin;
+  const int M = a.M, N = a.N, K = a.K;
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  // wave-uniform (SGPR) wave index: MFMAs never sit under divergent control flow
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int wr = wave >> 1;
+  const int wc = wave & 1;
+  const int l32 = lane & 31;
+  const int lh = lane >> 5;
+
+  int tmi, tni;
+  tile_of(blockIdx.x, g.ntm, g.ntn, tmi, tni);
+  // (tile coordinates are made provably wave-uniform, so that everything
+  // derived from them -- buffer descriptors, LDS bases -- lives in SGPRs)
+  const int m0 = __builtin_amdgcn_readfirstlane(tmi * BM);
+  const int n0 = __builtin_amdgcn_readfirstlane(tni * BN);
+  const int nkt = (K + BK - 1) / BK;
+  if (nkt < 1) __builtin_unreachable();  // K >= 8 is validated by the caller
+
+  // ---- epilogue operands, fetched before the main loop so that they have
+  // arrived long before it ends: the sampled tokens of this lane's four rows,
+  // the rows of [hi | lo] (s*T split in bf16, 2 RP per row) and the rows of B
+  // (zero padded to RP; B rows have r elements, so they are read as bf16).
+  constexpr int KT = 2 * RP / 16;           // 16-wide k-steps of the LoRA update
+  constexpr int KB = RP > 0 ? RP / 16 : 1;  // distinct B fragments per 32-row tile
+  constexpr bool EARLY = false;
+  int tk[MT];
+#pragma unroll
+  for (int mi = 0; mi < MT; ++mi) {
+    const int row = m0 + wr * WM + mi * 32 + l32;
+    tk[mi] = row < M ? g.tokens[row] : -1;
+  }
+  uint4 tf[MT][KT > 0 ? KT : 1];
+  uint4 bfr[NTL][KB];
+  auto load_lora = [&]() __attribute__((always_inline)) {
+    if constexpr (RP > 0) {
+      const __amdgpu_buffer_rsrc_t trs = make_rsrc(g.ts + (size_t)m0 * 2 * RP, (uint32_t)min(BM, M - m0) * 2 * RP * 2u);
+#pragma unroll
+      for (int mi = 0; mi < MT; ++mi)
+#pragma unroll
+        for (int ks = 0; ks < KT; ++ks)
+          tf[mi][ks] = buf_load16(trs, ((wr * WM + mi * 32 + l32) * 2 * RP + ks * 16 + lh * 8) * 2);
+      const __amdgpu_buffer_rsrc_t brs = make_rsrc(a.B + (size_t)n0 * a.r, (uint32_t)min(BN, N - n0) * a.r * 2u);
+#pragma unroll
+      for (int ni = 0; ni < NTL; ++ni)
+#pragma unroll
+        for (int kq = 0; kq < KB; ++kq) {
+          const int n = wc * WN + ni * 32 + l32;
+          uint32_t v[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int j = kq * 16 + lh * 8 + e;
+            v[e] = __builtin_amdgcn_raw_buffer_load_b16(brs, j < a.r ? (n * a.r + j) * 2 : kOutOfRange, 0, 0);
+          }
+          bfr[ni][kq] = make_uint4((v[0] & 0xFFFFu) | (v[1] << 16), (v[2] & 0xFFFFu) | (v[3] << 16),
+                                   (v[4] & 0xFFFFu) | (v[5] << 16), (v[6] & 0xFFFFu) | (v[7] << 16));
+        }
+    }
+  };
+  if constexpr (EARLY) load_lora();
+
+  // ---- copies.  One copy instruction moves 16 rows x 64 bytes (64 lanes x
+  // 16 bytes) into 1 KB of LDS; lane i fills LDS chunk i of it, so it fetches
+  // the global chunk that the swizzle maps there.  Buffer resources cover
+  // exactly the tile's valid rows (rows past M or N read as zeros); a chunk
+  // past K gets an out-of-range offset (zeros as well), and so do all copies
+  // of the slabs past the last one, which land in stages that are not read
+  // again.  Wave w copies 16-row blocks w, w + 4, w + 8, w + 12 of x (j < 4)
+  // and of W (j >= 4).
+  const i32x4_t xr = make_rsrc_raw(a.x + (size_t)m0 * K, (uint32_t)min(BM, M - m0) * K * 2u);
+  const i32x4_t wrs = make_rsrc_raw(a.W + (size_t)n0 * K, (uint32_t)min(BN, N - n0) * K * 2u);
+  const int row_bytes = K * 2;
+  const int cg = (lane & 3) ^ ((lane >> 4) & 3);  // global chunk fetched by this lane
+  const int rl = lane >> 2;                       // row within the 16-row copy
+  auto dma_one = [&](uint4* st, int kt, int j) __attribute__((always_inline)) {
+    const int k0 = kt * BK;
+    const bool kv = k0 + cg * 8 < K;
+    const int kofs = k0 * 2 + cg * 16;
+    const int ci = wave + 4 * (j & 3);
+    if (j < 4)
+      dma16(xr, st + XOFF + ci * 64, kv ? (ci * 16 + rl) * row_bytes + kofs : kOutOfRange);
+    else
+      dma16(wrs, st + WOFF + ci * 64, kv ? (ci * 16 + rl) * row_bytes + kofs : kOutOfRange);
+  };
+
+  f32x16_t acc[MT][NTL];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NTL; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // Fragments of one 16-wide k-step: W rows (A operand) and h rows (B
+  // operand), double buffered across k-steps.
+  struct Frag {
+    uint4 w[NTL];
+    uint4 x[MT];
+  };
+  Frag F0, F1;
+  auto read_one = [&](Frag& F, const uint4* st, int s, int r) __attribute__((always_inline)) {
+    const int ch = 2 * s + lh;
+    if (r < NTL)
+      F.w[r] = st[WOFF + sidx(wc * WN + r * 32 + l32, ch)];
+    else
+      F.x[r - NTL] = st[XOFF + sidx(wr * WM + (r - NTL) * 32 + l32, ch)];
+  };
+
+  // k-step S of slab kt (stage `cur`): MFMAs on Fc, reads of the next k-step
+  // into Fn (k-step 1 of this slab, or k-step 0 of slab kt + 1 from `nxt`),
+  // and four copies: k-step 0 finishes slab kt + 3 (W blocks, into `c0dst`),
+  // k-step 1 starts slab kt + 4 (x blocks, into `cur`, free after the
+  // barrier).
+  auto kstep = [&](auto S, const Frag& Fc, Frag& Fn, const uint4* rs, uint4* ddst, int dkt)
+      __attribute__((always_inline)) {
+    constexpr int s = decltype(S)::value;
+#pragma unroll
+    for (int m = 0; m < MT * NTL; ++m) {
+      const int mi = m / NTL, ni = m % NTL;
+      acc[mi][ni] = mfma32(Fc.w[ni], Fc.x[mi], acc[mi][ni]);
+      if (m < NTL + MT) read_one(Fn, rs, s ^ 1, m);
+      if (m >= 8 && (m & 1) == 1) dma_one(ddst, dkt, (s == 0 ? 4 : 0) + ((m - 9) >> 1));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  auto slab = [&](uint4* cur, uint4* nxt, uint4* prev, int kt) __attribute__((always_inline)) {
+    kstep(IC<0>{}, F0, F1, cur, prev, kt + 3);
+    // slab kt + 1 must have landed: only the copies of slabs kt + 2 and kt + 3
+    // (2 x DPW per wave) may still be in flight
+    wait_vm_lds_barrier<2 * DPW>();
+    kstep(IC<1>{}, F1, F0, nxt, cur, kt + 4);
+  };
+
+  // prologue: slabs 0..2 and the x half of slab 3
+#pragma unroll
+  for (int j = 0; j < DPW; ++j) dma_one(sm[0], 0, j);
+#pragma unroll
+  for (int j = 0; j < DPW; ++j) dma_one(sm[1], 1, j);
+#pragma unroll
+  for (int j = 0; j < DPW; ++j) dma_one(sm[2], 2, j);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) dma_one(sm[3], 3, j);
+  wait_vm_lds_barrier<2 * DPW + 4>();
+#pragma unroll
+  for (int r = 0; r < NTL + MT; ++r) read_one(F0, sm[0], 0, r);
+  for (int kt = 0; kt < nkt; kt += NS) {
+    slab(sm[0], sm[1], sm[3], kt);
+    if (kt + 1 < nkt) slab(sm[1], sm[2], sm[0], kt + 1);
+    if (kt + 2 < nkt) slab(sm[2], sm[3], sm[1], kt + 2);
+    if (kt + 3 < nkt) slab(sm[3], sm[0], sm[2], kt + 3);
+  }
+  wait_vm_lds_barrier<0>();  // every copy has landed and every wave is done with the ring
+
+  // ---------------------------------------------------------------- epilogue
+  if constexpr (!EARLY) load_lora();
+  float* red = reinterpret_cast<float*>(sm[0]);  // [2][BM][4]: per wave column, (max, sum) off / on
+  const int wcol0 = n0 + wc * WN;
+
+  // acc[mi][ni][4 i + e] holds z_off[m0 + wr*128 + mi*32 + l32][wcol0 + ni*32 + 8 i + 4 lh + e].
+  // Row block mi at a time, on a register copy z of its 64 logits per lane:
+  // statistics of the LoRA-off logits; then z += D, D = s*T*B^T of the row
+  // block by MFMA (A operand = rows of [B | B], B operand = rows of
+  // [hi | lo], zero accumulator), and the statistics of the LoRA-on logits.
+  // With B = 0 or s = 0, D is exactly zero.  For a ragged vocabulary the
+  // logits of columns past N are set to -inf (branch-free), so the
+  // statistics need no column test.
+  auto row_stats = [&](const float* z, int mi, int slot) __attribute__((always_inline)) {
+    const int rloc = wr * WM + mi * 32 + l32;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < NTL * 16; ++q) mx = fmaxf(mx, z[q]);
+    // the lane holding the sampled token's column records its logit
+    const int rel = tk[mi] - wcol0 - 4 * lh;  // column offset within this lane's half
+    if (rel >= 0 && rel < WN && ((rel >> 2) & 1) == 0) {
+      float v = 0.f;
+#pragma unroll
+      for (int q = 0; q < NTL * 16; ++q) v = ((q >> 4) * 32 + 8 * ((q & 15) >> 2) + (q & 3) == rel) ? z[q] : v;
+      g.zt[(size_t)(m0 + rloc) * 2 + (slot >> 1)] = v;
+    }
+    float sm_ = 0.f;
+    if (mx != -INFINITY) {
+#pragma unroll
+      for (int q = 0; q < NTL * 16; ++q) sm_ += exp_e(z[q] - mx);
+    }
+    const float mo = __shfl_xor(mx, 32);
+    const float so = __shfl_xor(sm_, 32);
+    lse_merge(mx, sm_, mo, so);
+    if (lh == 0) {
+      red[(wc * BM + rloc) * 4 + slot] = mx;
+      red[(wc * BM + rloc) * 4 + slot + 1] = sm_;
+    }
+  };
+  auto mask_tail = [&](float* z) __attribute__((always_inline)) {
+    if constexpr (RAGGED) {
+      const int lim = N - wcol0 - 4 * lh;  // columns q of this lane with offset >= lim are past N
+#pragma unroll
+      for (int q = 0; q < NTL * 16; ++q)
+        z[q] = (q >> 4) * 32 + 8 * ((q & 15) >> 2) + (q & 3) < lim ? z[q] : -INFINITY;
+    }
+  };
+
+  // (scheduling barriers keep the row blocks apart, so that only one row
+  // block's logits are held in VGPRs at a time)
+#pragma unroll
+  for (int mi = 0; mi < MT; ++mi) {
+    __builtin_amdgcn_sched_barrier(0);
+    float z[NTL * 16];
+#pragma unroll
+    for (int ni = 0; ni < NTL; ++ni)
+#pragma unroll
+      for (int k = 0; k < 16; ++k) z[ni * 16 + k] = acc[mi][ni][k];
+    mask_tail(z);
+    row_stats(z, mi, 0);  // LoRA off
+    if constexpr (RP > 0) {
+#pragma unroll
+      for (int ni = 0; ni < NTL; ++ni) {
+        f32x16_t d;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) d[e] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KT; ++ks) d = mfma32(bfr[ni][ks % KB], tf[mi][ks], d);
+#pragma unroll
+        for (int k = 0; k < 16; ++k) z[ni * 16 + k] += d[k];
+      }
+      mask_tail(z);
+    }
+    row_stats(z, mi, 2);  // LoRA on
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  __syncthreads();
+  {
+    const int row = m0 + t;
+    if (t < BM && row < M) {
+      float mo = red[t * 4 + 0], so = red[t * 4 + 1];
+      float mn = red[t * 4 + 2], sn = red[t * 4 + 3];
+      lse_merge(mo, so, red[(BM + t) * 4 + 0], red[(BM + t) * 4 + 1]);
+      lse_merge(mn, sn, red[(BM + t) * 4 + 2], red[(BM + t) * 4 + 3]);
+      g.part[(size_t)row * g.ntn + tni] = make_float4(mo, so, mn, sn);
+    }
+  }
+}
+
+// T = h A^T for 16 rows per workgroup; the 8 waves split K.  Writes the bf16
+// hi and lo parts of s*T: ts[row][j] = hi, ts[row][RP + j] = lo (zero for
+// j >= r), the B operand rows of the scoring GEMM's LoRA update.
+constexpr int T_WAVES = 8;
+constexpr int T_UNROLL = 4;
+
+template <int RP>
+__global__ __launch_bounds__(T_WAVES * 64) void score_t_kernel(ScoreGemmArgs g) {
+  constexpr int TJ = RP / 16;
+  __shared__ f32x4_t red[T_WAVES][TJ][64];
+  const LinearArgs& a = g.lin;
+  const int M = a.M, K = a.K;
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int l16 = lane & 15;
+  const int lg = lane >> 4;
+  const int m0 = blockIdx.x * 16;
+  const __amdgpu_buffer_rsrc_t hrs = make_rsrc(a.x + (size_t)m0 * K, (uint32_t)min(16, M - m0) * K * 2u);
+  const __amdgpu_buffer_rsrc_t ars = make_rsrc(a.A, (uint32_t)min(a.r, RP) * K * 2u);
+  f32x4_t acc[TJ];
+#pragma unroll
+  for (int j = 0; j < TJ; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int ksteps = (K + 31) / 32;
+  for (int k0 = wave; k0 < ksteps; k0 += T_WAVES * T_UNROLL) {
+    uint4 hf[T_UNROLL], af[T_UNROLL][TJ];
+#pragma unroll
+    for (int u = 0; u < T_UNROLL; ++u) {
+      const int k = (k0 + u * T_WAVES) * 32 + lg * 8;
+      const bool kv = k0 + u * T_WAVES < ksteps && k < K;
+      hf[u] = buf_load16(hrs, kv ? (l16 * K + k) * 2 : kOutOfRange);
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) af[u][j] = buf_load16(ars, kv ? ((j * 16 + l16) * K + k) * 2 : kOutOfRange);
+    }
+#pragma unroll
+    for (int u = 0; u < T_UNROLL; ++u)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) acc[j] = mfma16(hf[u], af[u][j], acc[j]);
+  }
+  // acc[j] lane l holds T[m0 + 4 (l / 16) + i][16 j + l % 16]
+#pragma unroll
+  for (int j = 0; j < TJ; ++j) red[wave][j][lane] = acc[j];
+  __syncthreads();
+  for (int e = t; e < 16 * RP; e += T_WAVES * 64) {
+    const int rl = e / RP, j = e % RP;
+    const int row = m0 + rl;
+    if (row >= M) continue;
+    const int src = (rl >> 2) * 16 + (j & 15);
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < T_WAVES; ++w) v += red[w][j >> 4][src][rl & 3];
+    v *= a.s;
+    const uint32_t hi = f32_to_bf16_rne(v);
+    const uint32_t lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
+    g.ts[(size_t)row * 2 * RP + j] = (uint16_t)hi;
+    g.ts[(size_t)row * 2 * RP + RP + j] = (uint16_t)lo;
+  }
+}
+
+template <int RP>
+hipError_t launch_rp(const ScoreGemmArgs& s, hipStream_t stream) {
+  const bool ragged = s.lin.N % BN != 0;
+  if constexpr (RP > 0) {
+    hipLaunchKernelGGL((score_t_kernel<RP>), dim3((s.lin.M + 15) / 16), dim3(T_WAVES * 64), 0, stream, s);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (ragged)
+    hipLaunchKernelGGL((score_gemm_kernel<RP, true>), dim3(s.ntm * s.ntn), dim3(NT), 0, stream, s);
+  else
+    hipLaunchKernelGGL((score_gemm_kernel<RP, false>), dim3(s.ntm * s.ntn), dim3(NT), 0, stream, s);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_score_gemm(const ScoreGemmArgs& s_in, hipStream_t stream) {
+  ScoreGemmArgs s = s_in;
+  s.ntm = (s.lin.M + BM - 1) / BM;
+  const int r = s.lin.r;
+  switch (r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : 64) {
+    case 0: return launch_rp<0>(s, stream);
+    case 16: return launch_rp<16>(s, stream);
+    case 32: return launch_rp<32>(s, stream);
+    default: return launch_rp<64>(s, stream);
+  }
+}
+
+}  // namespace hydra
