@@ -51,9 +51,11 @@ constexpr int NTL = WN / 32;   // 32-row W tiles per wave
 constexpr int CPR = BK / 8;    // 16-byte chunks per LDS row
 constexpr int GROUP_M = 8;     // row tiles walked together (L2 reuse of W)
 
-// LDS chunk index of (row, 16-byte chunk c): chunks are XOR-swizzled by the
-// row so that the lanes reading one column of chunks hit distinct banks.
-__device__ __forceinline__ int lds_idx(int row, int c) { return row * CPR + (c ^ (row & 7)); }
+// LDS chunk index of (row, 16-byte chunk c): rows of 128 bytes, the chunk is
+// XOR-ed with (row / 2) % 8, so that the 16 lanes of one read phase (16
+// consecutive rows, one chunk: 8 even and 8 odd rows, each set covering the
+// 8 chunk positions once) hit all 64 banks exactly once.
+__device__ __forceinline__ int lds_idx(int row, int c) { return row * CPR + (c ^ ((row >> 1) & 7)); }
 
 template <int RP>
 struct Layout {
@@ -184,8 +186,11 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
     const i32x4_t wrs = make_rsrc_raw(a.W + (size_t)n0 * K, (uint32_t)min(BN, N - n0) * K * 2u);
     const i32x4_t arsrc = make_rsrc_raw(a.A, (uint32_t)min(a.r, RP) * K * 2u);
     const int row_bytes = K * 2;
-    const int c = (lane & 7) ^ (lane >> 3);  // global chunk fetched by this lane
-    const int rl = lane >> 3;                // row within the 8-row copy
+    // Lane i fills LDS chunk i & 7 of row 8 ci + i / 8; every block ci this
+    // wave copies has the parity of cw, so the global chunk it fetches is
+    // (i & 7) ^ ((row / 2) % 8) = (i & 7) ^ (4 (cw & 1) + i / 16).
+    const int c = (lane & 7) ^ (((cw & 1) << 2) | (lane >> 4));  // global chunk fetched by this lane
+    const int rl = lane >> 3;                                    // row within the 8-row copy
     constexpr int XD = BM / 8, WD = BN / 8, AD = RP / 8;
     static_assert(XD % 4 == 0 && WD % 4 == 0, "x and W blocks split evenly over the copy waves");
     constexpr int XJ = XD / 4, WJ = WD / 4;
