@@ -23,13 +23,15 @@ hydra_status from_hip(hipError_t e) { return e == hipSuccess ? HYDRA_OK : HYDRA_
 int64_t score_tiles(int64_t V) { return (V + hydra::kScoreTileN - 1) / hydra::kScoreTileN; }
 size_t score_part_bytes(int64_t M, int64_t V) { return size_t(M) * size_t(score_tiles(V)) * sizeof(float4); }
 // Workspace of hydra_score: per (row, column tile) partials, then per row the
-// gathered token logits (2 fp32), then per row the bf16 hi and lo parts of
-// s * h A^T at the largest padded rank (2 x 64 bf16), 16-byte aligned.
+// gathered token logits (2 fp32), then (16-byte aligned) per row the bf16 hi
+// and lo parts of s * h A^T (room for 2 x 64 bf16), then per vocabulary row
+// B zero padded to the padded rank (room for 64 bf16).
 size_t score_zt_offset(int64_t M, int64_t V) { return score_part_bytes(M, V); }
 size_t score_ts_offset(int64_t M, int64_t V) {
   return (score_zt_offset(M, V) + size_t(M) * 2 * sizeof(float) + 15) & ~size_t(15);
 }
-size_t score_ws_bytes(int64_t M, int64_t V) { return score_ts_offset(M, V) + size_t(M) * 2 * HYDRA_MAX_RANK * 2; }
+size_t score_bp_offset(int64_t M, int64_t V) { return score_ts_offset(M, V) + size_t(M) * 2 * HYDRA_MAX_RANK * 2; }
+size_t score_ws_bytes(int64_t M, int64_t V) { return score_bp_offset(M, V) + size_t(V) * HYDRA_MAX_RANK * 2; }
 
 }  // namespace
 
@@ -137,6 +139,7 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
   float4* part = reinterpret_cast<float4*>(workspace);
   float* zt = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + score_zt_offset(M, V));
   uint16_t* ts = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(workspace) + score_ts_offset(M, V));
+  uint16_t* bp = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(workspace) + score_bp_offset(M, V));
 
   hydra::ScoreGemmArgs g{};
   g.lin.x = h;
@@ -152,6 +155,7 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
   g.part = part;
   g.zt = zt;
   g.ts = ts;
+  g.bp = bp;
   g.ntn = int(score_tiles(V));
   hipError_t e = hydra::launch_score_gemm(g, st);
   if (e != hipSuccess) return HYDRA_ERR_HIP;

@@ -87,7 +87,8 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
 
 // e^x and ln x from the hardware base-2 transcendental units:
 // e^x = 2^(x log2 e), ln x = log2(x) ln 2.
-__device__ __forceinline__ float exp_e(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
+constexpr float kLog2e = 1.4426950408889634f;
+__device__ __forceinline__ float exp_e(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
 __device__ __forceinline__ float log_e(float x) { return __builtin_amdgcn_logf(x) * 0.6931471805599453f; }
 
 // Merge two (running max, sum of exp(v - max)) pairs.  The products and the

@@ -41,6 +41,7 @@ struct ScoreGemmArgs {
   float4* part;            // [M x ntn]
   float* zt;               // [M x 2]: (z_off[token], z_on[token])
   uint16_t* ts;            // [M x 2 RP] bf16: hi and lo parts of s * h A^T (RP = padded rank)
+  uint16_t* bp;            // [V x RP] bf16: B zero padded to RP columns
   int ntn;                 // number of column tiles
   int ntm;                 // number of row tiles (set by the launcher)
 };

@@ -20,11 +20,13 @@
 //    stage is refilled;
 //  * the rank-r product T = h A^T is the same for every column tile of a row
 //    block, so it is computed once by score_t_kernel (bf16 hi + lo parts of
-//    s*T in the workspace) instead of in the main loop;
-//  * epilogue: per-row (max, sum exp) of the LoRA-off logits, then the LoRA
-//    update s*T*B^T added to the accumulators by MFMA (A operand = rows of
-//    [B | B], B operand = rows of [hi | lo]), then the same statistics of the
-//    LoRA-on logits; the lane holding the sampled token's column records its
+//    s*T in the workspace, with B zero padded to the padded rank RP next to
+//    it) instead of in the main loop;
+//  * the LoRA update s*T*B^T is then a GEMM with 2 RP more k values ([hi | lo]
+//    against [B | B]); it runs as 2 RP / 32 more slabs through the same ring,
+//    right after the per-row (max, sum exp) of the LoRA-off logits have been
+//    taken from the accumulators, and the same statistics of the LoRA-on
+//    logits follow.  The lane holding the sampled token's column records its
 //    logit.  One float4 (max_off, sum_off, max_on, sum_on) per (row, column
 //    tile) goes to the workspace for score_combine_kernel.
 // With B = 0 or s = 0 the LoRA update adds exact zeros, so the on and off
@@ -115,48 +117,20 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
   const int n0 = __builtin_amdgcn_readfirstlane(tni * BN);
   const int nkt = (K + BK - 1) / BK;
   if (nkt < 1) __builtin_unreachable();  // K >= 8 is validated by the caller
+  // The LoRA update s*T*B^T is a GEMM with 2 RP more k values: the rows of
+  // [hi | lo] (s*T in bf16 hi and lo parts) against the rows of [Bp | Bp]
+  // (B zero padded to RP).  Those run as LS more slabs of the same ring,
+  // after the LoRA-off statistics have been taken from the accumulators.
+  constexpr int LS = 2 * RP / BK;
+  const int nsl = nkt + LS;
 
-  // ---- epilogue operands, fetched before the main loop so that they have
-  // arrived long before it ends: the sampled tokens of this lane's four rows,
-  // the rows of [hi | lo] (s*T split in bf16, 2 RP per row) and the rows of B
-  // (zero padded to RP; B rows have r elements, so they are read as bf16).
-  constexpr int KT = 2 * RP / 16;           // 16-wide k-steps of the LoRA update
-  constexpr int KB = RP > 0 ? RP / 16 : 1;  // distinct B fragments per 32-row tile
-  constexpr bool EARLY = false;
+  // the sampled tokens of this lane's four rows, fetched early
   int tk[MT];
 #pragma unroll
   for (int mi = 0; mi < MT; ++mi) {
     const int row = m0 + wr * WM + mi * 32 + l32;
     tk[mi] = row < M ? g.tokens[row] : -1;
   }
-  uint4 tf[MT][KT > 0 ? KT : 1];
-  uint4 bfr[NTL][KB];
-  auto load_lora = [&]() __attribute__((always_inline)) {
-    if constexpr (RP > 0) {
-      const __amdgpu_buffer_rsrc_t trs = make_rsrc(g.ts + (size_t)m0 * 2 * RP, (uint32_t)min(BM, M - m0) * 2 * RP * 2u);
-#pragma unroll
-      for (int mi = 0; mi < MT; ++mi)
-#pragma unroll
-        for (int ks = 0; ks < KT; ++ks)
-          tf[mi][ks] = buf_load16(trs, ((wr * WM + mi * 32 + l32) * 2 * RP + ks * 16 + lh * 8) * 2);
-      const __amdgpu_buffer_rsrc_t brs = make_rsrc(a.B + (size_t)n0 * a.r, (uint32_t)min(BN, N - n0) * a.r * 2u);
-#pragma unroll
-      for (int ni = 0; ni < NTL; ++ni)
-#pragma unroll
-        for (int kq = 0; kq < KB; ++kq) {
-          const int n = wc * WN + ni * 32 + l32;
-          uint32_t v[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int j = kq * 16 + lh * 8 + e;
-            v[e] = __builtin_amdgcn_raw_buffer_load_b16(brs, j < a.r ? (n * a.r + j) * 2 : kOutOfRange, 0, 0);
-          }
-          bfr[ni][kq] = make_uint4((v[0] & 0xFFFFu) | (v[1] << 16), (v[2] & 0xFFFFu) | (v[3] << 16),
-                                   (v[4] & 0xFFFFu) | (v[5] << 16), (v[6] & 0xFFFFu) | (v[7] << 16));
-        }
-    }
-  };
-  if constexpr (EARLY) load_lora();
 
   // ---- copies.  One copy instruction moves 16 rows x 64 bytes (64 lanes x
   // 16 bytes) into 1 KB of LDS; lane i fills LDS chunk i of it, so it fetches
@@ -164,22 +138,33 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
   // exactly the tile's valid rows (rows past M or N read as zeros); a chunk
   // past K gets an out-of-range offset (zeros as well), and so do all copies
   // of the slabs past the last one, which land in stages that are not read
-  // again.  Wave w copies 16-row blocks w, w + 4, w + 8, w + 12 of x (j < 4)
-  // and of W (j >= 4).
+  // again.  Wave w copies 16-row blocks w, w + 4, w + 8, w + 12 of the x side
+  // (j < 4) and of the W side (j >= 4) of every slab.
   const i32x4_t xr = make_rsrc_raw(a.x + (size_t)m0 * K, (uint32_t)min(BM, M - m0) * K * 2u);
   const i32x4_t wrs = make_rsrc_raw(a.W + (size_t)n0 * K, (uint32_t)min(BN, N - n0) * K * 2u);
+  const i32x4_t tsr = make_rsrc_raw(g.ts + (size_t)m0 * 2 * RP, (uint32_t)min(BM, M - m0) * 2 * RP * 2u);
+  const i32x4_t bpr = make_rsrc_raw(g.bp + (size_t)n0 * RP, (uint32_t)min(BN, N - n0) * RP * 2u);
   const int row_bytes = K * 2;
   const int cg = (lane & 3) ^ ((lane >> 4) & 3);  // global chunk fetched by this lane
   const int rl = lane >> 2;                       // row within the 16-row copy
-  auto dma_one = [&](uint4* st, int kt, int j) __attribute__((always_inline)) {
-    const int k0 = kt * BK;
-    const bool kv = k0 + cg * 8 < K;
-    const int kofs = k0 * 2 + cg * 16;
+  // Copy j of slab kt.  MAIN: kt is known to be a slab of h and W (the
+  // steady state); otherwise kt may also be a LoRA slab or past the end, and
+  // source and offset are selected without branches.
+  auto dma_one = [&](auto MAIN, uint4* st, int kt, int j) __attribute__((always_inline)) {
     const int ci = wave + 4 * (j & 3);
-    if (j < 4)
-      dma16(xr, st + XOFF + ci * 64, kv ? (ci * 16 + rl) * row_bytes + kofs : kOutOfRange);
-    else
-      dma16(wrs, st + WOFF + ci * 64, kv ? (ci * 16 + rl) * row_bytes + kofs : kOutOfRange);
+    const int row = ci * 16 + rl;
+    uint4* dst = st + (j < 4 ? XOFF : WOFF) + ci * 64;
+    const int k0 = kt * BK;
+    const int off_main = k0 + cg * 8 < K ? row * row_bytes + k0 * 2 + cg * 16 : kOutOfRange;
+    if constexpr (decltype(MAIN)::value) {
+      dma16(j < 4 ? xr : wrs, dst, off_main);
+    } else {
+      const bool is_main = kt < nkt, is_lora = LS > 0 && kt >= nkt && kt < nsl;
+      const int k = (kt - nkt) * BK + cg * 8;  // k within [0, 2 RP) in a LoRA slab
+      const int off_lora = j < 4 ? (row * 2 * RP + k) * 2 : (row * RP + (k & (RP > 0 ? RP - 1 : 0))) * 2;
+      const int off = is_main ? off_main : (is_lora ? off_lora : kOutOfRange);
+      dma16(is_main ? (j < 4 ? xr : wrs) : (j < 4 ? tsr : bpr), dst, off);
+    }
   };
 
   f32x16_t acc[MT][NTL];
@@ -207,10 +192,10 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
 
   // k-step S of slab kt (stage `cur`): MFMAs on Fc, reads of the next k-step
   // into Fn (k-step 1 of this slab, or k-step 0 of slab kt + 1 from `nxt`),
-  // and four copies: k-step 0 finishes slab kt + 3 (W blocks, into `c0dst`),
-  // k-step 1 starts slab kt + 4 (x blocks, into `cur`, free after the
-  // barrier).
-  auto kstep = [&](auto S, const Frag& Fc, Frag& Fn, const uint4* rs, uint4* ddst, int dkt)
+  // and four copies: k-step 0 finishes slab kt + 3 (W side, into the stage
+  // of slab kt - 1), k-step 1 starts slab kt + 4 (x side, into `cur`, free
+  // after the barrier).
+  auto kstep = [&](auto S, auto MAIN, const Frag& Fc, Frag& Fn, const uint4* rs, uint4* ddst, int dkt)
       __attribute__((always_inline)) {
     constexpr int s = decltype(S)::value;
 #pragma unroll
@@ -218,122 +203,140 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
       const int mi = m / NTL, ni = m % NTL;
       acc[mi][ni] = mfma32(Fc.w[ni], Fc.x[mi], acc[mi][ni]);
       if (m < NTL + MT) read_one(Fn, rs, s ^ 1, m);
-      if (m >= 8 && (m & 1) == 1) dma_one(ddst, dkt, (s == 0 ? 4 : 0) + ((m - 9) >> 1));
+      if (m >= 8 && (m & 1) == 1) dma_one(MAIN, ddst, dkt, (s == 0 ? 4 : 0) + ((m - 9) >> 1));
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  auto slab = [&](uint4* cur, uint4* nxt, uint4* prev, int kt) __attribute__((always_inline)) {
-    kstep(IC<0>{}, F0, F1, cur, prev, kt + 3);
+  auto slab = [&](auto MAIN, uint4* cur, uint4* nxt, uint4* prev, int kt) __attribute__((always_inline)) {
+    kstep(IC<0>{}, MAIN, F0, F1, cur, prev, kt + 3);
     // slab kt + 1 must have landed: only the copies of slabs kt + 2 and kt + 3
     // (2 x DPW per wave) may still be in flight
     wait_vm_lds_barrier<2 * DPW>();
-    kstep(IC<1>{}, F1, F0, nxt, cur, kt + 4);
+    kstep(IC<1>{}, MAIN, F1, F0, nxt, cur, kt + 4);
   };
 
-  // prologue: slabs 0..2 and the x half of slab 3
+  // prologue: slabs 0..2 and the x side of slab 3
 #pragma unroll
-  for (int j = 0; j < DPW; ++j) dma_one(sm[0], 0, j);
+  for (int j = 0; j < DPW; ++j) dma_one(IC<0>{}, sm[0], 0, j);
 #pragma unroll
-  for (int j = 0; j < DPW; ++j) dma_one(sm[1], 1, j);
+  for (int j = 0; j < DPW; ++j) dma_one(IC<0>{}, sm[1], 1, j);
 #pragma unroll
-  for (int j = 0; j < DPW; ++j) dma_one(sm[2], 2, j);
+  for (int j = 0; j < DPW; ++j) dma_one(IC<0>{}, sm[2], 2, j);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) dma_one(sm[3], 3, j);
+  for (int j = 0; j < 4; ++j) dma_one(IC<0>{}, sm[3], 3, j);
   wait_vm_lds_barrier<2 * DPW + 4>();
 #pragma unroll
   for (int r = 0; r < NTL + MT; ++r) read_one(F0, sm[0], 0, r);
-  for (int kt = 0; kt < nkt; kt += NS) {
-    slab(sm[0], sm[1], sm[3], kt);
-    if (kt + 1 < nkt) slab(sm[1], sm[2], sm[0], kt + 1);
-    if (kt + 2 < nkt) slab(sm[2], sm[3], sm[1], kt + 2);
-    if (kt + 3 < nkt) slab(sm[3], sm[0], sm[2], kt + 3);
+  // steady state: every copy issued by slabs kt .. kt + 3 (slabs up to kt + 7)
+  // is a copy of h and W
+  int kt = 0;
+  for (; kt + 2 * NS <= nkt; kt += NS) {
+    slab(IC<1>{}, sm[0], sm[1], sm[3], kt);
+    slab(IC<1>{}, sm[1], sm[2], sm[0], kt + 1);
+    slab(IC<1>{}, sm[2], sm[3], sm[1], kt + 2);
+    slab(IC<1>{}, sm[3], sm[0], sm[2], kt + 3);
   }
-  wait_vm_lds_barrier<0>();  // every copy has landed and every wave is done with the ring
+  for (; kt < nkt; kt += NS) {
+    slab(IC<0>{}, sm[0], sm[1], sm[3], kt);
+    if (kt + 1 < nkt) slab(IC<0>{}, sm[1], sm[2], sm[0], kt + 1);
+    if (kt + 2 < nkt) slab(IC<0>{}, sm[2], sm[3], sm[1], kt + 2);
+    if (kt + 3 < nkt) slab(IC<0>{}, sm[3], sm[0], sm[2], kt + 3);
+  }
 
   // ---------------------------------------------------------------- epilogue
-  if constexpr (!EARLY) load_lora();
-  float* red = reinterpret_cast<float*>(sm[0]);  // [2][BM][4]: per wave column, (max, sum) off / on
+  // acc[mi][ni][4 i + e] holds z[m0 + wr*128 + mi*32 + l32][n0 + wc*128 + ni*32 + 8 i + 4 lh + e].
+  // Per row block mi: (max, sum exp) over this lane's 64 logits, merged with
+  // the lane holding the row's other 64 (lane ^ 32).  For a ragged
+  // vocabulary the logits of columns past N are taken as -inf (branch-free).
+  // The lane holding the sampled token's column records its logit.
   const int wcol0 = n0 + wc * WN;
-
-  // acc[mi][ni][4 i + e] holds z_off[m0 + wr*128 + mi*32 + l32][wcol0 + ni*32 + 8 i + 4 lh + e].
-  // Row block mi at a time, on a register copy z of its 64 logits per lane:
-  // statistics of the LoRA-off logits; then z += D, D = s*T*B^T of the row
-  // block by MFMA (A operand = rows of [B | B], B operand = rows of
-  // [hi | lo], zero accumulator), and the statistics of the LoRA-on logits.
-  // With B = 0 or s = 0, D is exactly zero.  For a ragged vocabulary the
-  // logits of columns past N are set to -inf (branch-free), so the
-  // statistics need no column test.
-  auto row_stats = [&](const float* z, int mi, int slot) __attribute__((always_inline)) {
-    const int rloc = wr * WM + mi * 32 + l32;
-    float mx = -INFINITY;
-#pragma unroll
-    for (int q = 0; q < NTL * 16; ++q) mx = fmaxf(mx, z[q]);
-    // the lane holding the sampled token's column records its logit
-    const int rel = tk[mi] - wcol0 - 4 * lh;  // column offset within this lane's half
-    if (rel >= 0 && rel < WN && ((rel >> 2) & 1) == 0) {
-      float v = 0.f;
-#pragma unroll
-      for (int q = 0; q < NTL * 16; ++q) v = ((q >> 4) * 32 + 8 * ((q & 15) >> 2) + (q & 3) == rel) ? z[q] : v;
-      g.zt[(size_t)(m0 + rloc) * 2 + (slot >> 1)] = v;
-    }
-    float sm_ = 0.f;
-    if (mx != -INFINITY) {
-#pragma unroll
-      for (int q = 0; q < NTL * 16; ++q) sm_ += exp_e(z[q] - mx);
-    }
-    const float mo = __shfl_xor(mx, 32);
-    const float so = __shfl_xor(sm_, 32);
-    lse_merge(mx, sm_, mo, so);
-    if (lh == 0) {
-      red[(wc * BM + rloc) * 4 + slot] = mx;
-      red[(wc * BM + rloc) * 4 + slot + 1] = sm_;
-    }
-  };
-  auto mask_tail = [&](float* z) __attribute__((always_inline)) {
-    if constexpr (RAGGED) {
-      const int lim = N - wcol0 - 4 * lh;  // columns q of this lane with offset >= lim are past N
-#pragma unroll
-      for (int q = 0; q < NTL * 16; ++q)
-        z[q] = (q >> 4) * 32 + 8 * ((q & 15) >> 2) + (q & 3) < lim ? z[q] : -INFINITY;
-    }
-  };
-
-  // (scheduling barriers keep the row blocks apart, so that only one row
-  // block's logits are held in VGPRs at a time)
-#pragma unroll
-  for (int mi = 0; mi < MT; ++mi) {
-    __builtin_amdgcn_sched_barrier(0);
+  auto row_stats = [&](int mi, int pass, float& mx, float& sm_) __attribute__((always_inline)) {
     float z[NTL * 16];
 #pragma unroll
     for (int ni = 0; ni < NTL; ++ni)
 #pragma unroll
       for (int k = 0; k < 16; ++k) z[ni * 16 + k] = acc[mi][ni][k];
-    mask_tail(z);
-    row_stats(z, mi, 0);  // LoRA off
-    if constexpr (RP > 0) {
+    if constexpr (RAGGED) {
+      const int lim = N - wcol0 - 4 * lh;  // offsets at or past lim are past N
 #pragma unroll
-      for (int ni = 0; ni < NTL; ++ni) {
-        f32x16_t d;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) d[e] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KT; ++ks) d = mfma32(bfr[ni][ks % KB], tf[mi][ks], d);
-#pragma unroll
-        for (int k = 0; k < 16; ++k) z[ni * 16 + k] += d[k];
-      }
-      mask_tail(z);
+      for (int q = 0; q < NTL * 16; ++q)
+        z[q] = (q >> 4) * 32 + 8 * ((q & 15) >> 2) + (q & 3) < lim ? z[q] : -INFINITY;
     }
-    row_stats(z, mi, 2);  // LoRA on
+    mx = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < NTL * 16; ++q) mx = fmaxf(mx, z[q]);
+    const int rel = tk[mi] - wcol0 - 4 * lh;  // column offset within this lane's half
+    if (rel >= 0 && rel < WN && ((rel >> 2) & 1) == 0) {
+      float v = 0.f;
+#pragma unroll
+      for (int q = 0; q < NTL * 16; ++q) v = ((q >> 4) * 32 + 8 * ((q & 15) >> 2) + (q & 3) == rel) ? z[q] : v;
+      g.zt[(size_t)(m0 + wr * WM + mi * 32 + l32) * 2 + pass] = v;
+    }
+    sm_ = 0.f;
+    if (mx != -INFINITY) {
+      // e^(z - mx) = 2^(z log2 e - mx log2 e)
+      const float mxs = mx * kLog2e;
+#pragma unroll
+      for (int q = 0; q < NTL * 16; ++q) sm_ += __builtin_amdgcn_exp2f(fmaf(z[q], kLog2e, -mxs));
+    }
+    const float mo = __shfl_xor(mx, 32);
+    const float so = __shfl_xor(sm_, 32);
+    lse_merge(mx, sm_, mo, so);
+  };
+
+  float st_off[MT][2], st_on[MT][2];
+#pragma unroll
+  for (int mi = 0; mi < MT; ++mi) {
     __builtin_amdgcn_sched_barrier(0);
+    row_stats(mi, 0, st_off[mi][0], st_off[mi][1]);  // LoRA off
+  }
+  if constexpr (LS > 0) {
+    // The LoRA slabs nkt .. nkt + LS - 1 (stage (nkt + q) % NS; the last main
+    // slab already read the first k-step of slab nkt into F0).
+#pragma unroll
+    for (int q = 0; q < LS; ++q) {
+      const int kq = nkt + q;
+      slab(IC<0>{}, sm[kq % NS], sm[(kq + 1) % NS], sm[(kq + NS - 1) % NS], kq);
+    }
+#pragma unroll
+    for (int mi = 0; mi < MT; ++mi) {
+      __builtin_amdgcn_sched_barrier(0);
+      row_stats(mi, 1, st_on[mi][0], st_on[mi][1]);  // LoRA on
+    }
+  } else {
+    // no adapter: the LoRA-on logits are the LoRA-off logits
+#pragma unroll
+    for (int mi = 0; mi < MT; ++mi) {
+      st_on[mi][0] = st_off[mi][0];
+      st_on[mi][1] = st_off[mi][1];
+      const int rel = tk[mi] - wcol0 - 4 * lh;
+      if (rel >= 0 && rel < WN && ((rel >> 2) & 1) == 0) {
+        const size_t zi = (size_t)(m0 + wr * WM + mi * 32 + l32) * 2;
+        g.zt[zi + 1] = g.zt[zi];
+      }
+    }
+  }
+  wait_vm_lds_barrier<0>();  // every copy has landed and every wave is done with the ring
+
+  // the two waves of a row block column pair merge their row statistics
+  float* red = reinterpret_cast<float*>(sm[0]);  // [2][BM][4]
+  if (lh == 0) {
+#pragma unroll
+    for (int mi = 0; mi < MT; ++mi) {
+      const int rloc = wr * WM + mi * 32 + l32;
+      *reinterpret_cast<float4*>(red + (wc * BM + rloc) * 4) =
+          make_float4(st_off[mi][0], st_off[mi][1], st_on[mi][0], st_on[mi][1]);
+    }
   }
   __syncthreads();
   {
     const int row = m0 + t;
     if (t < BM && row < M) {
-      float mo = red[t * 4 + 0], so = red[t * 4 + 1];
-      float mn = red[t * 4 + 2], sn = red[t * 4 + 3];
-      lse_merge(mo, so, red[(BM + t) * 4 + 0], red[(BM + t) * 4 + 1]);
-      lse_merge(mn, sn, red[(BM + t) * 4 + 2], red[(BM + t) * 4 + 3]);
+      const float4 p0 = *reinterpret_cast<const float4*>(red + t * 4);
+      const float4 p1 = *reinterpret_cast<const float4*>(red + (BM + t) * 4);
+      float mo = p0.x, so = p0.y, mn = p0.z, sn = p0.w;
+      lse_merge(mo, so, p1.x, p1.y);
+      lse_merge(mn, sn, p1.z, p1.w);
       g.part[(size_t)row * g.ntn + tni] = make_float4(mo, so, mn, sn);
     }
   }
@@ -341,7 +344,7 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
 
 // T = h A^T for 16 rows per workgroup; the 8 waves split K.  Writes the bf16
 // hi and lo parts of s*T: ts[row][j] = hi, ts[row][RP + j] = lo (zero for
-// j >= r), the B operand rows of the scoring GEMM's LoRA update.
+// j >= r), the x-side rows of the scoring GEMM's LoRA slabs.
 constexpr int T_WAVES = 8;
 constexpr int T_UNROLL = 4;
 
@@ -398,12 +401,30 @@ __global__ __launch_bounds__(T_WAVES * 64) void score_t_kernel(ScoreGemmArgs g) 
   }
 }
 
+// B zero padded to RP columns (bp[n][j] = B[n][j] for j < r, else 0): the
+// W-side rows of the scoring GEMM's LoRA slabs, 16-byte aligned for its
+// copies whatever r is.
+template <int RP>
+__global__ __launch_bounds__(256) void score_bpad_kernel(ScoreGemmArgs g) {
+  const LinearArgs& a = g.lin;
+  const size_t total = (size_t)a.N * RP;
+  for (size_t e = blockIdx.x * 256 + threadIdx.x; e < total; e += (size_t)gridDim.x * 256) {
+    const int n = (int)(e / RP), j = (int)(e % RP);
+    g.bp[e] = j < a.r ? a.B[(size_t)n * a.r + j] : (uint16_t)0;
+  }
+}
+
 template <int RP>
 hipError_t launch_rp(const ScoreGemmArgs& s, hipStream_t stream) {
   const bool ragged = s.lin.N % BN != 0;
   if constexpr (RP > 0) {
     hipLaunchKernelGGL((score_t_kernel<RP>), dim3((s.lin.M + 15) / 16), dim3(T_WAVES * 64), 0, stream, s);
-    const hipError_t e = hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const size_t total = (size_t)s.lin.N * RP;
+    const unsigned blocks = (unsigned)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
+    hipLaunchKernelGGL((score_bpad_kernel<RP>), dim3(blocks), dim3(256), 0, stream, s);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   if (ragged)

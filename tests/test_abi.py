@@ -109,15 +109,16 @@ def test_score_rejects(kw, code):
 def _ws(M, V):
     # one float4 partial per (row, 256-column tile), two floats per row (the
     # gathered token logits), then, 16-byte aligned, 2 x 64 bf16 per row (the hi
-    # and lo parts of s * h A^T at the largest rank)
+    # and lo parts of s * h A^T at the largest rank) and 64 bf16 per vocabulary
+    # row (B zero padded to the padded rank)
     tiles = (V + 255) // 256
     zt_end = M * tiles * 16 + M * 8
-    return ((zt_end + 15) // 16) * 16 + M * 2 * 64 * 2
+    return ((zt_end + 15) // 16) * 16 + M * 2 * 64 * 2 + V * 64 * 2
 
 
 def test_score_workspace_bytes():
-    assert H.hydra_score_workspace_bytes(2048, 32000) == _ws(2048, 32000) == 4636672
-    assert H.hydra_score_workspace_bytes(3, 257) == _ws(3, 257) == 896
+    assert H.hydra_score_workspace_bytes(2048, 32000) == _ws(2048, 32000) == 4636672 + 32000 * 128
+    assert H.hydra_score_workspace_bytes(3, 257) == _ws(3, 257) == 896 + 257 * 128
     out = ctypes.c_size_t(0)
     assert H.lib().hydra_score_workspace_bytes(0, 10, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
     assert H.lib().hydra_score_workspace_bytes(10, 10, None) == H.HYDRA_ERR_NULL

@@ -38,9 +38,12 @@ def _score(c, device, B=None, ids=None, s=None, with_lse=True):
 
 SCORE_SHAPES = [
     # (n_seq, seq_len, K, V, r): ragged row tiles, ragged vocabulary tiles
-    # (V = 300 leaves a whole wave's half-tile past V), tiny V, every rank class.
+    # (V = 300 leaves a whole wave's half-tile past V), tiny V, every padded
+    # rank (0, 16, 32, 64) with and without a ragged last column tile, several
+    # 256-row tiles, K tails inside a 32-wide slab.
     (2, 100, 64, 1000, 8), (1, 7, 72, 300, 16), (3, 50, 128, 7, 1), (2, 64, 512, 2048, 64),
     (1, 129, 256, 513, 0), (4, 40, 1024, 4000, 33),
+    (3, 200, 96, 1280, 24), (2, 256, 64, 512, 16), (1, 300, 40, 768, 0), (2, 150, 200, 777, 20),
 ]
 
 
@@ -89,6 +92,22 @@ def test_score_deterministic(dev):
     b = _score(c, dev)
     for k in ("lp_on", "lp_off", "kl", "reward"):
         assert np.array_equal(a[k], b[k])
+
+
+def test_score_workspace_contents_do_not_matter(dev):
+    """A workspace full of NaN bit patterns gives bit-identical results."""
+    import torch
+    say("score dirty workspace")
+    c = WL.gen_score_head(2400, 3, 90, 160, 1100, 24)
+    clean = _score(c, dev)
+    ws = torch.full((H.hydra_score_workspace_bytes(c.M, c.V),), 0xFF, dtype=torch.uint8, device=dev)
+    out = {k: torch.full((c.M,), float("nan"), device=dev) for k in ("lp_on", "lp_off", "kl")}
+    H.hydra_score(dev_bf16(c.h, dev), dev_bf16(c.W_lm, dev), dev_bf16(c.A, dev), dev_bf16(c.B, dev), c.s,
+                  torch.from_numpy(c.ids.astype(np.int32)).to(dev), dev_bf16(c.w_rm, dev), c.n_seq, c.seq_len,
+                  out["lp_on"], out["lp_off"], out["kl"], workspace=ws)
+    torch.cuda.synchronize()
+    for k in ("lp_on", "lp_off", "kl"):
+        assert np.array_equal(host(out[k]), clean[k]), k
 
 
 def test_two_head_score_full_size_sampled_rows(dev):
