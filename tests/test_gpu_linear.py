@@ -28,7 +28,7 @@ SHAPES = [
     # (M, K, N, r): decode kernel (M <= 16) and MFMA GEMM (M > 16), ragged
     # rows / columns / K tails, every padded-rank class, rank 0.
     (1, 64, 40, 8), (3, 520, 300, 16), (4, 4096, 256, 16), (16, 512, 512, 8), (16, 72, 1000, 64),
-    (5, 136, 33, 1), (7, 256, 20, 0), (2, 8, 17, 33),
+    (5, 136, 33, 1), (7, 256, 20, 0), (2, 8, 17, 33), (6, 520, 300, 64), (8, 4104, 130, 32), (12, 1032, 77, 16),
     (17, 64, 256, 8), (33, 520, 300, 16), (128, 512, 256, 16), (130, 72, 513, 1), (257, 1024, 700, 33),
     (200, 64, 256, 0), (64, 128, 96, 64), (300, 2048, 1200, 17), (129, 8, 255, 16),
 ]
