@@ -206,8 +206,10 @@ def main():
     else:
         roof = dict(bound="mfma", achieved=dcomp["tflops"], peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
                     frac=dcomp["frac"])
-    roof["kernel"] = {"prefill": "lora_gemm_kernel<16,false>", "score": "lora_gemm_kernel<16,true>+combine",
-                      "decode": "lora_gemv_kernel<16,32,16,8> (grouped q/k/v/o)"}[dom]
+    roof["kernel"] = {"prefill": "lora_gemm_kernel<16> (4 copy + 4 MFMA waves, 128x256 tiles)",
+                      "score": "score_t_kernel<16> + score_bpad_kernel<16> + score_gemm_kernel<16,false> + "
+                               "score_combine_kernel",
+                      "decode": "lora_gemv_dot_kernel<4,8,2> (grouped q/k/v/o)"}[dom]
     tr = committed_traffic(dom)
     roof["traffic"] = None if tr is None else tr["bytes_per_launch"]
     if tr is not None:
