@@ -7,3 +7,8 @@ from .hydra_oracle import (  # noqa: F401
     reward_ref,
     score_head_ref,
 )
+from .ppo_oracle import (  # noqa: F401
+    gae_ref,
+    ppo_rewards_ref,
+    value_head_ref,
+)

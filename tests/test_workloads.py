@@ -48,3 +48,15 @@ def test_distribution_scales():
 def test_shared_activation_per_width():
     cases = WL.gen_linears(3, 8, WL.PREFILL_PROJ[:2] + WL.PREFILL_PROJ[-1:], 4)
     assert cases[0].x is cases[1].x and cases[2].x.shape == (8, 11008)
+
+
+def test_advantage_generator():
+    a = WL.gen_advantages(5, 2, 16, 64, start=3)
+    b = WL.gen_advantages(5, 2, 16, 64, start=3)
+    assert a.h.shape == (32, 64) and a.w_v.shape == (64,) and a.kl.shape == (32,) and a.reward.shape == (2,)
+    assert a.kl.dtype == np.float32 and a.reward.dtype == np.float32 and a.M == 32 and a.K == 64
+    for k in ("kl", "reward", "h", "w_v"):
+        assert np.array_equal(getattr(a, k), getattr(b, k))
+    big = WL.gen_advantages(5, 4, 512, 256)
+    assert abs(big.kl.std() - 0.1) < 0.005
+    assert WL.WORKLOADS["ppo_advantages"]["seed"] == 5

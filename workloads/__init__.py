@@ -24,7 +24,11 @@ weights are not available, so Gaussian stand-ins are drawn):
   to bf16;
 * activations ~ N(0, 1); base weights and LoRA-down ~ N(0, 1/K) with the
   layer's own K; LoRA-up ~ N(0, 1/r); the reward head ~ N(0, 1/K);
-* token ids uniform in [0, V), drawn last.
+* token ids uniform in [0, V), drawn last;
+* the PPO advantage step: critic hidden states ~ N(0, 1), value head
+  ~ N(0, 1/K), per-token KL estimates ~ N(0, 0.1^2) (the spread of lp_on -
+  lp_off when the LoRA-on and LoRA-off logits differ by N(0, 0.1^2) noise),
+  sequence rewards ~ N(0, 1).
 """
 from __future__ import annotations
 
@@ -41,6 +45,8 @@ __all__ = [
     "gen_linears",
     "gen_logits",
     "gen_score_head",
+    "AdvantageCase",
+    "gen_advantages",
     "WORKLOADS",
     "DECODE_PROJ",
     "PREFILL_PROJ",
@@ -202,13 +208,50 @@ def gen_score_head(seed: int, n_seq: int, seq_len: int, K: int, V: int, r: int, 
     return ScoreCase(h, W_lm, A, B, w_rm, ids, float(s), n_seq, seq_len)
 
 
-# The five workloads, by what they are.  "seed" doubles as the workload index.
+@dataclasses.dataclass
+class AdvantageCase:
+    """PPO advantage-step input: per-token KL kl[M] and sequence rewards reward[n_seq] (fp32), the critic's
+    hidden states h[M x K] and value head w_v[K] (bf16); M = n_seq * seq_len, sequence-major."""
+    kl: np.ndarray
+    reward: np.ndarray
+    h: np.ndarray
+    w_v: np.ndarray
+    n_seq: int
+    seq_len: int
+    start: int
+    beta: float
+    gamma: float
+    lam: float
+
+    @property
+    def M(self) -> int:
+        return self.n_seq * self.seq_len
+
+    @property
+    def K(self) -> int:
+        return self.h.shape[1]
+
+
+def gen_advantages(seed: int, n_seq: int, seq_len: int, K: int, start: int = 0, beta: float = 0.02,
+                   gamma: float = 1.0, lam: float = 0.95) -> AdvantageCase:
+    """Draw order: h, w_v, kl, reward."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    M = n_seq * seq_len
+    h = _normal_bf16(rng, (M, K), 1.0)
+    w_v = _normal_bf16(rng, (K,), 1.0 / np.sqrt(K))
+    kl = (rng.standard_normal(M) * 0.1).astype(np.float32)
+    reward = rng.standard_normal(n_seq).astype(np.float32)
+    return AdvantageCase(kl, reward, h, w_v, n_seq, seq_len, start, float(beta), float(gamma), float(lam))
+
+
+# The workloads, by what they are.  "seed" doubles as the workload index.
 WORKLOADS = {
     "single_linear": dict(seed=0, M=16, K=512, N=512, r=8, s=2.0),
     "score_logits": dict(seed=1, n_seq=4, seq_len=128, V=32000),
     "decode_qkvo": dict(seed=2, M=4, proj=DECODE_PROJ, r=16, s=2.0),
     "prefill_layer": dict(seed=3, M=2048, proj=PREFILL_PROJ, r=16, s=2.0),
     "two_head_score": dict(seed=4, n_seq=4, seq_len=512, K=4096, V=32000, r=16, s=2.0),
+    "ppo_advantages": dict(seed=5, n_seq=4, seq_len=512, K=4096, start=0, beta=0.02, gamma=1.0, lam=0.95),
 }
 
 
@@ -223,4 +266,6 @@ def make(name: str, M: Optional[int] = None):
         return gen_linears(w["seed"], M or w["M"], w["proj"], w["r"], w["s"])
     if name == "two_head_score":
         return gen_score_head(w["seed"], w["n_seq"], w["seq_len"], w["K"], w["V"], w["r"], w["s"])
+    if name == "ppo_advantages":
+        return gen_advantages(w["seed"], w["n_seq"], w["seq_len"], w["K"], w["start"], w["beta"], w["gamma"], w["lam"])
     raise KeyError(name)
