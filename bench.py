@@ -18,7 +18,9 @@ in HBM when the timed region starts.  Each kernel launch is bracketed by HIP
 events on the stream it runs on.  The standalone scoring epilogue over
 materialised logits (hydra_score_logits, 512 x 32000) is timed separately
 (rotating four input sets so that the 256 MB last-level cache does not serve
-it) and reported under "aux"; it is not part of the step.
+it) and reported under "aux"; it is not part of the step.  So is the PPO
+advantage step that follows scoring (hydra_value_head on the 2048 critic
+hidden states, then hydra_ppo_advantages).
 
 Prints one JSON line.  ``--gpus`` above 1 is refused: this path is built and
 measured on a single GPU.
@@ -56,7 +58,8 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--parts", default="decode,prefill,score",
-                   help="comma list of step parts to run (profiling aid; the metric needs all three)")
+                   help="comma list of step parts to run (profiling aid; the metric needs all three; "
+                        "'advantages' adds the PPO advantage step, which is also timed under aux)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-aux", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU oracle sample")
@@ -130,6 +133,22 @@ def main():
         fl = lin_flops(M, sc.K, sc.V, sc.r) + 2.0 * sc.n_seq * sc.K
         by = 2.0 * (M * sc.K + sc.V * sc.K + sc.r * sc.K + sc.V * sc.r + sc.K) + 4.0 * M + 3 * 4.0 * M + 4.0 * sc.n_seq
         launches.append(("score", "clm_rm_head", fn, fl, by))
+    if "advantages" in parts:
+        # the critic's value head on every token, then per-token rewards, GAE advantages and returns
+        adv = host["advantages"] = WL.make("ppo_advantages")
+        Ma = adv.M
+        ha, wv = bf(adv.h), bf(adv.w_v)
+        kl_a = torch.from_numpy(adv.kl).to(dev)
+        rw_a = torch.from_numpy(adv.reward).to(dev)
+        vals = torch.empty(Ma, device=dev)
+        r_out, a_out, ret_out = (torch.empty(Ma, device=dev) for _ in range(3))
+        launches.append(("advantages", "value_head", (lambda: H.hydra_value_head(ha, wv, vals)),
+                         2.0 * Ma * adv.K, 2.0 * Ma * adv.K + 2.0 * adv.K + 4.0 * Ma))
+        launches.append(("advantages", "gae",
+                         (lambda: H.hydra_ppo_advantages(kl_a, rw_a, vals, adv.n_seq, adv.seq_len, a_out, ret_out,
+                                                         rewards=r_out, start=adv.start, beta=adv.beta,
+                                                         gamma=adv.gamma, lam=adv.lam)),
+                         10.0 * Ma, 4.0 * Ma * 2 + 4.0 * adv.n_seq + 4.0 * Ma * 3))
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
 
@@ -175,7 +194,7 @@ def main():
     avg = dur.mean(0)
 
     comp = {}
-    for part in ("decode", "prefill", "score"):
+    for part in ("decode", "prefill", "score", "advantages"):
         idx = [i for i, l in enumerate(launches) if l[0] == part]
         if not idx:
             continue
@@ -184,7 +203,7 @@ def main():
         by = sum(launches[i][4] for i in idx)
         d = dict(launches=len(idx), us=round(t * 1e6, 2), tflops=round(fl / t / 1e12, 2),
                  gbps=round(by / t / 1e9, 1))
-        if part == "decode":
+        if part in ("decode", "advantages"):
             d["bound"] = "hbm"
             d["frac"] = round(by / t / 1e9 / PEAK_HBM_GBPS, 4)
         else:
@@ -209,7 +228,8 @@ def main():
     roof["kernel"] = {"prefill": "lora_gemm_kernel<16> (4 copy + 4 MFMA waves, 128x256 tiles)",
                       "score": "score_t_kernel<16> + score_bpad_kernel<16> + score_gemm_kernel<16,false> + "
                                "score_combine_kernel",
-                      "decode": "lora_gemv_dot_kernel<4,8,2> (grouped q/k/v/o)"}[dom]
+                      "decode": "lora_gemv_dot_kernel<4,8,2> (grouped q/k/v/o)",
+                      "advantages": "value_head_kernel + gae_kernel"}[dom]
     tr = committed_traffic(dom)
     roof["traffic"] = None if tr is None else tr["bytes_per_launch"]
     if tr is not None:
@@ -243,7 +263,8 @@ def main():
     }
 
     if not args.no_aux:
-        out["aux"] = {"score_logits": bench_score_logits(torch, H, WL, dev)}
+        out["aux"] = {"score_logits": bench_score_logits(torch, H, WL, dev),
+                      "ppo_advantages": bench_advantages(torch, H, WL, dev)}
 
     if not args.no_cpu_baseline:
         hi = None
@@ -319,6 +340,51 @@ def bench_score_logits(torch, H, WL, dev, iters=20):
     return dict(rows=M, vocab=V, us=round(us, 2), gbps=round(by / us / 1e3, 1),
                 frac_hbm=round(by / us / 1e3 / PEAK_HBM_GBPS, 4), tokens_per_s=round(M / us * 1e6, 1),
                 note="median of per-launch HIP events over 4 rotating input sets (1.05 GB > last-level cache)")
+
+
+def bench_advantages(torch, H, WL, dev, iters=30):
+    """The PPO advantage step after scoring: the critic value head on all 2048 tokens (K = 4096), then the
+    per-token rewards, GAE advantages and returns (4 sequences x 512 tokens)."""
+    adv = WL.make("ppo_advantages")
+    M, K = adv.M, adv.K
+    h = torch.from_numpy(adv.h.view(np.int16)).to(dev)
+    w = torch.from_numpy(adv.w_v.view(np.int16)).to(dev)
+    kl = torch.from_numpy(adv.kl).to(dev)
+    rw = torch.from_numpy(adv.reward).to(dev)
+    vals = torch.empty(M, device=dev)
+    r_out, a_out, ret_out = (torch.empty(M, device=dev) for _ in range(3))
+
+    def vh():
+        H.hydra_value_head(h, w, vals)
+
+    def gae():
+        H.hydra_ppo_advantages(kl, rw, vals, adv.n_seq, adv.seq_len, a_out, ret_out, rewards=r_out, start=adv.start,
+                               beta=adv.beta, gamma=adv.gamma, lam=adv.lam)
+
+    # launches queued back to back, one event pair per launch on the launch stream, one sync at the end
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        vh()
+        gae()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(iters)]
+    for i in range(iters):
+        ev[i][0].record(stream)
+        vh()
+        ev[i][1].record(stream)
+        ev[i][2].record(stream)
+        gae()
+        ev[i][3].record(stream)
+    torch.cuda.synchronize()
+    t_vh = float(np.median([e[0].elapsed_time(e[1]) for e in ev])) * 1e3
+    t_gae = float(np.median([e[2].elapsed_time(e[3]) for e in ev])) * 1e3
+    vh_bytes = 2.0 * M * K + 2.0 * K + 4.0 * M
+    gae_bytes = 4.0 * M * 2 + 4.0 * adv.n_seq + 4.0 * M * 3
+    return dict(tokens=M, K=K, value_head_us=round(t_vh, 2), value_head_gbps=round(vh_bytes / t_vh / 1e3, 1),
+                value_head_frac_hbm=round(vh_bytes / t_vh / 1e3 / PEAK_HBM_GBPS, 4), gae_us=round(t_gae, 2),
+                gae_bytes=int(gae_bytes),
+                note="median of per-launch HIP events over back-to-back launches; the 16 MB of hidden states "
+                     "stay in the last-level cache between iterations")
 
 
 def cpu_baseline(target_s: float, host_inputs=None):

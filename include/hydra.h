@@ -165,6 +165,48 @@ hydra_status hydra_score_logits(const float* logits_on, const float* logits_off,
                                 int64_t M, int64_t V, float* lp_on, float* lp_off, float* kl,
                                 float* lse_on, float* lse_off, int32_t* err_flag, void* stream);
 
+/*
+ * hydra_value_head -- the critic's scalar head on every token row.
+ * Defined by: Sec. 2 Stage 3 (V(x, y) of the critic, used by generalized
+ * advantage estimation), App. A Alg. 2 ("turn on the critic LoRA ... calculate
+ * critic values on the generated sequence"; h is the critic pass's final
+ * hidden state).  No bias.
+ *
+ *   h       [M x K] bf16   hidden states, row-major, 16-byte aligned
+ *   w_v     [K] bf16       value head weight, 16-byte aligned
+ *   values  [M] fp32       out: values[m] = sum_k h[m][k] * w_v[k] (fp32 accumulation)
+ * Requires M >= 1, 1 <= K <= 2^21, K % 8 == 0.  Buffers are the caller's.
+ */
+hydra_status hydra_value_head(const uint16_t* h, const uint16_t* w_v, int64_t M, int64_t K, float* values,
+                              void* stream);
+
+/*
+ * hydra_ppo_advantages -- per-token PPO reward and generalized advantage
+ * estimates for n_seq sequences of seq_len tokens (M = n_seq * seq_len,
+ * sequence-major).
+ * Defined by: Sec. 2 Stage 3 (GAE builds the advantage estimates from the
+ * reward using V; V is trained on the returns), App. A Alg. 2 ("use reward and
+ * reference log probability to calculate A-hat"), App. B (KL beta = 0.02,
+ * GAE gamma = 1.0, lambda = 0.95).
+ *
+ *   kl      [M] fp32       per-token KL estimate lp_on - lp_off (hydra_score)
+ *   reward  [n_seq] fp32   sequence reward (hydra_score), credited to the last token
+ *   values  [M] fp32       critic values (hydra_value_head)
+ *   start                  first response position, 0 <= start < seq_len
+ *   beta, gamma, lam       KL weight and GAE discount / lambda
+ *   rewards [M] fp32       out, optional: r_t = -beta * kl_t (t >= start) + (t == T-1) * reward
+ *   advantages [M] fp32    out: A_t = delta_t + gamma * lam * A_{t+1},
+ *                          delta_t = r_t + gamma * V_{t+1} - V_t, V_T = A_T = 0
+ *   returns [M] fp32       out: A_t + V_t
+ * Positions before `start` get advantage and return 0 (and reward 0).  No
+ * output may be one of the inputs or another output (HYDRA_ERR_SHAPE);
+ * partial overlaps are not detected and are not allowed.  Requires
+ * n_seq, seq_len >= 1 and M below 2^31; buffers 4-byte aligned.
+ */
+hydra_status hydra_ppo_advantages(const float* kl, const float* reward, const float* values, int64_t n_seq,
+                                  int64_t seq_len, int64_t start, float beta, float gamma, float lam, float* rewards,
+                                  float* advantages, float* returns, void* stream);
+
 /* A static, human-readable name for a status code. */
 const char* hydra_status_string(hydra_status status);
 

@@ -1,4 +1,4 @@
-"""MI355X-native Hydra-PPO hot path: LoRA-switchable linear and PPO scoring epilogue.
+"""MI355X-native Hydra-PPO hot path: LoRA-switchable linear, PPO scoring epilogue and advantage step.
 
 The compute runs in libhydra.so (hand-written HIP kernels for gfx950 behind the
 C ABI of include/hydra.h); this package only marshals PyTorch tensors into it.
@@ -19,9 +19,11 @@ from ._binding import (  # noqa: F401
     LIB_PATH,
     hydra_lora_linear,
     hydra_lora_linear_group,
+    hydra_ppo_advantages,
     hydra_score,
     hydra_score_logits,
     hydra_score_workspace_bytes,
+    hydra_value_head,
     lib,
     status_string,
 )

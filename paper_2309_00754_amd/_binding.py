@@ -32,6 +32,8 @@ EXPORTED = (
     "hydra_score_workspace_bytes",
     "hydra_score",
     "hydra_score_logits",
+    "hydra_value_head",
+    "hydra_ppo_advantages",
     "hydra_status_string",
     "hydra_abi_version",
 )
@@ -76,6 +78,10 @@ def lib() -> ctypes.CDLL:
     L.hydra_score.restype = ctypes.c_int
     L.hydra_score_logits.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
     L.hydra_score_logits.restype = ctypes.c_int
+    L.hydra_value_head.argtypes = [_vp, _vp, _i64, _i64, _vp, _vp]
+    L.hydra_value_head.restype = ctypes.c_int
+    L.hydra_ppo_advantages.argtypes = [_vp, _vp, _vp, _i64, _i64, _i64, _f32, _f32, _f32, _vp, _vp, _vp, _vp]
+    L.hydra_ppo_advantages.restype = ctypes.c_int
     L.hydra_status_string.argtypes = [ctypes.c_int]
     L.hydra_status_string.restype = ctypes.c_char_p
     L.hydra_abi_version.argtypes = []
@@ -244,3 +250,30 @@ def hydra_score_logits(logits_on, logits_off, tokens, lp_on, lp_off, kl,
     st = lib().hydra_score_logits(_ptr(logits_on), _ptr(logits_off), _ptr(tokens), M, V, _ptr(lp_on), _ptr(lp_off),
                                   _ptr(kl), _ptr(lse_on), _ptr(lse_off), _ptr(err_flag), _stream_handle(stream))
     _check(st, "hydra_score_logits")
+
+
+def hydra_value_head(h, w_v, values, stream=None) -> None:
+    """values[m] = <h[m], w_v>: the critic's scalar head on every row (see include/hydra.h)."""
+    torch = _torch()
+    bf = _bf16_types()
+    M, K = h.shape
+    _need(h, "h", bf)
+    _need(w_v, "w_v", bf, (K,))
+    _need(values, "values", (torch.float32,), (M,))
+    st = lib().hydra_value_head(_ptr(h), _ptr(w_v), M, K, _ptr(values), _stream_handle(stream))
+    _check(st, "hydra_value_head")
+
+
+def hydra_ppo_advantages(kl, reward, values, n_seq: int, seq_len: int, advantages, returns, rewards=None,
+                         start: int = 0, beta: float = 0.02, gamma: float = 1.0, lam: float = 0.95,
+                         stream=None) -> None:
+    """Per-token PPO reward and GAE advantages / returns (see include/hydra.h)."""
+    torch = _torch()
+    M = int(n_seq) * int(seq_len)
+    for name, t, n in (("kl", kl, M), ("reward", reward, n_seq), ("values", values, M), ("advantages", advantages, M),
+                       ("returns", returns, M), ("rewards", rewards, M)):
+        _need(t, name, (torch.float32,), (n,))
+    st = lib().hydra_ppo_advantages(_ptr(kl), _ptr(reward), _ptr(values), int(n_seq), int(seq_len), int(start),
+                                    float(beta), float(gamma), float(lam), _ptr(rewards), _ptr(advantages),
+                                    _ptr(returns), _stream_handle(stream))
+    _check(st, "hydra_ppo_advantages")

@@ -182,6 +182,54 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
   return from_hip(hydra::launch_score_combine(c, st));
 }
 
+hydra_status hydra_value_head(const uint16_t* h, const uint16_t* w_v, int64_t M, int64_t K, float* values,
+                              void* stream) {
+  if (!h || !w_v || !values) return HYDRA_ERR_NULL;
+  if (!dim_ok(M) || !dim_ok(K) || (K % 8) != 0 || K > kMaxK) return HYDRA_ERR_SHAPE;
+  if (!aligned(h, 16) || !aligned(w_v, 16) || !aligned(values, 4)) return HYDRA_ERR_ALIGN;
+  hydra::ValueHeadArgs a{};
+  a.h = h;
+  a.w = w_v;
+  a.M = int(M);
+  a.K = int(K);
+  a.values = values;
+  return from_hip(hydra::launch_value_head(a, reinterpret_cast<hipStream_t>(stream)));
+}
+
+hydra_status hydra_ppo_advantages(const float* kl, const float* reward, const float* values, int64_t n_seq,
+                                  int64_t seq_len, int64_t start, float beta, float gamma, float lam, float* rewards,
+                                  float* advantages, float* returns, void* stream) {
+  if (!kl || !reward || !values || !advantages || !returns) return HYDRA_ERR_NULL;
+  if (!dim_ok(n_seq) || !dim_ok(seq_len) || n_seq > kMaxDim / seq_len) return HYDRA_ERR_SHAPE;
+  if (start < 0 || start >= seq_len) return HYDRA_ERR_SHAPE;
+  // outputs are written while inputs are still read: no output may be an input
+  const void* ins[3] = {kl, reward, values};
+  const void* outs[3] = {rewards, advantages, returns};
+  for (const void* o : outs) {
+    if (!o) continue;
+    for (const void* i : ins)
+      if (o == i) return HYDRA_ERR_SHAPE;
+  }
+  if (advantages == returns || (rewards && (rewards == advantages || rewards == returns))) return HYDRA_ERR_SHAPE;
+  if (!aligned(kl, 4) || !aligned(reward, 4) || !aligned(values, 4) || !aligned(advantages, 4) ||
+      !aligned(returns, 4) || (rewards && !aligned(rewards, 4)))
+    return HYDRA_ERR_ALIGN;
+  hydra::GaeArgs a{};
+  a.kl = kl;
+  a.reward = reward;
+  a.values = values;
+  a.n_seq = int(n_seq);
+  a.seq_len = int(seq_len);
+  a.start = int(start);
+  a.beta = beta;
+  a.gamma = gamma;
+  a.lam = lam;
+  a.rewards = rewards;
+  a.advantages = advantages;
+  a.returns = returns;
+  return from_hip(hydra::launch_gae(a, reinterpret_cast<hipStream_t>(stream)));
+}
+
 hydra_status hydra_score_logits(const float* logits_on, const float* logits_off, const int32_t* tokens, int64_t M,
                                 int64_t V, float* lp_on, float* lp_off, float* kl, float* lse_on, float* lse_off,
                                 int32_t* err_flag, void* stream) {

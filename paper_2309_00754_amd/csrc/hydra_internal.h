@@ -77,6 +77,27 @@ struct LogitsArgs {
   int32_t* err;
 };
 
+// Critic scalar head: values[m] = <h[m], w> (fp32 accumulation).
+struct ValueHeadArgs {
+  const uint16_t* h;  // [M x K] bf16
+  const uint16_t* w;  // [K] bf16
+  int M, K;
+  float* values;      // [M]
+};
+
+// Per-token PPO reward and generalized advantage estimation over n_seq
+// sequences of seq_len tokens (sequence-major).
+struct GaeArgs {
+  const float* kl;      // [M]
+  const float* reward;  // [n_seq]
+  const float* values;  // [M]
+  int n_seq, seq_len, start;
+  float beta, gamma, lam;
+  float* rewards;       // [M] or nullptr
+  float* advantages;    // [M]
+  float* returns;       // [M]
+};
+
 // Column-tile width of the fused scoring GEMM (number of vocabulary entries
 // one workgroup reduces).
 constexpr int kScoreTileN = 256;
@@ -84,6 +105,8 @@ constexpr int kScoreTileN = 256;
 hipError_t launch_lora_gemm(const LinearArgs& a, hipStream_t stream);
 hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream);
 hipError_t launch_score_gemm(const ScoreGemmArgs& a, hipStream_t stream);
+hipError_t launch_value_head(const ValueHeadArgs& a, hipStream_t stream);
+hipError_t launch_gae(const GaeArgs& a, hipStream_t stream);
 hipError_t launch_score_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_score_logits(const LogitsArgs& a, hipStream_t stream);
 

@@ -174,3 +174,41 @@ def _grp(G=2, xs=(P, P), Ws=(P, P), As=(P, P), Bs=(P, P), ss=(2.0, 2.0), M=4, N=
 ])
 def test_lora_linear_group_rejects(kw, code):
     assert _grp(**kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(h=None), H.HYDRA_ERR_NULL),
+    (dict(values=None), H.HYDRA_ERR_NULL),
+    (dict(M=0), H.HYDRA_ERR_SHAPE),
+    (dict(K=12), H.HYDRA_ERR_SHAPE),
+    (dict(K=(1 << 21) + 8), H.HYDRA_ERR_SHAPE),
+    (dict(h=P8), H.HYDRA_ERR_ALIGN),
+    (dict(w=P + 4), H.HYDRA_ERR_ALIGN),
+    (dict(values=P + 2), H.HYDRA_ERR_ALIGN),
+])
+def test_value_head_rejects(kw, code):
+    a = dict(h=P, w=P, M=16, K=64, values=P + 0x1000)
+    a.update(kw)
+    assert H.lib().hydra_value_head(a["h"], a["w"], a["M"], a["K"], a["values"], None) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(kl=None), H.HYDRA_ERR_NULL),
+    (dict(adv=None), H.HYDRA_ERR_NULL),
+    (dict(n_seq=0), H.HYDRA_ERR_SHAPE),
+    (dict(seq_len=0), H.HYDRA_ERR_SHAPE),
+    (dict(n_seq=1 << 20, seq_len=1 << 12), H.HYDRA_ERR_SHAPE),
+    (dict(start=-1), H.HYDRA_ERR_SHAPE),
+    (dict(start=8), H.HYDRA_ERR_SHAPE),
+    (dict(adv=P + 0x300), H.HYDRA_ERR_SHAPE),          # advantages written over values
+    (dict(ret=P + 0x400), H.HYDRA_ERR_SHAPE),          # returns == advantages
+    (dict(rew=P + 0x500), H.HYDRA_ERR_SHAPE),          # rewards == returns
+    (dict(kl=P + 2), H.HYDRA_ERR_ALIGN),
+    (dict(rew=P + 0x602), H.HYDRA_ERR_ALIGN),
+])
+def test_ppo_advantages_rejects(kw, code):
+    a = dict(kl=P + 0x100, reward=P + 0x200, values=P + 0x300, n_seq=4, seq_len=8, start=0,
+             rew=P + 0x600, adv=P + 0x400, ret=P + 0x500)
+    a.update(kw)
+    assert H.lib().hydra_ppo_advantages(a["kl"], a["reward"], a["values"], a["n_seq"], a["seq_len"], a["start"],
+                                        0.02, 1.0, 0.95, a["rew"], a["adv"], a["ret"], None) == code
