@@ -28,7 +28,7 @@ Every function is the plain definition.  ``gae_ref`` evaluates the sum over
 the rest of the sequence for every position (no recurrence), so it checks a
 recursive or scanned evaluation independently.
 
-Pins: see ``tests/test_oracle_pins.py`` (Fraction brute force, the lambda = 1
+Pins: see ``tests/test_oracle_ppo_pins.py`` (Fraction brute force, the lambda = 1
 telescoping closed form, lambda = 0, constant-residual geometric series, the
 one-step recurrence as a property).
 """
