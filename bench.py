@@ -6,7 +6,7 @@ rank 16, scale 2), i.e. the inference stage of one PPO iteration for one
 decoder layer plus the heads:
 
   * decode: one generation step of the four attention projections, M = 4
-    (hydra_lora_linear, bandwidth-bound kernel), both LoRA-off and LoRA-on outputs;
+    (hydra_lora_linear_group, bandwidth-bound kernels), both LoRA-off and LoRA-on outputs;
   * prefill: the seven LoRA linears of a layer over all 2048 tokens
     (hydra_lora_linear, dual-output MFMA GEMM), both outputs;
   * score: the CLM head with LoRA on and off, sampled-token log-probabilities,
@@ -14,8 +14,13 @@ decoder layer plus the heads:
     logits are never materialised).
 
 Inputs are synthetic (seeded Gaussians, see workloads/) and already resident
-in HBM when the timed region starts.  Each kernel launch is bracketed by HIP
-events on the stream it runs on.  The standalone scoring epilogue over
+in HBM when the timed region starts.  Inside the timed region a HIP event on
+the launch stream marks the start of each part of the step (and the step's
+end), so each part's time covers its launches back to back; a separate detail
+pass afterwards brackets every launch with its own pair of events (those
+figures include the events' own overhead, a few microseconds each).  The
+decode step's two kernels (base stream, LoRA update) form one launch of
+hydra_lora_linear_group.  The standalone scoring epilogue over
 materialised logits (hydra_score_logits, 512 x 32000) is timed separately
 (rotating four input sets so that the 256 MB last-level cache does not serve
 it) and reported under "aux"; it is not part of the step.  So is the PPO
@@ -162,22 +167,38 @@ def main():
 
     stream = torch.cuda.current_stream()
 
-    def step(evs=None):
-        for i, (_, _, fn, _, _) in enumerate(launches):
-            if evs is not None:
+    part_order = []
+    for l in launches:
+        if l[0] not in part_order:
+            part_order.append(l[0])
+
+    def step(evs=None, per_launch=False):
+        # evs: one event per part boundary (the part's first launch) plus a closing one; with per_launch, a
+        # pair of events around every launch instead (a detail pass: each pair adds its own overhead)
+        cur = None
+        for i, (part, _, fn, _, _) in enumerate(launches):
+            if evs is not None and per_launch:
                 evs[i][0].record(stream)
+            elif evs is not None and part != cur:
+                evs[part_order.index(part)].record(stream)
+                cur = part
             fn()
-            if evs is not None:
+            if evs is not None and per_launch:
                 evs[i][1].record(stream)
+        if evs is not None and not per_launch:
+            evs[-1].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
     K = args.steps
-    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in launches]
-           for _ in range(K)]
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def new_event():
+        return torch.cuda.Event(enable_timing=True)
+
+    evs = [[new_event() for _ in range(len(part_order) + 1)] for _ in range(K)]
+    start, end = new_event(), new_event()
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     start.record(stream)
@@ -189,16 +210,23 @@ def main():
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / K
 
-    # per-launch kernel durations (ms), averaged over the timed steps
-    dur = np.array([[evs[k][i][0].elapsed_time(evs[k][i][1]) for i in range(len(launches))] for k in range(K)])
-    avg = dur.mean(0)
+    # per-part durations (ms) from the boundary events, averaged over the timed steps
+    part_ms = {p: float(np.mean([evs[k][j].elapsed_time(evs[k][j + 1]) for k in range(K)]))
+               for j, p in enumerate(part_order)}
+
+    # detail pass, outside the timed region: each launch between its own pair of events
+    KD = min(K, 10)
+    devs = [[(new_event(), new_event()) for _ in launches] for _ in range(KD)]
+    for k in range(KD):
+        step(devs[k], per_launch=True)
+    torch.cuda.synchronize()
+    avg = np.array([[devs[k][i][0].elapsed_time(devs[k][i][1]) for i in range(len(launches))]
+                    for k in range(KD)]).mean(0)
 
     comp = {}
-    for part in ("decode", "prefill", "score", "advantages"):
+    for part in part_order:
         idx = [i for i, l in enumerate(launches) if l[0] == part]
-        if not idx:
-            continue
-        t = float(sum(avg[i] for i in idx)) * 1e-3
+        t = part_ms[part] * 1e-3
         fl = sum(launches[i][3] for i in idx)
         by = sum(launches[i][4] for i in idx)
         d = dict(launches=len(idx), us=round(t * 1e6, 2), tflops=round(fl / t / 1e12, 2),
@@ -228,7 +256,7 @@ def main():
     roof["kernel"] = {"prefill": "lora_gemm_kernel<16> (4 copy + 4 MFMA waves, 128x256 tiles)",
                       "score": "score_t_kernel<16> + score_bpad_kernel<16> + score_gemm_kernel<16,false> + "
                                "score_combine_kernel",
-                      "decode": "lora_gemv_dot_kernel<4,8,2> (grouped q/k/v/o)",
+                      "decode": "gemv_stream_kernel<4> + lora_update_kernel<4,16> (grouped q/k/v/o)",
                       "advantages": "value_head_kernel + gae_kernel"}[dom]
     tr = committed_traffic(dom)
     roof["traffic"] = None if tr is None else tr["bytes_per_launch"]

@@ -1,25 +1,26 @@
 // Decode-shaped (M <= 16) LoRA-switchable linear for gfx950, for one or a
-// group of linears in a single launch.
+// group of linears in a single call.
 //
 // At decode time (App. A, Alg. 1 / Alg. 2: "generate ... for T steps") each
 // linear sees one new token per sequence, so the work is a stream over W at
-// HBM rate with almost no arithmetic intensity.  Two kernels:
-//  * M <= 8 (lora_gemv_dot_kernel): grid = (blocks of NB rows of W) x
-//    (linears of the group), 8 waves per workgroup, each wave owning NB / 8
-//    rows of W over all of K.  A wave reads a W row as whole 1 KB lines (lane
-//    l takes 8 consecutive k values of every 512-wide chunk), the matching 16
-//    bytes of each x row, and accumulates with v_dot2c_f32_bf16 in fp32.  The
-//    loads of the next chunk are issued before the current chunk is used.
-//    The rank-r LoRA-down rows A are streamed the same way (AR rows per
-//    wave), giving T = x A^T next to the base product.  At the end each
-//    wave's per-lane partial sums are reduced across the 64 lanes by a
-//    halving exchange (32 values in 32 shuffles), and one thread per output
-//    forms y_off and y_on = y_off + s * sum_j T[m][j] B[n][j];
+// HBM rate with almost no arithmetic intensity.
+//  * M <= 8: two kernels.  gemv_stream_kernel computes the base product x W^T
+//    with one wave per row of W (16 rows per workgroup): the many small work
+//    units let the hardware dispatcher balance the HBM stream across the
+//    chip, which a static split of the rows over persistent workgroups does
+//    not (per-wave bandwidth varies by a factor of two).  A wave reads its
+//    row as whole 1 KB lines (lane l takes 8 consecutive k of every 512-wide
+//    chunk), the workgroup's x rows come from LDS, the dot products run on
+//    v_dot2c_f32_bf16 in fp32, and the 64 lanes are summed by a halving
+//    exchange.  It writes y_off and the base part of y_on.  Then, for the
+//    members with an adapter, lora_update_kernel adds s * (x A^T) B^T to y_on:
+//    forming T = x A^T once per workgroup of 256 columns instead of once per
+//    16 rows keeps the reads of A off the stream.
 //  * 8 < M <= 16 (lora_gemv_mfma_kernel): x rows fill the A operand of
 //    v_mfma_f32_16x16x32_bf16, the W rows its B operand; the waves split K
 //    and their partial tiles are combined in LDS in a fixed order.
-// Both reduce in a fixed order (results are deterministic and the same for a
-// linear called alone or inside a group).
+// Every reduction runs in a fixed order (results are deterministic and the
+// same for a linear called alone or inside a group).
 #include "hydra_device.h"
 #include "hydra_internal.h"
 
@@ -166,8 +167,13 @@ __device__ __forceinline__ void wave_reduce_scatter(float (&v)[V], int lane) {
     const bool up = (lane & o) != 0;
 #pragma unroll
     for (int q = 0; q < cnt / 2; ++q) {
-      const float send = up ? v[q] : v[q + cnt / 2];
-      const float keep = up ? v[q + cnt / 2] : v[q];
+      // (the empty asm keeps the two values in registers: without it the
+      // compiler turns the lane-dependent choice into a dynamically indexed
+      // read of the whole array, a long chain of selects)
+      float lo = v[q], hi = v[q + cnt / 2];
+      asm volatile("" : "+v"(lo), "+v"(hi));
+      const float send = up ? lo : hi;
+      const float keep = up ? hi : lo;
       v[q] = keep + __shfl_xor(send, o);
     }
   }
@@ -190,174 +196,207 @@ __device__ __forceinline__ bool reduced_writer(int lane) {
   return (lane & low) == 0;
 }
 
-constexpr int DW = 8;     // waves per workgroup
 constexpr int DKC = 512;  // k values per chunk (64 lanes x 8)
 
-// MB >= M x rows, RPW rows of W and AR rows of A per wave.
-template <int MB, int RPW, int AR>
-__global__ __launch_bounds__(DW * 64) void lora_gemv_dot_kernel(GroupArgs ga) {
-  constexpr int NB = RPW * DW;  // W rows per workgroup
-  constexpr int RP = AR * DW;   // padded rank
-  constexpr int VY = RPW * MB;  // partial sums per lane: base product
-  constexpr int VT = AR * MB;   //                       T
-  static_assert(VY <= 64 && VT <= 64, "at most 64 partial sums per lane");
-  __shared__ float ysh[NB][MB];
-  __shared__ float tsh[RP > 0 ? RP : 1][MB];
-  __shared__ uint16_t bsh[NB][RP > 0 ? RP : 1];
+// x rows staged in LDS per K segment: MB rows x SEG chunks of 512 k (32 KB).
+template <int MB>
+struct XSeg {
+  static constexpr int SEG = MB <= 4 ? 8 : 4;  // chunks per segment
+  static constexpr int ELEMS = MB * SEG * 64;   // uint4 per segment
+};
 
+// Stage x[m][c0 * 512 ... (c0 + SEG) * 512) for m < MB in LDS: element
+// (m, u, lane) holds the 8 k values that lane `lane` of any wave uses in chunk
+// c0 + u.  Rows past M and k past K read as zeros.
+template <int MB, int NT>
+__device__ __forceinline__ void stage_x(uint4* xsh, __amdgpu_buffer_rsrc_t xrs, int c0, int nch, int K, int t) {
+  constexpr int SEG = XSeg<MB>::SEG;
+  for (int e = t; e < XSeg<MB>::ELEMS; e += NT) {
+    const int m = e / (SEG * 64), u = (e / 64) % SEG, l = e % 64;
+    const int c = c0 + u, k = c * DKC + l * 8;
+    xsh[e] = buf_load16(xrs, (c < nch && k < K) ? (m * K + k) * 2 : kOutOfRange);
+  }
+}
+
+constexpr int SW = 16;  // waves (= rows of W) per workgroup of the base kernel
+
+// Base product of one linear of the group: y[m][n] = <x[m], W[n]> for m < M,
+// one wave per row n of W.  Small work units let the hardware dispatcher
+// balance the HBM stream across the chip; the x rows are shared by the
+// workgroup's 16 rows through LDS.  Writes y_off and y_on (the LoRA update of
+// y_on, when there is one, is added by lora_update_kernel afterwards).
+template <int MB>
+__global__ __launch_bounds__(SW * 64) void gemv_stream_kernel(GroupArgs ga) {
+  constexpr int SEG = XSeg<MB>::SEG;
+  __shared__ uint4 xsh[XSeg<MB>::ELEMS];
   const int gi = blockIdx.y;
   const uint16_t* __restrict__ X = ga.x[gi];
   const uint16_t* __restrict__ Wt = ga.W[gi];
-  const uint16_t* __restrict__ At = ga.A[gi];
-  const uint16_t* __restrict__ Bt = ga.B[gi];
   float* __restrict__ y_off = ga.y_off[gi];
   float* __restrict__ y_on = ga.y_on[gi];
-  const float s = ga.s[gi];
-  const int M = ga.M, N = ga.N, K = ga.K, r = ga.r;
-  const int t = threadIdx.x;
-  const int lane = t & 63;
+  const int M = ga.M, N = ga.N, K = ga.K;
+  const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int n0 = blockIdx.x * NB;
-
-  // A member of the group without y_on has no adapter (A, B may be NULL):
-  // its A and B descriptors cover zero bytes, so every read of them is a zero.
-  const bool has_lora = y_on != nullptr && At != nullptr && Bt != nullptr;
-
-  // Rows of B of this block, zero padded to RP: loaded now into registers
-  // (thread t holds elements t, t + 512, ... of the NB x RP block) and
-  // written to LDS only after the main loop, so that nothing waits for them.
-  constexpr int BPT = RP > 0 ? (NB * RP + DW * 64 - 1) / (DW * 64) : 1;
-  uint32_t bv[BPT];
-  if constexpr (RP > 0) {
-    const __amdgpu_buffer_rsrc_t brs =
-        make_rsrc(has_lora ? Bt + (size_t)n0 * r : nullptr, has_lora ? (uint32_t)min(NB, N - n0) * r * 2u : 0u);
-#pragma unroll
-    for (int q = 0; q < BPT; ++q) {
-      const int e = t + q * DW * 64;
-      const int n = e / RP, j = e % RP;
-      bv[q] = __builtin_amdgcn_raw_buffer_load_b16(brs, (e < NB * RP && j < r) ? (n * r + j) * 2 : kOutOfRange, 0, 0);
-    }
-  }
-
-  // Buffer resources cover exactly the valid rows of x (M), of this block's
-  // rows of W and of A (r): other rows read as zeros, as does a chunk past K.
+  const int n = blockIdx.x * SW + wave;
+  const bool row_ok = n < N;
   const __amdgpu_buffer_rsrc_t xrs = make_rsrc(X, (uint32_t)M * K * 2u);
-  const __amdgpu_buffer_rsrc_t wrs = make_rsrc(Wt + (size_t)n0 * K, (uint32_t)min(NB, N - n0) * K * 2u);
-  const __amdgpu_buffer_rsrc_t ars = make_rsrc(has_lora ? At : nullptr, has_lora ? (uint32_t)min(r, RP) * K * 2u : 0u);
+  const __amdgpu_buffer_rsrc_t wrs = make_rsrc(Wt + (size_t)min(n, N - 1) * K, row_ok ? (uint32_t)K * 2u : 0u);
   const int nch = (K + DKC - 1) / DKC;
 
-  struct Ld {
-    uint4 x[MB];
-    uint4 w[RPW];
-    uint4 a[AR > 0 ? AR : 1];
+  auto load_seg = [&](uint4 (&b)[SEG], int c0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < SEG; ++u) {
+      const int c = c0 + u, k = c * DKC + lane * 8;
+      b[u] = buf_load16(wrs, (c < nch && k < K) ? k * 2 : kOutOfRange);
+    }
   };
-  float acc[VY], acct[VT > 0 ? VT : 1];
+  float acc[MB];
 #pragma unroll
-  for (int q = 0; q < VY; ++q) acc[q] = 0.f;
+  for (int m = 0; m < MB; ++m) acc[m] = 0.f;
+  // (a second segment buffer would take the kernel past 64 VGPRs, i.e. below
+  // two 16-wave workgroups per CU; segments after the first are rare: K > 4096)
+  for (int c0 = 0; c0 < nch; c0 += SEG) {
+    uint4 wb[SEG];
+    load_seg(wb, c0);
+    if (c0 > 0) __syncthreads();  // every wave is done with the previous x segment
+    stage_x<MB, SW * 64>(xsh, xrs, c0, nch, K, t);
+    __syncthreads();
 #pragma unroll
-  for (int q = 0; q < (VT > 0 ? VT : 1); ++q) acct[q] = 0.f;
-
-  // Each workgroup walks the chunks starting at its own offset (wrapping
-  // around): all workgroups read the same x rows and LoRA-down rows, and
-  // this keeps them from all asking for the same lines at the same moment.
-  // The order depends only on the column block, so a linear gives the same
-  // bits alone or inside a group.
-  const int c0 = blockIdx.x % nch;
-  auto load = [&](Ld& L, int cc) __attribute__((always_inline)) {
-    const int c = cc < nch ? (cc + c0 >= nch ? cc + c0 - nch : cc + c0) : nch;
-    const int k = c * DKC + lane * 8;
-    const bool kv = c < nch && k < K;
+    for (int u = 0; u < SEG; ++u)
 #pragma unroll
-    for (int m = 0; m < MB; ++m) L.x[m] = buf_load16(xrs, kv ? (m * K + k) * 2 : kOutOfRange);
-#pragma unroll
-    for (int i = 0; i < RPW; ++i) L.w[i] = buf_load16(wrs, kv ? ((wave * RPW + i) * K + k) * 2 : kOutOfRange);
-#pragma unroll
-    for (int j = 0; j < AR; ++j) L.a[j] = buf_load16(ars, kv ? ((wave * AR + j) * K + k) * 2 : kOutOfRange);
-  };
-  auto use = [&](const Ld& L) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < RPW; ++i)
-#pragma unroll
-      for (int m = 0; m < MB; ++m) acc[i * MB + m] = dot8(L.w[i], L.x[m], acc[i * MB + m]);
-#pragma unroll
-    for (int j = 0; j < AR; ++j)
-#pragma unroll
-      for (int m = 0; m < MB; ++m) acct[j * MB + m] = dot8(L.a[j], L.x[m], acct[j * MB + m]);
-  };
-  // Two chunks in flight when both load sets fit in the register budget.
-  constexpr bool DOUBLE = MB + RPW + AR <= 16;
-  if constexpr (DOUBLE) {
-    Ld L0, L1;
-    load(L0, 0);
-    load(L1, 1);
-    // (scheduling barriers keep each refill right after the use of its
-    // buffer, so that one chunk is always in flight while the other is used)
-    for (int c = 0; c < nch; c += 2) {
-      use(L0);
-      __builtin_amdgcn_sched_barrier(0);
-      load(L0, c + 2);
-      __builtin_amdgcn_sched_barrier(0);
-      use(L1);  // zeros past the last chunk
-      __builtin_amdgcn_sched_barrier(0);
-      load(L1, c + 3);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  } else {
-    Ld L0;
-    for (int c = 0; c < nch; ++c) {
-      load(L0, c);
-      use(L0);
-    }
+      for (int m = 0; m < MB; ++m) acc[m] = dot8(wb[u], xsh[(m * SEG + u) * 64 + lane], acc[m]);
   }
-
-  if constexpr (RP > 0) {
-#pragma unroll
-    for (int q = 0; q < BPT; ++q) {
-      const int e = t + q * DW * 64;
-      if (e < NB * RP) bsh[e / RP][e % RP] = (uint16_t)bv[q];
-    }
-  }
-  // partial sums of the wave -> totals over the 64 lanes -> LDS
-  wave_reduce_scatter<VY>(acc, lane);
-  if (reduced_writer<VY>(lane)) {
-    const int q = reduced_index<VY>(lane);
-    ysh[wave * RPW + q / MB][q % MB] = acc[0];
-  }
-  if constexpr (VT > 0) {
-    wave_reduce_scatter<VT>(acct, lane);
-    if (reduced_writer<VT>(lane)) {
-      const int q = reduced_index<VT>(lane);
-      tsh[wave * AR + q / MB][q % MB] = acct[0];
-    }
-  }
-  __syncthreads();
-
-  // one thread per output (m, n): y_off = x W^T, y_on = y_off + s * T B^T
-  for (int e = t; e < M * NB; e += DW * 64) {
-    const int m = e / NB, nl = e % NB;
-    const int n = n0 + nl;
-    if (n >= N) continue;
-    const float yo = ysh[nl][m];
-    if (y_off) y_off[(size_t)m * N + n] = yo;
-    if (y_on) {
-      float d = 0.f;
-      if constexpr (RP > 0) {
-#pragma unroll
-        for (int j = 0; j < RP; ++j) d = fmaf(tsh[j][m], bf16_to_f32(bsh[nl][j]), d);
-      }
-      y_on[(size_t)m * N + n] = yo + s * d;
+  wave_reduce_scatter<MB>(acc, lane);
+  if (row_ok && reduced_writer<MB>(lane)) {
+    const int m = reduced_index<MB>(lane);
+    if (m < M) {
+      if (y_off) y_off[(size_t)m * N + n] = acc[0];
+      if (y_on) y_on[(size_t)m * N + n] = acc[0];
     }
   }
 }
 
-template <int MB, int RPW>
-hipError_t launch_dot_mb(const GroupArgs& g, int rp, hipStream_t stream) {
-  const dim3 grid((g.N + RPW * DW - 1) / (RPW * DW), g.G), block(DW * 64);
+constexpr int UW = 16;   // waves per workgroup of the LoRA update
+constexpr int UNB = 256; // columns of y_on per workgroup
+constexpr int URW = 8;   // rows of A per wave in the T pass
+
+// y_on += s * T B^T with T = x A^T, for the members of the group that have an
+// adapter.  Every workgroup forms T itself: the 16 waves split A into RP / 8
+// row groups of 8 rows and the K chunks into 128 / RP chunk groups; a wave
+// requests its rows of A and its pieces of x for one chunk at a time (both
+// L2 hits once the first workgroup has touched them), reduces its partial
+// sums across its lanes, and the partials of the chunk groups are added in a
+// fixed order.  The rows of B and the current values of y_on are requested
+// first, so that their latency overlaps the T pass.
+template <int MB, int RP>
+__global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
+  constexpr int NT = UW * 64;
+  constexpr int GR = RP / URW;                     // row groups
+  constexpr int GC = UW / GR;                      // chunk groups
+  constexpr int VT = URW * MB;                     // partial sums of T per lane
+  constexpr int BPT = UNB * RP / NT;               // bf16 of B per thread
+  constexpr int OPT = (UNB * MB + NT - 1) / NT;    // outputs per thread
+  static_assert(GR * GC == UW && VT <= 64 && BPT >= 1, "shape");
+  __shared__ float part[UW][VT];      // per-wave partial T, index j_local * MB + m
+  __shared__ float4 tsh[MB][RP / 4];  // T[m][j]
+  __shared__ uint16_t bsh[UNB][RP];
+  const int gi = blockIdx.y;
+  const uint16_t* __restrict__ X = ga.x[gi];
+  const uint16_t* __restrict__ At = ga.A[gi];
+  const uint16_t* __restrict__ Bt = ga.B[gi];
+  float* __restrict__ y_on = ga.y_on[gi];
+  if (y_on == nullptr || At == nullptr || Bt == nullptr) return;  // member without an adapter
+  const float s = ga.s[gi];
+  const int M = ga.M, N = ga.N, K = ga.K, r = ga.r;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int n0 = blockIdx.x * UNB;
+  const int nb = min(UNB, N - n0);
+
+  // B block [nb x r], zero padded to RP: requested now into registers,
+  // written to LDS after the T pass.
+  const __amdgpu_buffer_rsrc_t brs = make_rsrc(Bt + (size_t)n0 * r, (uint32_t)nb * r * 2u);
+  uint32_t bv[BPT];
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    const int e = t + q * NT, nl = e / RP, j = e % RP;
+    bv[q] = __builtin_amdgcn_raw_buffer_load_b16(brs, j < r ? (nl * r + j) * 2 : kOutOfRange, 0, 0);
+  }
+  float yv[OPT];
+#pragma unroll
+  for (int q = 0; q < OPT; ++q) {
+    const int e = t + q * NT, m = e / UNB, nl = e % UNB;
+    yv[q] = (e < UNB * MB && m < M && nl < nb) ? y_on[(size_t)m * N + n0 + nl] : 0.f;
+  }
+
+  // T pass: wave = (row group, chunk group); rows of A beyond r read as zeros
+  const int rg = wave / GC, cg = wave % GC;
+  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(X, (uint32_t)M * K * 2u);
+  const __amdgpu_buffer_rsrc_t ars = make_rsrc(At, (uint32_t)r * K * 2u);
+  const int nch = (K + DKC - 1) / DKC;
+  float acc[VT];
+#pragma unroll
+  for (int q = 0; q < VT; ++q) acc[q] = 0.f;
+  for (int c = cg; c < nch; c += GC) {
+    const int k = c * DKC + lane * 8;
+    const bool kv = k < K;
+    uint4 av[URW], xv[MB];
+#pragma unroll
+    for (int j = 0; j < URW; ++j) av[j] = buf_load16(ars, kv ? ((rg * URW + j) * K + k) * 2 : kOutOfRange);
+#pragma unroll
+    for (int m = 0; m < MB; ++m) xv[m] = buf_load16(xrs, kv ? (m * K + k) * 2 : kOutOfRange);
+    __builtin_amdgcn_sched_barrier(0);  // all of the chunk's loads in flight before the first use
+#pragma unroll
+    for (int j = 0; j < URW; ++j)
+#pragma unroll
+      for (int m = 0; m < MB; ++m) acc[j * MB + m] = dot8(av[j], xv[m], acc[j * MB + m]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  wave_reduce_scatter<VT>(acc, lane);
+  if (reduced_writer<VT>(lane)) part[wave][reduced_index<VT>(lane)] = acc[0];
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    const int e = t + q * NT;
+    bsh[e / RP][e % RP] = (uint16_t)bv[q];
+  }
+  __syncthreads();
+  // T[m][j] = sum over the chunk groups, in chunk-group order
+  if (t < RP * MB) {
+    const int j = t / MB, m = t % MB;
+    const int g = j / URW, q = (j % URW) * MB + m;
+    float v = part[g * GC][q];
+    for (int c2 = 1; c2 < GC; ++c2) v += part[g * GC + c2][q];
+    reinterpret_cast<float*>(&tsh[m][0])[j] = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < OPT; ++q) {
+    const int e = t + q * NT, m = e / UNB, nl = e % UNB;
+    if (e < UNB * MB && m < M && nl < nb) {
+      float d = 0.f;
+#pragma unroll
+      for (int j4 = 0; j4 < RP / 4; ++j4) {
+        const float4 tv = tsh[m][j4];
+        d = fmaf(tv.x, bf16_to_f32(bsh[nl][4 * j4 + 0]), d);
+        d = fmaf(tv.y, bf16_to_f32(bsh[nl][4 * j4 + 1]), d);
+        d = fmaf(tv.z, bf16_to_f32(bsh[nl][4 * j4 + 2]), d);
+        d = fmaf(tv.w, bf16_to_f32(bsh[nl][4 * j4 + 3]), d);
+      }
+      y_on[(size_t)m * N + n0 + nl] = yv[q] + s * d;
+    }
+  }
+}
+
+template <int MB>
+hipError_t launch_stream_mb(const GroupArgs& g, int rp, hipStream_t stream) {
+  hipLaunchKernelGGL((gemv_stream_kernel<MB>), dim3((g.N + SW - 1) / SW, g.G), dim3(SW * 64), 0, stream, g);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || rp == 0) return e;
+  const dim3 grid((g.N + UNB - 1) / UNB, g.G), block(UW * 64);
   switch (rp) {
-    case 0: hipLaunchKernelGGL((lora_gemv_dot_kernel<MB, RPW, 0>), grid, block, 0, stream, g); break;
-    case 16: hipLaunchKernelGGL((lora_gemv_dot_kernel<MB, RPW, 2>), grid, block, 0, stream, g); break;
-    case 32: hipLaunchKernelGGL((lora_gemv_dot_kernel<MB, RPW, 4>), grid, block, 0, stream, g); break;
-    default: hipLaunchKernelGGL((lora_gemv_dot_kernel<MB, RPW, 8>), grid, block, 0, stream, g); break;
+    case 16: hipLaunchKernelGGL((lora_update_kernel<MB, 16>), grid, block, 0, stream, g); break;
+    case 32: hipLaunchKernelGGL((lora_update_kernel<MB, 32>), grid, block, 0, stream, g); break;
+    default: hipLaunchKernelGGL((lora_update_kernel<MB, 64>), grid, block, 0, stream, g); break;
   }
   return hipGetLastError();
 }
@@ -388,8 +427,10 @@ hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream) {
   for (int i = 0; i < g.G; ++i) any_on = any_on || g.y_on[i] != nullptr;
   const int r = any_on ? g.r : 0;
   const int rp = r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : 64;
-  if (g.M <= 4) return launch_dot_mb<4, 8>(g, rp, stream);
-  if (g.M <= 8) return launch_dot_mb<8, 4>(g, rp, stream);
+  if (g.M <= 1) return launch_stream_mb<1>(g, rp, stream);
+  if (g.M <= 2) return launch_stream_mb<2>(g, rp, stream);
+  if (g.M <= 4) return launch_stream_mb<4>(g, rp, stream);
+  if (g.M <= 8) return launch_stream_mb<8>(g, rp, stream);
   // The widest column block that still gives at least one workgroup per CU:
   // wider blocks amortise the per-workgroup reads of A over more of W.
   const long wg64 = (long)((g.N + 63) / 64) * g.G;

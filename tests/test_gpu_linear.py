@@ -31,6 +31,8 @@ SHAPES = [
     (5, 136, 33, 1), (7, 256, 20, 0), (2, 8, 17, 33), (6, 520, 300, 64), (8, 4104, 130, 32), (12, 1032, 77, 16),
     (17, 64, 256, 8), (33, 520, 300, 16), (128, 512, 256, 16), (130, 72, 513, 1), (257, 1024, 700, 33),
     (200, 64, 256, 0), (64, 128, 96, 64), (300, 2048, 1200, 17), (129, 8, 255, 16),
+    # decode shapes whose x rows span several LDS segments (K > 4096, or K > 2048 at M > 4)
+    (4, 11008, 96, 16), (2, 8200, 50, 64), (1, 4096, 300, 32), (8, 2056, 70, 8),
 ]
 
 
@@ -123,10 +125,11 @@ def _group_run(cases, device, want_on=None):
     import torch
     G = len(cases)
     want_on = want_on or [True] * G
+    adapter = want_on
     xs = [dev_bf16(c.x, device) for c in cases]
     Ws = [dev_bf16(c.W, device) for c in cases]
-    As = [dev_bf16(c.A, device) if (c.r and want_on[i]) else None for i, c in enumerate(cases)]
-    Bs = [dev_bf16(c.B, device) if (c.r and want_on[i]) else None for i, c in enumerate(cases)]
+    As = [dev_bf16(c.A, device) if (c.r and adapter[i]) else None for i, c in enumerate(cases)]
+    Bs = [dev_bf16(c.B, device) if (c.r and adapter[i]) else None for i, c in enumerate(cases)]
     yo = [torch.full((c.M, c.N), float("nan"), device=device) for c in cases]
     yn = [torch.full((c.M, c.N), float("nan"), device=device) if want_on[i] else None for i, c in enumerate(cases)]
     H.hydra_lora_linear_group(xs, Ws, As, Bs, [c.s for c in cases], yo, yn)
@@ -155,6 +158,21 @@ def test_group_mixed_members(dev):
         e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
         assert_rel(go[i], e_off, f"member {i} y_off")
         if gn[i] is not None:
+            assert_rel(gn[i], e_on, f"member {i} y_on")
+
+
+@pytest.mark.parametrize("M", [1, 4, 8])
+def test_group_lora_off_member_between_lora_members(dev, M):
+    """At every decode row class, a LoRA-off member (no y_on, no adapter) sits between two members whose y_on
+    gets the LoRA update; the update must touch only its own members."""
+    say("group lora-off member", M)
+    base = [WL.gen_linear(70 + i, M, 1032, 200, 16) for i in range(3)]
+    go, gn = _group_run(base, dev, want_on=[True, False, True])
+    assert gn[1] is None
+    for i in range(3):
+        e_off, e_on = lora_linear_ref(base[i].x, base[i].W, base[i].A, base[i].B, base[i].s)
+        assert_rel(go[i], e_off, f"member {i} y_off")
+        if i != 1:
             assert_rel(gn[i], e_on, f"member {i} y_on")
 
 
