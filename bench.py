@@ -292,7 +292,8 @@ def main():
 
     if not args.no_aux:
         out["aux"] = {"score_logits": bench_score_logits(torch, H, WL, dev),
-                      "ppo_advantages": bench_advantages(torch, H, WL, dev)}
+                      "ppo_advantages": bench_advantages(torch, H, WL, dev),
+                      "decode_multi": bench_decode_multi(torch, H, WL, dev)}
 
     if not args.no_cpu_baseline:
         hi = None
@@ -413,6 +414,50 @@ def bench_advantages(torch, H, WL, dev, iters=30):
                 gae_bytes=int(gae_bytes),
                 note="median of per-launch HIP events over back-to-back launches; the 16 MB of hidden states "
                      "stay in the last-level cache between iterations")
+
+
+def bench_decode_multi(torch, H, WL, dev, iters=20, sets=3):
+    """One 4096 x 4096 decode projection serving three passes at M = 4 (reference with LoRA off, actor and
+    critic with their adapters): one hydra_lora_linear_multi call against three hydra_lora_linear calls.
+    Three weight sets rotate (402 MB, more than the last-level cache); each figure is the average over a
+    block of back-to-back launches between one pair of events."""
+    c = WL.make("decode_multi")
+    bf = (lambda u: torch.from_numpy(np.ascontiguousarray(u).view(np.int16)).to(dev))
+    Ws = [bf(c.W)] + [bf(WL.gen_multi(60 + i, 1, c.K, c.N, 0, 0).W) for i in range(sets - 1)]
+    x_off, xs = bf(c.x_off), [bf(x) for x in c.x_on]
+    As, Bs = [bf(a) for a in c.A], [bf(b) for b in c.B]
+    y_off = torch.empty(c.M, c.N, device=dev)
+    y_ons = [torch.empty(c.M, c.N, device=dev) for _ in xs]
+
+    def multi(W):
+        H.hydra_lora_linear_multi(x_off, W, xs, As, Bs, c.s, y_off, y_ons)
+
+    def separate(W):
+        H.hydra_lora_linear(x_off, W, None, None, 0.0, y_off, None)
+        for a in range(len(xs)):
+            H.hydra_lora_linear(xs[a], W, As[a], Bs[a], c.s[a], None, y_ons[a])
+
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for i in range(2 * sets):
+            fn(Ws[i % sets])
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(iters):
+            fn(Ws[i % sets])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters * 1e3
+
+    t_multi, t_sep = timed(multi), timed(separate)
+    passes = 1 + len(xs)
+    by = passes * lin_bytes(c.M, c.K, c.N, c.r)   # what the passes move when each reads W itself
+    return dict(passes=passes, M=c.M, K=c.K, N=c.N, r=c.r, multi_us=round(t_multi, 2), separate_us=round(t_sep, 2),
+                speedup=round(t_sep / t_multi, 3), multi_pass_equiv_gbps=round(by / t_multi / 1e3, 1),
+                note="multi stacks the 12 input rows into two reads of W (8 + 4 rows); separate reads W three "
+                     "times; GB/s counts the bytes of three independent passes")
 
 
 def cpu_baseline(target_s: float, host_inputs=None):

@@ -111,6 +111,40 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
                                      int64_t M, int64_t N, int64_t K, int64_t r,
                                      float* const* y_off, float* const* y_on, void* stream);
 
+/* Largest number of LoRA-on inputs in one hydra_lora_linear_multi call. */
+#define HYDRA_MAX_ADAPTERS 4
+
+/*
+ * hydra_lora_linear_multi -- one frozen W serving a LoRA-off input and up to
+ * HYDRA_MAX_ADAPTERS LoRA-on inputs, each with its own adapter.
+ * Defined by: App. A, Alg. 2 (in each PPO iteration the same base weights run
+ * the actor pass with the actor adapter, the critic pass with the critic
+ * adapter, and the reference / reward passes with LoRA turned off, over the
+ * same sequences), Sec. 3 "Dynamic LoRA" (LO(.) on the same W).  In a
+ * multi-layer model the passes' activations differ after the first layer, so
+ * every pass brings its own input.
+ *
+ *   x_off  [M x K] bf16 or NULL     input of the LoRA-off pass
+ *   W      [N x K] bf16             frozen base weight
+ *   n_on   0 <= n_on <= HYDRA_MAX_ADAPTERS
+ *   x_on, A, B, y_on   HOST arrays of n_on device pointers: x_on[a] [M x K] bf16,
+ *                      A[a] [r x K] bf16, B[a] [N x r] bf16, y_on[a] [M x N] fp32
+ *                      (A and B may be NULL arrays iff r == 0)
+ *   s      HOST array of n_on scales (NULL iff n_on == 0)
+ *   y_off  [M x N] fp32  out: x_off W^T (NULL iff x_off is NULL)
+ *   y_on[a]              out: x_on[a] W^T + s[a] (x_on[a] A[a]^T) B[a]^T
+ * Shape, rank and alignment rules as in hydra_lora_linear; the outputs must be
+ * distinct buffers (HYDRA_ERR_SHAPE otherwise) and at least one input given.
+ * At M <= 8 the inputs' rows are stacked, at most 8 rows per pass, and each
+ * pass reads W from HBM once for all its rows (M = 4 with the off input and
+ * one adapter: one read of W instead of two); larger M runs one GEMM per input.
+ * Every output has the bits of the corresponding hydra_lora_linear call.
+ */
+hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, int64_t n_on,
+                                     const uint16_t* const* x_on, const uint16_t* const* A,
+                                     const uint16_t* const* B, const float* s, int64_t M, int64_t N, int64_t K,
+                                     int64_t r, float* y_off, float* const* y_on, void* stream);
+
 /*
  * hydra_score_workspace_bytes -- device workspace that hydra_score needs for
  * M = n_seq * seq_len token rows and a vocabulary of V.  Writes *bytes.

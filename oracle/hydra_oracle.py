@@ -39,6 +39,7 @@ from typing import Optional, Tuple
 import numpy as np
 
 __all__ = [
+    "lora_linear_multi_ref",
     "bf16_to_f64",
     "lora_linear_ref",
     "log_softmax_gather_ref",
@@ -80,6 +81,30 @@ def lora_linear_ref(x, W, A, B, s: float) -> Tuple[np.ndarray, np.ndarray]:
     T = _mm(X, Ad)                      # [M x r]
     y_on = y_off + float(s) * _mm(T, Bd)
     return y_off, y_on
+
+
+def lora_linear_multi_ref(x_off, W, x_ons, As, Bs, ss):
+    """One frozen W serving several passes (App. A, Alg. 2: the actor pass with the
+    actor adapter, the critic pass with the critic adapter, the reference / reward
+    passes with LoRA off, all over the same base weights; Sec. 3 Dynamic LoRA).
+
+    x_off: [M x K] bf16 bits or None; x_ons[a]: [M x K]; As[a]: [r x K]; Bs[a]: [N x r].
+    Returns (y_off or None, [y_on[a]]) in float64:
+      y_off   = X_off W^T
+      y_on[a] = X_on[a] W^T + s[a] (X_on[a] A[a]^T) B[a]^T
+    Each pass is its own plain product; sharing the reads of W is a property of
+    the kernel, not of what is computed.
+    """
+    Wd = bf16_to_f64(W)
+    y_off = None if x_off is None else _mm(bf16_to_f64(x_off), Wd)
+    y_ons = []
+    for x, A, B, s in zip(x_ons, As, Bs, ss):
+        X = bf16_to_f64(x)
+        y = _mm(X, Wd)
+        if A is not None and np.asarray(A).size:
+            y = y + float(s) * _mm(_mm(X, bf16_to_f64(A)), bf16_to_f64(B))
+        y_ons.append(y)
+    return y_off, y_ons
 
 
 def log_softmax_gather_ref(z, ids) -> Tuple[np.ndarray, np.ndarray]:

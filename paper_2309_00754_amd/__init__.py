@@ -11,6 +11,7 @@ from ._binding import (  # noqa: F401
     HYDRA_ERR_SHAPE,
     HYDRA_ERR_UNSUPPORTED,
     HYDRA_ERR_WORKSPACE,
+    HYDRA_MAX_ADAPTERS,
     HYDRA_MAX_GROUP,
     HYDRA_MAX_RANK,
     HYDRA_OK,
@@ -19,6 +20,7 @@ from ._binding import (  # noqa: F401
     LIB_PATH,
     hydra_lora_linear,
     hydra_lora_linear_group,
+    hydra_lora_linear_multi,
     hydra_ppo_advantages,
     hydra_score,
     hydra_score_logits,

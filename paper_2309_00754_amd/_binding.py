@@ -24,11 +24,13 @@ HYDRA_ERR_WORKSPACE = -5
 HYDRA_ERR_HIP = -6
 HYDRA_MAX_RANK = 64
 HYDRA_MAX_GROUP = 8
+HYDRA_MAX_ADAPTERS = 4
 
 # Every symbol include/hydra.h declares.
 EXPORTED = (
     "hydra_lora_linear",
     "hydra_lora_linear_group",
+    "hydra_lora_linear_multi",
     "hydra_score_workspace_bytes",
     "hydra_score",
     "hydra_score_logits",
@@ -71,6 +73,9 @@ def lib() -> ctypes.CDLL:
     L.hydra_lora_linear_group.argtypes = [_i64, _pp, _pp, _pp, _pp, ctypes.POINTER(ctypes.c_float), _i64, _i64, _i64,
                                           _i64, _pp, _pp, _vp]
     L.hydra_lora_linear_group.restype = ctypes.c_int
+    L.hydra_lora_linear_multi.argtypes = [_vp, _vp, _i64, _pp, _pp, _pp, ctypes.POINTER(ctypes.c_float), _i64, _i64,
+                                          _i64, _i64, _vp, _pp, _vp]
+    L.hydra_lora_linear_multi.restype = ctypes.c_int
     L.hydra_score_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(ctypes.c_size_t)]
     L.hydra_score_workspace_bytes.restype = ctypes.c_int
     L.hydra_score.argtypes = [_vp, _vp, _vp, _vp, _f32, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
@@ -196,6 +201,41 @@ def hydra_lora_linear_group(xs, Ws, As, Bs, ss, y_offs=None, y_ons=None, stream=
     st = lib().hydra_lora_linear_group(G, _ptr_array(xs), _ptr_array(Ws), _ptr_array(As), _ptr_array(Bs), svals,
                                        M, N, K, r, _ptr_array(y_offs), _ptr_array(y_ons), _stream_handle(stream))
     _check(st, "hydra_lora_linear_group")
+
+
+def hydra_lora_linear_multi(x_off, W, x_ons, As, Bs, ss, y_off=None, y_ons=None, stream=None) -> None:
+    """One W for a LoRA-off input and several LoRA-on inputs with their own adapters (see include/hydra.h).
+
+    x_off, y_off: tensors or None (together); x_ons, As, Bs, y_ons: sequences of n_on tensors (As, Bs may be
+    None or all-None when r == 0); ss: n_on scales.
+    """
+    torch = _torch()
+    bf = _bf16_types()
+    n_on = len(x_ons)
+    As = list(As) if As is not None else [None] * n_on
+    Bs = list(Bs) if Bs is not None else [None] * n_on
+    y_ons = list(y_ons) if y_ons is not None else [None] * n_on
+    if not (len(As) == len(Bs) == len(ss) == len(y_ons) == n_on):
+        raise ValueError("all per-input sequences must have the same length")
+    ref = x_off if x_off is not None else (x_ons[0] if n_on else None)
+    if ref is None:
+        raise ValueError("at least one input is needed")
+    M, K = ref.shape
+    N = W.shape[0]
+    r = next((a.shape[0] for a in As if a is not None), 0)
+    _need(W, "W", bf, (N, K))
+    _need(x_off, "x_off", bf, (M, K))
+    _need(y_off, "y_off", (torch.float32,), (M, N))
+    for a in range(n_on):
+        _need(x_ons[a], "x_on", bf, (M, K))
+        _need(As[a], "A", bf, (r, K))
+        _need(Bs[a], "B", bf, (N, r))
+        _need(y_ons[a], "y_on", (torch.float32,), (M, N))
+    svals = (ctypes.c_float * max(n_on, 1))(*[float(v) for v in ss])
+    st = lib().hydra_lora_linear_multi(_ptr(x_off), _ptr(W), n_on, _ptr_array(x_ons), _ptr_array(As),
+                                       _ptr_array(Bs), svals if n_on else None, M, N, K, r, _ptr(y_off),
+                                       _ptr_array(y_ons), _stream_handle(stream))
+    _check(st, "hydra_lora_linear_multi")
 
 
 def hydra_score_workspace_bytes(M: int, V: int) -> int:

@@ -107,6 +107,85 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
   return HYDRA_OK;
 }
 
+hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, int64_t n_on,
+                                     const uint16_t* const* x_on, const uint16_t* const* A,
+                                     const uint16_t* const* B, const float* s, int64_t M, int64_t N, int64_t K,
+                                     int64_t r, float* y_off, float* const* y_on, void* stream) {
+  if (!W) return HYDRA_ERR_NULL;
+  if (n_on < 0 || n_on > HYDRA_MAX_ADAPTERS) return HYDRA_ERR_SHAPE;
+  if ((x_off == nullptr) != (y_off == nullptr)) return HYDRA_ERR_NULL;
+  if (!x_off && n_on == 0) return HYDRA_ERR_NULL;
+  if (n_on > 0 && (!x_on || !y_on || !s || (r > 0 && (!A || !B)))) return HYDRA_ERR_NULL;
+  if (!dim_ok(M) || !dim_ok(N) || !dim_ok(K) || (K % 8) != 0 || K > kMaxK) return HYDRA_ERR_SHAPE;
+  if (r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
+  if (!aligned(W, 16) || (x_off && !aligned(x_off, 16)) || (y_off && !aligned(y_off, 4))) return HYDRA_ERR_ALIGN;
+  for (int64_t a = 0; a < n_on; ++a) {
+    if (!x_on[a] || !y_on[a] || (r > 0 && (!A[a] || !B[a]))) return HYDRA_ERR_NULL;
+    if (!aligned(x_on[a], 16) || !aligned(y_on[a], 4)) return HYDRA_ERR_ALIGN;
+    if (r > 0 && (!aligned(A[a], 16) || !aligned(B[a], 2))) return HYDRA_ERR_ALIGN;
+    if (y_on[a] == y_off) return HYDRA_ERR_SHAPE;
+    for (int64_t b = 0; b < a; ++b)
+      if (y_on[b] == y_on[a]) return HYDRA_ERR_SHAPE;
+  }
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (M > hydra::kStreamRows) {
+    // One launch per input (the MFMA kernels are bound by arithmetic, not by reads of W).
+    if (x_off) {
+      const hydra_status e = hydra_lora_linear(x_off, W, nullptr, nullptr, 0.f, M, N, K, 0, y_off, nullptr, stream);
+      if (e != HYDRA_OK) return e;
+    }
+    for (int64_t a = 0; a < n_on; ++a) {
+      const hydra_status e = hydra_lora_linear(x_on[a], W, r > 0 ? A[a] : nullptr, r > 0 ? B[a] : nullptr, s[a], M,
+                                               N, K, r, nullptr, y_on[a], stream);
+      if (e != HYDRA_OK) return e;
+    }
+    return HYDRA_OK;
+  }
+  // Decode shape: the inputs' rows are stacked, up to kStreamRows rows per
+  // pass, and every pass reads W once for all of its rows; then the LoRA
+  // update of each y_on.
+  const int n_in = (x_off ? 1 : 0) + int(n_on);
+  hydra::StreamArgs sa{};
+  sa.G = 1;
+  sa.N = int(N);
+  sa.K = int(K);
+  sa.W[0] = W;
+  for (int i = 0; i < n_in; ++i) {
+    const bool off = x_off && i == 0;
+    const uint16_t* xi = off ? x_off : x_on[i - (x_off ? 1 : 0)];
+    float* yi = off ? y_off : y_on[i - (x_off ? 1 : 0)];
+    if (sa.rows + M > hydra::kStreamRows) {
+      if (hydra::launch_gemv_stream(sa, st) != hipSuccess) return HYDRA_ERR_HIP;
+      sa = hydra::StreamArgs{};
+      sa.G = 1;
+      sa.N = int(N);
+      sa.K = int(K);
+      sa.W[0] = W;
+    }
+    for (int m = 0; m < M; ++m) {
+      sa.xr[0][sa.rows] = xi + size_t(m) * size_t(K);
+      sa.ya[0][sa.rows] = yi + size_t(m) * size_t(N);
+      ++sa.rows;
+    }
+  }
+  if (hydra::launch_gemv_stream(sa, st) != hipSuccess) return HYDRA_ERR_HIP;
+  if (r == 0 || n_on == 0) return HYDRA_OK;
+  hydra::GroupArgs g{};
+  g.G = int(n_on);
+  g.M = int(M);
+  g.N = int(N);
+  g.K = int(K);
+  g.r = int(r);
+  for (int64_t a = 0; a < n_on; ++a) {
+    g.x[a] = x_on[a];
+    g.A[a] = A[a];
+    g.B[a] = B[a];
+    g.y_on[a] = y_on[a];
+    g.s[a] = s[a];
+  }
+  return from_hip(hydra::launch_lora_update(g, st));
+}
+
 hydra_status hydra_score_workspace_bytes(int64_t M, int64_t V, size_t* bytes) {
   if (!bytes) return HYDRA_ERR_NULL;
   if (!dim_ok(M) || !dim_ok(V)) return HYDRA_ERR_SHAPE;

@@ -33,6 +33,18 @@ struct GroupArgs {
   int G, M, N, K, r;
 };
 
+// Base product y[m] = x[m] W^T for up to kStreamRows rows per W, each row
+// with its own input and output rows (one or several LoRA-off / LoRA-on
+// inputs sharing one read of W), for G weights in one launch.
+constexpr int kStreamRows = 8;
+struct StreamArgs {
+  const uint16_t* W[kMaxGroup];                 // [N x K] bf16
+  const uint16_t* xr[kMaxGroup][kStreamRows];   // input row m ([K] bf16); nullptr: a zero row
+  float* ya[kMaxGroup][kStreamRows];            // output row m ([N] fp32); nullptr: not written
+  float* yb[kMaxGroup][kStreamRows];            // second copy of output row m; nullptr: not written
+  int G, rows, N, K;
+};
+
 // Per (row, column tile) partial log-sum-exp state written by the fused
 // CLM-head GEMM: (max_off, sumexp_off, max_on, sumexp_on).
 struct ScoreGemmArgs {
@@ -104,6 +116,10 @@ constexpr int kScoreTileN = 256;
 
 hipError_t launch_lora_gemm(const LinearArgs& a, hipStream_t stream);
 hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream);
+// y[m] = x[m] W^T for the rows of a StreamArgs (rows <= kStreamRows).
+hipError_t launch_gemv_stream(const StreamArgs& a, hipStream_t stream);
+// y_on += s (x A^T) B^T for the members of g with an adapter (M <= 8 rows).
+hipError_t launch_lora_update(const GroupArgs& g, hipStream_t stream);
 hipError_t launch_score_gemm(const ScoreGemmArgs& a, hipStream_t stream);
 hipError_t launch_value_head(const ValueHeadArgs& a, hipStream_t stream);
 hipError_t launch_gae(const GaeArgs& a, hipStream_t stream);

@@ -218,28 +218,39 @@ __device__ __forceinline__ void stage_x(uint4* xsh, __amdgpu_buffer_rsrc_t xrs, 
   }
 }
 
+// The same from a table of row pointers (a null row reads as zeros).
+template <int MB, int NT>
+__device__ __forceinline__ void stage_x_rows(uint4* xsh, const uint16_t* const* xr, int c0, int nch, int K, int t) {
+  constexpr int SEG = XSeg<MB>::SEG;
+  for (int e = t; e < XSeg<MB>::ELEMS; e += NT) {
+    const int m = e / (SEG * 64), u = (e / 64) % SEG, l = e % 64;
+    const int c = c0 + u, k = c * DKC + l * 8;
+    const uint16_t* row = xr[m];
+    xsh[e] = (row != nullptr && c < nch && k < K) ? *reinterpret_cast<const uint4*>(row + k) : make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
 constexpr int SW = 16;  // waves (= rows of W) per workgroup of the base kernel
 
-// Base product of one linear of the group: y[m][n] = <x[m], W[n]> for m < M,
-// one wave per row n of W.  Small work units let the hardware dispatcher
-// balance the HBM stream across the chip; the x rows are shared by the
-// workgroup's 16 rows through LDS.  Writes y_off and y_on (the LoRA update of
-// y_on, when there is one, is added by lora_update_kernel afterwards).
+// Base product of one weight of the launch: y[m][n] = <x[m], W[n]> for the
+// rows of the row table, one wave per row n of W.  Small work units let the
+// hardware dispatcher balance the HBM stream across the chip; the x rows are
+// shared by the workgroup's 16 rows of W through LDS.  Each output row is
+// written to its first (ya) and second (yb) destination when present: for a
+// single linear these are y_off and the base part of y_on (the LoRA update of
+// y_on, when there is one, is added by lora_update_kernel afterwards); for
+// several inputs sharing W they are the inputs' own outputs.
 template <int MB>
-__global__ __launch_bounds__(SW * 64) void gemv_stream_kernel(GroupArgs ga) {
+__global__ __launch_bounds__(SW * 64) void gemv_stream_kernel(StreamArgs sa) {
   constexpr int SEG = XSeg<MB>::SEG;
   __shared__ uint4 xsh[XSeg<MB>::ELEMS];
   const int gi = blockIdx.y;
-  const uint16_t* __restrict__ X = ga.x[gi];
-  const uint16_t* __restrict__ Wt = ga.W[gi];
-  float* __restrict__ y_off = ga.y_off[gi];
-  float* __restrict__ y_on = ga.y_on[gi];
-  const int M = ga.M, N = ga.N, K = ga.K;
+  const uint16_t* __restrict__ Wt = sa.W[gi];
+  const int N = sa.N, K = sa.K;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int n = blockIdx.x * SW + wave;
   const bool row_ok = n < N;
-  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(X, (uint32_t)M * K * 2u);
   const __amdgpu_buffer_rsrc_t wrs = make_rsrc(Wt + (size_t)min(n, N - 1) * K, row_ok ? (uint32_t)K * 2u : 0u);
   const int nch = (K + DKC - 1) / DKC;
 
@@ -259,7 +270,7 @@ __global__ __launch_bounds__(SW * 64) void gemv_stream_kernel(GroupArgs ga) {
     uint4 wb[SEG];
     load_seg(wb, c0);
     if (c0 > 0) __syncthreads();  // every wave is done with the previous x segment
-    stage_x<MB, SW * 64>(xsh, xrs, c0, nch, K, t);
+    stage_x_rows<MB, SW * 64>(xsh, sa.xr[gi], c0, nch, K, t);
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < SEG; ++u)
@@ -269,9 +280,11 @@ __global__ __launch_bounds__(SW * 64) void gemv_stream_kernel(GroupArgs ga) {
   wave_reduce_scatter<MB>(acc, lane);
   if (row_ok && reduced_writer<MB>(lane)) {
     const int m = reduced_index<MB>(lane);
-    if (m < M) {
-      if (y_off) y_off[(size_t)m * N + n] = acc[0];
-      if (y_on) y_on[(size_t)m * N + n] = acc[0];
+    if (m < sa.rows) {
+      float* ya = sa.ya[gi][m];
+      float* yb = sa.yb[gi][m];
+      if (ya) ya[n] = acc[0];
+      if (yb) yb[n] = acc[0];
     }
   }
 }
@@ -388,10 +401,7 @@ __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
 }
 
 template <int MB>
-hipError_t launch_stream_mb(const GroupArgs& g, int rp, hipStream_t stream) {
-  hipLaunchKernelGGL((gemv_stream_kernel<MB>), dim3((g.N + SW - 1) / SW, g.G), dim3(SW * 64), 0, stream, g);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || rp == 0) return e;
+hipError_t launch_update_mb(const GroupArgs& g, int rp, hipStream_t stream) {
   const dim3 grid((g.N + UNB - 1) / UNB, g.G), block(UW * 64);
   switch (rp) {
     case 16: hipLaunchKernelGGL((lora_update_kernel<MB, 16>), grid, block, 0, stream, g); break;
@@ -400,6 +410,8 @@ hipError_t launch_stream_mb(const GroupArgs& g, int rp, hipStream_t stream) {
   }
   return hipGetLastError();
 }
+
+int padded_rank_of(int r) { return r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : 64; }
 
 template <int RP, int NB>
 hipError_t launch_cfg(const GroupArgs& g, hipStream_t stream) {
@@ -422,15 +434,48 @@ hipError_t launch_nb(const GroupArgs& g, int rp, hipStream_t stream) {
 
 }  // namespace
 
+hipError_t launch_gemv_stream(const StreamArgs& a, hipStream_t stream) {
+  const dim3 grid((a.N + SW - 1) / SW, a.G), block(SW * 64);
+  if (a.rows <= 1) hipLaunchKernelGGL((gemv_stream_kernel<1>), grid, block, 0, stream, a);
+  else if (a.rows <= 2) hipLaunchKernelGGL((gemv_stream_kernel<2>), grid, block, 0, stream, a);
+  else if (a.rows <= 4) hipLaunchKernelGGL((gemv_stream_kernel<4>), grid, block, 0, stream, a);
+  else hipLaunchKernelGGL((gemv_stream_kernel<8>), grid, block, 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_lora_update(const GroupArgs& g, hipStream_t stream) {
+  const int rp = padded_rank_of(g.r);
+  if (rp == 0) return hipSuccess;
+  if (g.M <= 1) return launch_update_mb<1>(g, rp, stream);
+  if (g.M <= 2) return launch_update_mb<2>(g, rp, stream);
+  if (g.M <= 4) return launch_update_mb<4>(g, rp, stream);
+  return launch_update_mb<8>(g, rp, stream);
+}
+
 hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream) {
   bool any_on = false;
   for (int i = 0; i < g.G; ++i) any_on = any_on || g.y_on[i] != nullptr;
   const int r = any_on ? g.r : 0;
   const int rp = r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : 64;
-  if (g.M <= 1) return launch_stream_mb<1>(g, rp, stream);
-  if (g.M <= 2) return launch_stream_mb<2>(g, rp, stream);
-  if (g.M <= 4) return launch_stream_mb<4>(g, rp, stream);
-  if (g.M <= 8) return launch_stream_mb<8>(g, rp, stream);
+  if (g.M <= kStreamRows) {
+    // base product of every member into y_off and y_on, then the LoRA update of y_on
+    StreamArgs sa{};
+    sa.G = g.G;
+    sa.rows = g.M;
+    sa.N = g.N;
+    sa.K = g.K;
+    for (int i = 0; i < g.G; ++i) {
+      sa.W[i] = g.W[i];
+      for (int m = 0; m < g.M; ++m) {
+        sa.xr[i][m] = g.x[i] + (size_t)m * g.K;
+        sa.ya[i][m] = g.y_off[i] ? g.y_off[i] + (size_t)m * g.N : nullptr;
+        sa.yb[i][m] = g.y_on[i] ? g.y_on[i] + (size_t)m * g.N : nullptr;
+      }
+    }
+    hipError_t e = launch_gemv_stream(sa, stream);
+    if (e != hipSuccess || rp == 0) return e;
+    return launch_lora_update(g, stream);
+  }
   // The widest column block that still gives at least one workgroup per CU:
   // wider blocks amortise the per-workgroup reads of A over more of W.
   const long wg64 = (long)((g.N + 63) / 64) * g.G;

@@ -176,6 +176,53 @@ def test_lora_linear_group_rejects(kw, code):
     assert _grp(**kw) == code
 
 
+def _multi(x_off=P, W=P, n_on=2, xs=(P, P), As=(P, P), Bs=(P, P), ss=(2.0, 2.0), M=4, N=64, K=64, r=8,
+           y_off=P + 0x2000, yn=(P + 0x3000, P + 0x4000)):
+    def arr(v):
+        if v is None:
+            return None
+        a = (ctypes.c_void_p * max(len(v), 1))()
+        for i, p in enumerate(v):
+            a[i] = p
+        return a
+    svals = None if ss is None else (ctypes.c_float * max(len(ss), 1))(*ss)
+    return H.lib().hydra_lora_linear_multi(x_off, W, n_on, arr(xs), arr(As), arr(Bs), svals, M, N, K, r, y_off,
+                                           arr(yn), None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(W=None), H.HYDRA_ERR_NULL),
+    (dict(n_on=-1), H.HYDRA_ERR_SHAPE),
+    (dict(n_on=5), H.HYDRA_ERR_SHAPE),
+    (dict(y_off=None), H.HYDRA_ERR_NULL),                       # x_off without y_off
+    (dict(x_off=None), H.HYDRA_ERR_NULL),                       # y_off without x_off
+    (dict(x_off=None, y_off=None, n_on=0), H.HYDRA_ERR_NULL),   # nothing to compute
+    (dict(xs=None), H.HYDRA_ERR_NULL),
+    (dict(ss=None), H.HYDRA_ERR_NULL),
+    (dict(As=None), H.HYDRA_ERR_NULL),
+    (dict(xs=(P, None)), H.HYDRA_ERR_NULL),
+    (dict(Bs=(P, None)), H.HYDRA_ERR_NULL),
+    (dict(yn=(P + 0x3000, None)), H.HYDRA_ERR_NULL),
+    (dict(K=20), H.HYDRA_ERR_SHAPE),
+    (dict(r=65), H.HYDRA_ERR_SHAPE),
+    (dict(M=0), H.HYDRA_ERR_SHAPE),
+    (dict(W=P8), H.HYDRA_ERR_ALIGN),
+    (dict(x_off=P8), H.HYDRA_ERR_ALIGN),
+    (dict(xs=(P, P8)), H.HYDRA_ERR_ALIGN),
+    (dict(As=(P8, P)), H.HYDRA_ERR_ALIGN),
+    (dict(yn=(P + 0x3000, P + 0x4002)), H.HYDRA_ERR_ALIGN),
+    (dict(yn=(P + 0x2000, P + 0x4000)), H.HYDRA_ERR_SHAPE),    # y_on[0] == y_off
+    (dict(yn=(P + 0x3000, P + 0x3000)), H.HYDRA_ERR_SHAPE),    # y_on[0] == y_on[1]
+])
+def test_lora_linear_multi_rejects(kw, code):
+    assert _multi(**kw) == code
+
+
+def test_lora_linear_multi_adapters_unused_at_rank_zero():
+    """r == 0: A and B may be NULL arrays; validation then fails only on the deliberate bad alignment."""
+    assert _multi(r=0, As=None, Bs=None, W=P8) == H.HYDRA_ERR_ALIGN
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(h=None), H.HYDRA_ERR_NULL),
     (dict(values=None), H.HYDRA_ERR_NULL),

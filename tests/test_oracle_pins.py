@@ -111,6 +111,72 @@ def test_lora_linear_adapter_selection():
     assert not np.allclose(on_a, on_b)
 
 
+def _multi_case(seed, M=3, K=8, N=5, r=2, n_on=2):
+    rng = np.random.default_rng(seed)
+    x_off = _int_bf16(rng, (M, K))
+    W = _int_bf16(rng, (N, K))
+    xs = [_int_bf16(rng, (M, K)) for _ in range(n_on)]
+    As = [_int_bf16(rng, (r, K)) for _ in range(n_on)]
+    Bs = [_int_bf16(rng, (N, r)) for _ in range(n_on)]
+    ss = [2.0, -0.5, 0.25, 1.0][:n_on]
+    return x_off, W, xs, As, Bs, ss
+
+
+def _multi_pins_hold(fn):
+    """True when fn reproduces the exact per-pass brute force (used to show the pin catches mistakes)."""
+    for seed in (31, 32):
+        x_off, W, xs, As, Bs, ss = _multi_case(seed)
+        y_off, y_ons = fn(x_off[0], W[0], [x[0] for x in xs], [a[0] for a in As], [b[0] for b in Bs], ss)
+        e_off, _ = _frac_lora(x_off[1], W[1], As[0][1], Bs[0][1], 0.0)
+        if not np.array_equal(y_off, np.array([[float(v) for v in row] for row in e_off])):
+            return False
+        for a in range(len(xs)):
+            _, e_on = _frac_lora(xs[a][1], W[1], As[a][1], Bs[a][1], ss[a])
+            if not np.array_equal(y_ons[a], np.array([[float(v) for v in row] for row in e_on])):
+                return False
+    return True
+
+
+def test_lora_linear_multi_exact_per_pass_bruteforce():
+    """Several passes over one W (Alg. 2): each output is its own input's exact product with its own adapter."""
+    assert _multi_pins_hold(O.lora_linear_multi_ref)
+
+
+def test_lora_linear_multi_merged_weight_per_adapter():
+    c = [gen_linear(40 + i, M=7, K=64, N=24, r=4, s=[2.0, 0.5][i]) for i in range(2)]
+    off = gen_linear(42, M=7, K=64, N=24, r=4)
+    y_off, y_ons = O.lora_linear_multi_ref(off.x, c[0].W, [c[0].x, c[1].x], [c[0].A, c[1].A], [c[0].B, c[1].B],
+                                           [c[0].s, c[1].s])
+    Wd = O.bf16_to_f64(c[0].W)
+    assert np.max(np.abs(y_off - O.bf16_to_f64(off.x) @ Wd.T)) == 0.0
+    for i in range(2):
+        merged = Wd + c[i].s * (O.bf16_to_f64(c[i].B) @ O.bf16_to_f64(c[i].A))
+        expect = O.bf16_to_f64(c[i].x) @ merged.T
+        assert np.max(np.abs(y_ons[i] - expect)) <= 1e-12 * np.max(np.abs(expect))
+    none_off, only_off = O.lora_linear_multi_ref(None, c[0].W, [], [], [], [])
+    assert none_off is None and only_off == []
+
+
+def _mut_multi_swapped_adapters(x_off, W, xs, As, Bs, ss):
+    return O.lora_linear_multi_ref(x_off, W, xs, As[::-1], Bs[::-1], ss)
+
+
+def _mut_multi_off_from_first_on_input(x_off, W, xs, As, Bs, ss):
+    _, y_ons = O.lora_linear_multi_ref(x_off, W, xs, As, Bs, ss)
+    y_off, _ = O.lora_linear_multi_ref(xs[0], W, [], [], [], [])
+    return y_off, y_ons
+
+
+def _mut_multi_shared_input(x_off, W, xs, As, Bs, ss):
+    return O.lora_linear_multi_ref(x_off, W, [xs[0]] * len(xs), As, Bs, ss)
+
+
+@pytest.mark.parametrize("mut", [_mut_multi_swapped_adapters, _mut_multi_off_from_first_on_input,
+                                 _mut_multi_shared_input])
+def test_pins_catch_multi_mutations(mut):
+    assert not _multi_pins_hold(mut)
+
+
 # ---------------------------------------------------------------- log-softmax / gather
 
 def test_log_softmax_rows_normalise():

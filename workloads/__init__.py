@@ -168,6 +168,49 @@ def gen_logits(seed: int, M: int, V: int, noise_std: float = 0.1, logit_std: flo
 
 
 @dataclasses.dataclass
+class MultiCase:
+    """One W shared by a LoRA-off input and n_on LoRA-on inputs with their own adapters."""
+    name: str
+    W: np.ndarray                 # [N x K] bf16 bits
+    x_off: Optional[np.ndarray]   # [M x K] or None
+    x_on: List[np.ndarray]        # n_on x [M x K]
+    A: List[np.ndarray]           # n_on x [r x K]
+    B: List[np.ndarray]           # n_on x [N x r]
+    s: List[float]
+
+    @property
+    def M(self) -> int:
+        return (self.x_off if self.x_off is not None else self.x_on[0]).shape[0]
+
+    @property
+    def K(self) -> int:
+        return self.W.shape[1]
+
+    @property
+    def N(self) -> int:
+        return self.W.shape[0]
+
+    @property
+    def r(self) -> int:
+        return self.A[0].shape[0] if self.A else 0
+
+
+def gen_multi(seed: int, M: int, K: int, N: int, r: int, n_on: int, with_off: bool = True,
+              scales=(2.0, 2.0, 2.0, 2.0), name: str = "multi") -> MultiCase:
+    """Draw order: W, then x_off (when present), then (x_on, A, B) per adapter.  W, A ~ N(0, 1/K),
+    B ~ N(0, 1/r), inputs ~ N(0, 1), as for the single linear."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    W = _normal_bf16(rng, (N, K), (1.0 / K) ** 0.5)
+    x_off = _normal_bf16(rng, (M, K), 1.0) if with_off else None
+    xs, As, Bs = [], [], []
+    for _ in range(n_on):
+        xs.append(_normal_bf16(rng, (M, K), 1.0))
+        As.append(_normal_bf16(rng, (r, K), (1.0 / K) ** 0.5))
+        Bs.append(_normal_bf16(rng, (N, r), (1.0 / max(r, 1)) ** 0.5))
+    return MultiCase(name, W, x_off, xs, As, Bs, [float(v) for v in scales[:n_on]])
+
+
+@dataclasses.dataclass
 class ScoreCase:
     """Two-head scoring input: final hidden h[M x K], CLM head W_lm[V x K] + LoRA, RM head w_rm[K]."""
     h: np.ndarray
@@ -252,6 +295,8 @@ WORKLOADS = {
     "prefill_layer": dict(seed=3, M=2048, proj=PREFILL_PROJ, r=16, s=2.0),
     "two_head_score": dict(seed=4, n_seq=4, seq_len=512, K=4096, V=32000, r=16, s=2.0),
     "ppo_advantages": dict(seed=5, n_seq=4, seq_len=512, K=4096, start=0, beta=0.02, gamma=1.0, lam=0.95),
+    # one decode projection serving the reference (LoRA off), actor and critic passes (M = 4 each)
+    "decode_multi": dict(seed=6, M=4, K=4096, N=4096, r=16, n_on=2),
 }
 
 
@@ -266,6 +311,8 @@ def make(name: str, M: Optional[int] = None):
         return gen_linears(w["seed"], M or w["M"], w["proj"], w["r"], w["s"])
     if name == "two_head_score":
         return gen_score_head(w["seed"], w["n_seq"], w["seq_len"], w["K"], w["V"], w["r"], w["s"])
+    if name == "decode_multi":
+        return gen_multi(w["seed"], M or w["M"], w["K"], w["N"], w["r"], w["n_on"], name=name)
     if name == "ppo_advantages":
         return gen_advantages(w["seed"], w["n_seq"], w["seq_len"], w["K"], w["start"], w["beta"], w["gamma"], w["lam"])
     raise KeyError(name)
