@@ -61,7 +61,7 @@ typedef enum {
 } hydra_status;
 
 /* Largest LoRA rank accepted. */
-#define HYDRA_MAX_RANK 64
+#define HYDRA_MAX_RANK 128
 
 /*
  * hydra_lora_linear -- the LoRA-switchable linear layer.
@@ -78,12 +78,44 @@ typedef enum {
  *   y_on  [M x N] fp32   out: x W^T + s (x A^T) B^T  (NULL: not written)
  * At least one output must be non-NULL.  Requires M, N, K >= 1, K % 8 == 0,
  * K <= 2^21, 0 <= r <= HYDRA_MAX_RANK, and M, N below 2^31.  With r == 0, y_on equals
- * y_off.  M <= 16 selects the bandwidth-bound (decode) kernel, larger M the
- * MFMA GEMM; both compute the same function.
+ * y_off.  M <= 16 selects the bandwidth-bound (decode) kernels, larger M the
+ * MFMA GEMM; both compute the same function.  At M > 16 with y_on and r > 64
+ * the update needs the pre-pass workspace of hydra_lora_linear_ws: this call
+ * then returns HYDRA_ERR_WORKSPACE and launches nothing.
  */
 hydra_status hydra_lora_linear(const uint16_t* x, const uint16_t* W, const uint16_t* A, const uint16_t* B,
                                float s, int64_t M, int64_t N, int64_t K, int64_t r,
                                float* y_off, float* y_on, void* stream);
+
+/*
+ * hydra_lora_linear_workspace_bytes -- device workspace that hydra_lora_linear_ws
+ * needs for M rows, N outputs and rank r (0 when none is needed: r == 0).
+ * Writes *bytes.  HYDRA_ERR_NULL for a NULL `bytes`, HYDRA_ERR_SHAPE for M or
+ * N < 1 or r outside [0, HYDRA_MAX_RANK].
+ */
+hydra_status hydra_lora_linear_workspace_bytes(int64_t M, int64_t N, int64_t r, size_t* bytes);
+
+/*
+ * hydra_lora_linear_ws -- hydra_lora_linear with a caller-provided workspace,
+ * which lets the MFMA GEMM (M > 16) take the LoRA update from a pre-pass:
+ * s x A^T is computed once per row (instead of once per 256-column tile) as
+ * bf16 hi and lo parts, and added with B as 2 RP more k values of the GEMM
+ * (RP = r rounded up to 16, 32, 64 or 128) after y_off has been stored.
+ * This is the path for the paper's rank 128 (App. B) and the faster one at
+ * every rank.  Defined by: the same passages as hydra_lora_linear.
+ *
+ *   workspace, workspace_bytes   device memory of at least
+ *       hydra_lora_linear_workspace_bytes(M, N, r) bytes, 16-byte aligned,
+ *       contents ignored and overwritten; NULL allowed when that size is 0 or
+ *       when no GEMM update runs (M <= 16, no y_on, or r == 0).
+ * Other arguments and rules as in hydra_lora_linear; HYDRA_ERR_WORKSPACE for a
+ * workspace that is needed and too small, HYDRA_ERR_ALIGN for a misaligned one.
+ * y_off has the bits of hydra_lora_linear's; y_on agrees with it to the
+ * rounding of T (different summation order).
+ */
+hydra_status hydra_lora_linear_ws(const uint16_t* x, const uint16_t* W, const uint16_t* A, const uint16_t* B,
+                                  float s, int64_t M, int64_t N, int64_t K, int64_t r, float* y_off, float* y_on,
+                                  void* workspace, size_t workspace_bytes, void* stream);
 
 /* Largest number of linears in one hydra_lora_linear_group call. */
 #define HYDRA_MAX_GROUP 8

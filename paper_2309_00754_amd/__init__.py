@@ -20,6 +20,8 @@ from ._binding import (  # noqa: F401
     LIB_PATH,
     hydra_lora_linear,
     hydra_lora_linear_group,
+    hydra_lora_linear_workspace_bytes,
+    hydra_lora_linear_ws,
     hydra_lora_linear_multi,
     hydra_ppo_advantages,
     hydra_score,

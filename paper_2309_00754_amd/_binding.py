@@ -22,13 +22,15 @@ HYDRA_ERR_ALIGN = -3
 HYDRA_ERR_UNSUPPORTED = -4
 HYDRA_ERR_WORKSPACE = -5
 HYDRA_ERR_HIP = -6
-HYDRA_MAX_RANK = 64
+HYDRA_MAX_RANK = 128
 HYDRA_MAX_GROUP = 8
 HYDRA_MAX_ADAPTERS = 4
 
 # Every symbol include/hydra.h declares.
 EXPORTED = (
     "hydra_lora_linear",
+    "hydra_lora_linear_workspace_bytes",
+    "hydra_lora_linear_ws",
     "hydra_lora_linear_group",
     "hydra_lora_linear_multi",
     "hydra_score_workspace_bytes",
@@ -73,6 +75,11 @@ def lib() -> ctypes.CDLL:
     L.hydra_lora_linear_group.argtypes = [_i64, _pp, _pp, _pp, _pp, ctypes.POINTER(ctypes.c_float), _i64, _i64, _i64,
                                           _i64, _pp, _pp, _vp]
     L.hydra_lora_linear_group.restype = ctypes.c_int
+    L.hydra_lora_linear_workspace_bytes.argtypes = [_i64, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]
+    L.hydra_lora_linear_workspace_bytes.restype = ctypes.c_int
+    L.hydra_lora_linear_ws.argtypes = [_vp, _vp, _vp, _vp, _f32, _i64, _i64, _i64, _i64, _vp, _vp, _vp,
+                                       ctypes.c_size_t, _vp]
+    L.hydra_lora_linear_ws.restype = ctypes.c_int
     L.hydra_lora_linear_multi.argtypes = [_vp, _vp, _i64, _pp, _pp, _pp, ctypes.POINTER(ctypes.c_float), _i64, _i64,
                                           _i64, _i64, _vp, _pp, _vp]
     L.hydra_lora_linear_multi.restype = ctypes.c_int
@@ -165,6 +172,36 @@ def hydra_lora_linear(x, W, A, B, s: float, y_off=None, y_on=None, stream=None) 
     st = lib().hydra_lora_linear(_ptr(x), _ptr(W), _ptr(A), _ptr(B), float(s), M, N, K, r,
                                  _ptr(y_off), _ptr(y_on), _stream_handle(stream))
     _check(st, "hydra_lora_linear")
+
+
+def hydra_lora_linear_workspace_bytes(M: int, N: int, r: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().hydra_lora_linear_workspace_bytes(int(M), int(N), int(r), ctypes.byref(out)),
+           "hydra_lora_linear_workspace_bytes")
+    return int(out.value)
+
+
+def hydra_lora_linear_ws(x, W, A, B, s: float, y_off=None, y_on=None, workspace=None, stream=None) -> None:
+    """hydra_lora_linear with the pre-pass workspace (see include/hydra.h); allocates one if none is given."""
+    torch = _torch()
+    bf = _bf16_types()
+    M, K = x.shape
+    N = W.shape[0]
+    r = 0 if A is None else A.shape[0]
+    _need(x, "x", bf)
+    _need(W, "W", bf, (N, K))
+    _need(A, "A", bf, (r, K))
+    _need(B, "B", bf, (N, r))
+    _need(y_off, "y_off", (torch.float32,), (M, N))
+    _need(y_on, "y_on", (torch.float32,), (M, N))
+    need = hydra_lora_linear_workspace_bytes(M, N, r)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    _need(workspace, "workspace", (torch.uint8,))
+    nbytes = 0 if workspace is None else workspace.numel()
+    st = lib().hydra_lora_linear_ws(_ptr(x), _ptr(W), _ptr(A), _ptr(B), float(s), M, N, K, r, _ptr(y_off),
+                                    _ptr(y_on), _ptr(workspace), nbytes, _stream_handle(stream))
+    _check(st, "hydra_lora_linear_ws")
 
 
 def _ptr_array(ts):

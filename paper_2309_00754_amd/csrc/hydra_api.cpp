@@ -24,14 +24,32 @@ int64_t score_tiles(int64_t V) { return (V + hydra::kScoreTileN - 1) / hydra::kS
 size_t score_part_bytes(int64_t M, int64_t V) { return size_t(M) * size_t(score_tiles(V)) * sizeof(float4); }
 // Workspace of hydra_score: per (row, column tile) partials, then per row the
 // gathered token logits (2 fp32), then (16-byte aligned) per row the bf16 hi
-// and lo parts of s * h A^T (room for 2 x 64 bf16), then per vocabulary row
-// B zero padded to the padded rank (room for 64 bf16).
+// and lo parts of s * h A^T (room for 2 x 128 bf16), then per vocabulary row
+// B zero padded to the padded rank (room for 128 bf16), then (16-byte
+// aligned) the LoRA pre-pass's partial sums over K chunks (room for 8 chunks
+// x 128 fp32 per row).
 size_t score_zt_offset(int64_t M, int64_t V) { return score_part_bytes(M, V); }
 size_t score_ts_offset(int64_t M, int64_t V) {
   return (score_zt_offset(M, V) + size_t(M) * 2 * sizeof(float) + 15) & ~size_t(15);
 }
 size_t score_bp_offset(int64_t M, int64_t V) { return score_ts_offset(M, V) + size_t(M) * 2 * HYDRA_MAX_RANK * 2; }
-size_t score_ws_bytes(int64_t M, int64_t V) { return score_bp_offset(M, V) + size_t(V) * HYDRA_MAX_RANK * 2; }
+size_t score_part_offset(int64_t M, int64_t V) {
+  return (score_bp_offset(M, V) + size_t(V) * HYDRA_MAX_RANK * 2 + 15) & ~size_t(15);
+}
+size_t score_ws_bytes(int64_t M, int64_t V) {
+  return score_part_offset(M, V) + size_t(hydra::kTpreMaxChunks) * size_t(M) * HYDRA_MAX_RANK * 4;
+}
+
+// Workspace of the GEMM's LoRA pre-pass: ts [M][2 RP] bf16, then (16-byte
+// aligned) bp [N][RP] bf16, then (16-byte aligned) the partial sums over K
+// chunks [8][M][RP] fp32.
+size_t linear_bp_offset(int64_t M, int rp) { return (size_t(M) * 2 * rp * 2 + 15) & ~size_t(15); }
+size_t linear_part_offset(int64_t M, int64_t N, int rp) {
+  return (linear_bp_offset(M, rp) + size_t(N) * rp * 2 + 15) & ~size_t(15);
+}
+size_t linear_ws_bytes(int64_t M, int64_t N, int rp) {
+  return rp == 0 ? 0 : linear_part_offset(M, N, rp) + size_t(hydra::kTpreMaxChunks) * size_t(M) * rp * 4;
+}
 
 }  // namespace
 
@@ -88,6 +106,7 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
     if (!any_on) g.r = 0;
     return from_hip(hydra::launch_lora_gemv_group(g, st));
   }
+  if (any_on && hydra::padded_rank(g.r) > 64) return HYDRA_ERR_WORKSPACE;  // see hydra_lora_linear_ws
   for (int i = 0; i < g.G; ++i) {
     hydra::LinearArgs a{};
     a.x = g.x[i];
@@ -105,6 +124,52 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
     if (e != hipSuccess) return HYDRA_ERR_HIP;
   }
   return HYDRA_OK;
+}
+
+hydra_status hydra_lora_linear_workspace_bytes(int64_t M, int64_t N, int64_t r, size_t* bytes) {
+  if (!bytes) return HYDRA_ERR_NULL;
+  if (!dim_ok(M) || !dim_ok(N) || r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
+  *bytes = linear_ws_bytes(M, N, hydra::padded_rank(int(r)));
+  return HYDRA_OK;
+}
+
+hydra_status hydra_lora_linear_ws(const uint16_t* x, const uint16_t* W, const uint16_t* A, const uint16_t* B,
+                                  float s, int64_t M, int64_t N, int64_t K, int64_t r, float* y_off, float* y_on,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  if (!x || !W) return HYDRA_ERR_NULL;
+  if (!y_off && !y_on) return HYDRA_ERR_NULL;
+  if (!dim_ok(M) || !dim_ok(N) || !dim_ok(K) || (K % 8) != 0 || K > kMaxK) return HYDRA_ERR_SHAPE;
+  if (r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
+  const bool lora = y_on && r > 0;
+  if (lora && (!A || !B)) return HYDRA_ERR_NULL;
+  if (y_off && y_off == y_on) return HYDRA_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(W, 16)) return HYDRA_ERR_ALIGN;
+  if (lora && (!aligned(A, 16) || !aligned(B, 2))) return HYDRA_ERR_ALIGN;
+  if ((y_off && !aligned(y_off, 4)) || (y_on && !aligned(y_on, 4))) return HYDRA_ERR_ALIGN;
+  if (M <= kDecodeMaxRows || !lora)  // no GEMM update: the workspace is not used
+    return hydra_lora_linear_group(1, &x, &W, &A, &B, &s, M, N, K, lora ? r : 0, &y_off, &y_on, stream);
+  const int rp = hydra::padded_rank(int(r));
+  const size_t need = linear_ws_bytes(M, N, rp);
+  if (!workspace) return HYDRA_ERR_NULL;
+  if (workspace_bytes < need) return HYDRA_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return HYDRA_ERR_ALIGN;
+  hydra::LinearArgs a{};
+  a.x = x;
+  a.W = W;
+  a.A = A;
+  a.B = B;
+  a.s = s;
+  a.M = int(M);
+  a.N = int(N);
+  a.K = int(K);
+  a.r = int(r);
+  a.y_off = y_off;
+  a.y_on = y_on;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  return from_hip(hydra::launch_lora_gemm_tpre(a, reinterpret_cast<uint16_t*>(ws),
+                                               reinterpret_cast<uint16_t*>(ws + linear_bp_offset(M, rp)),
+                                               reinterpret_cast<float*>(ws + linear_part_offset(M, N, rp)),
+                                               reinterpret_cast<hipStream_t>(stream)));
 }
 
 hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, int64_t n_on,
@@ -235,6 +300,8 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
   g.zt = zt;
   g.ts = ts;
   g.bp = bp;
+  g.bp_buf = bp;
+  g.tpart = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + score_part_offset(M, V));
   g.ntn = int(score_tiles(V));
   hipError_t e = hydra::launch_score_gemm(g, st);
   if (e != hipSuccess) return HYDRA_ERR_HIP;

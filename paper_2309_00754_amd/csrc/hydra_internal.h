@@ -45,6 +45,35 @@ struct StreamArgs {
   int G, rows, N, K;
 };
 
+// Pre-pass of the LoRA update for the MFMA GEMMs: ts = bf16 hi and lo parts
+// of s * x A^T ([M x 2 RP], hi in columns 0..RP, lo in RP..2 RP) and bp = B
+// zero padded to RP columns ([N x RP]), RP = padded rank.
+struct TpreArgs {
+  const uint16_t* x;  // [M x K] bf16
+  const uint16_t* A;  // [r x K] bf16
+  const uint16_t* B;  // [N x r] bf16
+  float s;
+  int M, N, K, r;
+  uint16_t* ts;
+  uint16_t* bp;       // used only when B itself cannot serve (r != RP or B not 16-byte aligned)
+  float* part;        // [kTpreMaxChunks x M x RP] fp32 partial sums over K chunks
+};
+// K is split into at most kTpreMaxChunks chunks of at least 1024, so that
+// the pre-pass spreads over many workgroups; the partial products are then
+// added in chunk order (deterministic).
+constexpr int kTpreMaxChunks = 8;
+inline void tpre_chunks(int K, int& nkc, int& kch) {
+  const int want = (K + 1023) / 1024;
+  nkc = want < kTpreMaxChunks ? want : kTpreMaxChunks;
+  kch = ((K + nkc - 1) / nkc + 31) / 32 * 32;  // a multiple of the 32-wide k-step
+  nkc = (K + kch - 1) / kch;
+}
+// Launches the pre-pass; *bp_used is where the padded B rows are (a.bp, or
+// a.B itself when it already has that layout).
+hipError_t launch_lora_tpre(const TpreArgs& a, int rp, const uint16_t** bp_used, hipStream_t stream);
+// Padded rank: the smallest of 16, 32, 64, 128 that holds r (0 for r == 0).
+inline int padded_rank(int r) { return r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : r <= 64 ? 64 : 128; }
+
 // Per (row, column tile) partial log-sum-exp state written by the fused
 // CLM-head GEMM: (max_off, sumexp_off, max_on, sumexp_on).
 struct ScoreGemmArgs {
@@ -53,7 +82,9 @@ struct ScoreGemmArgs {
   float4* part;            // [M x ntn]
   float* zt;               // [M x 2]: (z_off[token], z_on[token])
   uint16_t* ts;            // [M x 2 RP] bf16: hi and lo parts of s * h A^T (RP = padded rank)
-  uint16_t* bp;            // [V x RP] bf16: B zero padded to RP columns
+  const uint16_t* bp;      // [V x RP] bf16: B zero padded to RP columns (or B itself when r == RP)
+  uint16_t* bp_buf;        // room for the padded copy
+  float* tpart;            // LoRA pre-pass partial sums over K chunks
   int ntn;                 // number of column tiles
   int ntm;                 // number of row tiles (set by the launcher)
 };
@@ -115,6 +146,9 @@ struct GaeArgs {
 constexpr int kScoreTileN = 256;
 
 hipError_t launch_lora_gemm(const LinearArgs& a, hipStream_t stream);
+// The same with the LoRA update from the pre-pass: ts [M x 2 RP] and bp [N x RP]
+// bf16 workspace (RP = padded rank of a.r, up to 128).
+hipError_t launch_lora_gemm_tpre(const LinearArgs& a, uint16_t* ts, uint16_t* bp, float* part, hipStream_t stream);
 hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream);
 // y[m] = x[m] W^T for the rows of a StreamArgs (rows <= kStreamRows).
 hipError_t launch_gemv_stream(const StreamArgs& a, hipStream_t stream);

@@ -73,6 +73,11 @@ struct GemmArgs {
   LinearArgs lin;
   int ntm, ntn;
   int vec4;  // outputs may be written with 16-byte stores (N % 4 == 0, 16-byte aligned)
+  // LoRA update from a pre-pass (TPRE kernels): ts [M x 2 RP] bf16 hi | lo parts
+  // of s x A^T, bp [N x RP] bf16 B zero padded; nls extra slabs (0: no update)
+  const uint16_t* ts;
+  const uint16_t* bp;
+  int nls;
 };
 
 // Workgroup id -> (row tile, column tile).  Consecutive workgroup ids are
@@ -112,9 +117,14 @@ __device__ __forceinline__ void lds_barrier() {
 template <int V>
 using IC = std::integral_constant<int, V>;
 
-template <int RP>
+// RP: padded rank.  TPRE: the LoRA update comes from the pre-pass in the
+// workspace and runs as g.nls extra slabs of the ring after the LoRA-off
+// result has been stored; otherwise T is accumulated in the main loop and the
+// update is applied in the epilogue.
+template <int RP, bool TPRE>
 __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
-  using L = Layout<RP>;
+  constexpr int RA = TPRE ? 0 : RP;  // rows of A in every ring stage
+  using L = Layout<RA>;
   constexpr int NS = L::NSTAGES;
   // One array per pipeline stage, always addressed with compile-time stage
   // indices.
@@ -143,9 +153,11 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   const int nkt = (K + BK - 1) / BK;
   const bool want_on = a.y_on != nullptr;
 
-  constexpr int TJ = RP / 16;
+  constexpr int TJ = RA / 16;
   constexpr int TJ1 = TJ > 0 ? TJ : 1;
-  constexpr int RP2 = RP > 0 ? RP / 2 : 1;
+  constexpr int RP2 = RA > 0 ? RA / 2 : 1;
+  const int nls = TPRE ? g.nls : 0;  // LoRA slabs after the nkt main slabs
+  const int total = nkt + nls;
 
   // Epilogue layout (the stages are free again by then):
   //   stage 0: Ts [BM][2 RP] bf16, s*T split into hi (columns 0..RP) and lo (RP..2RP)
@@ -162,7 +174,7 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
     // register).
     uint32_t breg[RP2];
 
-    if constexpr (RP > 0) {
+    if constexpr (RA > 0) {
       static_assert(BN == NT - NTM, "one B row per copy thread");
       const __amdgpu_buffer_rsrc_t brs = make_rsrc(a.B + (size_t)n0 * a.r, (uint32_t)min(BN, N - n0) * a.r * 2u);
       uint32_t v[RP];
@@ -184,14 +196,14 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
     // blocks 16..47, A blocks 48.., copy wave cw takes blocks cw, cw + 4, ...
     const i32x4_t xr = make_rsrc_raw(a.x + (size_t)m0 * K, (uint32_t)min(BM, M - m0) * K * 2u);
     const i32x4_t wrs = make_rsrc_raw(a.W + (size_t)n0 * K, (uint32_t)min(BN, N - n0) * K * 2u);
-    const i32x4_t arsrc = make_rsrc_raw(a.A, (uint32_t)min(a.r, RP) * K * 2u);
+    const i32x4_t arsrc = make_rsrc_raw(RA > 0 ? a.A : nullptr, RA > 0 ? (uint32_t)min(a.r, RA) * K * 2u : 0u);
     const int row_bytes = K * 2;
     // Lane i fills LDS chunk i & 7 of row 8 ci + i / 8; every block ci this
     // wave copies has the parity of cw, so the global chunk it fetches is
     // (i & 7) ^ ((row / 2) % 8) = (i & 7) ^ (4 (cw & 1) + i / 16).
     const int c = (lane & 7) ^ (((cw & 1) << 2) | (lane >> 4));  // global chunk fetched by this lane
     const int rl = lane >> 3;                                    // row within the 8-row copy
-    constexpr int XD = BM / 8, WD = BN / 8, AD = RP / 8;
+    constexpr int XD = BM / 8, WD = BN / 8, AD = RA / 8;
     static_assert(XD % 4 == 0 && WD % 4 == 0, "x and W blocks split evenly over the copy waves");
     constexpr int XJ = XD / 4, WJ = WD / 4;
     constexpr int DMAX = XJ + WJ + (AD + 3) / 4;  // copies per slab of copy wave 0
@@ -215,6 +227,33 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
         }
       }
     };
+    // LoRA slab ls (TPRE): k in [64 ls, 64 ls + 64) of the 2 RP-long update; the
+    // x-side rows are the tile's rows of ts ([hi | lo]), the W-side rows its
+    // rows of bp, read at column k mod RP ([Bp | Bp]); k >= 2 RP reads zeros.
+    // Same number of copies per wave as a main slab.
+    const i32x4_t tsr = make_rsrc_raw(TPRE ? g.ts + (size_t)m0 * 2 * RP : nullptr,
+                                      TPRE ? (uint32_t)min(BM, M - m0) * 2 * RP * 2u : 0u);
+    const i32x4_t bpr = make_rsrc_raw(TPRE ? g.bp + (size_t)n0 * RP : nullptr,
+                                      TPRE ? (uint32_t)min(BN, N - n0) * RP * 2u : 0u);
+    auto issue_lora = [&](uint4* st, int ls) __attribute__((always_inline)) {
+      const int kk = ls * BK + c * 8;
+      const bool kv = kk < 2 * RP;
+      const int kb = RP > 0 ? kk % (RP > 0 ? RP : 1) : 0;
+#pragma unroll
+      for (int j = 0; j < XJ + WJ; ++j) {
+        if (j < XJ) {
+          const int ci = cw + 4 * j;
+          dma16(tsr, st + L::XOFF + ci * 64, kv ? (ci * 8 + rl) * (4 * RP) + kk * 2 : kOutOfRange);
+        } else {
+          const int ci = cw + 4 * (j - XJ);
+          dma16(bpr, st + L::WOFF + ci * 64, kv ? (ci * 8 + rl) * (2 * RP) + kb * 2 : kOutOfRange);
+        }
+      }
+    };
+    auto issue_any = [&](uint4* st, int kt) __attribute__((always_inline)) {
+      if (!TPRE || kt < nkt) issue(st, kt);
+      else issue_lora(st, kt - nkt);
+    };
     // Wait until only the copies of the `later` most recent slabs may still
     // be in flight.
     auto wait_slabs = [&](int later) __attribute__((always_inline)) {
@@ -227,35 +266,36 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
       }
     };
 
-    issue(sm0, 0);
-    if (nkt > 1) issue(sm1, 1);
+    issue_any(sm0, 0);
+    if (total > 1) issue_any(sm1, 1);
     if constexpr (NS == 3) {
-      if (nkt > 2) issue(sm2, 2);
+      if (total > 2) issue_any(sm2, 2);
     }
-    wait_slabs(min(NS - 1, nkt - 1));
+    wait_slabs(min(NS - 1, total - 1));
     lds_barrier();  // slab 0 is in LDS
     // Before barrier kt: slab kt + 1 has landed.  After it: stage kt % NS is
     // no longer read and receives slab kt + NS.
     auto step_copy = [&](uint4* st, int kt) __attribute__((always_inline)) {
-      wait_slabs(min(kt + NS - 1, nkt - 1) - (kt + 1));
+      wait_slabs(min(kt + NS - 1, total - 1) - (kt + 1));
       lds_barrier();
-      if (kt + NS < nkt) issue(st, kt + NS);
+      if (kt + NS < total) issue_any(st, kt + NS);
     };
     if constexpr (NS == 3) {
-      for (int kt = 0; kt < nkt; kt += 3) {
+      for (int kt = 0; kt < total; kt += 3) {
         step_copy(sm0, kt);
-        if (kt + 1 < nkt) step_copy(sm1, kt + 1);
-        if (kt + 2 < nkt) step_copy(sm2, kt + 2);
+        if (kt + 1 < total) step_copy(sm1, kt + 1);
+        if (kt + 2 < total) step_copy(sm2, kt + 2);
       }
     } else {
-      for (int kt = 0; kt < nkt; kt += 2) {
+      for (int kt = 0; kt < total; kt += 2) {
         step_copy(sm0, kt);
-        if (kt + 1 < nkt) step_copy(sm1, kt + 1);
+        if (kt + 1 < total) step_copy(sm1, kt + 1);
       }
     }
     wait_vm<0>();
     lds_barrier();  // every wave is done with the stages
-    if constexpr (RP > 0) {
+    if constexpr (TPRE) return;
+    if constexpr (RA > 0) {
 #pragma unroll
       for (int j = 0; j < RP; j += 2) *reinterpret_cast<uint32_t*>(Bs + tl * RP + j) = breg[j / 2];
     }
@@ -364,20 +404,67 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
     kstep(IC<3>{}, F1, F0, cur, nxt);
   };
 
+  // acc[mi][ni][4 i + e] holds y[wr*64 + mi*32 + l32][wc*128 + ni*32 + 8 i + 4 lh + e]
+  auto store = [&](float* y) __attribute__((always_inline)) {
+#pragma unroll
+    for (int mi = 0; mi < MT; ++mi) {
+      const int row = m0 + wr * WM + mi * 32 + l32;
+      if (row >= M) continue;
+      float* yr = y + (size_t)row * N;
+#pragma unroll
+      for (int ni = 0; ni < NTL; ++ni)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int col = n0 + wc * WN + ni * 32 + 8 * i + 4 * lh;
+          const f32x16_t& v = acc[mi][ni];
+          if (g.vec4 && col + 3 < N) {
+            *reinterpret_cast<float4*>(yr + col) = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (col + e < N) yr[col + e] = v[4 * i + e];
+          }
+        }
+    }
+  };
   lds_barrier();  // slab 0 is in LDS
 #pragma unroll
   for (int r = 0; r < NRM; ++r) read_main(F0, sm0, 0, r);
+  // TPRE: after the last main slab the accumulators are the LoRA-off result;
+  // it is stored there, and the LoRA slabs (whose first fragments the last
+  // main slab's k-step 3 has read) go on adding to the same accumulators.
+  auto after = [&](int kt) __attribute__((always_inline)) {
+    if constexpr (TPRE) {
+      if (kt == nkt - 1 && a.y_off) store(a.y_off);
+    }
+  };
   if constexpr (NS == 3) {
-    for (int kt = 0; kt < nkt; kt += 3) {
+    for (int kt = 0; kt < total; kt += 3) {
       slab(sm0, sm1);
-      if (kt + 1 < nkt) slab(sm1, sm2);
-      if (kt + 2 < nkt) slab(sm2, sm0);
+      after(kt);
+      if (kt + 1 < total) {
+        slab(sm1, sm2);
+        after(kt + 1);
+      }
+      if (kt + 2 < total) {
+        slab(sm2, sm0);
+        after(kt + 2);
+      }
     }
   } else {
-    for (int kt = 0; kt < nkt; kt += 2) {
+    for (int kt = 0; kt < total; kt += 2) {
       slab(sm0, sm1);
-      if (kt + 1 < nkt) slab(sm1, sm0);
+      after(kt);
+      if (kt + 1 < total) {
+        slab(sm1, sm0);
+        after(kt + 1);
+      }
     }
+  }
+  if constexpr (TPRE) {
+    lds_barrier();  // every wave is done with the stages
+    if (a.y_on) store(a.y_on);
+    return;
   }
   lds_barrier();  // every wave is done with the stages before the epilogue reuses them
 
@@ -428,29 +515,6 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
     }
   };
 
-  // acc[mi][ni][4 i + e] holds y[wr*64 + mi*32 + l32][wc*128 + ni*32 + 8 i + 4 lh + e]
-  auto store = [&](float* y) __attribute__((always_inline)) {
-#pragma unroll
-    for (int mi = 0; mi < MT; ++mi) {
-      const int row = m0 + wr * WM + mi * 32 + l32;
-      if (row >= M) continue;
-      float* yr = y + (size_t)row * N;
-#pragma unroll
-      for (int ni = 0; ni < NTL; ++ni)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int col = n0 + wc * WN + ni * 32 + 8 * i + 4 * lh;
-          const f32x16_t& v = acc[mi][ni];
-          if (g.vec4 && col + 3 < N) {
-            *reinterpret_cast<float4*>(yr + col) = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (col + e < N) yr[col + e] = v[4 * i + e];
-          }
-        }
-    }
-  };
   if (a.y_off) store(a.y_off);
   if (a.y_on) {
     apply_lora();
@@ -458,19 +522,27 @@ __global__ __launch_bounds__(NT, 1) void lora_gemm_kernel(GemmArgs g) {
   }
 }
 
-hipError_t launch(const GemmArgs& g, int rp, hipStream_t stream) {
+hipError_t launch(const GemmArgs& g, int rp, bool tpre, hipStream_t stream) {
   const dim3 grid(g.ntm * g.ntn), block(NT);
+  if (tpre) {
+    switch (rp) {
+      case 16: hipLaunchKernelGGL((lora_gemm_kernel<16, true>), grid, block, 0, stream, g); break;
+      case 32: hipLaunchKernelGGL((lora_gemm_kernel<32, true>), grid, block, 0, stream, g); break;
+      case 64: hipLaunchKernelGGL((lora_gemm_kernel<64, true>), grid, block, 0, stream, g); break;
+      case 128: hipLaunchKernelGGL((lora_gemm_kernel<128, true>), grid, block, 0, stream, g); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   switch (rp) {
-    case 0: hipLaunchKernelGGL((lora_gemm_kernel<0>), grid, block, 0, stream, g); break;
-    case 16: hipLaunchKernelGGL((lora_gemm_kernel<16>), grid, block, 0, stream, g); break;
-    case 32: hipLaunchKernelGGL((lora_gemm_kernel<32>), grid, block, 0, stream, g); break;
-    case 64: hipLaunchKernelGGL((lora_gemm_kernel<64>), grid, block, 0, stream, g); break;
+    case 0: hipLaunchKernelGGL((lora_gemm_kernel<0, false>), grid, block, 0, stream, g); break;
+    case 16: hipLaunchKernelGGL((lora_gemm_kernel<16, false>), grid, block, 0, stream, g); break;
+    case 32: hipLaunchKernelGGL((lora_gemm_kernel<32, false>), grid, block, 0, stream, g); break;
+    case 64: hipLaunchKernelGGL((lora_gemm_kernel<64, false>), grid, block, 0, stream, g); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
-
-int padded_rank(int r) { return r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : 64; }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
@@ -483,7 +555,37 @@ hipError_t launch_lora_gemm(const LinearArgs& a, hipStream_t stream) {
   g.ntn = (a.N + BN - 1) / BN;
   g.vec4 = (a.N % 4 == 0) && (!a.y_off || aligned16(a.y_off)) && (!a.y_on || aligned16(a.y_on));
   const int rp = a.y_on ? padded_rank(a.r) : 0;
-  return launch(g, rp, stream);
+  if (rp > 64) return hipErrorInvalidValue;  // needs the pre-pass workspace
+  return launch(g, rp, false, stream);
+}
+
+hipError_t launch_lora_gemm_tpre(const LinearArgs& a, uint16_t* ts, uint16_t* bp, float* part, hipStream_t stream) {
+  const int rp = a.y_on ? padded_rank(a.r) : 0;
+  if (rp == 0) return launch_lora_gemm(a, stream);
+  TpreArgs t{};
+  t.x = a.x;
+  t.A = a.A;
+  t.B = a.B;
+  t.s = a.s;
+  t.M = a.M;
+  t.N = a.N;
+  t.K = a.K;
+  t.r = a.r;
+  t.ts = ts;
+  t.bp = bp;
+  t.part = part;
+  const uint16_t* bp_used = nullptr;
+  hipError_t e = launch_lora_tpre(t, rp, &bp_used, stream);
+  if (e != hipSuccess) return e;
+  GemmArgs g{};
+  g.lin = a;
+  g.ntm = (a.M + BM - 1) / BM;
+  g.ntn = (a.N + BN - 1) / BN;
+  g.vec4 = (a.N % 4 == 0) && (!a.y_off || aligned16(a.y_off)) && aligned16(a.y_on);
+  g.ts = ts;
+  g.bp = bp_used;
+  g.nls = (2 * rp + BK - 1) / BK;
+  return launch(g, rp, true, stream);
 }
 
 }  // namespace hydra

@@ -290,7 +290,9 @@ __global__ __launch_bounds__(SW * 64) void gemv_stream_kernel(StreamArgs sa) {
 }
 
 constexpr int UW = 16;   // waves per workgroup of the LoRA update
-constexpr int UNB = 256; // columns of y_on per workgroup
+// columns of y_on per workgroup (fewer at rank 128, for the registers and LDS
+// that hold the block of B)
+constexpr int update_cols(int rp) { return rp <= 64 ? 256 : 128; }
 constexpr int URW = 8;   // rows of A per wave in the T pass
 
 // y_on += s * T B^T with T = x A^T, for the members of the group that have an
@@ -304,6 +306,7 @@ constexpr int URW = 8;   // rows of A per wave in the T pass
 template <int MB, int RP>
 __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
   constexpr int NT = UW * 64;
+  constexpr int UNB = update_cols(RP);
   constexpr int GR = RP / URW;                     // row groups
   constexpr int GC = UW / GR;                      // chunk groups
   constexpr int VT = URW * MB;                     // partial sums of T per lane
@@ -402,16 +405,16 @@ __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
 
 template <int MB>
 hipError_t launch_update_mb(const GroupArgs& g, int rp, hipStream_t stream) {
-  const dim3 grid((g.N + UNB - 1) / UNB, g.G), block(UW * 64);
+  const int cols = update_cols(rp);
+  const dim3 grid((g.N + cols - 1) / cols, g.G), block(UW * 64);
   switch (rp) {
     case 16: hipLaunchKernelGGL((lora_update_kernel<MB, 16>), grid, block, 0, stream, g); break;
     case 32: hipLaunchKernelGGL((lora_update_kernel<MB, 32>), grid, block, 0, stream, g); break;
-    default: hipLaunchKernelGGL((lora_update_kernel<MB, 64>), grid, block, 0, stream, g); break;
+    case 64: hipLaunchKernelGGL((lora_update_kernel<MB, 64>), grid, block, 0, stream, g); break;
+    default: hipLaunchKernelGGL((lora_update_kernel<MB, 128>), grid, block, 0, stream, g); break;
   }
   return hipGetLastError();
 }
-
-int padded_rank_of(int r) { return r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : 64; }
 
 template <int RP, int NB>
 hipError_t launch_cfg(const GroupArgs& g, hipStream_t stream) {
@@ -428,7 +431,7 @@ hipError_t launch_nb(const GroupArgs& g, int rp, hipStream_t stream) {
     case 0: return launch_cfg<0, NB>(g, stream);
     case 16: return launch_cfg<16, NB>(g, stream);
     case 32: return launch_cfg<32, NB>(g, stream);
-    default: return launch_cfg<64, NB>(g, stream);
+    default: return launch_cfg<64, NB>(g, stream);  // (rank 128 is split into row halves above)
   }
 }
 
@@ -444,7 +447,7 @@ hipError_t launch_gemv_stream(const StreamArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_lora_update(const GroupArgs& g, hipStream_t stream) {
-  const int rp = padded_rank_of(g.r);
+  const int rp = padded_rank(g.r);
   if (rp == 0) return hipSuccess;
   if (g.M <= 1) return launch_update_mb<1>(g, rp, stream);
   if (g.M <= 2) return launch_update_mb<2>(g, rp, stream);
@@ -456,7 +459,21 @@ hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream) {
   bool any_on = false;
   for (int i = 0; i < g.G; ++i) any_on = any_on || g.y_on[i] != nullptr;
   const int r = any_on ? g.r : 0;
-  const int rp = r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : 64;
+  const int rp = padded_rank(r);
+  if (g.M > kStreamRows && rp > 64) {
+    // rank 128 above 8 rows: the MFMA kernel's per-workgroup T does not fit;
+    // the rows go through the stream and update kernels in two halves
+    GroupArgs lo = g, hi = g;
+    lo.M = kStreamRows;
+    hi.M = g.M - kStreamRows;
+    for (int i = 0; i < g.G; ++i) {
+      hi.x[i] = g.x[i] + (size_t)kStreamRows * g.K;
+      hi.y_off[i] = g.y_off[i] ? g.y_off[i] + (size_t)kStreamRows * g.N : nullptr;
+      hi.y_on[i] = g.y_on[i] ? g.y_on[i] + (size_t)kStreamRows * g.N : nullptr;
+    }
+    const hipError_t e = launch_lora_gemv_group(lo, stream);
+    return e != hipSuccess ? e : launch_lora_gemv_group(hi, stream);
+  }
   if (g.M <= kStreamRows) {
     // base product of every member into y_off and y_on, then the LoRA update of y_on
     StreamArgs sa{};

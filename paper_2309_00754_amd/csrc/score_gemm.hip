@@ -19,7 +19,7 @@
 //    fragments and waited for its copies of the next slab, after it the freed
 //    stage is refilled;
 //  * the rank-r product T = h A^T is the same for every column tile of a row
-//    block, so it is computed once by score_t_kernel (bf16 hi + lo parts of
+//    block, so it is computed once by lora_t_kernel (bf16 hi + lo parts of
 //    s*T in the workspace, with B zero padded to the padded rank RP next to
 //    it) instead of in the main loop;
 //  * the LoRA update s*T*B^T is then a GEMM with 2 RP more k values ([hi | lo]
@@ -345,86 +345,24 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
 // T = h A^T for 16 rows per workgroup; the 8 waves split K.  Writes the bf16
 // hi and lo parts of s*T: ts[row][j] = hi, ts[row][RP + j] = lo (zero for
 // j >= r), the x-side rows of the scoring GEMM's LoRA slabs.
-constexpr int T_WAVES = 8;
-constexpr int T_UNROLL = 4;
-
 template <int RP>
-__global__ __launch_bounds__(T_WAVES * 64) void score_t_kernel(ScoreGemmArgs g) {
-  constexpr int TJ = RP / 16;
-  __shared__ f32x4_t red[T_WAVES][TJ][64];
-  const LinearArgs& a = g.lin;
-  const int M = a.M, K = a.K;
-  const int t = threadIdx.x;
-  const int lane = t & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int l16 = lane & 15;
-  const int lg = lane >> 4;
-  const int m0 = blockIdx.x * 16;
-  const __amdgpu_buffer_rsrc_t hrs = make_rsrc(a.x + (size_t)m0 * K, (uint32_t)min(16, M - m0) * K * 2u);
-  const __amdgpu_buffer_rsrc_t ars = make_rsrc(a.A, (uint32_t)min(a.r, RP) * K * 2u);
-  f32x4_t acc[TJ];
-#pragma unroll
-  for (int j = 0; j < TJ; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  const int ksteps = (K + 31) / 32;
-  for (int k0 = wave; k0 < ksteps; k0 += T_WAVES * T_UNROLL) {
-    uint4 hf[T_UNROLL], af[T_UNROLL][TJ];
-#pragma unroll
-    for (int u = 0; u < T_UNROLL; ++u) {
-      const int k = (k0 + u * T_WAVES) * 32 + lg * 8;
-      const bool kv = k0 + u * T_WAVES < ksteps && k < K;
-      hf[u] = buf_load16(hrs, kv ? (l16 * K + k) * 2 : kOutOfRange);
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) af[u][j] = buf_load16(ars, kv ? ((j * 16 + l16) * K + k) * 2 : kOutOfRange);
-    }
-#pragma unroll
-    for (int u = 0; u < T_UNROLL; ++u)
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) acc[j] = mfma16(hf[u], af[u][j], acc[j]);
-  }
-  // acc[j] lane l holds T[m0 + 4 (l / 16) + i][16 j + l % 16]
-#pragma unroll
-  for (int j = 0; j < TJ; ++j) red[wave][j][lane] = acc[j];
-  __syncthreads();
-  for (int e = t; e < 16 * RP; e += T_WAVES * 64) {
-    const int rl = e / RP, j = e % RP;
-    const int row = m0 + rl;
-    if (row >= M) continue;
-    const int src = (rl >> 2) * 16 + (j & 15);
-    float v = 0.f;
-#pragma unroll
-    for (int w = 0; w < T_WAVES; ++w) v += red[w][j >> 4][src][rl & 3];
-    v *= a.s;
-    const uint32_t hi = f32_to_bf16_rne(v);
-    const uint32_t lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
-    g.ts[(size_t)row * 2 * RP + j] = (uint16_t)hi;
-    g.ts[(size_t)row * 2 * RP + RP + j] = (uint16_t)lo;
-  }
-}
-
-// B zero padded to RP columns (bp[n][j] = B[n][j] for j < r, else 0): the
-// W-side rows of the scoring GEMM's LoRA slabs, 16-byte aligned for its
-// copies whatever r is.
-template <int RP>
-__global__ __launch_bounds__(256) void score_bpad_kernel(ScoreGemmArgs g) {
-  const LinearArgs& a = g.lin;
-  const size_t total = (size_t)a.N * RP;
-  for (size_t e = blockIdx.x * 256 + threadIdx.x; e < total; e += (size_t)gridDim.x * 256) {
-    const int n = (int)(e / RP), j = (int)(e % RP);
-    g.bp[e] = j < a.r ? a.B[(size_t)n * a.r + j] : (uint16_t)0;
-  }
-}
-
-template <int RP>
-hipError_t launch_rp(const ScoreGemmArgs& s, hipStream_t stream) {
+hipError_t launch_rp(const ScoreGemmArgs& s_in, hipStream_t stream) {
+  ScoreGemmArgs s = s_in;
   const bool ragged = s.lin.N % BN != 0;
   if constexpr (RP > 0) {
-    hipLaunchKernelGGL((score_t_kernel<RP>), dim3((s.lin.M + 15) / 16), dim3(T_WAVES * 64), 0, stream, s);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const size_t total = (size_t)s.lin.N * RP;
-    const unsigned blocks = (unsigned)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
-    hipLaunchKernelGGL((score_bpad_kernel<RP>), dim3(blocks), dim3(256), 0, stream, s);
-    e = hipGetLastError();
+    TpreArgs t{};
+    t.x = s.lin.x;
+    t.A = s.lin.A;
+    t.B = s.lin.B;
+    t.s = s.lin.s;
+    t.M = s.lin.M;
+    t.N = s.lin.N;
+    t.K = s.lin.K;
+    t.r = s.lin.r;
+    t.ts = s.ts;
+    t.bp = s.bp_buf;
+    t.part = s.tpart;
+    const hipError_t e = launch_lora_tpre(t, RP, &s.bp, stream);
     if (e != hipSuccess) return e;
   }
   if (ragged)
@@ -440,11 +378,12 @@ hipError_t launch_score_gemm(const ScoreGemmArgs& s_in, hipStream_t stream) {
   ScoreGemmArgs s = s_in;
   s.ntm = (s.lin.M + BM - 1) / BM;
   const int r = s.lin.r;
-  switch (r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : 64) {
+  switch (padded_rank(r)) {
     case 0: return launch_rp<0>(s, stream);
     case 16: return launch_rp<16>(s, stream);
     case 32: return launch_rp<32>(s, stream);
-    default: return launch_rp<64>(s, stream);
+    case 64: return launch_rp<64>(s, stream);
+    default: return launch_rp<128>(s, stream);
   }
 }
 

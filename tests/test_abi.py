@@ -59,7 +59,7 @@ def _lin(x=P, W=P, A=P, B=P, s=2.0, M=32, N=64, K=64, r=8, y_off=P, y_on=P + 0x1
     (dict(K=(1 << 21) + 8), H.HYDRA_ERR_SHAPE),
     (dict(M=1 << 31), H.HYDRA_ERR_SHAPE),
     (dict(r=-1), H.HYDRA_ERR_SHAPE),
-    (dict(r=65), H.HYDRA_ERR_SHAPE),
+    (dict(r=129), H.HYDRA_ERR_SHAPE),
     (dict(y_on=P), H.HYDRA_ERR_SHAPE),          # aliased outputs
     (dict(x=P8), H.HYDRA_ERR_ALIGN),
     (dict(W=P + 4), H.HYDRA_ERR_ALIGN),
@@ -93,7 +93,7 @@ def _score(h=P, W=P, A=P, B=P, tok=P, w_rm=P, n_seq=4, seq_len=8, K=64, V=1000, 
     (dict(n_seq=0, ws_bytes=0), H.HYDRA_ERR_SHAPE),
     (dict(V=0, ws_bytes=0), H.HYDRA_ERR_SHAPE),
     (dict(K=12), H.HYDRA_ERR_SHAPE),
-    (dict(r=100), H.HYDRA_ERR_SHAPE),
+    (dict(r=129), H.HYDRA_ERR_SHAPE),
     (dict(n_seq=1 << 20, seq_len=1 << 12, ws_bytes=1), H.HYDRA_ERR_SHAPE),
     (dict(ws=None), H.HYDRA_ERR_WORKSPACE),
     (dict(ws_bytes=16), H.HYDRA_ERR_WORKSPACE),
@@ -108,17 +108,19 @@ def test_score_rejects(kw, code):
 
 def _ws(M, V):
     # one float4 partial per (row, 256-column tile), two floats per row (the
-    # gathered token logits), then, 16-byte aligned, 2 x 64 bf16 per row (the hi
-    # and lo parts of s * h A^T at the largest rank) and 64 bf16 per vocabulary
-    # row (B zero padded to the padded rank)
+    # gathered token logits), then, 16-byte aligned, 2 x 128 bf16 per row (the
+    # hi and lo parts of s * h A^T at the largest rank) and 128 bf16 per
+    # vocabulary row (B zero padded to the padded rank)
+    # then, 16-byte aligned, the LoRA pre-pass's partial sums (8 K chunks x 128 fp32 per row)
     tiles = (V + 255) // 256
     zt_end = M * tiles * 16 + M * 8
-    return ((zt_end + 15) // 16) * 16 + M * 2 * 64 * 2 + V * 64 * 2
+    bp_end = ((zt_end + 15) // 16) * 16 + M * 2 * 128 * 2 + V * 128 * 2
+    return ((bp_end + 15) // 16) * 16 + 8 * M * 128 * 4
 
 
 def test_score_workspace_bytes():
-    assert H.hydra_score_workspace_bytes(2048, 32000) == _ws(2048, 32000) == 4636672 + 32000 * 128
-    assert H.hydra_score_workspace_bytes(3, 257) == _ws(3, 257) == 896 + 257 * 128
+    assert H.hydra_score_workspace_bytes(2048, 32000) == _ws(2048, 32000) == 5160960 + 32000 * 256 + 8 * 2048 * 512
+    assert H.hydra_score_workspace_bytes(3, 257) == _ws(3, 257) == 1664 + 257 * 256 + 8 * 3 * 512
     out = ctypes.c_size_t(0)
     assert H.lib().hydra_score_workspace_bytes(0, 10, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
     assert H.lib().hydra_score_workspace_bytes(10, 10, None) == H.HYDRA_ERR_NULL
@@ -176,6 +178,52 @@ def test_lora_linear_group_rejects(kw, code):
     assert _grp(**kw) == code
 
 
+def test_linear_workspace_bytes():
+    # ts: 2 RP bf16 per row, then (16-byte aligned) bp: RP bf16 per output row, then (16-byte aligned) the
+    # pre-pass partial sums: 8 K chunks x RP fp32 per row; RP = r rounded up to 16/32/64/128
+    def lws(M, N, rp):
+        a16 = lambda v: (v + 15) // 16 * 16
+        return a16(a16(M * 4 * rp) + N * 2 * rp) + 8 * M * rp * 4
+    assert H.hydra_lora_linear_workspace_bytes(2048, 4096, 16) == lws(2048, 4096, 16) == 2048 * 64 + 4096 * 32 + 2048 * 512
+    assert H.hydra_lora_linear_workspace_bytes(2048, 11008, 128) == lws(2048, 11008, 128)
+    assert H.hydra_lora_linear_workspace_bytes(3, 5, 33) == lws(3, 5, 64)
+    assert H.hydra_lora_linear_workspace_bytes(7, 9, 0) == 0
+    out = ctypes.c_size_t(0)
+    L = H.lib()
+    assert L.hydra_lora_linear_workspace_bytes(0, 5, 16, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
+    assert L.hydra_lora_linear_workspace_bytes(5, 5, 129, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
+    assert L.hydra_lora_linear_workspace_bytes(5, 5, 16, None) == H.HYDRA_ERR_NULL
+
+
+def _lws(x=P, W=P, A=P, B=P, s=2.0, M=64, N=64, K=64, r=128, y_off=P + 0x2000, y_on=P + 0x3000,
+         ws=P + 0x10000, nbytes=1 << 20):
+    return H.lib().hydra_lora_linear_ws(x, W, A, B, s, M, N, K, r, y_off, y_on, ws, nbytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(x=None), H.HYDRA_ERR_NULL),
+    (dict(y_off=None, y_on=None), H.HYDRA_ERR_NULL),
+    (dict(A=None), H.HYDRA_ERR_NULL),
+    (dict(ws=None), H.HYDRA_ERR_NULL),                     # GEMM update needs the workspace
+    (dict(nbytes=100), H.HYDRA_ERR_WORKSPACE),
+    (dict(ws=P + 0x10008), H.HYDRA_ERR_ALIGN),
+    (dict(r=129), H.HYDRA_ERR_SHAPE),
+    (dict(K=20), H.HYDRA_ERR_SHAPE),
+    (dict(y_on=P + 0x2000), H.HYDRA_ERR_SHAPE),            # y_on == y_off
+    (dict(W=P8), H.HYDRA_ERR_ALIGN),
+])
+def test_lora_linear_ws_rejects(kw, code):
+    assert _lws(**kw) == code
+
+
+def test_rank_above_64_needs_the_workspace_in_the_gemm():
+    """hydra_lora_linear (and the group call) at M > 16 with r > 64 and y_on: HYDRA_ERR_WORKSPACE, nothing launched."""
+    L = H.lib()
+    assert L.hydra_lora_linear(P, P, P, P, 2.0, 64, 64, 64, 100, P + 0x2000, P + 0x3000, None) == \
+        H.HYDRA_ERR_WORKSPACE
+    assert _grp(M=64, r=100, G=2) == H.HYDRA_ERR_WORKSPACE
+
+
 def _multi(x_off=P, W=P, n_on=2, xs=(P, P), As=(P, P), Bs=(P, P), ss=(2.0, 2.0), M=4, N=64, K=64, r=8,
            y_off=P + 0x2000, yn=(P + 0x3000, P + 0x4000)):
     def arr(v):
@@ -204,7 +252,7 @@ def _multi(x_off=P, W=P, n_on=2, xs=(P, P), As=(P, P), Bs=(P, P), ss=(2.0, 2.0),
     (dict(Bs=(P, None)), H.HYDRA_ERR_NULL),
     (dict(yn=(P + 0x3000, None)), H.HYDRA_ERR_NULL),
     (dict(K=20), H.HYDRA_ERR_SHAPE),
-    (dict(r=65), H.HYDRA_ERR_SHAPE),
+    (dict(r=129), H.HYDRA_ERR_SHAPE),
     (dict(M=0), H.HYDRA_ERR_SHAPE),
     (dict(W=P8), H.HYDRA_ERR_ALIGN),
     (dict(x_off=P8), H.HYDRA_ERR_ALIGN),

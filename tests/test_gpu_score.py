@@ -44,6 +44,8 @@ SCORE_SHAPES = [
     (2, 100, 64, 1000, 8), (1, 7, 72, 300, 16), (3, 50, 128, 7, 1), (2, 64, 512, 2048, 64),
     (1, 129, 256, 513, 0), (4, 40, 1024, 4000, 33),
     (3, 200, 96, 1280, 24), (2, 256, 64, 512, 16), (1, 300, 40, 768, 0), (2, 150, 200, 777, 20),
+    # the paper's rank 128 (and a rank that pads to it), ragged and whole vocabulary tiles
+    (2, 100, 512, 1000, 128), (1, 260, 264, 512, 100),
 ]
 
 
