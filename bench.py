@@ -253,8 +253,8 @@ def main():
     else:
         roof = dict(bound="mfma", achieved=dcomp["tflops"], peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
                     frac=dcomp["frac"])
-    roof["kernel"] = {"prefill": "lora_gemm_kernel<16> (4 copy + 4 MFMA waves, 128x256 tiles)",
-                      "score": "score_t_kernel<16> + score_bpad_kernel<16> + score_gemm_kernel<16,false> + "
+    roof["kernel"] = {"prefill": "lora_gemm_kernel<16,false> (4 copy + 4 MFMA waves, 128x256 tiles)",
+                      "score": "lora_t_part_kernel<16> + lora_t_finish_kernel<16> + score_gemm_kernel<16,false> + "
                                "score_combine_kernel",
                       "decode": "gemv_stream_kernel<4> + lora_update_kernel<4,16> (grouped q/k/v/o)",
                       "advantages": "value_head_kernel + gae_kernel"}[dom]

@@ -211,27 +211,24 @@ hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, i
   // update of each y_on.
   const int n_in = (x_off ? 1 : 0) + int(n_on);
   hydra::StreamArgs sa{};
-  sa.G = 1;
-  sa.N = int(N);
-  sa.K = int(K);
-  sa.W[0] = W;
+  auto fresh = [&]() {
+    sa = hydra::StreamArgs{};
+    sa.G = 1;
+    sa.seg_rows = int(M);
+    sa.N = int(N);
+    sa.K = int(K);
+    sa.W[0] = W;
+  };
+  fresh();
   for (int i = 0; i < n_in; ++i) {
     const bool off = x_off && i == 0;
-    const uint16_t* xi = off ? x_off : x_on[i - (x_off ? 1 : 0)];
-    float* yi = off ? y_off : y_on[i - (x_off ? 1 : 0)];
-    if (sa.rows + M > hydra::kStreamRows) {
+    if ((sa.nseg[0] + 1) * M > hydra::kStreamRows) {
       if (hydra::launch_gemv_stream(sa, st) != hipSuccess) return HYDRA_ERR_HIP;
-      sa = hydra::StreamArgs{};
-      sa.G = 1;
-      sa.N = int(N);
-      sa.K = int(K);
-      sa.W[0] = W;
+      fresh();
     }
-    for (int m = 0; m < M; ++m) {
-      sa.xr[0][sa.rows] = xi + size_t(m) * size_t(K);
-      sa.ya[0][sa.rows] = yi + size_t(m) * size_t(N);
-      ++sa.rows;
-    }
+    const int sg = sa.nseg[0]++;
+    sa.x[sg] = off ? x_off : x_on[i - (x_off ? 1 : 0)];
+    sa.ya[sg] = off ? y_off : y_on[i - (x_off ? 1 : 0)];
   }
   if (hydra::launch_gemv_stream(sa, st) != hipSuccess) return HYDRA_ERR_HIP;
   if (r == 0 || n_on == 0) return HYDRA_OK;

@@ -33,17 +33,34 @@ struct GroupArgs {
   int G, M, N, K, r;
 };
 
-// Base product y[m] = x[m] W^T for up to kStreamRows rows per W, each row
-// with its own input and output rows (one or several LoRA-off / LoRA-on
-// inputs sharing one read of W), for G weights in one launch.
+// Base product y[m] = x[m] W^T for up to kStreamRows rows per W, G weights in
+// one launch.  The rows of weight g come from segments seg0[g] ..
+// seg0[g] + nseg[g] - 1, each a block of seg_rows consecutive input rows
+// ([seg_rows x K] bf16 at x[s]) with its output rows ([seg_rows x N] fp32 at
+// ya[s], and a second copy at yb[s]; either may be null): one segment per
+// linear of a group, or one per input when several inputs share one W.
 constexpr int kStreamRows = 8;
+constexpr int kStreamSegs = 8;
 struct StreamArgs {
-  const uint16_t* W[kMaxGroup];                 // [N x K] bf16
-  const uint16_t* xr[kMaxGroup][kStreamRows];   // input row m ([K] bf16); nullptr: a zero row
-  float* ya[kMaxGroup][kStreamRows];            // output row m ([N] fp32); nullptr: not written
-  float* yb[kMaxGroup][kStreamRows];            // second copy of output row m; nullptr: not written
-  int G, rows, N, K;
+  const uint16_t* W[kMaxGroup];
+  const uint16_t* x[kStreamSegs];
+  float* ya[kStreamSegs];
+  float* yb[kStreamSegs];
+  int seg0[kMaxGroup];
+  int nseg[kMaxGroup];
+  // segment (counted from seg0) of every row slot; kStreamSegs: no row
+  // (32-bit entries: read with scalar loads)
+  int seg_of[kMaxGroup][kStreamRows];
+  int G, seg_rows, N, K;
 };
+// Fills seg_of from seg0 / nseg / seg_rows.
+inline void stream_finish_args(StreamArgs& a) {
+  for (int g = 0; g < a.G; ++g)
+    for (int m = 0; m < kStreamRows; ++m) {
+      const int sg = m / a.seg_rows;
+      a.seg_of[g][m] = sg < a.nseg[g] ? sg : kStreamSegs;
+    }
+}
 
 // Pre-pass of the LoRA update for the MFMA GEMMs: ts = bf16 hi and lo parts
 // of s * x A^T ([M x 2 RP], hi in columns 0..RP, lo in RP..2 RP) and bp = B

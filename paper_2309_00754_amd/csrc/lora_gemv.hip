@@ -218,15 +218,36 @@ __device__ __forceinline__ void stage_x(uint4* xsh, __amdgpu_buffer_rsrc_t xrs, 
   }
 }
 
-// The same from a table of row pointers (a null row reads as zeros).
+// The same from the segments of a StreamArgs weight (row m: segment
+// seg0 + m / seg_rows, row m % seg_rows of it; rows past the weight's
+// segments read as zeros).  Every wave stages whole 64-element runs of one
+// row (the runs are 64-aligned and the stride is a multiple of 64), so the row
+// index, and with it the segment pointer, is wave-uniform: scalar loads of
+// the kernel arguments, then a buffer load per lane.
 template <int MB, int NT>
-__device__ __forceinline__ void stage_x_rows(uint4* xsh, const uint16_t* const* xr, int c0, int nch, int K, int t) {
+__device__ __forceinline__ void stage_x_segs(uint4* xsh, const StreamArgs& sa, int gi, int c0, int nch, int t) {
   constexpr int SEG = XSeg<MB>::SEG;
-  for (int e = t; e < XSeg<MB>::ELEMS; e += NT) {
-    const int m = e / (SEG * 64), u = (e / 64) % SEG, l = e % 64;
+  constexpr int ELEMS = XSeg<MB>::ELEMS;
+  constexpr int PER = (ELEMS + NT - 1) / NT;  // elements per thread
+  static_assert(NT % 64 == 0, "whole waves");
+  const int K = sa.K;
+  uint4 v[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {  // every load in flight before the first LDS write
+    const int e = t + q * NT;
+    const int m = __builtin_amdgcn_readfirstlane(e / (SEG * 64));
+    const int u = (e / 64) % SEG, l = e % 64;
     const int c = c0 + u, k = c * DKC + l * 8;
-    const uint16_t* row = xr[m];
-    xsh[e] = (row != nullptr && c < nch && k < K) ? *reinterpret_cast<const uint4*>(row + k) : make_uint4(0u, 0u, 0u, 0u);
+    const int sg = m < kStreamRows ? sa.seg_of[gi][m] : kStreamSegs;
+    const bool have = sg < kStreamSegs;
+    const uint16_t* row = have ? sa.x[sa.seg0[gi] + sg] + (size_t)(m - sg * sa.seg_rows) * K : nullptr;
+    const __amdgpu_buffer_rsrc_t rrs = make_rsrc(row, have ? (uint32_t)K * 2u : 0u);
+    v[q] = buf_load16(rrs, (e < ELEMS && c < nch && k < K) ? k * 2 : kOutOfRange);
+  }
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int e = t + q * NT;
+    if (e < ELEMS) xsh[e] = v[q];
   }
 }
 
@@ -270,7 +291,7 @@ __global__ __launch_bounds__(SW * 64) void gemv_stream_kernel(StreamArgs sa) {
     uint4 wb[SEG];
     load_seg(wb, c0);
     if (c0 > 0) __syncthreads();  // every wave is done with the previous x segment
-    stage_x_rows<MB, SW * 64>(xsh, sa.xr[gi], c0, nch, K, t);
+    stage_x_segs<MB, SW * 64>(xsh, sa, gi, c0, nch, t);
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < SEG; ++u)
@@ -278,14 +299,27 @@ __global__ __launch_bounds__(SW * 64) void gemv_stream_kernel(StreamArgs sa) {
       for (int m = 0; m < MB; ++m) acc[m] = dot8(wb[u], xsh[(m * SEG + u) * 64 + lane], acc[m]);
   }
   wave_reduce_scatter<MB>(acc, lane);
-  if (row_ok && reduced_writer<MB>(lane)) {
-    const int m = reduced_index<MB>(lane);
-    if (m < sa.rows) {
-      float* ya = sa.ya[gi][m];
-      float* yb = sa.yb[gi][m];
-      if (ya) ya[n] = acc[0];
-      if (yb) yb[n] = acc[0];
+  // the output row pointers are read as wave-uniform values (scalar loads of
+  // the kernel arguments) and chosen per lane afterwards
+  const int m = reduced_index<MB>(lane);
+  float* ya = nullptr;
+  float* yb = nullptr;
+#pragma unroll
+  for (int q = 0; q < MB; ++q) {
+    const int sg = sa.seg_of[gi][q];
+    if (sg < kStreamSegs) {  // wave-uniform
+      const size_t mr = (size_t)(q - sg * sa.seg_rows);
+      float* pa = sa.ya[sa.seg0[gi] + sg];
+      float* pb = sa.yb[sa.seg0[gi] + sg];
+      pa = pa ? pa + mr * N : nullptr;
+      pb = pb ? pb + mr * N : nullptr;
+      ya = m == q ? pa : ya;
+      yb = m == q ? pb : yb;
     }
+  }
+  if (row_ok && reduced_writer<MB>(lane)) {
+    if (ya) ya[n] = acc[0];
+    if (yb) yb[n] = acc[0];
   }
 }
 
@@ -437,11 +471,15 @@ hipError_t launch_nb(const GroupArgs& g, int rp, hipStream_t stream) {
 
 }  // namespace
 
-hipError_t launch_gemv_stream(const StreamArgs& a, hipStream_t stream) {
+hipError_t launch_gemv_stream(const StreamArgs& a_in, hipStream_t stream) {
+  StreamArgs a = a_in;
+  stream_finish_args(a);
   const dim3 grid((a.N + SW - 1) / SW, a.G), block(SW * 64);
-  if (a.rows <= 1) hipLaunchKernelGGL((gemv_stream_kernel<1>), grid, block, 0, stream, a);
-  else if (a.rows <= 2) hipLaunchKernelGGL((gemv_stream_kernel<2>), grid, block, 0, stream, a);
-  else if (a.rows <= 4) hipLaunchKernelGGL((gemv_stream_kernel<4>), grid, block, 0, stream, a);
+  int rows = 0;
+  for (int i = 0; i < a.G; ++i) rows = a.nseg[i] * a.seg_rows > rows ? a.nseg[i] * a.seg_rows : rows;
+  if (rows <= 1) hipLaunchKernelGGL((gemv_stream_kernel<1>), grid, block, 0, stream, a);
+  else if (rows <= 2) hipLaunchKernelGGL((gemv_stream_kernel<2>), grid, block, 0, stream, a);
+  else if (rows <= 4) hipLaunchKernelGGL((gemv_stream_kernel<4>), grid, block, 0, stream, a);
   else hipLaunchKernelGGL((gemv_stream_kernel<8>), grid, block, 0, stream, a);
   return hipGetLastError();
 }
@@ -478,16 +516,16 @@ hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream) {
     // base product of every member into y_off and y_on, then the LoRA update of y_on
     StreamArgs sa{};
     sa.G = g.G;
-    sa.rows = g.M;
+    sa.seg_rows = g.M;
     sa.N = g.N;
     sa.K = g.K;
     for (int i = 0; i < g.G; ++i) {
       sa.W[i] = g.W[i];
-      for (int m = 0; m < g.M; ++m) {
-        sa.xr[i][m] = g.x[i] + (size_t)m * g.K;
-        sa.ya[i][m] = g.y_off[i] ? g.y_off[i] + (size_t)m * g.N : nullptr;
-        sa.yb[i][m] = g.y_on[i] ? g.y_on[i] + (size_t)m * g.N : nullptr;
-      }
+      sa.seg0[i] = i;
+      sa.nseg[i] = 1;
+      sa.x[i] = g.x[i];
+      sa.ya[i] = g.y_off[i];
+      sa.yb[i] = g.y_on[i];
     }
     hipError_t e = launch_gemv_stream(sa, stream);
     if (e != hipSuccess || rp == 0) return e;
