@@ -4,9 +4,10 @@
 // pi^hydra; App. A, Alg. 1 / Alg. 2, "compute reward and reference log
 // probabilities"; the KL weight beta of App. B is applied by the caller).
 //
-//  * score_logits_kernel: one workgroup per token row streams both fp32
-//    logit rows once (float4 loads), keeping a per-thread running
-//    (max, sum exp) and reducing it across the workgroup in a fixed tree.
+//  * score_logits_vec_kernel (V % 4 == 0) / score_logits_kernel (other V):
+//    one workgroup per token row streams both fp32 logit rows once, keeping
+//    a per-thread running (max, sum exp) and reducing it across the
+//    workgroup in a fixed tree.
 //  * score_combine_kernel: one wave per token row merges the per-column-tile
 //    partials written by the fused CLM-head GEMM in tile order, then forms
 //    lse, lp and KL; extra workgroups compute the reward head's dot products.
@@ -51,7 +52,8 @@ __device__ __forceinline__ void absorb_max(float& m, float& s, float bm) {
   }
 }
 
-template <int THREADS, int U, bool VEC>
+// General V (any alignment of the row length): scalar loads.
+template <int THREADS, int U>
 __global__ __launch_bounds__(THREADS) void score_logits_kernel(LogitsArgs o) {
   constexpr int NW = THREADS / 64;
   __shared__ float red[4][NW];
@@ -74,63 +76,29 @@ __global__ __launch_bounds__(THREADS) void score_logits_kernel(LogitsArgs o) {
   }
 
   float m_on = -INFINITY, s_on = 0.f, m_off = -INFINITY, s_off = 0.f;
-  if constexpr (VEC) {
-    const int nv4 = V >> 2;
-    const float4* pon = reinterpret_cast<const float4*>(zon);
-    const float4* poff = reinterpret_cast<const float4*>(zoff);
-    for (int base = t; base < nv4; base += THREADS * U) {
-      float4 a[U], b[U];
+  for (int base = t; base < V; base += THREADS * U) {
+    float a[U], b[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int i = base + u * THREADS;
-        const bool v = i < nv4;
-        a[u] = v ? pon[i] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-        b[u] = v ? poff[i] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-      }
-      float bm_on = -INFINITY, bm_off = -INFINITY;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        bm_on = fmaxf(bm_on, fmaxf(fmaxf(a[u].x, a[u].y), fmaxf(a[u].z, a[u].w)));
-        bm_off = fmaxf(bm_off, fmaxf(fmaxf(b[u].x, b[u].y), fmaxf(b[u].z, b[u].w)));
-      }
-      absorb_max(m_on, s_on, bm_on);
-      absorb_max(m_off, s_off, bm_off);
-      if (m_on != -INFINITY) {
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-          s_on += (exp_e(a[u].x - m_on) + exp_e(a[u].y - m_on)) + (exp_e(a[u].z - m_on) + exp_e(a[u].w - m_on));
-      }
-      if (m_off != -INFINITY) {
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-          s_off += (exp_e(b[u].x - m_off) + exp_e(b[u].y - m_off)) + (exp_e(b[u].z - m_off) + exp_e(b[u].w - m_off));
-      }
+    for (int u = 0; u < U; ++u) {
+      const int i = base + u * THREADS;
+      a[u] = i < V ? zon[i] : -INFINITY;
+      b[u] = i < V ? zoff[i] : -INFINITY;
     }
-  } else {
-    for (int base = t; base < V; base += THREADS * U) {
-      float a[U], b[U];
+    float bm_on = -INFINITY, bm_off = -INFINITY;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int i = base + u * THREADS;
-        a[u] = i < V ? zon[i] : -INFINITY;
-        b[u] = i < V ? zoff[i] : -INFINITY;
-      }
-      float bm_on = -INFINITY, bm_off = -INFINITY;
+    for (int u = 0; u < U; ++u) {
+      bm_on = fmaxf(bm_on, a[u]);
+      bm_off = fmaxf(bm_off, b[u]);
+    }
+    absorb_max(m_on, s_on, bm_on);
+    absorb_max(m_off, s_off, bm_off);
+    if (m_on != -INFINITY) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        bm_on = fmaxf(bm_on, a[u]);
-        bm_off = fmaxf(bm_off, b[u]);
-      }
-      absorb_max(m_on, s_on, bm_on);
-      absorb_max(m_off, s_off, bm_off);
-      if (m_on != -INFINITY) {
+      for (int u = 0; u < U; ++u) s_on += exp_e(a[u] - m_on);
+    }
+    if (m_off != -INFINITY) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) s_on += exp_e(a[u] - m_on);
-      }
-      if (m_off != -INFINITY) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) s_off += exp_e(b[u] - m_off);
-      }
+      for (int u = 0; u < U; ++u) s_off += exp_e(b[u] - m_off);
     }
   }
 
@@ -151,6 +119,112 @@ __global__ __launch_bounds__(THREADS) void score_logits_kernel(LogitsArgs o) {
       lse_merge(mf, sf, red[2][i], red[3][i]);
     }
     finish_row(row, tk, V, z_on, z_off, mo, so, mf, sf, o);
+  }
+}
+
+// The same for V % 4 == 0, streaming both rows as 16-byte buffer loads (zero
+// past the row; the block's last batch masks those to -inf).  Running state
+// per thread in base 2: m2 = max z * log2 e and s = sum 2^(z log2 e - m2),
+// one FMA and one exp2 per logit.  The block combines by a max first (wave
+// butterfly, then LDS), one rescale per thread, then sums (wave butterfly,
+// then LDS in wave order).
+template <int THREADS, int U>
+__global__ __launch_bounds__(THREADS) void score_logits_vec_kernel(LogitsArgs o) {
+  constexpr int NW = THREADS / 64;
+  constexpr int STEP = THREADS * U;  // float4 per batch
+  __shared__ float rmax[2][NW];
+  __shared__ float rsum[2][NW];
+  const int row = blockIdx.x, t = threadIdx.x, V = o.V;
+  const float* zon = o.on + (size_t)row * V;
+  const float* zoff = o.off + (size_t)row * V;
+  // the sampled token's two logits first: their latency overlaps the stream
+  int tk = 0;
+  float z_on = 0.f, z_off = 0.f;
+  if (t == 0) {
+    tk = o.tokens[row];
+    if (tk >= 0 && tk < V) {
+      z_on = zon[tk];
+      z_off = zoff[tk];
+    }
+  }
+  const int nv4 = V >> 2;
+  const __amdgpu_buffer_rsrc_t ron = make_rsrc(zon, (uint32_t)nv4 * 16u);
+  const __amdgpu_buffer_rsrc_t roff = make_rsrc(zoff, (uint32_t)nv4 * 16u);
+  float m_on = -INFINITY, s_on = 0.f, m_off = -INFINITY, s_off = 0.f;
+  auto absorb = [&](float& m, float& sum, const float4 (&a)[U]) __attribute__((always_inline)) {
+    float bm = a[0].x;
+#pragma unroll
+    for (int u = 0; u < U; ++u) bm = fmaxf(fmaxf(bm, a[u].x), fmaxf(fmaxf(a[u].y, a[u].z), a[u].w));
+    const float mn = fmaxf(m, bm * kLog2e);
+    sum = (m == -INFINITY) ? 0.f : sum * __builtin_amdgcn_exp2f(m - mn);
+    m = mn;
+    if (mn == -INFINITY) return;  // nothing but -inf so far
+    float acc = 0.f;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      acc += (__builtin_amdgcn_exp2f(fmaf(a[u].x, kLog2e, -mn)) + __builtin_amdgcn_exp2f(fmaf(a[u].y, kLog2e, -mn))) +
+             (__builtin_amdgcn_exp2f(fmaf(a[u].z, kLog2e, -mn)) + __builtin_amdgcn_exp2f(fmaf(a[u].w, kLog2e, -mn)));
+    sum += acc;
+  };
+  const int nb = (nv4 + STEP - 1) / STEP;  // batches (block-uniform)
+  for (int b = 0; b < nb; ++b) {
+    float4 a[U], c[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = t + b * STEP + u * THREADS;
+      const int off = i < nv4 ? i * 16 : kOutOfRange;
+      a[u] = __builtin_bit_cast(float4, buf_load16(ron, off));
+      c[u] = __builtin_bit_cast(float4, buf_load16(roff, off));
+    }
+    if (b == nb - 1) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (t + b * STEP + u * THREADS >= nv4) {
+          a[u] = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+          c[u] = a[u];
+        }
+    }
+    absorb(m_on, s_on, a);
+    absorb(m_off, s_off, c);
+  }
+  float wm_on = m_on, wm_off = m_off;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    wm_on = fmaxf(wm_on, __shfl_xor(wm_on, off));
+    wm_off = fmaxf(wm_off, __shfl_xor(wm_off, off));
+  }
+  const int lane = t & 63, w = t >> 6;
+  if (lane == 0) {
+    rmax[0][w] = wm_on;
+    rmax[1][w] = wm_off;
+  }
+  __syncthreads();
+  float bm_on = rmax[0][0], bm_off = rmax[1][0];
+#pragma unroll
+  for (int i = 1; i < NW; ++i) {
+    bm_on = fmaxf(bm_on, rmax[0][i]);
+    bm_off = fmaxf(bm_off, rmax[1][i]);
+  }
+  float v_on = (m_on == -INFINITY) ? 0.f : s_on * __builtin_amdgcn_exp2f(m_on - bm_on);
+  float v_off = (m_off == -INFINITY) ? 0.f : s_off * __builtin_amdgcn_exp2f(m_off - bm_off);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    v_on += __shfl_xor(v_on, off);
+    v_off += __shfl_xor(v_off, off);
+  }
+  if (lane == 0) {
+    rsum[0][w] = v_on;
+    rsum[1][w] = v_off;
+  }
+  __syncthreads();
+  if (t == 0) {
+    float so = rsum[0][0], sf = rsum[1][0];
+    for (int i = 1; i < NW; ++i) {
+      so += rsum[0][i];
+      sf += rsum[1][i];
+    }
+    // natural-log maxima for finish_row: lse = m + ln(s)
+    finish_row(row, tk, V, z_on, z_off, bm_on / kLog2e, so, bm_off / kLog2e, sf, o);
   }
 }
 
@@ -215,10 +289,10 @@ __global__ __launch_bounds__(CB_THREADS) void score_combine_kernel(CombineArgs c
 hipError_t launch_score_logits(const LogitsArgs& o, hipStream_t stream) {
   constexpr int THREADS = 512, U = 4;
   const dim3 grid(o.M), block(THREADS);
-  if ((o.V & 3) == 0)
-    hipLaunchKernelGGL((score_logits_kernel<THREADS, U, true>), grid, block, 0, stream, o);
+  if ((o.V & 3) == 0 && (reinterpret_cast<uintptr_t>(o.on) & 15) == 0 && (reinterpret_cast<uintptr_t>(o.off) & 15) == 0)
+    hipLaunchKernelGGL((score_logits_vec_kernel<THREADS, U>), grid, block, 0, stream, o);
   else
-    hipLaunchKernelGGL((score_logits_kernel<THREADS, U, false>), grid, block, 0, stream, o);
+    hipLaunchKernelGGL((score_logits_kernel<THREADS, U>), grid, block, 0, stream, o);
   return hipGetLastError();
 }
 
