@@ -10,6 +10,7 @@ from .hydra_oracle import (  # noqa: F401
 )
 from .ppo_oracle import (  # noqa: F401
     gae_ref,
+    ppo_loss_ref,
     ppo_rewards_ref,
     value_head_ref,
 )

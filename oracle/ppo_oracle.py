@@ -24,6 +24,15 @@ What is computed, and where the paper defines it
   delta_{t+l}`` over the rest of the sequence, the return ``A_t + V_t``.
   Positions before ``start`` get advantage and return 0.
 
+* The PPO losses of the update stage (Sec. 2, "Stage 3: PPO": the clipped
+  surrogate objective on the probability ratio of the new and old policy,
+  and the critic's squared-error loss on the returns).  Readings: the
+  ratio is ``exp(lp_new - lp_old)`` of the sampled tokens' log-probabilities;
+  the clip range eps is a parameter (the paper names it without a value);
+  both losses are means over the response tokens (``t >= start``) of all
+  sequences; the value loss is ``(V - R)^2 / 2`` without clipping; where the
+  clipped and unclipped terms are equal the unclipped term's gradient is used.
+
 Every function is the plain definition.  ``gae_ref`` evaluates the sum over
 the rest of the sequence for every position (no recurrence), so it checks a
 recursive or scanned evaluation independently.
@@ -38,7 +47,7 @@ import numpy as np
 
 from .hydra_oracle import bf16_to_f64
 
-__all__ = ["value_head_ref", "ppo_rewards_ref", "gae_ref"]
+__all__ = ["value_head_ref", "ppo_rewards_ref", "gae_ref", "ppo_loss_ref"]
 
 
 def value_head_ref(h, w_v) -> np.ndarray:
@@ -74,3 +83,36 @@ def gae_ref(rewards, values, n_seq: int, seq_len: int, start: int, gamma: float,
     ret = np.zeros_like(A)
     ret[:, start:] = A[:, start:] + V[:, start:]
     return A.reshape(-1), ret.reshape(-1)
+
+
+def ppo_loss_ref(lp_new, lp_old, adv, v_new, returns, n_seq: int, seq_len: int, start: int, eps: float):
+    """Clipped surrogate and value losses over the response tokens, and their gradients.
+
+    Returns a dict with
+      pg_loss   = -(1/n) sum_t min(rho_t A_t, clip(rho_t, 1 - eps, 1 + eps) A_t),  rho_t = exp(lp_new_t - lp_old_t)
+      v_loss    = (1/n) sum_t (V_t - R_t)^2 / 2
+      clip_frac = (1/n) #{t : the clipped term is strictly smaller}
+      d_lp[t]   = d pg_loss / d lp_new_t  (-rho_t A_t / n where the unclipped term is the minimum, else 0)
+      d_v[t]    = d v_loss / d V_t        ((V_t - R_t) / n)
+    with n = n_seq * (seq_len - start); positions before start contribute nothing (gradient 0).
+    """
+    shape = (n_seq, seq_len)
+    ln = np.asarray(lp_new, np.float64).reshape(shape)
+    lo = np.asarray(lp_old, np.float64).reshape(shape)
+    A = np.asarray(adv, np.float64).reshape(shape)
+    V = np.asarray(v_new, np.float64).reshape(shape)
+    R = np.asarray(returns, np.float64).reshape(shape)
+    mask = np.zeros(shape, dtype=bool)
+    mask[:, start:] = True
+    n = n_seq * (seq_len - start)
+    rho = np.exp(ln - lo)
+    unclipped = rho * A
+    clipped = np.clip(rho, 1.0 - eps, 1.0 + eps) * A
+    obj = np.minimum(unclipped, clipped)
+    pg_loss = -obj[mask].sum() / n
+    d_lp = np.where(mask & (unclipped <= clipped), -unclipped / n, 0.0)
+    v_loss = 0.5 * ((V - R)[mask] ** 2).sum() / n
+    d_v = np.where(mask, (V - R) / n, 0.0)
+    clip_frac = (clipped < unclipped)[mask].sum() / n
+    return dict(pg_loss=float(pg_loss), v_loss=float(v_loss), clip_frac=float(clip_frac),
+                d_lp=d_lp.reshape(-1), d_v=d_v.reshape(-1))

@@ -178,3 +178,116 @@ def _mut_returns_without_value(r, V, n, T, s, g, lam):
 def test_pins_catch_gae_mutations(mut):
     assert _pins_for_gae(P.gae_ref)
     assert not _pins_for_gae(mut)
+
+
+# ---------------------------------------------------------------- PPO losses (update stage)
+def _loss_case(seed, n_seq=3, T=20, start=5):
+    rng = np.random.default_rng(seed)
+    M = n_seq * T
+    lp_old = -rng.uniform(0.5, 6.0, M)
+    lp_new = lp_old + rng.normal(0, 0.3, M)
+    A = rng.normal(0, 1, M)
+    V = rng.normal(0, 1, M)
+    R = V + rng.normal(0, 0.5, M)
+    return lp_new, lp_old, A, V, R, n_seq, T, start
+
+
+def test_ppo_loss_zero_advantage_and_equal_policies():
+    lp_new, lp_old, A, V, R, n, T, st = _loss_case(21)
+    z = P.ppo_loss_ref(lp_new, lp_old, np.zeros_like(A), V, R, n, T, st, 0.2)
+    assert z["pg_loss"] == 0.0 and np.all(z["d_lp"] == 0.0)
+    e = P.ppo_loss_ref(lp_old, lp_old, A, V, R, n, T, st, 0.2)   # rho = 1: no clipping, objective = mean A
+    mask = (np.arange(n * T) % T) >= st
+    cnt = n * (T - st)
+    assert abs(e["pg_loss"] + A[mask].sum() / cnt) < 1e-12
+    np.testing.assert_allclose(e["d_lp"], np.where(mask, -A / cnt, 0.0), rtol=0, atol=1e-15)
+    assert e["clip_frac"] == 0.0
+
+
+@pytest.mark.parametrize("rho,A,obj,active", [(1.5, 1.0, 1.2, False), (0.5, 1.0, 0.5, True),
+                                              (0.5, -1.0, -0.8, False), (1.5, -1.0, -1.5, True),
+                                              (1.1, 2.0, 2.2, True), (0.9, -3.0, -2.7, True)])
+def test_ppo_loss_clip_cases_closed_form(rho, A, obj, active):
+    """One response token: the objective is the textbook min of the plain and clipped terms (eps = 0.2)."""
+    out = P.ppo_loss_ref([np.log(rho)], [0.0], [A], [0.0], [0.0], 1, 1, 0, 0.2)
+    assert abs(out["pg_loss"] + obj) < 1e-12
+    assert abs(out["d_lp"][0] - (-rho * A if active else 0.0)) < 1e-12
+    assert out["clip_frac"] == (0.0 if active else 1.0)
+
+
+def test_ppo_loss_gradients_match_finite_differences():
+    lp_new, lp_old, A, V, R, n, T, st = _loss_case(22)
+    base = P.ppo_loss_ref(lp_new, lp_old, A, V, R, n, T, st, 0.2)
+    h = 1e-6
+    rng = np.random.default_rng(0)
+    for t in rng.choice(n * T, 25, replace=False):
+        rho = np.exp(lp_new[t] - lp_old[t])
+        if abs(rho - 0.8) < 1e-4 or abs(rho - 1.2) < 1e-4:
+            continue   # a kink of the clip
+        up, dn = lp_new.copy(), lp_new.copy()
+        up[t] += h
+        dn[t] -= h
+        fd = (P.ppo_loss_ref(up, lp_old, A, V, R, n, T, st, 0.2)["pg_loss"] -
+              P.ppo_loss_ref(dn, lp_old, A, V, R, n, T, st, 0.2)["pg_loss"]) / (2 * h)
+        assert abs(fd - base["d_lp"][t]) < 1e-7
+        vu, vd = V.copy(), V.copy()
+        vu[t] += h
+        vd[t] -= h
+        fdv = (P.ppo_loss_ref(lp_new, lp_old, A, vu, R, n, T, st, 0.2)["v_loss"] -
+               P.ppo_loss_ref(lp_new, lp_old, A, vd, R, n, T, st, 0.2)["v_loss"]) / (2 * h)
+        assert abs(fdv - base["d_v"][t]) < 1e-7
+
+
+def test_ppo_value_loss_closed_form_and_prompt_mask():
+    lp_new, lp_old, A, V, R, n, T, st = _loss_case(23)
+    out = P.ppo_loss_ref(lp_new, lp_old, A, V, R, n, T, st, 0.2)
+    resp = np.concatenate([np.arange(b * T + st, (b + 1) * T) for b in range(n)])
+    assert abs(out["v_loss"] - 0.5 * np.mean((V[resp] - R[resp]) ** 2)) < 1e-13
+    prompt = np.setdiff1d(np.arange(n * T), resp)
+    assert np.all(out["d_lp"][prompt] == 0.0) and np.all(out["d_v"][prompt] == 0.0)
+
+
+def _loss_pins_hold(fn):
+    try:
+        for rho, A, obj, active in [(1.5, 1.0, 1.2, False), (0.5, 1.0, 0.5, True), (0.5, -1.0, -0.8, False),
+                                    (1.5, -1.0, -1.5, True)]:
+            out = fn([np.log(rho)], [0.0], [A], [0.0], [0.0], 1, 1, 0, 0.2)
+            if abs(out["pg_loss"] + obj) > 1e-12 or abs(out["d_lp"][0] - (-rho * A if active else 0.0)) > 1e-12:
+                return False
+        lp_new, lp_old, A, V, R, n, T, st = _loss_case(24)
+        out = fn(lp_new, lp_old, A, V, R, n, T, st, 0.2)
+        ref = P.ppo_loss_ref(lp_new, lp_old, A, V, R, n, T, st, 0.2)
+        resp = np.concatenate([np.arange(b * T + st, (b + 1) * T) for b in range(n)])
+        return abs(out["v_loss"] - 0.5 * np.mean((V[resp] - R[resp]) ** 2)) < 1e-13 and \
+            abs(out["pg_loss"] - ref["pg_loss"]) < 1e-13
+    except Exception:
+        return False
+
+
+def _mut_max_instead_of_min(ln, lo, A, V, R, n, T, st, eps):
+    out = P.ppo_loss_ref(ln, lo, A, V, R, n, T, st, eps)
+    rho = np.exp(np.asarray(ln, float) - np.asarray(lo, float))
+    A = np.asarray(A, float)
+    obj = np.maximum(rho * A, np.clip(rho, 1 - eps, 1 + eps) * A)
+    mask = (np.arange(len(A)) % T) >= st
+    out["pg_loss"] = -obj[mask].sum() / (n * (T - st))
+    return out
+
+
+def _mut_swapped_clip_bounds(ln, lo, A, V, R, n, T, st, eps):
+    return P.ppo_loss_ref(ln, lo, A, V, R, n, T, st, -eps)
+
+
+def _mut_mean_over_all_tokens(ln, lo, A, V, R, n, T, st, eps):
+    return P.ppo_loss_ref(ln, lo, A, V, R, n, T, 0, eps)
+
+
+def _mut_inverse_ratio(ln, lo, A, V, R, n, T, st, eps):
+    return P.ppo_loss_ref(lo, ln, A, V, R, n, T, st, eps)
+
+
+@pytest.mark.parametrize("mut", [_mut_max_instead_of_min, _mut_swapped_clip_bounds, _mut_mean_over_all_tokens,
+                                 _mut_inverse_ratio])
+def test_pins_catch_ppo_loss_mutations(mut):
+    assert _loss_pins_hold(P.ppo_loss_ref)
+    assert not _loss_pins_hold(mut)
