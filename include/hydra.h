@@ -273,6 +273,34 @@ hydra_status hydra_ppo_advantages(const float* kl, const float* reward, const fl
                                   int64_t seq_len, int64_t start, float beta, float gamma, float lam, float* rewards,
                                   float* advantages, float* returns, void* stream);
 
+/*
+ * hydra_ppo_loss -- the PPO update stage's losses for n_seq sequences of
+ * seq_len tokens (M = n_seq * seq_len, sequence-major), with their per-token
+ * gradients.
+ * Defined by: Sec. 2 Stage 3 (the clipped surrogate objective on the
+ * probability ratio of the new and old policy; V trained with squared-error
+ * loss on the returns).
+ *
+ *   lp_new, lp_old [M] fp32   sampled-token log-probabilities under the policy
+ *                             being trained and under the one that sampled
+ *   advantages, values, returns [M] fp32   A-hat (hydra_ppo_advantages), the
+ *                             critic's current values, the returns
+ *   start                     first response position, 0 <= start < seq_len
+ *   eps                       clip range, 0 <= eps < 1 (the paper leaves it open)
+ *   losses [3] fp32           out: policy loss -(1/n) sum min(rho A, clip(rho, 1-eps, 1+eps) A),
+ *                             rho = exp(lp_new - lp_old); value loss (1/n) sum (V - R)^2 / 2;
+ *                             the fraction of tokens where the clipped term is the smaller;
+ *                             n = n_seq * (seq_len - start), the response tokens
+ *   d_lp [M] fp32             out, optional: d policy loss / d lp_new (-rho A / n where the
+ *                             unclipped term is the minimum, else 0; 0 before start)
+ *   d_v [M] fp32              out, optional: d value loss / d V ((V - R) / n; 0 before start)
+ * One workgroup sums in a fixed order (deterministic).  No output may be an
+ * input or another output (HYDRA_ERR_SHAPE); buffers 4-byte aligned.
+ */
+hydra_status hydra_ppo_loss(const float* lp_new, const float* lp_old, const float* advantages, const float* values,
+                            const float* returns, int64_t n_seq, int64_t seq_len, int64_t start, float eps,
+                            float* losses, float* d_lp, float* d_v, void* stream);
+
 /* A static, human-readable name for a status code. */
 const char* hydra_status_string(hydra_status status);
 

@@ -24,6 +24,7 @@ from ._binding import (  # noqa: F401
     hydra_lora_linear_ws,
     hydra_lora_linear_multi,
     hydra_ppo_advantages,
+    hydra_ppo_loss,
     hydra_score,
     hydra_score_logits,
     hydra_score_workspace_bytes,

@@ -38,6 +38,7 @@ EXPORTED = (
     "hydra_score_logits",
     "hydra_value_head",
     "hydra_ppo_advantages",
+    "hydra_ppo_loss",
     "hydra_status_string",
     "hydra_abi_version",
 )
@@ -94,6 +95,8 @@ def lib() -> ctypes.CDLL:
     L.hydra_value_head.restype = ctypes.c_int
     L.hydra_ppo_advantages.argtypes = [_vp, _vp, _vp, _i64, _i64, _i64, _f32, _f32, _f32, _vp, _vp, _vp, _vp]
     L.hydra_ppo_advantages.restype = ctypes.c_int
+    L.hydra_ppo_loss.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _f32, _vp, _vp, _vp, _vp]
+    L.hydra_ppo_loss.restype = ctypes.c_int
     L.hydra_status_string.argtypes = [ctypes.c_int]
     L.hydra_status_string.restype = ctypes.c_char_p
     L.hydra_abi_version.argtypes = []
@@ -354,3 +357,18 @@ def hydra_ppo_advantages(kl, reward, values, n_seq: int, seq_len: int, advantage
                                     float(beta), float(gamma), float(lam), _ptr(rewards), _ptr(advantages),
                                     _ptr(returns), _stream_handle(stream))
     _check(st, "hydra_ppo_advantages")
+
+
+def hydra_ppo_loss(lp_new, lp_old, advantages, values, returns, n_seq: int, seq_len: int, losses, d_lp=None,
+                   d_v=None, start: int = 0, eps: float = 0.2, stream=None) -> None:
+    """PPO policy and value losses with their per-token gradients (see include/hydra.h)."""
+    torch = _torch()
+    M = int(n_seq) * int(seq_len)
+    for t, name in ((lp_new, "lp_new"), (lp_old, "lp_old"), (advantages, "advantages"), (values, "values"),
+                    (returns, "returns"), (d_lp, "d_lp"), (d_v, "d_v")):
+        _need(t, name, (torch.float32,), (M,))
+    _need(losses, "losses", (torch.float32,), (3,))
+    st = lib().hydra_ppo_loss(_ptr(lp_new), _ptr(lp_old), _ptr(advantages), _ptr(values), _ptr(returns),
+                              int(n_seq), int(seq_len), int(start), float(eps), _ptr(losses), _ptr(d_lp),
+                              _ptr(d_v), _stream_handle(stream))
+    _check(st, "hydra_ppo_loss")

@@ -23,6 +23,11 @@
 //    residuals in registers (all their loads issued up front); longer ones
 //    are recomputed in the second pass.  Fixed order throughout:
 //    deterministic.
+//  * ppo_loss_kernel: the update stage's losses (Sec. 2, "Stage 3: PPO"): the
+//    clipped surrogate on the ratio rho = exp(lp_new - lp_old) and the
+//    critic's squared-error loss on the returns, means over the response
+//    tokens, with their per-token gradients.  One workgroup: thread t takes
+//    tokens t, t + 1024, ..., and the partial sums meet in a fixed tree.
 #include "hydra_device.h"
 #include "hydra_internal.h"
 
@@ -177,11 +182,73 @@ __global__ __launch_bounds__(64) void gae_kernel(GaeArgs a) {
   }
 }
 
+constexpr int PL_THREADS = 1024;
+
+__global__ __launch_bounds__(PL_THREADS) void ppo_loss_kernel(PpoLossArgs a) {
+  __shared__ float red[3][PL_THREADS / 64];
+  const int t = threadIdx.x;
+  const int T = a.seq_len;
+  const int M = a.n_seq * T;
+  const float inv_n = 1.f / ((float)a.n_seq * (float)(T - a.start));
+  const float lo_b = 1.f - a.eps, hi_b = 1.f + a.eps;
+  float pg = 0.f, vl = 0.f, cf = 0.f;
+  for (int m = t; m < M; m += PL_THREADS) {
+    float dl = 0.f, dv = 0.f;
+    if (m % T >= a.start) {
+      const float rho = exp_e(a.lp_new[m] - a.lp_old[m]);
+      const float A = a.adv[m];
+      const float un = rho * A;
+      const float cl = fminf(fmaxf(rho, lo_b), hi_b) * A;
+      if (un <= cl) {
+        pg += un;
+        dl = -un * inv_n;
+      } else {
+        pg += cl;
+        cf += 1.f;
+      }
+      const float d = a.values[m] - a.returns[m];
+      vl = fmaf(0.5f * d, d, vl);
+      dv = d * inv_n;
+    }
+    if (a.d_lp) a.d_lp[m] = dl;
+    if (a.d_v) a.d_v[m] = dv;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    pg += __shfl_xor(pg, o);
+    vl += __shfl_xor(vl, o);
+    cf += __shfl_xor(cf, o);
+  }
+  const int lane = t & 63, w = t >> 6;
+  if (lane == 0) {
+    red[0][w] = pg;
+    red[1][w] = vl;
+    red[2][w] = cf;
+  }
+  __syncthreads();
+  if (t == 0) {
+    float sp = 0.f, sv = 0.f, sc = 0.f;
+    for (int i = 0; i < PL_THREADS / 64; ++i) {
+      sp += red[0][i];
+      sv += red[1][i];
+      sc += red[2][i];
+    }
+    a.losses[0] = -sp * inv_n;
+    a.losses[1] = sv * inv_n;
+    a.losses[2] = sc * inv_n;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_value_head(const ValueHeadArgs& a, hipStream_t stream) {
   const int rows_per_wg = VH_WAVES * VH_ROWS;
   hipLaunchKernelGGL(value_head_kernel, dim3((a.M + rows_per_wg - 1) / rows_per_wg), dim3(VH_WAVES * 64), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ppo_loss(const PpoLossArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(ppo_loss_kernel, dim3(1), dim3(PL_THREADS), 0, stream, a);
   return hipGetLastError();
 }
 

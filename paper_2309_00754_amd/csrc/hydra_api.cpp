@@ -339,6 +339,41 @@ hydra_status hydra_value_head(const uint16_t* h, const uint16_t* w_v, int64_t M,
   return from_hip(hydra::launch_value_head(a, reinterpret_cast<hipStream_t>(stream)));
 }
 
+hydra_status hydra_ppo_loss(const float* lp_new, const float* lp_old, const float* advantages, const float* values,
+                            const float* returns, int64_t n_seq, int64_t seq_len, int64_t start, float eps,
+                            float* losses, float* d_lp, float* d_v, void* stream) {
+  if (!lp_new || !lp_old || !advantages || !values || !returns || !losses) return HYDRA_ERR_NULL;
+  if (!dim_ok(n_seq) || !dim_ok(seq_len) || n_seq > kMaxDim / seq_len) return HYDRA_ERR_SHAPE;
+  if (start < 0 || start >= seq_len) return HYDRA_ERR_SHAPE;
+  if (!(eps >= 0.f && eps < 1.f)) return HYDRA_ERR_SHAPE;
+  const void* ins[5] = {lp_new, lp_old, advantages, values, returns};
+  const void* outs[3] = {losses, d_lp, d_v};
+  for (const void* o : outs) {
+    if (!o) continue;
+    for (const void* i : ins)
+      if (o == i) return HYDRA_ERR_SHAPE;
+  }
+  if (losses == d_lp || losses == d_v || (d_lp && d_lp == d_v)) return HYDRA_ERR_SHAPE;
+  for (const void* p : ins)
+    if (!aligned(p, 4)) return HYDRA_ERR_ALIGN;
+  for (const void* p : outs)
+    if (p && !aligned(p, 4)) return HYDRA_ERR_ALIGN;
+  hydra::PpoLossArgs a{};
+  a.lp_new = lp_new;
+  a.lp_old = lp_old;
+  a.adv = advantages;
+  a.values = values;
+  a.returns = returns;
+  a.n_seq = int(n_seq);
+  a.seq_len = int(seq_len);
+  a.start = int(start);
+  a.eps = eps;
+  a.losses = losses;
+  a.d_lp = d_lp;
+  a.d_v = d_v;
+  return from_hip(hydra::launch_ppo_loss(a, reinterpret_cast<hipStream_t>(stream)));
+}
+
 hydra_status hydra_ppo_advantages(const float* kl, const float* reward, const float* values, int64_t n_seq,
                                   int64_t seq_len, int64_t start, float beta, float gamma, float lam, float* rewards,
                                   float* advantages, float* returns, void* stream) {

@@ -158,6 +158,20 @@ struct GaeArgs {
   float* returns;       // [M]
 };
 
+// PPO update-stage losses over n_seq sequences of seq_len tokens.
+struct PpoLossArgs {
+  const float* lp_new;   // [M]
+  const float* lp_old;   // [M]
+  const float* adv;      // [M]
+  const float* values;   // [M]
+  const float* returns;  // [M]
+  int n_seq, seq_len, start;
+  float eps;
+  float* losses;         // [3]: policy loss, value loss, clipped fraction
+  float* d_lp;           // [M] or nullptr
+  float* d_v;            // [M] or nullptr
+};
+
 // Column-tile width of the fused scoring GEMM (number of vocabulary entries
 // one workgroup reduces).
 constexpr int kScoreTileN = 256;
@@ -174,6 +188,7 @@ hipError_t launch_lora_update(const GroupArgs& g, hipStream_t stream);
 hipError_t launch_score_gemm(const ScoreGemmArgs& a, hipStream_t stream);
 hipError_t launch_value_head(const ValueHeadArgs& a, hipStream_t stream);
 hipError_t launch_gae(const GaeArgs& a, hipStream_t stream);
+hipError_t launch_ppo_loss(const PpoLossArgs& a, hipStream_t stream);
 hipError_t launch_score_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_score_logits(const LogitsArgs& a, hipStream_t stream);
 

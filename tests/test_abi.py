@@ -307,3 +307,27 @@ def test_ppo_advantages_rejects(kw, code):
     a.update(kw)
     assert H.lib().hydra_ppo_advantages(a["kl"], a["reward"], a["values"], a["n_seq"], a["seq_len"], a["start"],
                                         0.02, 1.0, 0.95, a["rew"], a["adv"], a["ret"], None) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(lp_new=None), H.HYDRA_ERR_NULL),
+    (dict(losses=None), H.HYDRA_ERR_NULL),
+    (dict(n_seq=0), H.HYDRA_ERR_SHAPE),
+    (dict(start=8), H.HYDRA_ERR_SHAPE),
+    (dict(start=-1), H.HYDRA_ERR_SHAPE),
+    (dict(eps=1.0), H.HYDRA_ERR_SHAPE),
+    (dict(eps=-0.1), H.HYDRA_ERR_SHAPE),
+    (dict(eps=float("nan")), H.HYDRA_ERR_SHAPE),
+    (dict(d_lp=P), H.HYDRA_ERR_SHAPE),                  # gradient written over lp_new
+    (dict(d_v=P + 0x600), H.HYDRA_ERR_SHAPE),           # d_v == d_lp
+    (dict(losses=P + 0x600), H.HYDRA_ERR_SHAPE),        # losses == d_lp
+    (dict(values=P + 2), H.HYDRA_ERR_ALIGN),
+    (dict(d_v=P + 0x702), H.HYDRA_ERR_ALIGN),
+])
+def test_ppo_loss_rejects(kw, code):
+    a = dict(lp_new=P, lp_old=P + 0x100, adv=P + 0x200, values=P + 0x300, returns=P + 0x400, n_seq=2, seq_len=8,
+             start=0, eps=0.2, losses=P + 0x500, d_lp=P + 0x600, d_v=P + 0x700)
+    a.update(kw)
+    assert H.lib().hydra_ppo_loss(a["lp_new"], a["lp_old"], a["adv"], a["values"], a["returns"], a["n_seq"],
+                                  a["seq_len"], a["start"], a["eps"], a["losses"], a["d_lp"], a["d_v"],
+                                  None) == code

@@ -1,10 +1,10 @@
-"""GPU parity of hydra_value_head and hydra_ppo_advantages against the float64 oracle."""
+"""GPU parity of hydra_value_head, hydra_ppo_advantages and hydra_ppo_loss against the float64 oracle."""
 import numpy as np
 import pytest
 
 import paper_2309_00754_amd as H
 import workloads as WL
-from oracle import gae_ref, ppo_rewards_ref, value_head_ref
+from oracle import gae_ref, ppo_loss_ref, ppo_rewards_ref, value_head_ref
 from gpu_helpers import assert_rel, dev_bf16, host, say
 
 pytestmark = pytest.mark.gpu
@@ -92,3 +92,61 @@ def test_advantage_step_full_workload(dev):
     assert_rel(rew, e_rew, "rewards")
     assert_rel(adv, e_adv, "advantages")
     assert_rel(ret, e_ret, "returns")
+
+
+# ---------------------------------------------------------------- PPO losses
+def _loss_inputs(seed, n_seq, T):
+    rng = np.random.default_rng(seed)
+    M = n_seq * T
+    lp_old = -rng.uniform(0.5, 6.0, M).astype(np.float32)
+    lp_new = (lp_old + rng.normal(0, 0.3, M)).astype(np.float32)
+    A = rng.normal(0, 1, M).astype(np.float32)
+    V = rng.normal(0, 1, M).astype(np.float32)
+    R = (V + rng.normal(0, 0.5, M)).astype(np.float32)
+    return lp_new, lp_old, A, V, R
+
+
+def _run_loss(device, lp_new, lp_old, A, V, R, n_seq, T, start, eps):
+    import torch
+    t = [torch.from_numpy(np.ascontiguousarray(v)).to(device) for v in (lp_new, lp_old, A, V, R)]
+    losses = torch.full((3,), float("nan"), device=device)
+    d_lp = torch.full((n_seq * T,), float("nan"), device=device)
+    d_v = torch.full((n_seq * T,), float("nan"), device=device)
+    H.hydra_ppo_loss(*t, n_seq, T, losses, d_lp, d_v, start=start, eps=eps)
+    torch.cuda.synchronize()
+    return host(losses), host(d_lp), host(d_v)
+
+
+@pytest.mark.parametrize("n_seq,T,start,eps", [(4, 512, 0, 0.2), (4, 512, 256, 0.2), (3, 77, 5, 0.1), (1, 1, 0, 0.2),
+                                               (5, 3000, 100, 0.3), (2, 64, 10, 0.0)])
+def test_ppo_loss_matches_oracle(n_seq, T, start, eps, dev):
+    say("ppo_loss", n_seq, T, start, eps)
+    lp_new, lp_old, A, V, R = _loss_inputs(n_seq * 1000 + T + start, n_seq, T)
+    losses, d_lp, d_v = _run_loss(dev, lp_new, lp_old, A, V, R, n_seq, T, start, eps)
+    e = ppo_loss_ref(lp_new, lp_old, A, V, R, n_seq, T, start, eps)
+    for i, k in enumerate(("pg_loss", "v_loss")):
+        assert abs(losses[i] - e[k]) <= 1e-4 * max(abs(e[k]), 1e-3), (k, losses[i], e[k])
+    # the clipped fraction is a count: equal except where fp32 rounding moves rho across a clip bound
+    assert abs(losses[2] - e["clip_frac"]) <= 2.0 / (n_seq * (T - start))
+    assert_rel(d_lp, e["d_lp"], "d_lp")
+    assert_rel(d_v, e["d_v"], "d_v")
+    assert np.all(d_lp.reshape(n_seq, T)[:, :start] == 0) and np.all(d_v.reshape(n_seq, T)[:, :start] == 0)
+
+
+def test_ppo_loss_clip_cases_and_determinism(dev):
+    """The four sides of the clip on single-token sequences, and identical bits on a second run."""
+    say("ppo_loss clip cases")
+    rho = np.array([1.5, 0.5, 0.5, 1.5, 1.0], np.float64)
+    A = np.array([1.0, 1.0, -1.0, -1.0, 2.0], np.float32)
+    lp_old = np.zeros(5, np.float32)
+    lp_new = np.log(rho).astype(np.float32)
+    z = np.zeros(5, np.float32)
+    losses, d_lp, _ = _run_loss(dev, lp_new, lp_old, A, z, z, 5, 1, 0, 0.2)
+    # objective per token: 1.2, 0.5, -0.8, -1.5, 2.0 -> mean 0.28; unclipped gradient where active
+    assert abs(losses[0] + 0.28) < 1e-6
+    np.testing.assert_allclose(d_lp, [0.0, -0.1, 0.0, 0.3, -0.4], rtol=0, atol=1e-6)
+    assert abs(losses[2] - 0.4) < 1e-7
+    lp_new, lp_old, A, V, R = _loss_inputs(77, 4, 512)
+    a = _run_loss(dev, lp_new, lp_old, A, V, R, 4, 512, 0, 0.2)
+    b = _run_loss(dev, lp_new, lp_old, A, V, R, 4, 512, 0, 0.2)
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
