@@ -2,6 +2,7 @@
 from .hydra_oracle import (  # noqa: F401
     bf16_to_f64,
     lora_linear_ref,
+    lora_linear_backward_ref,
     lora_linear_multi_ref,
     log_softmax_gather_ref,
     score_logits_ref,

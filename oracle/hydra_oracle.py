@@ -39,6 +39,7 @@ from typing import Optional, Tuple
 import numpy as np
 
 __all__ = [
+    "lora_linear_backward_ref",
     "lora_linear_multi_ref",
     "bf16_to_f64",
     "lora_linear_ref",
@@ -81,6 +82,29 @@ def lora_linear_ref(x, W, A, B, s: float) -> Tuple[np.ndarray, np.ndarray]:
     T = _mm(X, Ad)                      # [M x r]
     y_on = y_off + float(s) * _mm(T, Bd)
     return y_off, y_on
+
+
+def lora_linear_backward_ref(x, W, A, B, s: float, dy):
+    """Gradients of the LoRA-on output with the base weight frozen (the PPO update
+    stage trains only the adapters: Sec. 2 Stage 3, LoRA on all linears; Table 1
+    update latency).  For y_on = X W^T + s (X A^T) B^T and an upstream gradient dY
+    of y_on (all bf16 bits but dY, which may be bf16 bits or float):
+      dX = dY W + s (dY B) A          [M x K]
+      dA = s (dY B)^T X               [r x K]
+      dB = s dY^T (X A^T)             [N x r]
+    in float64 (each is the plain chain rule of the forward definition).
+    """
+    X = bf16_to_f64(x)
+    Wd = bf16_to_f64(W)
+    Ad = bf16_to_f64(A)
+    Bd = bf16_to_f64(B)
+    dY = bf16_to_f64(dy) if np.asarray(dy).dtype == np.uint16 else np.asarray(dy, np.float64)
+    U = dY @ Bd                       # [M x r]
+    T = _mm(X, Ad)                    # [M x r]
+    dX = dY @ Wd + float(s) * (U @ Ad)
+    dA = float(s) * (U.T @ X)
+    dB = float(s) * (dY.T @ T)
+    return dX, dA, dB
 
 
 def lora_linear_multi_ref(x_off, W, x_ons, As, Bs, ss):

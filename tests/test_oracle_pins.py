@@ -177,6 +177,98 @@ def test_pins_catch_multi_mutations(mut):
     assert not _multi_pins_hold(mut)
 
 
+# ---------------------------------------------------------------- LoRA linear backward (update stage)
+def _frac_loss(xi, Wi, Ai, Bi, s, dyi):
+    """L = sum dY * y_on, exactly (Fractions): linear in each of x, A, B separately."""
+    _, y_on = _frac_lora(xi, Wi, Ai, Bi, s)
+    M, N = dyi.shape
+    return sum(Fraction(int(dyi[m, n])) * y_on[m][n] for m in range(M) for n in range(N))
+
+
+@pytest.mark.parametrize("M,K,N,r,s", [(2, 8, 3, 2, 2.0), (3, 8, 2, 1, -0.5), (1, 16, 4, 3, 0.25)])
+def test_lora_backward_exact_difference_quotients(M, K, N, r, s):
+    """L = <dY, y_on> is linear in x, in A and in B, so a unit step's difference quotient IS the derivative:
+    every entry of dX, dA, dB equals L(theta + e) - L(theta), computed exactly from the forward definition."""
+    rng = np.random.default_rng(M * 31 + K + r)
+    xb, xi = _int_bf16(rng, (M, K), -4, 4)
+    Wb, Wi = _int_bf16(rng, (N, K), -4, 4)
+    Ab, Ai = _int_bf16(rng, (r, K), -4, 4)
+    Bb, Bi = _int_bf16(rng, (N, r), -4, 4)
+    dyb, dyi = _int_bf16(rng, (M, N), -4, 4)
+    dX, dA, dB = O.lora_linear_backward_ref(xb, Wb, Ab, Bb, s, dyb)
+    L0 = _frac_loss(xi, Wi, Ai, Bi, s, dyi)
+    for m in range(M):
+        for k in range(K):
+            x2 = xi.copy()
+            x2[m, k] += 1
+            assert dX[m, k] == float(_frac_loss(x2, Wi, Ai, Bi, s, dyi) - L0)
+    for j in range(r):
+        for k in range(K):
+            a2 = Ai.copy()
+            a2[j, k] += 1
+            assert dA[j, k] == float(_frac_loss(xi, Wi, a2, Bi, s, dyi) - L0)
+    for n in range(N):
+        for j in range(r):
+            b2 = Bi.copy()
+            b2[n, j] += 1
+            assert dB[n, j] == float(_frac_loss(xi, Wi, Ai, b2, s, dyi) - L0)
+
+
+def test_lora_backward_b_zero_and_shapes():
+    """B = 0 (LoRA's zero init): dX is the base gradient dY W and dA vanishes, while dB does not."""
+    c = gen_linear(60, M=9, K=64, N=40, r=8, s=2.0)
+    rng = np.random.default_rng(1)
+    dy = rng.standard_normal((9, 40))
+    dX, dA, dB = O.lora_linear_backward_ref(c.x, c.W, c.A, np.zeros_like(c.B), c.s, dy)
+    np.testing.assert_allclose(dX, dy @ O.bf16_to_f64(c.W), rtol=1e-13, atol=1e-13)
+    assert np.all(dA == 0.0) and np.abs(dB).max() > 0
+    assert dX.shape == (9, 64) and dA.shape == (8, 64) and dB.shape == (40, 8)
+
+
+def _mut_bwd_db_from_swapped_factors(x, W, A, B, s, dy):
+    # dB from the LoRA-down product of dY instead of X: s dY^T (dY B) is the wrong chain
+    dX, dA, _ = O.lora_linear_backward_ref(x, W, A, B, s, dy)
+    dYd = O.bf16_to_f64(dy)
+    return dX, dA, s * dYd.T @ (dYd @ O.bf16_to_f64(B))
+
+
+def _mut_bwd_missing_scale(x, W, A, B, s, dy):
+    return O.lora_linear_backward_ref(x, W, A, B, 1.0, dy)
+
+
+def _mut_bwd_lora_dx_dropped(x, W, A, B, s, dy):
+    dX, dA, dB = O.lora_linear_backward_ref(x, W, A, B, s, dy)
+    base, _, _ = O.lora_linear_backward_ref(x, W, A, np.zeros_like(B), s, dy)
+    return base, dA, dB
+
+
+@pytest.mark.parametrize("mut", [_mut_bwd_db_from_swapped_factors, _mut_bwd_missing_scale, _mut_bwd_lora_dx_dropped])
+def test_pins_catch_backward_mutations(mut):
+    rng = np.random.default_rng(77)
+    M, K, N, r, s = 2, 8, 3, 2, 2.0
+    xb, xi = _int_bf16(rng, (M, K), -4, 4)
+    Wb, Wi = _int_bf16(rng, (N, K), -4, 4)
+    Ab, Ai = _int_bf16(rng, (r, K), -4, 4)
+    Bb, Bi = _int_bf16(rng, (N, r), -4, 4)
+    dyb, dyi = _int_bf16(rng, (M, N), -4, 4)
+    L0 = _frac_loss(xi, Wi, Ai, Bi, s, dyi)
+    dX, dA, dB = mut(xb, Wb, Ab, Bb, s, dyb)
+    ok = True
+    for (m, k) in [(0, 0), (1, 5)]:
+        x2 = xi.copy()
+        x2[m, k] += 1
+        ok &= dX[m, k] == float(_frac_loss(x2, Wi, Ai, Bi, s, dyi) - L0)
+    for (j, k) in [(0, 1), (1, 7)]:
+        a2 = Ai.copy()
+        a2[j, k] += 1
+        ok &= dA[j, k] == float(_frac_loss(xi, Wi, a2, Bi, s, dyi) - L0)
+    for (n, j) in [(0, 0), (2, 1)]:
+        b2 = Bi.copy()
+        b2[n, j] += 1
+        ok &= dB[n, j] == float(_frac_loss(xi, Wi, Ai, b2, s, dyi) - L0)
+    assert not ok
+
+
 # ---------------------------------------------------------------- log-softmax / gather
 
 def test_log_softmax_rows_normalise():
