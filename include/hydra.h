@@ -301,6 +301,57 @@ hydra_status hydra_ppo_loss(const float* lp_new, const float* lp_old, const floa
                             const float* returns, int64_t n_seq, int64_t seq_len, int64_t start, float eps,
                             float* losses, float* d_lp, float* d_v, void* stream);
 
+/*
+ * hydra_transpose_bf16 -- dst = src^T for a bf16 matrix: src [R x C]
+ * row-major, dst [C x R] row-major (dst[c * R + q] = src[q * C + c]).  The
+ * update stage's backward reads the frozen base weight as W^T [K x N]; the
+ * caller makes that copy once with this call (W does not change during
+ * training) and keeps it beside W.
+ *   src, dst   device, 2-byte aligned, not overlapping (HYDRA_ERR_SHAPE if equal)
+ *   R, C       >= 1, R * C below 2^62
+ * Bit-exact (a copy).
+ */
+hydra_status hydra_transpose_bf16(const uint16_t* src, int64_t R, int64_t C, uint16_t* dst, void* stream);
+
+/*
+ * hydra_lora_linear_backward_workspace_bytes -- device workspace that
+ * hydra_lora_linear_backward needs for M rows, N outputs, K inputs and rank r
+ * (0 for r == 0).  HYDRA_ERR_NULL for a NULL `bytes`, HYDRA_ERR_SHAPE for
+ * sizes outside the limits of hydra_lora_linear_backward.
+ */
+hydra_status hydra_lora_linear_backward_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t r, size_t* bytes);
+
+/*
+ * hydra_lora_linear_backward -- gradients of the LoRA-on output
+ * y = x W^T + s (x A^T) B^T with the base weight W frozen (the update stage
+ * trains only the adapter: Sec. 3 and App. A, Alg. 2; LoRA as in Sec. 2):
+ *   dx = dy W + s (dy B) A,   dA = s (dy B)^T x,   dB = s dy^T (x A^T).
+ *
+ *   x [M x K] bf16           the layer's input (device, 16-byte aligned)
+ *   Wt [K x N] bf16          W transposed (hydra_transpose_bf16 of W [N x K]);
+ *                            16-byte aligned; only read when dx is wanted
+ *   A [r x K], B [N x r] bf16   the adapter (A 16-byte aligned, B 2-byte)
+ *   s                        LoRA scale
+ *   dy [M x N] bf16          gradient of the loss with respect to y (16-byte aligned)
+ *   M >= 1; N, K >= 1, multiples of 8, at most 2^21; 0 <= r <= HYDRA_MAX_RANK
+ *   dx [M x K] fp32          out, optional
+ *   dA [r x K] fp32          out, optional (ignored for r == 0)
+ *   dB [N x r] fp32          out, optional (ignored for r == 0)
+ *   workspace, workspace_bytes   device memory of at least
+ *       hydra_lora_linear_backward_workspace_bytes(M, N, K, r) bytes, 16-byte
+ *       aligned, contents ignored and overwritten (NULL allowed for r == 0)
+ * dx comes from the MFMA GEMM of hydra_lora_linear_ws run on (dy, W^T) with
+ * s (dy B) as its pre-pass; dA and dB are fp32 sums of outer products over
+ * the M rows.  Every sum has a fixed order: repeated calls give the same bits.
+ * At least one output is required (HYDRA_ERR_NULL); outputs 4-byte aligned
+ * and distinct (HYDRA_ERR_SHAPE); HYDRA_ERR_WORKSPACE for a workspace that is
+ * too small.  Calls that share a workspace on different streams race.
+ */
+hydra_status hydra_lora_linear_backward(const uint16_t* x, const uint16_t* Wt, const uint16_t* A, const uint16_t* B,
+                                        float s, const uint16_t* dy, int64_t M, int64_t N, int64_t K, int64_t r,
+                                        float* dx, float* dA, float* dB, void* workspace, size_t workspace_bytes,
+                                        void* stream);
+
 /* A static, human-readable name for a status code. */
 const char* hydra_status_string(hydra_status status);
 

@@ -19,6 +19,8 @@ from ._binding import (  # noqa: F401
     HydraLibraryMissing,
     LIB_PATH,
     hydra_lora_linear,
+    hydra_lora_linear_backward,
+    hydra_lora_linear_backward_workspace_bytes,
     hydra_lora_linear_group,
     hydra_lora_linear_workspace_bytes,
     hydra_lora_linear_ws,
@@ -28,6 +30,7 @@ from ._binding import (  # noqa: F401
     hydra_score,
     hydra_score_logits,
     hydra_score_workspace_bytes,
+    hydra_transpose_bf16,
     hydra_value_head,
     lib,
     status_string,

@@ -39,6 +39,9 @@ EXPORTED = (
     "hydra_value_head",
     "hydra_ppo_advantages",
     "hydra_ppo_loss",
+    "hydra_transpose_bf16",
+    "hydra_lora_linear_backward_workspace_bytes",
+    "hydra_lora_linear_backward",
     "hydra_status_string",
     "hydra_abi_version",
 )
@@ -97,6 +100,13 @@ def lib() -> ctypes.CDLL:
     L.hydra_ppo_advantages.restype = ctypes.c_int
     L.hydra_ppo_loss.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _f32, _vp, _vp, _vp, _vp]
     L.hydra_ppo_loss.restype = ctypes.c_int
+    L.hydra_transpose_bf16.argtypes = [_vp, _i64, _i64, _vp, _vp]
+    L.hydra_transpose_bf16.restype = ctypes.c_int
+    L.hydra_lora_linear_backward_workspace_bytes.argtypes = [_i64, _i64, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]
+    L.hydra_lora_linear_backward_workspace_bytes.restype = ctypes.c_int
+    L.hydra_lora_linear_backward.argtypes = [_vp, _vp, _vp, _vp, _f32, _vp, _i64, _i64, _i64, _i64, _vp, _vp, _vp,
+                                             _vp, ctypes.c_size_t, _vp]
+    L.hydra_lora_linear_backward.restype = ctypes.c_int
     L.hydra_status_string.argtypes = [ctypes.c_int]
     L.hydra_status_string.restype = ctypes.c_char_p
     L.hydra_abi_version.argtypes = []
@@ -372,3 +382,52 @@ def hydra_ppo_loss(lp_new, lp_old, advantages, values, returns, n_seq: int, seq_
                               int(n_seq), int(seq_len), int(start), float(eps), _ptr(losses), _ptr(d_lp),
                               _ptr(d_v), _stream_handle(stream))
     _check(st, "hydra_ppo_loss")
+
+
+def hydra_transpose_bf16(src, dst, stream=None) -> None:
+    """dst [C,R] = src [R,C]^T for 16-bit tensors (see include/hydra.h)."""
+    bf = _bf16_types()
+    R, C = src.shape
+    _need(src, "src", bf)
+    _need(dst, "dst", bf, (C, R))
+    _check(lib().hydra_transpose_bf16(_ptr(src), R, C, _ptr(dst), _stream_handle(stream)), "hydra_transpose_bf16")
+
+
+def hydra_lora_linear_backward_workspace_bytes(M: int, N: int, K: int, r: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().hydra_lora_linear_backward_workspace_bytes(int(M), int(N), int(K), int(r), ctypes.byref(out)),
+           "hydra_lora_linear_backward_workspace_bytes")
+    return int(out.value)
+
+
+def hydra_lora_linear_backward(x, Wt, A, B, s: float, dy, dx=None, dA=None, dB=None, workspace=None,
+                               stream=None) -> None:
+    """dx, dA, dB of y = x W^T + s (x A^T) B^T with W frozen (see include/hydra.h).
+
+    x [M,K], Wt [K,N] (W transposed, may be None when dx is not wanted), A [r,K],
+    B [N,r], dy [M,N]: bf16 (or 16-bit integer tensors holding bf16 bits);
+    dx [M,K], dA [r,K], dB [N,r] float32 outputs (each optional).  Allocates
+    the workspace if none is given.
+    """
+    torch = _torch()
+    bf = _bf16_types()
+    M, N = dy.shape
+    K = A.shape[1] if A is not None else (x.shape[1] if x is not None else Wt.shape[0])
+    r = 0 if A is None else A.shape[0]
+    _need(x, "x", bf, (M, K))
+    _need(Wt, "Wt", bf, (K, N))
+    _need(A, "A", bf, (r, K))
+    _need(B, "B", bf, (N, r))
+    _need(dy, "dy", bf)
+    _need(dx, "dx", (torch.float32,), (M, K))
+    _need(dA, "dA", (torch.float32,), (r, K))
+    _need(dB, "dB", (torch.float32,), (N, r))
+    need = hydra_lora_linear_backward_workspace_bytes(M, N, K, r)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dy.device)
+    _need(workspace, "workspace", (torch.uint8,))
+    nbytes = 0 if workspace is None else workspace.numel()
+    st = lib().hydra_lora_linear_backward(_ptr(x), _ptr(Wt), _ptr(A), _ptr(B), float(s), _ptr(dy), M, N, K, r,
+                                          _ptr(dx), _ptr(dA), _ptr(dB), _ptr(workspace), nbytes,
+                                          _stream_handle(stream))
+    _check(st, "hydra_lora_linear_backward")

@@ -374,6 +374,66 @@ hydra_status hydra_ppo_loss(const float* lp_new, const float* lp_old, const floa
   return from_hip(hydra::launch_ppo_loss(a, reinterpret_cast<hipStream_t>(stream)));
 }
 
+hydra_status hydra_transpose_bf16(const uint16_t* src, int64_t R, int64_t C, uint16_t* dst, void* stream) {
+  if (!src || !dst) return HYDRA_ERR_NULL;
+  if (R < 1 || C < 1 || R > kMaxK || C > kMaxK) return HYDRA_ERR_SHAPE;
+  if (static_cast<const void*>(src) == static_cast<const void*>(dst)) return HYDRA_ERR_SHAPE;
+  if (!aligned(src, 2) || !aligned(dst, 2)) return HYDRA_ERR_ALIGN;
+  return from_hip(hydra::launch_transpose_pad(src, int(R), int(C), dst, int(R), int(C),
+                                              reinterpret_cast<hipStream_t>(stream)));
+}
+
+namespace {
+// Sizes the backward accepts: N and K as the forward's K (multiples of 8,
+// at most 2^21), M up to 2^24 rows (the pre-pass indexes M x 128 with 32 bits).
+bool backward_shape_ok(int64_t M, int64_t N, int64_t K, int64_t r) {
+  return M >= 1 && M <= (int64_t(1) << 24) && dim_ok(N) && dim_ok(K) && N % 8 == 0 && K % 8 == 0 && N <= kMaxK &&
+         K <= kMaxK && r >= 0 && r <= HYDRA_MAX_RANK;
+}
+}  // namespace
+
+hydra_status hydra_lora_linear_backward_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t r, size_t* bytes) {
+  if (!bytes) return HYDRA_ERR_NULL;
+  if (!backward_shape_ok(M, N, K, r)) return HYDRA_ERR_SHAPE;
+  *bytes = hydra::backward_ws_bytes(int(M), int(N), int(K), hydra::padded_rank(int(r)));
+  return HYDRA_OK;
+}
+
+hydra_status hydra_lora_linear_backward(const uint16_t* x, const uint16_t* Wt, const uint16_t* A, const uint16_t* B,
+                                        float s, const uint16_t* dy, int64_t M, int64_t N, int64_t K, int64_t r,
+                                        float* dx, float* dA, float* dB, void* workspace, size_t workspace_bytes,
+                                        void* stream) {
+  if (!backward_shape_ok(M, N, K, r)) return HYDRA_ERR_SHAPE;
+  if (r == 0) dA = dB = nullptr;  // empty
+  if (!dx && !dA && !dB) return HYDRA_ERR_NULL;
+  if (!dy || (dx && !Wt) || (r > 0 && (!A || !B)) || ((dA || dB) && !x)) return HYDRA_ERR_NULL;
+  if ((dx && (dx == dA || dx == dB)) || (dA && dA == dB)) return HYDRA_ERR_SHAPE;
+  if (!aligned(dy, 16) || (x && !aligned(x, 16)) || (dx && !aligned(Wt, 16))) return HYDRA_ERR_ALIGN;
+  if (r > 0 && (!aligned(A, 16) || !aligned(B, 2))) return HYDRA_ERR_ALIGN;
+  if ((dx && !aligned(dx, 4)) || (dA && !aligned(dA, 4)) || (dB && !aligned(dB, 4))) return HYDRA_ERR_ALIGN;
+  const size_t need = hydra::backward_ws_bytes(int(M), int(N), int(K), hydra::padded_rank(int(r)));
+  if (need > 0) {
+    if (!workspace) return HYDRA_ERR_NULL;
+    if (workspace_bytes < need) return HYDRA_ERR_WORKSPACE;
+    if (!aligned(workspace, 16)) return HYDRA_ERR_ALIGN;
+  }
+  hydra::BackwardArgs a{};
+  a.x = x;
+  a.Wt = Wt;
+  a.A = A;
+  a.B = B;
+  a.dy = dy;
+  a.s = s;
+  a.M = int(M);
+  a.N = int(N);
+  a.K = int(K);
+  a.r = int(r);
+  a.dx = dx;
+  a.dA = dA;
+  a.dB = dB;
+  return from_hip(hydra::launch_lora_backward(a, workspace, reinterpret_cast<hipStream_t>(stream)));
+}
+
 hydra_status hydra_ppo_advantages(const float* kl, const float* reward, const float* values, int64_t n_seq,
                                   int64_t seq_len, int64_t start, float beta, float gamma, float lam, float* rewards,
                                   float* advantages, float* returns, void* stream) {

@@ -71,9 +71,10 @@ struct TpreArgs {
   const uint16_t* B;  // [N x r] bf16
   float s;
   int M, N, K, r;
-  uint16_t* ts;
+  uint16_t* ts;       // [M x 2 RP] hi | lo of s T, or nullptr
   uint16_t* bp;       // used only when B itself cannot serve (r != RP or B not 16-byte aligned)
   float* part;        // [kTpreMaxChunks x M x RP] fp32 partial sums over K chunks
+  float* t32;         // [M x RP] fp32 s T, or nullptr
 };
 // K is split into at most kTpreMaxChunks chunks of at least 1024, so that
 // the pre-pass spreads over many workgroups; the partial products are then
@@ -171,6 +172,30 @@ struct PpoLossArgs {
   float* d_lp;           // [M] or nullptr
   float* d_v;            // [M] or nullptr
 };
+
+// Backward of the LoRA-switchable linear with W frozen (see lora_backward.hip).
+struct BackwardArgs {
+  const uint16_t* x;   // [M x K]
+  const uint16_t* Wt;  // [K x N], W transposed
+  const uint16_t* A;   // [r x K]
+  const uint16_t* B;   // [N x r]
+  const uint16_t* dy;  // [M x N]
+  float s;
+  int M, N, K, r;
+  float* dx;           // [M x K] or nullptr
+  float* dA;           // [r x K] or nullptr
+  float* dB;           // [N x r] or nullptr
+};
+// Workspace bytes of the backward, and the launcher (which assumes a
+// workspace of at least that size, 16-byte aligned).
+size_t backward_ws_bytes(int M, int N, int K, int rp);
+hipError_t launch_lora_backward(const BackwardArgs& a, void* ws, hipStream_t stream);
+// dst [Cp x Rp] bf16: dst[c][q] = src[q][c] for c < C, q < R (src [R x C]), else 0.
+hipError_t launch_transpose_pad(const uint16_t* src, int R, int C, uint16_t* dst, int Rp, int Cp, hipStream_t stream);
+// The GEMM of lora_gemm_kernel<RP, true> with its LoRA slabs already in memory
+// (ts [M x 2 RP] hi | lo, bp [N x RP]).
+hipError_t launch_lora_gemm_slabs(const LinearArgs& a, const uint16_t* ts, const uint16_t* bp, int rp,
+                                  hipStream_t stream);
 
 // Column-tile width of the fused scoring GEMM (number of vocabulary entries
 // one workgroup reduces).

@@ -588,4 +588,17 @@ hipError_t launch_lora_gemm_tpre(const LinearArgs& a, uint16_t* ts, uint16_t* bp
   return launch(g, rp, true, stream);
 }
 
+hipError_t launch_lora_gemm_slabs(const LinearArgs& a, const uint16_t* ts, const uint16_t* bp, int rp,
+                                  hipStream_t stream) {
+  GemmArgs g{};
+  g.lin = a;
+  g.ntm = (a.M + BM - 1) / BM;
+  g.ntn = (a.N + BN - 1) / BN;
+  g.vec4 = (a.N % 4 == 0) && (!a.y_off || aligned16(a.y_off)) && aligned16(a.y_on);
+  g.ts = ts;
+  g.bp = bp;
+  g.nls = (2 * rp + BK - 1) / BK;
+  return launch(g, rp, true, stream);
+}
+
 }  // namespace hydra

@@ -78,8 +78,8 @@ __global__ __launch_bounds__(T_WAVES * 64) void lora_t_part_kernel(TpreArgs a, i
 }
 
 // s * T from the chunk partials (added in chunk order), split into bf16 hi and
-// lo parts; the workgroups past the rows write B zero padded to RP when the
-// GEMM cannot read B itself.
+// lo parts (and / or kept in fp32); the workgroups past the rows write B zero
+// padded to RP when the GEMM cannot read B itself.
 template <int RP>
 __global__ __launch_bounds__(256) void lora_t_finish_kernel(TpreArgs a, int nkc, int tblocks) {
   if ((int)blockIdx.x < tblocks) {
@@ -89,10 +89,13 @@ __global__ __launch_bounds__(256) void lora_t_finish_kernel(TpreArgs a, int nkc,
     float v = 0.f;
     for (int c = 0; c < nkc; ++c) v += a.part[((size_t)c * a.M + row) * RP + j];
     v *= a.s;
-    const uint32_t hi = f32_to_bf16_rne(v);
-    const uint32_t lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
-    a.ts[row * 2 * RP + j] = (uint16_t)hi;
-    a.ts[row * 2 * RP + RP + j] = (uint16_t)lo;
+    if (a.t32) a.t32[e] = v;
+    if (a.ts) {
+      const uint32_t hi = f32_to_bf16_rne(v);
+      const uint32_t lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
+      a.ts[row * 2 * RP + j] = (uint16_t)hi;
+      a.ts[row * 2 * RP + RP + j] = (uint16_t)lo;
+    }
     return;
   }
   const size_t total = (size_t)a.N * RP;
@@ -110,9 +113,10 @@ hipError_t launch_rp(const TpreArgs& a, const uint16_t** bp_used, hipStream_t st
   hipLaunchKernelGGL((lora_t_part_kernel<RP>), dim3((a.M + 15) / 16, nkc), dim3(T_WAVES * 64), 0, stream, a, kch);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // B serves as its own padded copy when its rows already are RP bf16, 16-byte aligned
-  const bool direct = a.r == RP && (reinterpret_cast<uintptr_t>(a.B) & 15) == 0;
-  *bp_used = direct ? a.B : a.bp;
+  // B serves as its own padded copy when its rows already are RP bf16, 16-byte
+  // aligned; no B at all (a.B null): nothing to pad
+  const bool direct = a.B == nullptr || (a.r == RP && (reinterpret_cast<uintptr_t>(a.B) & 15) == 0);
+  if (bp_used) *bp_used = a.B == nullptr ? nullptr : direct ? a.B : a.bp;
   const int tblocks = (int)(((size_t)a.M * RP + 255) / 256);
   const size_t total = (size_t)a.N * RP;
   const int bblocks = direct ? 0 : (int)((total + 255) / 256 < 2048 ? (total + 255) / 256 : 2048);

@@ -23,7 +23,7 @@ P8 = 0x10008     # only 8-byte aligned
 def _declared_functions():
     txt = open(HEADER).read()
     txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
-    return sorted(set(re.findall(r"\b(hydra_[a-z_]+)\s*\(", txt)))
+    return sorted(set(re.findall(r"\b(hydra_[a-z0-9_]+)\s*\(", txt)))
 
 
 def test_every_declared_symbol_is_exported():
@@ -331,3 +331,95 @@ def test_ppo_loss_rejects(kw, code):
     assert H.lib().hydra_ppo_loss(a["lp_new"], a["lp_old"], a["adv"], a["values"], a["returns"], a["n_seq"],
                                   a["seq_len"], a["start"], a["eps"], a["losses"], a["d_lp"], a["d_v"],
                                   None) == code
+
+
+# ------------------------------------------------------------------ backward of the LoRA linear, transpose
+
+def _bwd(x=P, Wt=P + 0x100, A=P + 0x200, B=P + 0x300, s=2.0, dy=P + 0x400, M=64, N=64, K=64, r=16,
+         dx=P + 0x1000, dA=P + 0x2000, dB=P + 0x3000, ws=P + 0x10000, nbytes=1 << 24):
+    return H.lib().hydra_lora_linear_backward(x, Wt, A, B, s, dy, M, N, K, r, dx, dA, dB, ws, nbytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dy=None), H.HYDRA_ERR_NULL),
+    (dict(dx=None, dA=None, dB=None), H.HYDRA_ERR_NULL),
+    (dict(r=0, dx=None), H.HYDRA_ERR_NULL),               # dA, dB are empty at rank 0: no output left
+    (dict(Wt=None), H.HYDRA_ERR_NULL),                    # dx needs W^T
+    (dict(A=None), H.HYDRA_ERR_NULL),
+    (dict(B=None), H.HYDRA_ERR_NULL),
+    (dict(x=None), H.HYDRA_ERR_NULL),                     # dA, dB need x
+    (dict(ws=None), H.HYDRA_ERR_NULL),
+    (dict(nbytes=1000), H.HYDRA_ERR_WORKSPACE),
+    (dict(M=0), H.HYDRA_ERR_SHAPE),
+    (dict(M=(1 << 24) + 1), H.HYDRA_ERR_SHAPE),
+    (dict(N=12), H.HYDRA_ERR_SHAPE),
+    (dict(K=20), H.HYDRA_ERR_SHAPE),
+    (dict(K=(1 << 21) + 8), H.HYDRA_ERR_SHAPE),
+    (dict(N=(1 << 21) + 8), H.HYDRA_ERR_SHAPE),
+    (dict(r=129), H.HYDRA_ERR_SHAPE),
+    (dict(r=-1), H.HYDRA_ERR_SHAPE),
+    (dict(dA=P + 0x1000), H.HYDRA_ERR_SHAPE),             # dA == dx
+    (dict(dB=P + 0x2000), H.HYDRA_ERR_SHAPE),             # dB == dA
+    (dict(dy=P8), H.HYDRA_ERR_ALIGN),
+    (dict(x=P8), H.HYDRA_ERR_ALIGN),
+    (dict(Wt=P8 + 0x100), H.HYDRA_ERR_ALIGN),
+    (dict(A=P8 + 0x200), H.HYDRA_ERR_ALIGN),
+    (dict(B=P + 0x301), H.HYDRA_ERR_ALIGN),
+    (dict(dB=P + 0x3002), H.HYDRA_ERR_ALIGN),
+    (dict(ws=P + 0x10008), H.HYDRA_ERR_ALIGN),
+])
+def test_lora_linear_backward_rejects(kw, code):
+    assert _bwd(**kw) == code
+
+
+def test_lora_linear_backward_optional_inputs():
+    """Pointers an output does not need may be NULL (W^T without dx, x without dA / dB, A / B and the
+    workspace at rank 0); the checks that remain still fire, so the call is rejected for the one left."""
+    assert _bwd(Wt=None, dx=None, x=P8) == H.HYDRA_ERR_ALIGN             # Wt unused, x still checked
+    assert _bwd(x=None, dA=None, dB=None, Wt=P8) == H.HYDRA_ERR_ALIGN     # x unused, Wt still checked
+    assert _bwd(r=0, A=None, B=None, ws=None, nbytes=0, dy=P8) == H.HYDRA_ERR_ALIGN
+
+
+def _outer_chunks(M, C, rp):
+    tiles = -(-C // 256) * (rp // 16)
+    want = max(1, -(-1024 // tiles))
+    rows = -(-M // want)
+    rows = max(16, -(-rows // 16) * 16)
+    return -(-M // rows)
+
+
+def _bwd_ws(M, N, K, rp):
+    if rp == 0:
+        return 0
+    up = lambda v: -(-v // 256) * 256  # noqa: E731
+    oa = _outer_chunks(M, K, rp) * rp * K
+    ob = _outer_chunks(M, N, rp) * rp * N
+    return (up(rp * N * 2) + up(K * rp * 2) + up(M * 2 * rp * 2) + 2 * up(M * rp * 4) + up(8 * M * rp * 4)
+            + up(max(oa, ob) * 4))
+
+
+def test_backward_workspace_bytes():
+    for M, N, K, r, rp in [(2048, 4096, 4096, 16, 16), (2048, 11008, 4096, 16, 16), (2048, 4096, 11008, 128, 128),
+                           (3, 8, 16, 33, 64), (1, 8, 8, 1, 16)]:
+        assert H.hydra_lora_linear_backward_workspace_bytes(M, N, K, r) == _bwd_ws(M, N, K, rp)
+    assert H.hydra_lora_linear_backward_workspace_bytes(7, 8, 8, 0) == 0
+    # the outer-product partials stay near 16 MiB however the shape grows (about 1024 workgroups' worth)
+    assert H.hydra_lora_linear_backward_workspace_bytes(65536, 4096, 4096, 16) < 64 << 20
+    L = H.lib()
+    out = ctypes.c_size_t(0)
+    assert L.hydra_lora_linear_backward_workspace_bytes(0, 8, 8, 16, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
+    assert L.hydra_lora_linear_backward_workspace_bytes(8, 12, 8, 16, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
+    assert L.hydra_lora_linear_backward_workspace_bytes(8, 8, 8, 129, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
+    assert L.hydra_lora_linear_backward_workspace_bytes(8, 8, 8, 16, None) == H.HYDRA_ERR_NULL
+
+
+@pytest.mark.parametrize("src,R,C,dst,code", [
+    (None, 4, 4, P + 0x100, H.HYDRA_ERR_NULL),
+    (P, 4, 4, None, H.HYDRA_ERR_NULL),
+    (P, 0, 4, P + 0x100, H.HYDRA_ERR_SHAPE),
+    (P, 4, (1 << 21) + 1, P + 0x100, H.HYDRA_ERR_SHAPE),
+    (P, 4, 4, P, H.HYDRA_ERR_SHAPE),                      # in place
+    (P + 1, 4, 4, P + 0x100, H.HYDRA_ERR_ALIGN),
+])
+def test_transpose_rejects(src, R, C, dst, code):
+    assert H.lib().hydra_transpose_bf16(src, R, C, dst, None) == code

@@ -1,0 +1,117 @@
+"""GPU parity of the LoRA-linear backward (W frozen) and of the bf16 transpose it uses, against the float64
+oracle (dx = dy W + s (dy B) A, dA = s (dy B)^T x, dB = s dy^T (x A^T))."""
+import numpy as np
+import pytest
+
+import paper_2309_00754_amd as H
+import workloads as WL
+from oracle import lora_linear_backward_ref
+from gpu_helpers import assert_rel, dev_bf16, host, say
+
+pytestmark = pytest.mark.gpu
+
+BWD_SHAPES = [
+    # (M, K, N, r): rows past one 256-row tile and ragged, K and N multiples of 8 with ragged column tiles,
+    # every padded rank (1, 16, 33 -> 64, 100 -> 128, 128), rank 0, one row, and a row count that leaves a
+    # partial outer-product chunk.
+    (17, 64, 256, 8), (130, 520, 304, 16), (257, 1024, 704, 33), (64, 128, 96, 64), (300, 2048, 1200, 100),
+    (130, 520, 304, 128), (1, 64, 40, 1), (5, 8, 8, 128), (200, 64, 256, 0), (1000, 72, 24, 16),
+]
+
+
+def _wt(W, device):
+    import torch
+    Wd = dev_bf16(W, device)
+    Wt = torch.empty((W.shape[1], W.shape[0]), dtype=Wd.dtype, device=device)
+    H.hydra_transpose_bf16(Wd, Wt)
+    return Wt
+
+
+def _run(case, device, want=("dx", "dA", "dB"), B=None, fill=0):
+    import torch
+    c = case.lin
+    x, dy = dev_bf16(c.x, device), dev_bf16(case.dy, device)
+    A = dev_bf16(c.A, device) if c.r > 0 else None
+    Bm = c.B if B is None else B
+    Bd = dev_bf16(Bm, device) if c.r > 0 else None
+    Wt = _wt(c.W, device) if "dx" in want else None
+    nan = float("nan")
+    dx = torch.full((c.M, c.K), nan, device=device) if "dx" in want else None
+    dA = torch.full((c.r, c.K), nan, device=device) if "dA" in want and c.r > 0 else None
+    dB = torch.full((c.N, c.r), nan, device=device) if "dB" in want and c.r > 0 else None
+    need = H.hydra_lora_linear_backward_workspace_bytes(c.M, c.N, c.K, c.r)
+    ws = torch.full((max(need, 1),), fill, dtype=torch.uint8, device=device)
+    H.hydra_lora_linear_backward(x, Wt, A, Bd, c.s, dy, dx, dA, dB, workspace=ws)
+    torch.cuda.synchronize()
+    return tuple(None if t is None else host(t) for t in (dx, dA, dB))
+
+
+@pytest.mark.parametrize("R,C", [(1, 1), (64, 64), (65, 130), (300, 7), (7, 300), (4096, 520)])
+def test_transpose_bit_exact(R, C, dev):
+    import torch
+    say("transpose", R, C)
+    rng = np.random.Generator(np.random.PCG64(R * 1000 + C))
+    src = rng.integers(0, 1 << 16, size=(R, C), dtype=np.uint16)
+    s = dev_bf16(src, dev)
+    d = torch.empty((C, R), dtype=s.dtype, device=dev)
+    H.hydra_transpose_bf16(s, d)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(d).view(np.uint16), src.T)
+
+
+@pytest.mark.parametrize("M,K,N,r", BWD_SHAPES)
+def test_backward_matches_oracle(M, K, N, r, dev):
+    say("backward", M, K, N, r)
+    case = WL.gen_backward(700 + M + r, M, K, N, r)
+    c = case.lin
+    dx, dA, dB = _run(case, dev)
+    e_dx, e_dA, e_dB = lora_linear_backward_ref(c.x, c.W, c.A, c.B, c.s, case.dy)
+    assert_rel(dx, e_dx, "dx")
+    if r > 0:
+        assert_rel(dA, e_dA, "dA")
+        assert_rel(dB, e_dB, "dB")
+
+
+def test_backward_outputs_independent_and_deterministic(dev):
+    """Each output alone has the bits of the full call; a workspace full of 0xFF bytes changes nothing."""
+    say("backward subsets")
+    case = WL.gen_backward(777, 260, 520, 304, 24)
+    full = _run(case, dev)
+    again = _run(case, dev, fill=0xFF)
+    for a, b in zip(full, again):
+        assert np.array_equal(a, b)
+    for i, name in enumerate(("dx", "dA", "dB")):
+        alone = _run(case, dev, want=(name,))
+        assert np.array_equal(alone[i], full[i]), name
+
+
+def test_backward_b_zero(dev):
+    """B = 0: dA is exactly 0 (U = dy B vanishes) and dx has the bits of the rank-0 call (dy W alone)."""
+    say("backward B=0")
+    case = WL.gen_backward(778, 130, 256, 264, 16)
+    c = case.lin
+    dx, dA, dB = _run(case, dev, B=np.zeros_like(c.B))
+    assert np.all(dA == 0.0)
+    base = WL.BackwardCase(WL.LinearCase("r0", c.x, c.W, c.A[:0], c.B[:, :0], c.s), case.dy)
+    dx0, _, _ = _run(base, dev)
+    assert np.array_equal(dx, dx0)
+    _, _, e_dB = lora_linear_backward_ref(c.x, c.W, c.A, np.zeros_like(c.B), c.s, case.dy)
+    assert_rel(dB, e_dB, "dB")
+
+
+@pytest.mark.parametrize("proj", ["q", "gate", "down"])
+def test_backward_llama_layer_full_size(proj, dev):
+    """The Llama-7B layer's backward at M = 2048, rank 16 (the bench's shapes): dA and dB whole, dx on
+    sampled rows (each row of dx depends on its own row of dy only)."""
+    say("backward full size", proj)
+    cases = {b.lin.name: b for b in WL.make("backward_layer")}
+    case = cases[proj]
+    c = case.lin
+    dx, dA, dB = _run(case, dev)
+    rows = np.random.Generator(np.random.PCG64(11)).choice(c.M, 24, replace=False)
+    rows[:2] = [0, c.M - 1]
+    e_dx, _, _ = lora_linear_backward_ref(c.x[rows], c.W, c.A, c.B, c.s, case.dy[rows])
+    assert_rel(dx[rows], e_dx, "dx rows")
+    _, e_dA, e_dB = lora_linear_backward_ref(c.x, c.W, c.A, c.B, c.s, case.dy)
+    assert_rel(dA, e_dA, "dA")
+    assert_rel(dB, e_dB, "dB")

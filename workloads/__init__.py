@@ -28,7 +28,9 @@ weights are not available, so Gaussian stand-ins are drawn):
 * the PPO advantage step: critic hidden states ~ N(0, 1), value head
   ~ N(0, 1/K), per-token KL estimates ~ N(0, 0.1^2) (the spread of lp_on -
   lp_off when the LoRA-on and LoRA-off logits differ by N(0, 0.1^2) noise),
-  sequence rewards ~ N(0, 1).
+  sequence rewards ~ N(0, 1);
+* the backward of the LoRA-switchable linear (update stage): the forward's
+  inputs as above, then one upstream gradient dy [M x N] ~ N(0, 1) per linear.
 """
 from __future__ import annotations
 
@@ -45,6 +47,9 @@ __all__ = [
     "gen_linears",
     "gen_logits",
     "gen_score_head",
+    "BackwardCase",
+    "gen_backward",
+    "gen_backward_layer",
     "AdvantageCase",
     "gen_advantages",
     "WORKLOADS",
@@ -150,6 +155,37 @@ def gen_linears(seed: int, M: int, proj, r: int, s: float = 2.0) -> List[LinearC
         W, A, B = _lora_weights(rng, K, N, r)
         cases.append(LinearCase(name, xs[K], W, A, B, float(s)))
     return cases
+
+
+@dataclasses.dataclass
+class BackwardCase:
+    """Backward of one LoRA-switchable linear: its forward inputs and the upstream gradient dy [M x N] (bf16 bits)."""
+    lin: LinearCase
+    dy: np.ndarray
+
+
+def gen_backward(seed: int, M: int, K: int, N: int, r: int, s: float = 2.0, name: str = "backward") -> BackwardCase:
+    """Draw order: x, W, A, B (as gen_linear), then dy."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    x = _normal_bf16(rng, (M, K), 1.0)
+    W, A, B = _lora_weights(rng, K, N, r)
+    dy = _normal_bf16(rng, (M, N), 1.0)
+    return BackwardCase(LinearCase(name, x, W, A, B, float(s)), dy)
+
+
+def gen_backward_layer(seed: int, M: int, proj, r: int, s: float = 2.0) -> List[BackwardCase]:
+    """The backward of every listed linear: the inputs of gen_linears (same draw order), then one dy per
+    projection in the listed order."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    xs: Dict[int, np.ndarray] = {}
+    for _, K, _ in proj:
+        if K not in xs:
+            xs[K] = _normal_bf16(rng, (M, K), 1.0)
+    lins = []
+    for name, K, N in proj:
+        W, A, B = _lora_weights(rng, K, N, r)
+        lins.append(LinearCase(name, xs[K], W, A, B, float(s)))
+    return [BackwardCase(c, _normal_bf16(rng, (M, c.N), 1.0)) for c in lins]
 
 
 def gen_logits(seed: int, M: int, V: int, noise_std: float = 0.1, logit_std: float = 2.0):
@@ -297,6 +333,8 @@ WORKLOADS = {
     "ppo_advantages": dict(seed=5, n_seq=4, seq_len=512, K=4096, start=0, beta=0.02, gamma=1.0, lam=0.95),
     # one decode projection serving the reference (LoRA off), actor and critic passes (M = 4 each)
     "decode_multi": dict(seed=6, M=4, K=4096, N=4096, r=16, n_on=2),
+    # the update stage's backward through every linear of one layer (W frozen, rank-16 adapters trained)
+    "backward_layer": dict(seed=7, M=2048, proj=PREFILL_PROJ, r=16, s=2.0),
 }
 
 
@@ -313,6 +351,8 @@ def make(name: str, M: Optional[int] = None):
         return gen_score_head(w["seed"], w["n_seq"], w["seq_len"], w["K"], w["V"], w["r"], w["s"])
     if name == "decode_multi":
         return gen_multi(w["seed"], M or w["M"], w["K"], w["N"], w["r"], w["n_on"], name=name)
+    if name == "backward_layer":
+        return gen_backward_layer(w["seed"], M or w["M"], w["proj"], w["r"], w["s"])
     if name == "ppo_advantages":
         return gen_advantages(w["seed"], w["n_seq"], w["seq_len"], w["K"], w["start"], w["beta"], w["gamma"], w["lam"])
     raise KeyError(name)
