@@ -293,7 +293,8 @@ def main():
     if not args.no_aux:
         out["aux"] = {"score_logits": bench_score_logits(torch, H, WL, dev),
                       "ppo_advantages": bench_advantages(torch, H, WL, dev),
-                      "decode_multi": bench_decode_multi(torch, H, WL, dev)}
+                      "decode_multi": bench_decode_multi(torch, H, WL, dev),
+                      "lora_backward_layer": bench_backward(torch, H, WL, dev)}
 
     if not args.no_cpu_baseline:
         hi = None
@@ -464,6 +465,56 @@ def bench_decode_multi(torch, H, WL, dev, iters=20, sets=3):
                 speedup=round(t_sep / t_multi, 3), multi_pass_equiv_gbps=round(by / t_multi / 1e3, 1),
                 note="multi stacks the 12 input rows into two reads of W (8 + 4 rows); separate reads W three "
                      "times; GB/s counts the bytes of three independent passes")
+
+
+def bench_backward(torch, H, WL, dev, iters=5):
+    """The update stage's backward through every linear of one Llama-7B layer at M = 2048, rank 16, W frozen
+    (hydra_lora_linear_backward: dx, dA, dB).  W^T is made once beforehand (W does not change while the adapters
+    train).  Each figure is the average over a block of back-to-back layer passes between one pair of events."""
+    cases = WL.make("backward_layer")
+    bf = (lambda u: torch.from_numpy(np.ascontiguousarray(u).view(np.int16)).to(dev))
+    xs, calls, flops = {}, [], []
+    for b in cases:
+        c = b.lin
+        if id(c.x) not in xs:
+            xs[id(c.x)] = bf(c.x)
+        W = bf(c.W)
+        Wt = torch.empty((c.K, c.N), dtype=W.dtype, device=dev)
+        H.hydra_transpose_bf16(W, Wt)
+        del W
+        A, B, dy = bf(c.A), bf(c.B), bf(b.dy)
+        dx = torch.empty(c.M, c.K, device=dev)
+        dA = torch.empty(c.r, c.K, device=dev)
+        dB = torch.empty(c.N, c.r, device=dev)
+        ws = torch.empty(H.hydra_lora_linear_backward_workspace_bytes(c.M, c.N, c.K, c.r), dtype=torch.uint8,
+                         device=dev)
+        x = xs[id(c.x)]
+        calls.append((c.name, lambda x=x, Wt=Wt, A=A, B=B, s=c.s, dy=dy, dx=dx, dA=dA, dB=dB, ws=ws:
+                      H.hydra_lora_linear_backward(x, Wt, A, B, s, dy, dx, dA, dB, workspace=ws)))
+        # dx = dy W (2MNK) + s U A (2MrK); U = dy B (2MNr); T = x A^T (2MKr); dA (2rKM); dB (2NrM)
+        flops.append(2.0 * c.M * c.N * c.K + 4.0 * c.M * c.N * c.r + 6.0 * c.M * c.K * c.r)
+    stream = torch.cuda.current_stream()
+
+    def timed(fns):
+        for fn in fns:
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            for fn in fns:
+                fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters * 1e3
+
+    t_layer = timed([fn for _, fn in calls])
+    per = {name: round(timed([fn]), 2) for name, fn in calls}
+    fl = sum(flops)
+    c0 = cases[0].lin
+    return dict(M=c0.M, r=c0.r, layer_us=round(t_layer, 2), per_linear_us=per,
+                tflops=round(fl / t_layer / 1e6, 2), frac_bf16_peak=round(fl / t_layer / 1e6 / PEAK_BF16_TFLOPS, 4),
+                note="dx, dA and dB of the 7 linears; FLOPs = 2MNK + 4MNr + 6MKr per linear; W^T prepared once")
 
 
 def cpu_baseline(target_s: float, host_inputs=None):

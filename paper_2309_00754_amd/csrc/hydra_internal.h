@@ -89,6 +89,9 @@ inline void tpre_chunks(int K, int& nkc, int& kch) {
 // Launches the pre-pass; *bp_used is where the padded B rows are (a.bp, or
 // a.B itself when it already has that layout).
 hipError_t launch_lora_tpre(const TpreArgs& a, int rp, const uint16_t** bp_used, hipStream_t stream);
+// Two pre-passes over the same M rows, neither with B to pad, in the same two
+// launches.
+hipError_t launch_lora_tpre2(const TpreArgs& a0, const TpreArgs& a1, int rp, hipStream_t stream);
 // Padded rank: the smallest of 16, 32, 64, 128 that holds r (0 for r == 0).
 inline int padded_rank(int r) { return r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : r <= 64 ? 64 : 128; }
 

@@ -14,7 +14,9 @@
 //    extra workgroups pad B to the padded rank when B's own rows cannot be
 //    read as they are (r not 16, 32, 64 or 128, or B not 16-byte aligned).
 // Both GEMMs then add s T B^T as 2 RP more k values of their main loop:
-// rows of [hi | lo] against rows of [Bp | Bp].
+// rows of [hi | lo] against rows of [Bp | Bp].  Both kernels can also run two
+// such pre-passes over the same rows in one launch (the backward's s dy B and
+// s x A^T).
 #include "hydra_device.h"
 #include "hydra_internal.h"
 
@@ -24,11 +26,12 @@ namespace {
 constexpr int T_WAVES = 8;
 constexpr int T_UNROLL = 4;
 
-// Partial T over K chunk blockIdx.y for 16 rows: the 8 waves take the chunk's
-// 32-wide k-steps in turn, T_UNROLL at a time (all their loads in flight
-// before the first MFMA); their partial tiles are summed in LDS in wave order.
+// Partial T over K chunk kc for the 16 rows of blockIdx.x: the 8 waves take
+// the chunk's 32-wide k-steps in turn, T_UNROLL at a time (all their loads in
+// flight before the first MFMA); their partial tiles are summed in LDS in
+// wave order.
 template <int RP>
-__global__ __launch_bounds__(T_WAVES * 64) void lora_t_part_kernel(TpreArgs a, int kch) {
+__device__ __forceinline__ void t_part(const TpreArgs& a, int kch, int kc) {
   constexpr int TJ = RP / 16;
   __shared__ f32x4_t red[T_WAVES][TJ][64];
   const int M = a.M, K = a.K;
@@ -38,7 +41,6 @@ __global__ __launch_bounds__(T_WAVES * 64) void lora_t_part_kernel(TpreArgs a, i
   const int l16 = lane & 15;
   const int lg = lane >> 4;
   const int m0 = blockIdx.x * 16;
-  const int kc = blockIdx.y;
   const __amdgpu_buffer_rsrc_t hrs = make_rsrc(a.x + (size_t)m0 * K, (uint32_t)min(16, M - m0) * K * 2u);
   const __amdgpu_buffer_rsrc_t ars = make_rsrc(a.A, (uint32_t)min(a.r, RP) * K * 2u);
   f32x4_t acc[TJ];
@@ -77,50 +79,79 @@ __global__ __launch_bounds__(T_WAVES * 64) void lora_t_part_kernel(TpreArgs a, i
   }
 }
 
-// s * T from the chunk partials (added in chunk order), split into bf16 hi and
-// lo parts (and / or kept in fp32); the workgroups past the rows write B zero
-// padded to RP when the GEMM cannot read B itself.
+// Up to two pre-passes over the same rows in one launch (the backward runs
+// s dy B and s x A^T together): K chunks [0, nkc0) of blockIdx.y belong to
+// a0, the rest to a1.
 template <int RP>
-__global__ __launch_bounds__(256) void lora_t_finish_kernel(TpreArgs a, int nkc, int tblocks) {
-  if ((int)blockIdx.x < tblocks) {
-    const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x;
-    if (e >= (size_t)a.M * RP) return;
-    const size_t row = e / RP, j = e % RP;
-    float v = 0.f;
-    for (int c = 0; c < nkc; ++c) v += a.part[((size_t)c * a.M + row) * RP + j];
-    v *= a.s;
-    if (a.t32) a.t32[e] = v;
-    if (a.ts) {
-      const uint32_t hi = f32_to_bf16_rne(v);
-      const uint32_t lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
-      a.ts[row * 2 * RP + j] = (uint16_t)hi;
-      a.ts[row * 2 * RP + RP + j] = (uint16_t)lo;
-    }
+__global__ __launch_bounds__(T_WAVES * 64) void lora_t_part_kernel(TpreArgs a0, int kch0, int nkc0, TpreArgs a1,
+                                                                   int kch1) {
+  const int y = blockIdx.y;
+  if (y < nkc0)
+    t_part<RP>(a0, kch0, y);
+  else
+    t_part<RP>(a1, kch1, y - nkc0);
+}
+
+// s * T of element e = row * RP + j from the chunk partials (added in chunk
+// order), split into bf16 hi and lo parts (and / or kept in fp32).
+template <int RP>
+__device__ __forceinline__ void t_finish(const TpreArgs& a, int nkc, size_t e) {
+  if (e >= (size_t)a.M * RP) return;
+  const size_t row = e / RP, j = e % RP;
+  float v = 0.f;
+  for (int c = 0; c < nkc; ++c) v += a.part[((size_t)c * a.M + row) * RP + j];
+  v *= a.s;
+  if (a.t32) a.t32[e] = v;
+  if (a.ts) {
+    const uint32_t hi = f32_to_bf16_rne(v);
+    const uint32_t lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
+    a.ts[row * 2 * RP + j] = (uint16_t)hi;
+    a.ts[row * 2 * RP + RP + j] = (uint16_t)lo;
+  }
+}
+
+// Workgroups [0, tb0) finish a0, [tb0, tb0 + tb1) finish a1; those past them
+// write a0's B zero padded to RP when the GEMM cannot read B itself.
+template <int RP>
+__global__ __launch_bounds__(256) void lora_t_finish_kernel(TpreArgs a0, int nkc0, int tb0, TpreArgs a1, int nkc1,
+                                                            int tb1) {
+  const int b = blockIdx.x;
+  if (b < tb0) {
+    t_finish<RP>(a0, nkc0, (size_t)b * 256 + threadIdx.x);
     return;
   }
-  const size_t total = (size_t)a.N * RP;
-  const size_t nb = gridDim.x - tblocks;
-  for (size_t e = (blockIdx.x - tblocks) * 256 + threadIdx.x; e < total; e += nb * 256) {
+  if (b < tb0 + tb1) {
+    t_finish<RP>(a1, nkc1, (size_t)(b - tb0) * 256 + threadIdx.x);
+    return;
+  }
+  const size_t total = (size_t)a0.N * RP;
+  const size_t nb = gridDim.x - tb0 - tb1;
+  for (size_t e = (size_t)(b - tb0 - tb1) * 256 + threadIdx.x; e < total; e += nb * 256) {
     const int n = (int)(e / RP), j = (int)(e % RP);
-    a.bp[e] = j < a.r ? a.B[(size_t)n * a.r + j] : (uint16_t)0;
+    a0.bp[e] = j < a0.r ? a0.B[(size_t)n * a0.r + j] : (uint16_t)0;
   }
 }
 
 template <int RP>
-hipError_t launch_rp(const TpreArgs& a, const uint16_t** bp_used, hipStream_t stream) {
-  int nkc, kch;
-  tpre_chunks(a.K, nkc, kch);
-  hipLaunchKernelGGL((lora_t_part_kernel<RP>), dim3((a.M + 15) / 16, nkc), dim3(T_WAVES * 64), 0, stream, a, kch);
+hipError_t launch_rp(const TpreArgs& a0, const TpreArgs* a1, const uint16_t** bp_used, hipStream_t stream) {
+  int nkc0, kch0, nkc1 = 0, kch1 = 0;
+  tpre_chunks(a0.K, nkc0, kch0);
+  if (a1) tpre_chunks(a1->K, nkc1, kch1);
+  const TpreArgs b1 = a1 ? *a1 : TpreArgs{};
+  hipLaunchKernelGGL((lora_t_part_kernel<RP>), dim3((a0.M + 15) / 16, nkc0 + nkc1), dim3(T_WAVES * 64), 0, stream,
+                     a0, kch0, nkc0, b1, kch1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // B serves as its own padded copy when its rows already are RP bf16, 16-byte
   // aligned; no B at all (a.B null): nothing to pad
-  const bool direct = a.B == nullptr || (a.r == RP && (reinterpret_cast<uintptr_t>(a.B) & 15) == 0);
-  if (bp_used) *bp_used = a.B == nullptr ? nullptr : direct ? a.B : a.bp;
-  const int tblocks = (int)(((size_t)a.M * RP + 255) / 256);
-  const size_t total = (size_t)a.N * RP;
+  const bool direct = a0.B == nullptr || (a0.r == RP && (reinterpret_cast<uintptr_t>(a0.B) & 15) == 0);
+  if (bp_used) *bp_used = a0.B == nullptr ? nullptr : direct ? a0.B : a0.bp;
+  const int tb0 = (int)(((size_t)a0.M * RP + 255) / 256);
+  const int tb1 = a1 ? (int)(((size_t)a1->M * RP + 255) / 256) : 0;
+  const size_t total = (size_t)a0.N * RP;
   const int bblocks = direct ? 0 : (int)((total + 255) / 256 < 2048 ? (total + 255) / 256 : 2048);
-  hipLaunchKernelGGL((lora_t_finish_kernel<RP>), dim3(tblocks + bblocks), dim3(256), 0, stream, a, nkc, tblocks);
+  hipLaunchKernelGGL((lora_t_finish_kernel<RP>), dim3(tb0 + tb1 + bblocks), dim3(256), 0, stream, a0, nkc0, tb0, b1,
+                     nkc1, tb1);
   return hipGetLastError();
 }
 
@@ -128,10 +159,21 @@ hipError_t launch_rp(const TpreArgs& a, const uint16_t** bp_used, hipStream_t st
 
 hipError_t launch_lora_tpre(const TpreArgs& a, int rp, const uint16_t** bp_used, hipStream_t stream) {
   switch (rp) {
-    case 16: return launch_rp<16>(a, bp_used, stream);
-    case 32: return launch_rp<32>(a, bp_used, stream);
-    case 64: return launch_rp<64>(a, bp_used, stream);
-    case 128: return launch_rp<128>(a, bp_used, stream);
+    case 16: return launch_rp<16>(a, nullptr, bp_used, stream);
+    case 32: return launch_rp<32>(a, nullptr, bp_used, stream);
+    case 64: return launch_rp<64>(a, nullptr, bp_used, stream);
+    case 128: return launch_rp<128>(a, nullptr, bp_used, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_lora_tpre2(const TpreArgs& a0, const TpreArgs& a1, int rp, hipStream_t stream) {
+  if (a0.M != a1.M || a0.B || a1.B) return hipErrorInvalidValue;
+  switch (rp) {
+    case 16: return launch_rp<16>(a0, &a1, nullptr, stream);
+    case 32: return launch_rp<32>(a0, &a1, nullptr, stream);
+    case 64: return launch_rp<64>(a0, &a1, nullptr, stream);
+    case 128: return launch_rp<128>(a0, &a1, nullptr, stream);
     default: return hipErrorInvalidValue;
   }
 }

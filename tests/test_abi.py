@@ -382,9 +382,9 @@ def test_lora_linear_backward_optional_inputs():
 
 def _outer_chunks(M, C, rp):
     tiles = -(-C // 256) * (rp // 16)
-    want = max(1, -(-1024 // tiles))
+    want = max(1, -(-512 // tiles))
     rows = -(-M // want)
-    rows = max(16, -(-rows // 16) * 16)
+    rows = max(64, -(-rows // 16) * 16)
     return -(-M // rows)
 
 
@@ -394,8 +394,8 @@ def _bwd_ws(M, N, K, rp):
     up = lambda v: -(-v // 256) * 256  # noqa: E731
     oa = _outer_chunks(M, K, rp) * rp * K
     ob = _outer_chunks(M, N, rp) * rp * N
-    return (up(rp * N * 2) + up(K * rp * 2) + up(M * 2 * rp * 2) + 2 * up(M * rp * 4) + up(8 * M * rp * 4)
-            + up(max(oa, ob) * 4))
+    return (up(rp * N * 2) + up(K * rp * 2) + up(M * 2 * rp * 2) + 2 * up(M * rp * 4) + 2 * up(8 * M * rp * 4)
+            + up(oa * 4) + up(ob * 4))
 
 
 def test_backward_workspace_bytes():
@@ -403,8 +403,9 @@ def test_backward_workspace_bytes():
                            (3, 8, 16, 33, 64), (1, 8, 8, 1, 16)]:
         assert H.hydra_lora_linear_backward_workspace_bytes(M, N, K, r) == _bwd_ws(M, N, K, rp)
     assert H.hydra_lora_linear_backward_workspace_bytes(7, 8, 8, 0) == 0
-    # the outer-product partials stay near 16 MiB however the shape grows (about 1024 workgroups' worth)
-    assert H.hydra_lora_linear_backward_workspace_bytes(65536, 4096, 4096, 16) < 64 << 20
+    # the outer-product partials stay near 2 x 8 MiB however the shape grows (about 512 workgroups' worth each)
+    assert H.hydra_lora_linear_backward_workspace_bytes(65536, 4096, 4096, 16) == _bwd_ws(65536, 4096, 4096, 16)
+    assert _outer_chunks(65536, 4096, 16) * 16 * 4096 * 4 <= 9 << 20
     L = H.lib()
     out = ctypes.c_size_t(0)
     assert L.hydra_lora_linear_backward_workspace_bytes(0, 8, 8, 16, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE

@@ -12,10 +12,12 @@ pytestmark = pytest.mark.gpu
 
 BWD_SHAPES = [
     # (M, K, N, r): rows past one 256-row tile and ragged, K and N multiples of 8 with ragged column tiles,
-    # every padded rank (1, 16, 33 -> 64, 100 -> 128, 128), rank 0, one row, and a row count that leaves a
+    # every padded rank (1, 16, 33 -> 64, 100 -> 128, 128), rank 0, one row, and row counts that leave a
     # partial outer-product chunk.
     (17, 64, 256, 8), (130, 520, 304, 16), (257, 1024, 704, 33), (64, 128, 96, 64), (300, 2048, 1200, 100),
     (130, 520, 304, 128), (1, 64, 40, 1), (5, 8, 8, 128), (200, 64, 256, 0), (1000, 72, 24, 16),
+    # outer-product chunks longer than the 256 rows staged at a time (dA: 560 rows, dB: 288 rows)
+    (1100, 8192, 4096, 128),
 ]
 
 
