@@ -552,10 +552,16 @@ def cpu_baseline(target_s: float, host_inputs=None):
     b = max((t2 - t1) / 48.0, 1e-6)
     a = max(t1 - 16 * b, 0.0)
     rows = int(min(2048, max(64, (target_s - a) / b)))
-    fl, t = run(rows)
+    # whole steps (all rows) are repeated until the sample holds about target_s of CPU work
+    reps = 1 if rows < 2048 else max(1, int(target_s / max(a + b * rows, 1e-3)))
+    fl = t = 0.0
+    for _ in range(reps):
+        f_, t_ = run(rows)
+        fl += f_
+        t += t_
     return dict(value=round(fl / t / 1e12, 5), unit="TFLOP/s", cores=int(threads), kind="oracle",
                 seconds=round(t, 2),
-                sample=f"float64 oracle on one step with the 2048-token parts cut to their first {rows} rows "
+                sample=f"float64 oracle on {reps} step(s) with the 2048-token parts cut to their first {rows} rows "
                        f"(decode 4 x M=4 in full; prefill 7 linears and two-head scoring on {rows} rows)",
                 host_cpus=len(os.sched_getaffinity(0)))
 
