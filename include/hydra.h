@@ -76,8 +76,10 @@ typedef enum {
  *   s     fp32           LoRA scale
  *   y_off [M x N] fp32   out: x W^T                  (NULL: not written)
  *   y_on  [M x N] fp32   out: x W^T + s (x A^T) B^T  (NULL: not written)
- * At least one output must be non-NULL.  Requires M, N, K >= 1, K % 8 == 0,
- * K <= 2^21, 0 <= r <= HYDRA_MAX_RANK, and M, N below 2^31.  With r == 0, y_on equals
+ * At least one output must be non-NULL.  Requires 1 <= M <= 2^20, 1 <= N <= 2^21,
+ * K >= 1, K % 8 == 0, K <= 2^21, 0 <= r <= HYDRA_MAX_RANK, and
+ * ceil(M / 128) * ceil(N / 256) < 2^23 (the GEMM's tile grid fits one
+ * dispatch; roughly M * N < 2^38).  With r == 0, y_on equals
  * y_off.  M <= 16 selects the bandwidth-bound (decode) kernels, larger M the
  * MFMA GEMM; both compute the same function.  At M > 16 with y_on and r > 64
  * the update needs the pre-pass workspace of hydra_lora_linear_ws: this call
@@ -90,8 +92,8 @@ hydra_status hydra_lora_linear(const uint16_t* x, const uint16_t* W, const uint1
 /*
  * hydra_lora_linear_workspace_bytes -- device workspace that hydra_lora_linear_ws
  * needs for M rows, N outputs and rank r (0 when none is needed: r == 0).
- * Writes *bytes.  HYDRA_ERR_NULL for a NULL `bytes`, HYDRA_ERR_SHAPE for M or
- * N < 1 or r outside [0, HYDRA_MAX_RANK].
+ * Writes *bytes.  HYDRA_ERR_NULL for a NULL `bytes`, HYDRA_ERR_SHAPE for M
+ * outside [1, 2^20], N outside [1, 2^21] or r outside [0, HYDRA_MAX_RANK].
  */
 hydra_status hydra_lora_linear_workspace_bytes(int64_t M, int64_t N, int64_t r, size_t* bytes);
 
@@ -180,7 +182,8 @@ hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, i
 /*
  * hydra_score_workspace_bytes -- device workspace that hydra_score needs for
  * M = n_seq * seq_len token rows and a vocabulary of V.  Writes *bytes.
- * Returns HYDRA_ERR_NULL for a NULL `bytes`, HYDRA_ERR_SHAPE for M or V < 1.
+ * Returns HYDRA_ERR_NULL for a NULL `bytes`, HYDRA_ERR_SHAPE for M outside
+ * [1, 2^20] or V outside [1, 2^21].
  */
 hydra_status hydra_score_workspace_bytes(int64_t M, int64_t V, size_t* bytes);
 
@@ -207,7 +210,8 @@ hydra_status hydra_score_workspace_bytes(int64_t M, int64_t V, size_t* bytes);
  *                           hydra_score_workspace_bytes(M, V) bytes, 16-byte aligned
  *   err_flag [1] int32      optional device flag; 1 is OR-ed in for an out-of-range token
  * The [M x V] logits are never written to memory.  Requires K % 8 == 0,
- * K <= 2^21, 0 <= r <= HYDRA_MAX_RANK, V >= 1, M and V below 2^31.
+ * K <= 2^21, 0 <= r <= HYDRA_MAX_RANK, 1 <= M <= 2^20, 1 <= V <= 2^21 and
+ * ceil(M / 256) * ceil(V / 256) < 2^24 (the GEMM's tile grid fits one dispatch).
  */
 hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t* A, const uint16_t* B, float s,
                          const int32_t* tokens, const uint16_t* w_rm,
@@ -225,7 +229,7 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
  *   lp_on, lp_off, kl [M] fp32           out (as in hydra_score)
  *   lse_on, lse_off [M] fp32             out, optional (NULL: not written)
  *   err_flag [1] int32                   optional, as in hydra_score
- * Requires M, V >= 1.
+ * Requires 1 <= M <= 2^20 and 1 <= V <= 2^21.
  */
 hydra_status hydra_score_logits(const float* logits_on, const float* logits_off, const int32_t* tokens,
                                 int64_t M, int64_t V, float* lp_on, float* lp_off, float* kl,
@@ -241,7 +245,7 @@ hydra_status hydra_score_logits(const float* logits_on, const float* logits_off,
  *   h       [M x K] bf16   hidden states, row-major, 16-byte aligned
  *   w_v     [K] bf16       value head weight, 16-byte aligned
  *   values  [M] fp32       out: values[m] = sum_k h[m][k] * w_v[k] (fp32 accumulation)
- * Requires M >= 1, 1 <= K <= 2^21, K % 8 == 0.  Buffers are the caller's.
+ * Requires 1 <= M <= 2^20, 1 <= K <= 2^21, K % 8 == 0.  Buffers are the caller's.
  */
 hydra_status hydra_value_head(const uint16_t* h, const uint16_t* w_v, int64_t M, int64_t K, float* values,
                               void* stream);
@@ -267,7 +271,8 @@ hydra_status hydra_value_head(const uint16_t* h, const uint16_t* w_v, int64_t M,
  * Positions before `start` get advantage and return 0 (and reward 0).  No
  * output may be one of the inputs or another output (HYDRA_ERR_SHAPE);
  * partial overlaps are not detected and are not allowed.  Requires
- * n_seq, seq_len >= 1 and M below 2^31; buffers 4-byte aligned.
+ * n_seq, seq_len >= 1, n_seq below 2^26 and M below 2^31; buffers 4-byte
+ * aligned.
  */
 hydra_status hydra_ppo_advantages(const float* kl, const float* reward, const float* values, int64_t n_seq,
                                   int64_t seq_len, int64_t start, float beta, float gamma, float lam, float* rewards,
@@ -308,7 +313,7 @@ hydra_status hydra_ppo_loss(const float* lp_new, const float* lp_old, const floa
  * caller makes that copy once with this call (W does not change during
  * training) and keeps it beside W.
  *   src, dst   device, 2-byte aligned, not overlapping (HYDRA_ERR_SHAPE if equal)
- *   R, C       >= 1, R * C below 2^62
+ *   R, C       1 ... 2^21, ceil(R / 64) * ceil(C / 64) < 2^24
  * Bit-exact (a copy).
  */
 hydra_status hydra_transpose_bf16(const uint16_t* src, int64_t R, int64_t C, uint16_t* dst, void* stream);
@@ -333,7 +338,8 @@ hydra_status hydra_lora_linear_backward_workspace_bytes(int64_t M, int64_t N, in
  *   A [r x K], B [N x r] bf16   the adapter (A 16-byte aligned, B 2-byte)
  *   s                        LoRA scale
  *   dy [M x N] bf16          gradient of the loss with respect to y (16-byte aligned)
- *   M >= 1; N, K >= 1, multiples of 8, at most 2^21; 0 <= r <= HYDRA_MAX_RANK
+ *   1 <= M <= 2^20; N, K >= 1, multiples of 8, at most 2^21;
+ *   ceil(M / 128) * ceil(K / 256) < 2^23; 0 <= r <= HYDRA_MAX_RANK
  *   dx [M x K] fp32          out, optional
  *   dA [r x K] fp32          out, optional (ignored for r == 0)
  *   dB [N x r] fp32          out, optional (ignored for r == 0)

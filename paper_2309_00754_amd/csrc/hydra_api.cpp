@@ -13,9 +13,25 @@ constexpr int64_t kMaxDim = (int64_t(1) << 31) - 1;
 // Largest K: a 256-row slab of W must stay addressable with 32-bit byte offsets.
 constexpr int64_t kMaxK = int64_t(1) << 21;
 constexpr int kDecodeMaxRows = 16;
+// Largest row count (tokens) of the linear, scoring and backward calls and
+// largest output width (N, V).  A dispatch counts its work-items in 32 bits;
+// with these limits every launch fits, the MFMA tile grids being checked on
+// top (grid_ok).
+constexpr int64_t kMaxRows = int64_t(1) << 20;
+constexpr int64_t kMaxCols = int64_t(1) << 21;
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 bool dim_ok(int64_t v) { return v >= 1 && v <= kMaxDim; }
+bool grid_ok(int64_t blocks, int64_t threads) { return blocks >= 1 && blocks * threads < (int64_t(1) << 32); }
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// M rows, N outputs, K inputs of one LoRA-switchable linear (and of the GEMM
+// of the backward): K a multiple of 8 up to 2^21, the limits above, and the
+// dual GEMM's tile grid within one dispatch.
+bool linear_shape_ok(int64_t M, int64_t N, int64_t K) {
+  return M >= 1 && M <= kMaxRows && N >= 1 && N <= kMaxCols && K >= 1 && K <= kMaxK && K % 8 == 0 &&
+         grid_ok(cdiv(M, hydra::kGemmTileM) * cdiv(N, hydra::kGemmTileN), hydra::kGemmThreads);
+}
 
 hydra_status from_hip(hipError_t e) { return e == hipSuccess ? HYDRA_OK : HYDRA_ERR_HIP; }
 
@@ -68,7 +84,7 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
   if (G < 1 || G > HYDRA_MAX_GROUP) return HYDRA_ERR_SHAPE;
   if (!x || !W || !s) return HYDRA_ERR_NULL;
   if (!y_off && !y_on) return HYDRA_ERR_NULL;
-  if (!dim_ok(M) || !dim_ok(N) || !dim_ok(K) || (K % 8) != 0 || K > kMaxK) return HYDRA_ERR_SHAPE;
+  if (!linear_shape_ok(M, N, K)) return HYDRA_ERR_SHAPE;
   if (r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
   hydra::GroupArgs g{};
   g.G = int(G);
@@ -128,7 +144,7 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
 
 hydra_status hydra_lora_linear_workspace_bytes(int64_t M, int64_t N, int64_t r, size_t* bytes) {
   if (!bytes) return HYDRA_ERR_NULL;
-  if (!dim_ok(M) || !dim_ok(N) || r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
+  if (M < 1 || M > kMaxRows || N < 1 || N > kMaxCols || r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
   *bytes = linear_ws_bytes(M, N, hydra::padded_rank(int(r)));
   return HYDRA_OK;
 }
@@ -138,7 +154,7 @@ hydra_status hydra_lora_linear_ws(const uint16_t* x, const uint16_t* W, const ui
                                   void* workspace, size_t workspace_bytes, void* stream) {
   if (!x || !W) return HYDRA_ERR_NULL;
   if (!y_off && !y_on) return HYDRA_ERR_NULL;
-  if (!dim_ok(M) || !dim_ok(N) || !dim_ok(K) || (K % 8) != 0 || K > kMaxK) return HYDRA_ERR_SHAPE;
+  if (!linear_shape_ok(M, N, K)) return HYDRA_ERR_SHAPE;
   if (r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
   const bool lora = y_on && r > 0;
   if (lora && (!A || !B)) return HYDRA_ERR_NULL;
@@ -181,7 +197,7 @@ hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, i
   if ((x_off == nullptr) != (y_off == nullptr)) return HYDRA_ERR_NULL;
   if (!x_off && n_on == 0) return HYDRA_ERR_NULL;
   if (n_on > 0 && (!x_on || !y_on || !s || (r > 0 && (!A || !B)))) return HYDRA_ERR_NULL;
-  if (!dim_ok(M) || !dim_ok(N) || !dim_ok(K) || (K % 8) != 0 || K > kMaxK) return HYDRA_ERR_SHAPE;
+  if (!linear_shape_ok(M, N, K)) return HYDRA_ERR_SHAPE;
   if (r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
   if (!aligned(W, 16) || (x_off && !aligned(x_off, 16)) || (y_off && !aligned(y_off, 4))) return HYDRA_ERR_ALIGN;
   for (int64_t a = 0; a < n_on; ++a) {
@@ -250,7 +266,7 @@ hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, i
 
 hydra_status hydra_score_workspace_bytes(int64_t M, int64_t V, size_t* bytes) {
   if (!bytes) return HYDRA_ERR_NULL;
-  if (!dim_ok(M) || !dim_ok(V)) return HYDRA_ERR_SHAPE;
+  if (M < 1 || M > kMaxRows || V < 1 || V > kMaxCols) return HYDRA_ERR_SHAPE;
   *bytes = score_ws_bytes(M, V);
   return HYDRA_OK;
 }
@@ -265,6 +281,9 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
     return HYDRA_ERR_SHAPE;
   if (n_seq > kMaxDim / seq_len) return HYDRA_ERR_SHAPE;
   const int64_t M = n_seq * seq_len;
+  if (M > kMaxRows || V > kMaxCols) return HYDRA_ERR_SHAPE;
+  if (!grid_ok(cdiv(M, hydra::kScoreTileM) * cdiv(V, hydra::kScoreTileN), hydra::kScoreThreads))
+    return HYDRA_ERR_SHAPE;
   if (r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
   if (r > 0 && (!A || !B)) return HYDRA_ERR_NULL;
   if (!workspace) return HYDRA_ERR_WORKSPACE;
@@ -328,7 +347,7 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
 hydra_status hydra_value_head(const uint16_t* h, const uint16_t* w_v, int64_t M, int64_t K, float* values,
                               void* stream) {
   if (!h || !w_v || !values) return HYDRA_ERR_NULL;
-  if (!dim_ok(M) || !dim_ok(K) || (K % 8) != 0 || K > kMaxK) return HYDRA_ERR_SHAPE;
+  if (M < 1 || M > kMaxRows || !dim_ok(K) || (K % 8) != 0 || K > kMaxK) return HYDRA_ERR_SHAPE;
   if (!aligned(h, 16) || !aligned(w_v, 16) || !aligned(values, 4)) return HYDRA_ERR_ALIGN;
   hydra::ValueHeadArgs a{};
   a.h = h;
@@ -376,7 +395,7 @@ hydra_status hydra_ppo_loss(const float* lp_new, const float* lp_old, const floa
 
 hydra_status hydra_transpose_bf16(const uint16_t* src, int64_t R, int64_t C, uint16_t* dst, void* stream) {
   if (!src || !dst) return HYDRA_ERR_NULL;
-  if (R < 1 || C < 1 || R > kMaxK || C > kMaxK) return HYDRA_ERR_SHAPE;
+  if (R < 1 || C < 1 || R > kMaxK || C > kMaxK || !grid_ok(cdiv(R, 64) * cdiv(C, 64), 256)) return HYDRA_ERR_SHAPE;
   if (static_cast<const void*>(src) == static_cast<const void*>(dst)) return HYDRA_ERR_SHAPE;
   if (!aligned(src, 2) || !aligned(dst, 2)) return HYDRA_ERR_ALIGN;
   return from_hip(hydra::launch_transpose_pad(src, int(R), int(C), dst, int(R), int(C),
@@ -384,11 +403,11 @@ hydra_status hydra_transpose_bf16(const uint16_t* src, int64_t R, int64_t C, uin
 }
 
 namespace {
-// Sizes the backward accepts: N and K as the forward's K (multiples of 8,
-// at most 2^21), M up to 2^24 rows (the pre-pass indexes M x 128 with 32 bits).
+// Sizes the backward accepts: N and K both serve as a GEMM's inner dimension
+// (multiples of 8, at most 2^21), M as for the forward, and the dx GEMM's
+// tile grid ([M x K] output) within one dispatch.
 bool backward_shape_ok(int64_t M, int64_t N, int64_t K, int64_t r) {
-  return M >= 1 && M <= (int64_t(1) << 24) && dim_ok(N) && dim_ok(K) && N % 8 == 0 && K % 8 == 0 && N <= kMaxK &&
-         K <= kMaxK && r >= 0 && r <= HYDRA_MAX_RANK;
+  return linear_shape_ok(M, K, N) && K % 8 == 0 && r >= 0 && r <= HYDRA_MAX_RANK;
 }
 }  // namespace
 
@@ -439,6 +458,7 @@ hydra_status hydra_ppo_advantages(const float* kl, const float* reward, const fl
                                   float* advantages, float* returns, void* stream) {
   if (!kl || !reward || !values || !advantages || !returns) return HYDRA_ERR_NULL;
   if (!dim_ok(n_seq) || !dim_ok(seq_len) || n_seq > kMaxDim / seq_len) return HYDRA_ERR_SHAPE;
+  if (!grid_ok(n_seq, 64)) return HYDRA_ERR_SHAPE;  // one wave per sequence
   if (start < 0 || start >= seq_len) return HYDRA_ERR_SHAPE;
   // outputs are written while inputs are still read: no output may be an input
   const void* ins[3] = {kl, reward, values};
@@ -472,7 +492,7 @@ hydra_status hydra_score_logits(const float* logits_on, const float* logits_off,
                                 int64_t V, float* lp_on, float* lp_off, float* kl, float* lse_on, float* lse_off,
                                 int32_t* err_flag, void* stream) {
   if (!logits_on || !logits_off || !tokens || !lp_on || !lp_off || !kl) return HYDRA_ERR_NULL;
-  if (!dim_ok(M) || !dim_ok(V)) return HYDRA_ERR_SHAPE;
+  if (M < 1 || M > kMaxRows || V < 1 || V > kMaxCols) return HYDRA_ERR_SHAPE;
   if (!aligned(logits_on, 16) || !aligned(logits_off, 16)) return HYDRA_ERR_ALIGN;
   if (!aligned(tokens, 4) || !aligned(lp_on, 4) || !aligned(lp_off, 4) || !aligned(kl, 4)) return HYDRA_ERR_ALIGN;
   if ((lse_on && !aligned(lse_on, 4)) || (lse_off && !aligned(lse_off, 4)) || (err_flag && !aligned(err_flag, 4)))

@@ -203,6 +203,13 @@ hipError_t launch_lora_gemm_slabs(const LinearArgs& a, const uint16_t* ts, const
 // Column-tile width of the fused scoring GEMM (number of vocabulary entries
 // one workgroup reduces).
 constexpr int kScoreTileN = 256;
+// Launch shapes the host validation needs: a dispatch counts work-items in
+// 32 bits, so (tiles x threads per workgroup) must stay below 2^32.
+constexpr int kScoreTileM = 256;
+constexpr int kScoreThreads = 256;
+constexpr int kGemmTileM = 128;
+constexpr int kGemmTileN = 256;
+constexpr int kGemmThreads = 512;
 
 hipError_t launch_lora_gemm(const LinearArgs& a, hipStream_t stream);
 // The same with the LoRA update from the pre-pass: ts [M x 2 RP] and bp [N x RP]

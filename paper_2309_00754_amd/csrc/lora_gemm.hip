@@ -44,6 +44,7 @@ constexpr int BN = 256;        // tile columns (outputs)
 constexpr int BK = 64;         // K slab
 constexpr int NTM = 256;       // MFMA threads (waves 0..3)
 constexpr int NT = 512;        // threads per workgroup (4 MFMA + 4 copy waves)
+static_assert(BM == kGemmTileM && BN == kGemmTileN && NT == kGemmThreads, "launch shape known to the host checks");
 constexpr int WM = 64;         // wave tile rows
 constexpr int WN = 128;        // wave tile columns
 constexpr int MT = WM / 32;    // 32-row x tiles per wave

@@ -54,6 +54,7 @@ constexpr int GROUP_M = 8;     // row tiles walked together (L2 reuse of W)
 constexpr int DPW = (BM + BN) / 16 / 4;  // copies per wave per slab (16 rows of 64 bytes each)
 
 static_assert(kScoreTileN == BN, "one partial per GEMM column tile");
+static_assert(kScoreTileM == BM && kScoreThreads == NT, "launch shape known to the host checks");
 static_assert(DPW == 8, "the k-step schedule issues four copies per k-step");
 static_assert(BM * 2 * 4 * 4 <= STAGE * 16, "the epilogue's row statistics fit in one stage");
 

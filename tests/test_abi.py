@@ -424,3 +424,43 @@ def test_backward_workspace_bytes():
 ])
 def test_transpose_rejects(src, R, C, dst, code):
     assert H.lib().hydra_transpose_bf16(src, R, C, dst, None) == code
+
+
+# ------------------------------------------------------------------ launch-size limits
+# A dispatch counts work-items in 32 bits; the calls bound M (2^20 rows), N / V (2^21) and the MFMA tile grids so
+# that every launch fits, and reject larger sizes on the host.
+
+def test_row_and_width_limits():
+    big = 1 << 20
+    assert _lin(M=big + 1, y_on=None) == H.HYDRA_ERR_SHAPE
+    assert _lin(N=(1 << 21) + 1, y_on=None) == H.HYDRA_ERR_SHAPE
+    # within the row and width limits but a GEMM tile grid of 8192 x 8192 x 512 threads: too large for a dispatch
+    assert _lin(M=big, N=1 << 21, y_on=None) == H.HYDRA_ERR_SHAPE
+    assert _lin(M=big, N=1 << 21, y_on=None, x=P8) == H.HYDRA_ERR_SHAPE     # shape is checked before alignment
+    assert _lws(M=big + 1) == H.HYDRA_ERR_SHAPE
+    assert _grp(M=big + 1) == H.HYDRA_ERR_SHAPE
+    assert _multi(M=big + 1) == H.HYDRA_ERR_SHAPE
+    out = ctypes.c_size_t(0)
+    L = H.lib()
+    assert L.hydra_lora_linear_workspace_bytes(big + 1, 8, 16, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
+    assert L.hydra_score_workspace_bytes(8, (1 << 21) + 1, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
+    assert _score(V=(1 << 21) + 1, ws_bytes=1 << 40) == H.HYDRA_ERR_SHAPE
+    assert _score(n_seq=1 << 10, seq_len=(1 << 10) + 1, ws_bytes=1 << 40) == H.HYDRA_ERR_SHAPE
+    assert L.hydra_score_logits(P, P, P, big + 1, 1000, P, P, P, None, None, None, None) == H.HYDRA_ERR_SHAPE
+    assert L.hydra_score_logits(P, P, P, 8, (1 << 21) + 1, P, P, P, None, None, None, None) == H.HYDRA_ERR_SHAPE
+    assert L.hydra_value_head(P, P, big + 1, 64, P + 0x1000, None) == H.HYDRA_ERR_SHAPE
+    assert L.hydra_ppo_advantages(P, P + 0x100, P + 0x200, 1 << 26, 1, 0, 0.02, 1.0, 0.95, None, P + 0x300,
+                                  P + 0x400, None) == H.HYDRA_ERR_SHAPE
+    assert L.hydra_transpose_bf16(P, 1 << 21, 1 << 21, P + 0x100, None) == H.HYDRA_ERR_SHAPE
+    assert _bwd(M=big + 1) == H.HYDRA_ERR_SHAPE
+    assert _bwd(M=big, K=1 << 21, N=64) == H.HYDRA_ERR_SHAPE                   # dx's tile grid
+
+
+def test_limits_admit_the_largest_realistic_shapes():
+    """At the limits that matter in practice the checks pass (the call then fails only on a planted misalignment):
+    a million rows through a Llama-7B MLP linear, the 32000-entry head on a million tokens."""
+    big = 1 << 20
+    assert _lin(M=big, N=11008, K=4096, y_on=None, x=P8) == H.HYDRA_ERR_ALIGN
+    assert _score(n_seq=1 << 11, seq_len=1 << 9, V=32000, K=4096, ws_bytes=1 << 40, h=P8) == H.HYDRA_ERR_ALIGN
+    assert _bwd(M=big, N=11008, K=4096, dy=P8, nbytes=1 << 40) == H.HYDRA_ERR_ALIGN
+    assert H.lib().hydra_transpose_bf16(P + 1, 32000, 4096, P + 0x100, None) == H.HYDRA_ERR_ALIGN
