@@ -74,7 +74,8 @@ struct TpreArgs {
   uint16_t* ts;       // [M x 2 RP] hi | lo of s T, or nullptr
   uint16_t* bp;       // used only when B itself cannot serve (r != RP or B not 16-byte aligned)
   float* part;        // [kTpreMaxChunks x M x RP] fp32 partial sums over K chunks
-  float* t32;         // [M x RP] fp32 s T, or nullptr
+  uint16_t* tT;       // [2][RP][Mp] bf16 hi and lo planes of (s T)^T, rows M..Mp zero, or nullptr
+  int Mp;             // leading dimension of tT (M rounded up to 32)
 };
 // K is split into at most kTpreMaxChunks chunks of at least 1024, so that
 // the pre-pass spreads over many workgroups; the partial products are then

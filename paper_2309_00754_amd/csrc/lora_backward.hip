@@ -6,14 +6,15 @@
 //  1. B^T and A^T, zero padded to the padded rank RP (transpose_pad_kernel,
 //     both in one launch);
 //  2. the LoRA pre-pass of the forward GEMM (lora_tpre.hip) twice, in one
-//     pair of launches: s U from dy against the rows of B^T (hi | lo bf16
-//     parts for step 3, fp32 for step 4), s T from x against A (fp32);
+//     pair of launches: s U from dy against the rows of B^T, s T from x
+//     against A, each as bf16 hi and lo parts (row-major for step 3,
+//     transposed for step 4);
 //  3. dx by the forward's MFMA GEMM run on (dy, W^T), its LoRA slabs being
 //     [hi | lo](s U) against rows of A^T: one pass over W^T, as in the forward;
 //  4. dA and dB as sums of outer products over the rows m:
 //     out[j][c] = sum_m P[m][j] Q[m][c] with (P, Q) = (s U, x) and (s T, dy),
-//     vector fp32 FMAs (lora_outer_part_kernel: per row chunk partials, laid
-//     out like the output), then the chunks added in chunk order
+//     on MFMAs (lora_outer_part_kernel: per row chunk partials, laid out like
+//     the output), then the chunks added in chunk order
 //     (lora_outer_finish_kernel, one thread per output element); dA and dB
 //     share each of the two launches.  Every sum has a fixed order: the results
 //     are the same from run to run.
@@ -75,139 +76,137 @@ TransposeJob transpose_job(const uint16_t* src, int R, int C, uint16_t* dst, int
 
 // ---------------------------------------------------------- outer products
 constexpr int O_WAVES = 4;
-constexpr int O_JT = 16;          // j values per workgroup
-constexpr int O_COLS = 256;       // columns per workgroup, 4 per lane
-constexpr int O_UNROLL = 16;      // rows per wave with loads in flight together
-constexpr int O_WIN = 256;        // rows of P staged in LDS at a time
-constexpr int O_TARGET_WG = 512;  // workgroups the chunking aims for
-constexpr int O_MIN_ROWS = 64;    // fewest rows per chunk
+constexpr int O_COLS = 256;        // columns per workgroup: 64 per wave, four 16-column MFMA tiles
+constexpr int O_KS = 32;           // rows per k-step (the k of one 16x16x32 MFMA)
+constexpr int O_LD = O_COLS + 4;   // LDS row stride in bf16 (130 dwords; see outer_part)
+constexpr int O_TARGET_WG = 256;   // workgroups the chunking aims for (both products together: twice that)
+constexpr int O_MIN_ROWS = 128;    // fewest rows per chunk
 
 struct OuterArgs {
-  const float* P;      // [M x RP] fp32
+  const uint16_t* PT;  // [2][RP][Mp] bf16: hi and lo planes of P^T (P = s U or s T)
   const uint16_t* Q;   // [M x C] bf16
   float* part;         // [nch x RP x C] (jc) or [nch x C x RP] fp32
   float* out;          // [r x C] (jc) or [C x r] fp32
-  int M, C, RP, r;
-  int mch, nch;        // rows per chunk (multiple of 16), chunks
+  int M, Mp, C, RP, r;
+  int mch, nch;        // rows per chunk (multiple of O_KS), chunks
   int jc;              // partials and output j-major
   int tiles;           // column tiles of O_COLS
 };
 
-__device__ __forceinline__ uint2 buf_load8(__amdgpu_buffer_rsrc_t r, int byte_off) {
-  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, byte_off, 0, 0));
-}
-
-// Partial out[j][c] over the rows of one chunk, for one 16-wide group of j and
-// the 256 columns of one tile (b = tile + tiles * (jg + RP / 16 * chunk)).  The
-// 4 waves take the rows in turn (row i of a window goes to wave i % 4), each
-// lane 4 columns x 16 j in registers; the wave sums are added in wave order
-// at the end.
+// Partial out[j][c] = sum_m P[m][j] Q[m][c] over the rows of one chunk, for
+// every j and the 256 columns of one tile (b = tile + tiles * chunk), on
+// v_mfma_f32_16x16x32_bf16: A operand = 16 j x 32 m of P^T (its hi plane,
+// then its lo plane: ~16 significant bits of P), B operand = 32 m x 16
+// columns of Q.  The MFMA wants eight consecutive m per lane, but m is Q's
+// row index, so each 32-row slab of Q goes through LDS (row-major, double
+// buffered, one barrier per slab) and every lane gathers its column's eight
+// values with 16-bit reads.  With a row stride of 130 dwords the four row
+// groups of one read land in disjoint bank windows.  Each wave owns 64
+// columns and all RP j, so one slab in LDS serves every 16-wide j group.
+template <int RP>
 __device__ __forceinline__ void outer_part(const OuterArgs& a, int b) {
-  __shared__ float ps[O_WIN][O_JT];
-  __shared__ f32x4_t red[O_WAVES - 1][O_JT / 2][64];
+  constexpr int JG = RP / 16;
+  __shared__ uint16_t qs[2][O_KS][O_LD];
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int l16 = lane & 15, lg = lane >> 4;
   const int tile = b % a.tiles;
-  const int rest = b / a.tiles;
-  const int jg = rest % (a.RP / O_JT);
-  const int ch = rest / (a.RP / O_JT);
-  const int c = tile * O_COLS + lane * 4;
+  const int ch = b / a.tiles;
+  const int c0 = tile * O_COLS;
   const int m_begin = ch * a.mch;
   const int m_end = min(a.M, m_begin + a.mch);
-  float acc[O_JT][4];
+  const int nks = (m_end - m_begin + O_KS - 1) / O_KS;
+  // slab copies: thread t moves 16 bytes (8 columns) of rows t / 32 + 8 u
+  const int lr = t >> 5, lc = (t & 31) * 8;
+  uint4 qv[4];
+  auto load = [&](int ks) __attribute__((always_inline)) {
+    const int m0 = m_begin + ks * O_KS;
+    const int rows = min(O_KS, m_end - m0);
+    const __amdgpu_buffer_rsrc_t qrs = make_rsrc(a.Q + (size_t)m0 * a.C, (uint32_t)rows * a.C * 2u);
 #pragma unroll
-  for (int j = 0; j < O_JT; ++j)
+    for (int u = 0; u < 4; ++u) {
+      const int row = lr + 8 * u;
+      qv[u] = buf_load16(qrs, (row < rows && c0 + lc < a.C) ? (row * a.C + c0 + lc) * 2 : kOutOfRange);
+    }
+  };
+  auto store = [&](int st) __attribute__((always_inline)) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) acc[j][e] = 0.f;
+    for (int u = 0; u < 4; ++u) {
+      uint2* d = reinterpret_cast<uint2*>(&qs[st][lr + 8 * u][lc]);
+      d[0] = uint2{qv[u].x, qv[u].y};
+      d[1] = uint2{qv[u].z, qv[u].w};
+    }
+  };
+  f32x4_t acc[JG][4];
+#pragma unroll
+  for (int g = 0; g < JG; ++g)
+#pragma unroll
+    for (int s = 0; s < 4; ++s) acc[g][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  for (int w0 = m_begin; w0 < m_end; w0 += O_WIN) {
-    const int rows = min(O_WIN, m_end - w0);
-    const __amdgpu_buffer_rsrc_t qrs = make_rsrc(a.Q + (size_t)w0 * a.C, (uint32_t)rows * a.C * 2u);
-    uint2 q[O_UNROLL];
-    auto load = [&](int r0) __attribute__((always_inline)) {
+  load(0);
+  store(0);
+  if (nks > 1) load(1);
+  __syncthreads();
+  for (int ks = 0; ks < nks; ++ks) {
+    const int st = ks & 1;
+    const int m0 = m_begin + ks * O_KS;
+    // B operands: column wave * 64 + 16 s + l16, rows 8 lg .. 8 lg + 7 of the slab
+    uint4 bq[4];
 #pragma unroll
-      for (int u = 0; u < O_UNROLL; ++u) {
-        const int rl = r0 + u * O_WAVES;
-        q[u] = buf_load8(qrs, (rl < rows && c < a.C) ? (rl * a.C + c) * 2 : kOutOfRange);
+    for (int s = 0; s < 4; ++s) {
+      const uint16_t* q = &qs[st][8 * lg][wave * 64 + s * 16 + l16];
+      uint32_t w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)q[(2 * i) * O_LD] | ((uint32_t)q[(2 * i + 1) * O_LD] << 16);
+      bq[s] = uint4{w[0], w[1], w[2], w[3]};
+    }
+#pragma unroll
+    for (int g = 0; g < JG; ++g) {
+      // A operands: rows 16 g + l16 of the hi and lo planes, m0 + 8 lg .. + 7 (Mp is a multiple of 32)
+      const uint16_t* p = a.PT + (size_t)(g * 16 + l16) * a.Mp + m0 + 8 * lg;
+      const uint4 ahi = *reinterpret_cast<const uint4*>(p);
+      const uint4 alo = *reinterpret_cast<const uint4*>(p + (size_t)a.RP * a.Mp);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        acc[g][s] = mfma16(ahi, bq[s], acc[g][s]);
+        acc[g][s] = mfma16(alo, bq[s], acc[g][s]);
       }
-    };
-    load(wave);  // the window's first rows of Q in flight while P is staged
-    __syncthreads();  // the previous window's P is no longer read
-    for (int e = t; e < rows * O_JT; e += O_WAVES * 64) {
-      const int rl = e / O_JT, jj = e % O_JT;
-      ps[rl][jj] = a.P[(size_t)(w0 + rl) * a.RP + jg * O_JT + jj];
+    }
+    if (ks + 1 < nks) {
+      store(st ^ 1);  // stage st ^ 1 was last read before the previous barrier
+      if (ks + 2 < nks) load(ks + 2);
     }
     __syncthreads();
-    for (int r0 = wave; r0 < rows; r0 += O_WAVES * O_UNROLL) {
-      if (r0 != wave) load(r0);
-#pragma unroll
-      for (int u = 0; u < O_UNROLL; ++u) {
-        const int rl = r0 + u * O_WAVES;  // wave-uniform
-        if (rl >= rows) break;
-        const float qf[4] = {bf16_to_f32(q[u].x & 0xFFFFu), bf16_to_f32(q[u].x >> 16),
-                             bf16_to_f32(q[u].y & 0xFFFFu), bf16_to_f32(q[u].y >> 16)};
-        const f32x4_t* pr = reinterpret_cast<const f32x4_t*>(&ps[rl][0]);
-#pragma unroll
-        for (int j4 = 0; j4 < O_JT / 4; ++j4) {
-          const f32x4_t p = pr[j4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            acc[j4 * 4 + 0][e] += p[0] * qf[e];
-            acc[j4 * 4 + 1][e] += p[1] * qf[e];
-            acc[j4 * 4 + 2][e] += p[2] * qf[e];
-            acc[j4 * 4 + 3][e] += p[3] * qf[e];
-          }
-        }
-      }
-    }
   }
 
-  // wave sums added in wave order, half of the j values at a time; the
-  // partials are laid out like the output (j-major or column-major), so that
-  // the finish reads them in the order it writes
+  // acc[g][s] lane l holds out[16 g + 4 lg + e][c0 + 64 wave + 16 s + l16]; partials laid out like the output
   const size_t zc = (size_t)ch * a.RP * a.C;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    __syncthreads();
-    if (wave > 0) {
+  for (int s = 0; s < 4; ++s) {
+    const int c = c0 + wave * 64 + s * 16 + l16;
+    if (c >= a.C) continue;
 #pragma unroll
-      for (int j = 0; j < O_JT / 2; ++j)
-        red[wave - 1][j][lane] = f32x4_t{acc[h * 8 + j][0], acc[h * 8 + j][1], acc[h * 8 + j][2], acc[h * 8 + j][3]};
-    }
-    __syncthreads();
-    if (wave == 0 && c < a.C) {
-      f32x4_t v[O_JT / 2];
-#pragma unroll
-      for (int j = 0; j < O_JT / 2; ++j) {
-        v[j] = f32x4_t{acc[h * 8 + j][0], acc[h * 8 + j][1], acc[h * 8 + j][2], acc[h * 8 + j][3]};
-#pragma unroll
-        for (int w = 0; w < O_WAVES - 1; ++w) v[j] += red[w][j][lane];
-      }
-      const int j0 = jg * O_JT + h * 8;
+    for (int g = 0; g < JG; ++g) {
+      const int j = g * 16 + 4 * lg;
       if (a.jc) {
 #pragma unroll
-        for (int j = 0; j < O_JT / 2; ++j)
-          *reinterpret_cast<f32x4_t*>(a.part + zc + (size_t)(j0 + j) * a.C + c) = v[j];
+        for (int e = 0; e < 4; ++e) a.part[zc + (size_t)(j + e) * a.C + c] = acc[g][s][e];
       } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float* o = a.part + zc + (size_t)(c + e) * a.RP + j0;
-          *reinterpret_cast<f32x4_t*>(o) = f32x4_t{v[0][e], v[1][e], v[2][e], v[3][e]};
-          *reinterpret_cast<f32x4_t*>(o + 4) = f32x4_t{v[4][e], v[5][e], v[6][e], v[7][e]};
-        }
+        *reinterpret_cast<f32x4_t*>(a.part + zc + (size_t)c * a.RP + j) = acc[g][s];
       }
     }
   }
 }
 
 // dA's and dB's partials in one launch: workgroups [0, n0) for o0, the rest o1.
+template <int RP>
 __global__ __launch_bounds__(O_WAVES * 64) void lora_outer_part_kernel(OuterArgs o0, int n0, OuterArgs o1) {
   const int b = blockIdx.x;
   if (b < n0)
-    outer_part(o0, b);
+    outer_part<RP>(o0, b);
   else
-    outer_part(o1, b - n0);
+    outer_part<RP>(o1, b - n0);
 }
 
 constexpr int F_UNROLL = 8;
@@ -241,31 +240,53 @@ __global__ __launch_bounds__(256) void lora_outer_finish_kernel(OuterArgs o0, in
 }
 
 // Rows per chunk and number of chunks of the outer products over M rows and
-// C columns at padded rank RP: enough chunks for about O_TARGET_WG
-// workgroups, each chunk a multiple of 16 rows and at least O_MIN_ROWS.
-void outer_chunks(int M, int C, int rp, int& mch, int& nch) {
-  const int64_t tiles = (int64_t)((C + O_COLS - 1) / O_COLS) * (rp / O_JT);
+// C columns: enough chunks for about O_TARGET_WG workgroups, each chunk a
+// multiple of O_KS rows and at least O_MIN_ROWS.
+void outer_chunks(int M, int C, int& mch, int& nch) {
+  const int64_t tiles = (C + O_COLS - 1) / O_COLS;
   const int64_t want = std::max<int64_t>(1, (O_TARGET_WG + tiles - 1) / tiles);
   int64_t rows = (M + want - 1) / want;
-  rows = std::max<int64_t>(O_MIN_ROWS, (rows + 15) / 16 * 16);
+  rows = std::max<int64_t>(O_MIN_ROWS, (rows + O_KS - 1) / O_KS * O_KS);
   mch = (int)rows;
   nch = (int)((M + rows - 1) / rows);
 }
 
-OuterArgs outer_job(const float* P, const uint16_t* Q, int M, int C, int rp, int r, float* part, float* out, bool jc,
-                    int& parts, int& finishes) {
-  OuterArgs o{P, Q, part, out, M, C, rp, r, 0, 0, jc ? 1 : 0, (C + O_COLS - 1) / O_COLS};
-  outer_chunks(M, C, rp, o.mch, o.nch);
-  parts = o.tiles * (rp / O_JT) * o.nch;
+int padded_rows(int M) { return (M + O_KS - 1) / O_KS * O_KS; }
+
+OuterArgs outer_job(const uint16_t* PT, const uint16_t* Q, int M, int C, int rp, int r, float* part, float* out,
+                    bool jc, int& parts, int& finishes) {
+  OuterArgs o{PT, Q, part, out, M, padded_rows(M), C, rp, r, 0, 0, jc ? 1 : 0, (C + O_COLS - 1) / O_COLS};
+  outer_chunks(M, C, o.mch, o.nch);
+  parts = o.tiles * o.nch;
   finishes = (int)(((size_t)r * C + 255) / 256);
   return o;
+}
+
+template <int RP>
+void launch_outer_rp(const OuterArgs& o0, int p0, const OuterArgs& o1, int p1, hipStream_t stream) {
+  hipLaunchKernelGGL((lora_outer_part_kernel<RP>), dim3(p0 + p1), dim3(O_WAVES * 64), 0, stream, o0, p0, o1);
+}
+
+hipError_t launch_outer(const OuterArgs& o0, int p0, int f0, const OuterArgs& o1, int p1, int f1, int rp,
+                        hipStream_t stream) {
+  switch (rp) {
+    case 16: launch_outer_rp<16>(o0, p0, o1, p1, stream); break;
+    case 32: launch_outer_rp<32>(o0, p0, o1, p1, stream); break;
+    case 64: launch_outer_rp<64>(o0, p0, o1, p1, stream); break;
+    case 128: launch_outer_rp<128>(o0, p0, o1, p1, stream); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(lora_outer_finish_kernel, dim3(f0 + f1), dim3(256), 0, stream, o0, f0, o1);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------- workspace layout
 size_t up256(size_t v) { return (v + 255) / 256 * 256; }
 
 struct BwdLayout {
-  size_t bt, at, tsu, u32, t32, tpart, tpart2, opa, opb, total;
+  size_t bt, at, tsu, uT, tT, tpart, tpart2, opa, opb, total;
 };
 
 BwdLayout layout(int M, int N, int K, int rp) {
@@ -274,13 +295,14 @@ BwdLayout layout(int M, int N, int K, int rp) {
   l.bt = o;    o += up256((size_t)rp * N * 2);                      // B^T [RP x N] bf16
   l.at = o;    o += up256((size_t)K * rp * 2);                      // A^T [K x RP] bf16
   l.tsu = o;   o += up256((size_t)M * 2 * rp * 2);                  // hi | lo of s U [M x 2 RP] bf16
-  l.u32 = o;   o += up256((size_t)M * rp * 4);                      // s U [M x RP] fp32
-  l.t32 = o;   o += up256((size_t)M * rp * 4);                      // s T [M x RP] fp32
+  const size_t Mp = (size_t)padded_rows(M);
+  l.uT = o;    o += up256(2 * (size_t)rp * Mp * 2);                 // hi | lo planes of (s U)^T [2][RP][Mp] bf16
+  l.tT = o;    o += up256(2 * (size_t)rp * Mp * 2);                 // hi | lo planes of (s T)^T [2][RP][Mp] bf16
   l.tpart = o; o += up256((size_t)kTpreMaxChunks * M * rp * 4);     // pre-pass partials (s U)
   l.tpart2 = o; o += up256((size_t)kTpreMaxChunks * M * rp * 4);    // pre-pass partials (s T)
   int mch, nch_a, nch_b;
-  outer_chunks(M, K, rp, mch, nch_a);
-  outer_chunks(M, N, rp, mch, nch_b);
+  outer_chunks(M, K, mch, nch_a);
+  outer_chunks(M, N, mch, nch_b);
   const size_t oa = (size_t)nch_a * rp * K, ob = (size_t)nch_b * rp * N;
   l.opa = o;   o += up256(oa * 4);                                  // dA's outer-product partials
   l.opb = o;   o += up256(ob * 4);                                  // dB's outer-product partials
@@ -342,7 +364,8 @@ hipError_t launch_lora_backward(const BackwardArgs& a, void* ws, hipStream_t str
   u.r = a.r;
   u.ts = a.dx ? reinterpret_cast<uint16_t*>(w + l.tsu) : nullptr;
   u.part = reinterpret_cast<float*>(w + l.tpart);
-  u.t32 = a.dA ? reinterpret_cast<float*>(w + l.u32) : nullptr;
+  u.tT = a.dA ? reinterpret_cast<uint16_t*>(w + l.uT) : nullptr;
+  u.Mp = padded_rows(a.M);
   tt.x = a.x;
   tt.A = a.A;
   tt.s = a.s;
@@ -350,7 +373,8 @@ hipError_t launch_lora_backward(const BackwardArgs& a, void* ws, hipStream_t str
   tt.K = a.K;
   tt.r = a.r;
   tt.part = reinterpret_cast<float*>(w + l.tpart2);
-  tt.t32 = reinterpret_cast<float*>(w + l.t32);
+  tt.tT = reinterpret_cast<uint16_t*>(w + l.tT);
+  tt.Mp = padded_rows(a.M);
   if (want_u && want_t)
     e = launch_lora_tpre2(u, tt, rp, stream);
   else
@@ -373,15 +397,11 @@ hipError_t launch_lora_backward(const BackwardArgs& a, void* ws, hipStream_t str
   int p0 = 0, f0 = 0, p1 = 0, f1 = 0;
   OuterArgs o0{}, o1{};
   if (a.dA)
-    o0 = outer_job(u.t32, a.x, a.M, a.K, rp, a.r, reinterpret_cast<float*>(w + l.opa), a.dA, true, p0, f0);
+    o0 = outer_job(u.tT, a.x, a.M, a.K, rp, a.r, reinterpret_cast<float*>(w + l.opa), a.dA, true, p0, f0);
   if (a.dB)
-    o1 = outer_job(tt.t32, a.dy, a.M, a.N, rp, a.r, reinterpret_cast<float*>(w + l.opb), a.dB, false, p1, f1);
-  if (p0 + p1 > 0) {
-    hipLaunchKernelGGL(lora_outer_part_kernel, dim3(p0 + p1), dim3(O_WAVES * 64), 0, stream, o0, p0, o1);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(lora_outer_finish_kernel, dim3(f0 + f1), dim3(256), 0, stream, o0, f0, o1);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
+    o1 = outer_job(tt.tT, a.dy, a.M, a.N, rp, a.r, reinterpret_cast<float*>(w + l.opb), a.dB, false, p1, f1);
+  if (p0 + p1 > 0)
+    if ((e = launch_outer(o0, p0, f0, o1, p1, f1, rp, stream)) != hipSuccess) return e;
   return hipSuccess;
 }
 

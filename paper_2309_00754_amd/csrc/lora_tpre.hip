@@ -93,20 +93,28 @@ __global__ __launch_bounds__(T_WAVES * 64) void lora_t_part_kernel(TpreArgs a0, 
 }
 
 // s * T of element e = row * RP + j from the chunk partials (added in chunk
-// order), split into bf16 hi and lo parts (and / or kept in fp32).
+// order), split into bf16 hi and lo parts, written row-major (ts) and / or
+// transposed (tT, whose rows M..Mp are written as zeros).
 template <int RP>
 __device__ __forceinline__ void t_finish(const TpreArgs& a, int nkc, size_t e) {
-  if (e >= (size_t)a.M * RP) return;
+  const int rows = a.tT ? a.Mp : a.M;
+  if (e >= (size_t)rows * RP) return;
   const size_t row = e / RP, j = e % RP;
-  float v = 0.f;
-  for (int c = 0; c < nkc; ++c) v += a.part[((size_t)c * a.M + row) * RP + j];
-  v *= a.s;
-  if (a.t32) a.t32[e] = v;
-  if (a.ts) {
-    const uint32_t hi = f32_to_bf16_rne(v);
-    const uint32_t lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
-    a.ts[row * 2 * RP + j] = (uint16_t)hi;
-    a.ts[row * 2 * RP + RP + j] = (uint16_t)lo;
+  uint32_t hi = 0, lo = 0;
+  if (row < (size_t)a.M) {
+    float v = 0.f;
+    for (int c = 0; c < nkc; ++c) v += a.part[((size_t)c * a.M + row) * RP + j];
+    v *= a.s;
+    hi = f32_to_bf16_rne(v);
+    lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
+    if (a.ts) {
+      a.ts[row * 2 * RP + j] = (uint16_t)hi;
+      a.ts[row * 2 * RP + RP + j] = (uint16_t)lo;
+    }
+  }
+  if (a.tT) {
+    a.tT[j * a.Mp + row] = (uint16_t)hi;
+    a.tT[(RP + j) * a.Mp + row] = (uint16_t)lo;
   }
 }
 
@@ -146,8 +154,8 @@ hipError_t launch_rp(const TpreArgs& a0, const TpreArgs* a1, const uint16_t** bp
   // aligned; no B at all (a.B null): nothing to pad
   const bool direct = a0.B == nullptr || (a0.r == RP && (reinterpret_cast<uintptr_t>(a0.B) & 15) == 0);
   if (bp_used) *bp_used = a0.B == nullptr ? nullptr : direct ? a0.B : a0.bp;
-  const int tb0 = (int)(((size_t)a0.M * RP + 255) / 256);
-  const int tb1 = a1 ? (int)(((size_t)a1->M * RP + 255) / 256) : 0;
+  const int tb0 = (int)(((size_t)(a0.tT ? a0.Mp : a0.M) * RP + 255) / 256);
+  const int tb1 = a1 ? (int)(((size_t)(a1->tT ? a1->Mp : a1->M) * RP + 255) / 256) : 0;
   const size_t total = (size_t)a0.N * RP;
   const int bblocks = direct ? 0 : (int)((total + 255) / 256 < 2048 ? (total + 255) / 256 : 2048);
   hipLaunchKernelGGL((lora_t_finish_kernel<RP>), dim3(tb0 + tb1 + bblocks), dim3(256), 0, stream, a0, nkc0, tb0, b1,

@@ -380,11 +380,11 @@ def test_lora_linear_backward_optional_inputs():
     assert _bwd(r=0, A=None, B=None, ws=None, nbytes=0, dy=P8) == H.HYDRA_ERR_ALIGN
 
 
-def _outer_chunks(M, C, rp):
-    tiles = -(-C // 256) * (rp // 16)
-    want = max(1, -(-512 // tiles))
+def _outer_chunks(M, C):
+    tiles = -(-C // 256)
+    want = max(1, -(-256 // tiles))
     rows = -(-M // want)
-    rows = max(64, -(-rows // 16) * 16)
+    rows = max(128, -(-rows // 32) * 32)
     return -(-M // rows)
 
 
@@ -392,9 +392,10 @@ def _bwd_ws(M, N, K, rp):
     if rp == 0:
         return 0
     up = lambda v: -(-v // 256) * 256  # noqa: E731
-    oa = _outer_chunks(M, K, rp) * rp * K
-    ob = _outer_chunks(M, N, rp) * rp * N
-    return (up(rp * N * 2) + up(K * rp * 2) + up(M * 2 * rp * 2) + 2 * up(M * rp * 4) + 2 * up(8 * M * rp * 4)
+    Mp = -(-M // 32) * 32
+    oa = _outer_chunks(M, K) * rp * K
+    ob = _outer_chunks(M, N) * rp * N
+    return (up(rp * N * 2) + up(K * rp * 2) + up(M * 2 * rp * 2) + 2 * up(2 * rp * Mp * 2) + 2 * up(8 * M * rp * 4)
             + up(oa * 4) + up(ob * 4))
 
 
@@ -403,9 +404,9 @@ def test_backward_workspace_bytes():
                            (3, 8, 16, 33, 64), (1, 8, 8, 1, 16)]:
         assert H.hydra_lora_linear_backward_workspace_bytes(M, N, K, r) == _bwd_ws(M, N, K, rp)
     assert H.hydra_lora_linear_backward_workspace_bytes(7, 8, 8, 0) == 0
-    # the outer-product partials stay near 2 x 8 MiB however the shape grows (about 512 workgroups' worth each)
+    # the outer-product partials stay near 2 x 4 MiB however the shape grows (about 256 workgroups' worth each)
     assert H.hydra_lora_linear_backward_workspace_bytes(65536, 4096, 4096, 16) == _bwd_ws(65536, 4096, 4096, 16)
-    assert _outer_chunks(65536, 4096, 16) * 16 * 4096 * 4 <= 9 << 20
+    assert _outer_chunks(65536, 4096) * 16 * 4096 * 4 <= 5 << 20
     L = H.lib()
     out = ctypes.c_size_t(0)
     assert L.hydra_lora_linear_backward_workspace_bytes(0, 8, 8, 16, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE

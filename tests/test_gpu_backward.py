@@ -16,7 +16,7 @@ BWD_SHAPES = [
     # partial outer-product chunk.
     (17, 64, 256, 8), (130, 520, 304, 16), (257, 1024, 704, 33), (64, 128, 96, 64), (300, 2048, 1200, 100),
     (130, 520, 304, 128), (1, 64, 40, 1), (5, 8, 8, 128), (200, 64, 256, 0), (1000, 72, 24, 16),
-    # outer-product chunks longer than the 256 rows staged at a time (dA: 560 rows, dB: 288 rows)
+    # outer-product chunks of several 32-row slabs, the last one ragged, at rank 128 (eight j groups per slab)
     (1100, 8192, 4096, 128),
 ]
 
