@@ -102,8 +102,14 @@ __device__ __forceinline__ void t_finish(const TpreArgs& a, int nkc, size_t e) {
   const size_t row = e / RP, j = e % RP;
   uint32_t hi = 0, lo = 0;
   if (row < (size_t)a.M) {
+    // all chunk loads in flight (nkc <= kTpreMaxChunks), then added in chunk order
+    float p[kTpreMaxChunks];
+#pragma unroll
+    for (int c = 0; c < kTpreMaxChunks; ++c) p[c] = c < nkc ? a.part[((size_t)c * a.M + row) * RP + j] : 0.f;
     float v = 0.f;
-    for (int c = 0; c < nkc; ++c) v += a.part[((size_t)c * a.M + row) * RP + j];
+#pragma unroll
+    for (int c = 0; c < kTpreMaxChunks; ++c)
+      if (c < nkc) v += p[c];
     v *= a.s;
     hi = f32_to_bf16_rne(v);
     lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
