@@ -184,3 +184,45 @@ def test_group_gemm_path(dev):
         e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
         assert_rel(go[i], e_off, "y_off")
         assert_rel(gn[i], e_on, "y_on")
+
+
+@pytest.mark.parametrize("M,K,N,r,G", [(300, 520, 300, 16, 3), (130, 72, 513, 64, 2), (17, 64, 256, 1, 8)])
+def test_group_gemm_matches_single_calls_bitwise(M, K, N, r, G, dev):
+    """At M > 16 (the dual GEMM) every member of a group call has the bits of its single call (ragged tiles,
+    members with different scales, up to 8 members)."""
+    say("group gemm", M, K, N, r, G)
+    cases = [WL.gen_linear(400 + 10 * G + i, M, K, N, r, s=1.0 + 0.5 * i) for i in range(G)]
+    go, gn = _group_run(cases, dev)
+    for i, c in enumerate(cases):
+        so, sn = _run(c, dev)
+        assert np.array_equal(go[i], so) and np.array_equal(gn[i], sn), c.name
+    e_off, e_on = lora_linear_ref(cases[-1].x, cases[-1].W, cases[-1].A, cases[-1].B, cases[-1].s)
+    assert_rel(go[-1], e_off, "last member y_off")
+    assert_rel(gn[-1], e_on, "last member y_on")
+
+
+def test_group_gemm_lora_off_member(dev):
+    """A member without an adapter and without y_on between two LoRA members, at M > 16."""
+    say("group gemm lora-off member")
+    base = [WL.gen_linear(480 + i, 200, 264, 520, 16) for i in range(3)]
+    go, gn = _group_run(base, dev, want_on=[True, False, True])
+    assert gn[1] is None
+    for i in range(3):
+        so, sn = _run(base[i], dev) if i != 1 else (None, None)
+        if i != 1:
+            assert np.array_equal(go[i], so) and np.array_equal(gn[i], sn)
+        e_off, _ = lora_linear_ref(base[i].x, base[i].W, base[i].A, base[i].B, base[i].s)
+        assert_rel(go[i], e_off, f"member {i} y_off")
+
+
+@pytest.mark.parametrize("names", [("q", "k", "v"), ("gate", "up")])
+def test_group_prefill_layer_full_size(names, dev):
+    """The prefill layer's linears that share an input (q/k/v; gate/up) as one group call: each member has the bits
+    of its single call at the full Llama-7B size."""
+    say("group prefill", names)
+    cases = {c.name: c for c in WL.make("prefill_layer")}
+    group = [cases[n] for n in names]
+    go, gn = _group_run(group, dev)
+    for i, c in enumerate(group):
+        so, sn = _run(c, dev)
+        assert np.array_equal(go[i], so) and np.array_equal(gn[i], sn), c.name
