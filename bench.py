@@ -299,7 +299,8 @@ def main():
         out["aux"] = {"score_logits": bench_score_logits(torch, H, WL, dev),
                       "ppo_advantages": bench_advantages(torch, H, WL, dev),
                       "decode_multi": bench_decode_multi(torch, H, WL, dev),
-                      "lora_backward_layer": bench_backward(torch, H, WL, dev)}
+                      "lora_backward_layer": bench_backward(torch, H, WL, dev),
+                      "opt13b_r128": bench_opt13b(torch, H, WL, dev)}
 
     if not args.no_cpu_baseline:
         hi = None
@@ -520,6 +521,82 @@ def bench_backward(torch, H, WL, dev, iters=5):
     return dict(M=c0.M, r=c0.r, layer_us=round(t_layer, 2), per_linear_us=per,
                 tflops=round(fl / t_layer / 1e6, 2), frac_bf16_peak=round(fl / t_layer / 1e6 / PEAK_BF16_TFLOPS, 4),
                 note="dx, dA and dB of the 7 linears; FLOPs = 2MNK + 4MNr + 6MKr per linear; W^T prepared once")
+
+
+def bench_opt13b(torch, H, WL, dev, iters=5):
+    """OPT-1.3b at the paper's LoRA rank 128: the six linears of a layer over a mini-batch of 8 x 512 tokens
+    (hydra_lora_linear_ws: the pre-pass GEMM), the CLM head with V = 50272 plus the reward head over the same tokens
+    (hydra_score), and a decode step of the generation batch of 6 through the four attention projections
+    (hydra_lora_linear_group).  Each figure is the average over a block of back-to-back calls between one pair of
+    events."""
+    bf = (lambda u: torch.from_numpy(np.ascontiguousarray(u).view(np.int16)).to(dev))
+    stream = torch.cuda.current_stream()
+
+    def timed(fns):
+        for fn in fns:
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            for fn in fns:
+                fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters * 1e3
+
+    out = {}
+    # layer
+    lay = WL.make("opt13b_layer_r128")
+    xs, calls = {}, []
+    for c in lay:
+        if id(c.x) not in xs:
+            xs[id(c.x)] = bf(c.x)
+        x, W, A, B = xs[id(c.x)], bf(c.W), bf(c.A), bf(c.B)
+        yo, yn = torch.empty(c.M, c.N, device=dev), torch.empty(c.M, c.N, device=dev)
+        ws = torch.empty(H.hydra_lora_linear_workspace_bytes(c.M, c.N, c.r), dtype=torch.uint8, device=dev)
+        calls.append((c.name, lambda x=x, W=W, A=A, B=B, s=c.s, yo=yo, yn=yn, ws=ws:
+                      H.hydra_lora_linear_ws(x, W, A, B, s, yo, yn, workspace=ws)))
+    t_layer = timed([fn for _, fn in calls])
+    fl = sum(lin_flops(c.M, c.K, c.N, c.r) for c in lay)
+    out["layer"] = dict(M=lay[0].M, r=lay[0].r, us=round(t_layer, 2), tflops=round(fl / t_layer / 1e6, 2),
+                        frac_bf16_peak=round(fl / t_layer / 1e6 / PEAK_BF16_TFLOPS, 4),
+                        per_linear_us={n: round(timed([fn]), 2) for n, fn in calls})
+    del calls, xs
+    # scoring head
+    sc = WL.make("opt13b_score_r128")
+    h, Wl, A, B, w_rm = bf(sc.h), bf(sc.W_lm), bf(sc.A), bf(sc.B), bf(sc.w_rm)
+    ids = torch.from_numpy(sc.ids).to(dev)
+    lp_on, lp_off, kl = (torch.empty(sc.M, device=dev) for _ in range(3))
+    reward = torch.empty(sc.n_seq, device=dev)
+    ws = torch.empty(H.hydra_score_workspace_bytes(sc.M, sc.V), dtype=torch.uint8, device=dev)
+    t_sc = timed([lambda: H.hydra_score(h, Wl, A, B, sc.s, ids, w_rm, sc.n_seq, sc.seq_len, lp_on, lp_off, kl,
+                                        reward=reward, workspace=ws)])
+    fl = lin_flops(sc.M, sc.K, sc.V, sc.r) + 2.0 * sc.n_seq * sc.K
+    out["score"] = dict(M=sc.M, V=sc.V, r=sc.r, us=round(t_sc, 2), tflops=round(fl / t_sc / 1e6, 2),
+                        frac_bf16_peak=round(fl / t_sc / 1e6 / PEAK_BF16_TFLOPS, 4),
+                        tokens_per_s=round(sc.M / (t_sc * 1e-6), 1))
+    del h, Wl, ws
+    # decode step
+    dec = WL.make("opt13b_decode_r128")
+    xd = bf(dec[0].x)
+    gW, gA, gB = [bf(c.W) for c in dec], [bf(c.A) for c in dec], [bf(c.B) for c in dec]
+    gyo = [torch.empty(c.M, c.N, device=dev) for c in dec]
+    gyn = [torch.empty(c.M, c.N, device=dev) for c in dec]
+    # ten weight sets in rotation (336 MB, more than the 256 MB last-level cache); the extra sets are seeded
+    # N(0, 1/K) draws on the device, for timing only
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1310)
+    sets = [gW] + [[(torch.randn(c.N, c.K, generator=gen, device=dev) / np.sqrt(c.K)).to(torch.bfloat16)
+                    .view(torch.int16) for c in dec] for _ in range(9)]
+    calls = [lambda Ws=Ws: H.hydra_lora_linear_group([xd] * len(dec), Ws, gA, gB, [c.s for c in dec], gyo, gyn)
+             for Ws in sets]
+    t_dec = timed(calls) / len(calls)
+    by = sum(lin_bytes(c.M, c.K, c.N, c.r) for c in dec)
+    out["decode"] = dict(M=dec[0].M, r=dec[0].r, us=round(t_dec, 2), gbps=round(by / t_dec / 1e3, 1),
+                         frac_hbm=round(by / t_dec / 1e3 / PEAK_HBM_GBPS, 4),
+                         note="four 2048 x 2048 projections per call, ten weight sets rotating (336 MB)")
+    return out
 
 
 def cpu_baseline(target_s: float, host_inputs=None):

@@ -3,11 +3,15 @@
 // for every column tile of a row block, so it is computed once here instead
 // of inside every tile (at rank 128 against 256-column tiles the in-tile
 // product would add half of the base MFMA work):
-//  * lora_t_part_kernel: one workgroup per 16 rows and K chunk (K split into
-//    up to 8 chunks of at least 1024, so that many workgroups share the
-//    work), 8 waves taking 32-wide k-steps in turn
+//  * lora_t_part_kernel (padded ranks 16, 32): one workgroup per 16 rows and
+//    K chunk (K split into up to 8 chunks of at least 1024, so that many
+//    workgroups share the work), 8 waves taking 32-wide k-steps in turn
 //    (v_mfma_f32_16x16x32_bf16, fp32 accumulation), their partial tiles
 //    summed in LDS in wave order and written to the workspace;
+//  * lora_t_part_wide_kernel (padded ranks 64, 128): one workgroup per 128
+//    rows and K chunk, each wave 32 rows x RP on v_mfma_f32_32x32x16_bf16,
+//    A staged in LDS per 256-wide sub-chunk, so that A is read once per 128
+//    rows;
 //  * lora_t_finish_kernel: the chunk partials added in chunk order, s * T
 //    split into a bf16 hi part and a bf16 lo part (the rounding error of hi),
 //    so that the GEMM's bf16 MFMAs add s T B^T to within ~2^-16 relative;
@@ -92,6 +96,116 @@ __global__ __launch_bounds__(T_WAVES * 64) void lora_t_part_kernel(TpreArgs a0, 
     t_part<RP>(a1, kch1, y - nkc0);
 }
 
+// Wide ranks (RP = 64, 128): a workgroup of W_WAVES waves owns W_WAVES x 32
+// rows and one K chunk; each wave accumulates its 32 rows x RP columns of T
+// with v_mfma_f32_32x32x16_bf16 (A rows as the A operand, x rows as the B
+// operand).  The chunk goes in sub-chunks of W_SUB k: the workgroup stages
+// the sub-chunk of A ([RP x W_SUB], rows padded by 16 bytes so that the
+// 32-row fragment reads hit every bank once) in LDS, so A is read once per
+// W_WAVES x 32 rows (the 16-row form above reads it once per 16 rows: 8x
+// the x traffic at RP = 128).  Each wave holds the x slice and A pieces of
+// two sub-chunks in registers: the next one's loads are in flight while the
+// current one is staged and multiplied.
+constexpr int W_WAVES = 4;
+constexpr int W_ROWS = W_WAVES * 32;
+constexpr int W_SUB = 128;
+constexpr int W_LDA = W_SUB + 8;  // LDS row stride of the A sub-chunk (bf16)
+
+// K chunks of the wide form: at most kTpreMaxChunks, each at least 256 wide
+// (a multiple of the 16-wide k-step), so that small M still spreads over
+// many workgroups.
+inline void tpre_wide_chunks(int K, int& nkc, int& kch) {
+  const int want = (K + 255) / 256;
+  nkc = want < kTpreMaxChunks ? want : kTpreMaxChunks;
+  kch = ((K + nkc - 1) / nkc + 15) / 16 * 16;
+  nkc = (K + kch - 1) / kch;
+}
+
+template <int RP>
+__device__ __forceinline__ void t_part_wide(const TpreArgs& a, int kch, int kc) {
+  constexpr int TJ = RP / 32;
+  constexpr int XS = W_SUB / 16;                   // 16-wide k-steps per sub-chunk
+  constexpr int AV = RP * (W_SUB / 8) / (W_WAVES * 64);  // 16-byte pieces of A per thread per sub-chunk
+  static_assert(AV * W_WAVES * 64 == RP * (W_SUB / 8), "the A sub-chunk splits evenly over the threads");
+  __shared__ uint16_t as[RP][W_LDA];
+  const int M = a.M, K = a.K;
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int l32 = lane & 31, lh = lane >> 5;
+  const int m0 = blockIdx.x * W_ROWS + wave * 32;
+  const int rows = max(0, min(32, M - m0));
+  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(a.x + (size_t)min(m0, M) * K, (uint32_t)rows * K * 2u);
+  const __amdgpu_buffer_rsrc_t ars = make_rsrc(a.A, (uint32_t)min(a.r, RP) * K * 2u);
+  f32x16_t acc[TJ];
+#pragma unroll
+  for (int j = 0; j < TJ; ++j)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[j][i] = 0.f;
+  const int k_begin = kc * kch;
+  const int k_end = min(K, k_begin + kch);
+  // x slice and A pieces of the sub-chunk at kb into registers
+  auto load = [&](int kb, uint4 (&xf)[XS], uint4 (&av)[AV]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < XS; ++u) {
+      const int k = kb + u * 16 + lh * 8;
+      xf[u] = buf_load16(xrs, k < k_end ? (l32 * K + k) * 2 : kOutOfRange);
+    }
+#pragma unroll
+    for (int i = 0; i < AV; ++i) {
+      const int c = t + i * W_WAVES * 64;
+      const int row = c / (W_SUB / 8), k = kb + (c % (W_SUB / 8)) * 8;
+      av[i] = buf_load16(ars, k < k_end ? (row * K + k) * 2 : kOutOfRange);
+    }
+  };
+  // A pieces into LDS (after every wave is done with the previous sub-chunk), then the MFMAs
+  auto stage_and_multiply = [&](const uint4 (&xf)[XS], const uint4 (&av)[AV]) __attribute__((always_inline)) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < AV; ++i) {
+      const int c = t + i * W_WAVES * 64;
+      *reinterpret_cast<uint4*>(&as[c / (W_SUB / 8)][(c % (W_SUB / 8)) * 8]) = av[i];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < XS; ++u)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+        acc[j] = mfma32(*reinterpret_cast<const uint4*>(&as[j * 32 + l32][u * 16 + lh * 8]), xf[u], acc[j]);
+  };
+  // two register sets: the next sub-chunk's loads are in flight while the current one is staged and multiplied
+  uint4 xf0[XS], av0[AV], xf1[XS], av1[AV];
+  if (k_begin < k_end) load(k_begin, xf0, av0);
+  for (int kb = k_begin; kb < k_end; kb += 2 * W_SUB) {
+    const int kb1 = kb + W_SUB;
+    if (kb1 < k_end) load(kb1, xf1, av1);
+    stage_and_multiply(xf0, av0);
+    if (kb1 >= k_end) break;
+    if (kb1 + W_SUB < k_end) load(kb1 + W_SUB, xf0, av0);
+    stage_and_multiply(xf1, av1);
+  }
+  // acc[j] element 4 i + e holds T[m0 + l32][32 j + 8 i + 4 lh + e]
+  const int row = m0 + l32;
+  if (row >= M) return;
+  float* out = a.part + ((size_t)kc * M + row) * RP;
+#pragma unroll
+  for (int j = 0; j < TJ; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<float4*>(out + 32 * j + 8 * i + 4 * lh) =
+          make_float4(acc[j][4 * i], acc[j][4 * i + 1], acc[j][4 * i + 2], acc[j][4 * i + 3]);
+}
+
+template <int RP>
+__global__ __launch_bounds__(W_WAVES * 64) void lora_t_part_wide_kernel(TpreArgs a0, int kch0, int nkc0,
+                                                                        TpreArgs a1, int kch1) {
+  const int y = blockIdx.y;
+  if (y < nkc0)
+    t_part_wide<RP>(a0, kch0, y);
+  else
+    t_part_wide<RP>(a1, kch1, y - nkc0);
+}
+
 // s * T of element e = row * RP + j from the chunk partials (added in chunk
 // order), split into bf16 hi and lo parts, written row-major (ts) and / or
 // transposed (tT, whose rows M..Mp are written as zeros).
@@ -148,12 +262,17 @@ __global__ __launch_bounds__(256) void lora_t_finish_kernel(TpreArgs a0, int nkc
 
 template <int RP>
 hipError_t launch_rp(const TpreArgs& a0, const TpreArgs* a1, const uint16_t** bp_used, hipStream_t stream) {
+  constexpr bool wide = RP >= 64;
   int nkc0, kch0, nkc1 = 0, kch1 = 0;
-  tpre_chunks(a0.K, nkc0, kch0);
-  if (a1) tpre_chunks(a1->K, nkc1, kch1);
+  (wide ? tpre_wide_chunks : tpre_chunks)(a0.K, nkc0, kch0);
+  if (a1) (wide ? tpre_wide_chunks : tpre_chunks)(a1->K, nkc1, kch1);
   const TpreArgs b1 = a1 ? *a1 : TpreArgs{};
-  hipLaunchKernelGGL((lora_t_part_kernel<RP>), dim3((a0.M + 15) / 16, nkc0 + nkc1), dim3(T_WAVES * 64), 0, stream,
-                     a0, kch0, nkc0, b1, kch1);
+  if constexpr (wide)
+    hipLaunchKernelGGL((lora_t_part_wide_kernel<RP>), dim3((a0.M + W_ROWS - 1) / W_ROWS, nkc0 + nkc1),
+                       dim3(W_WAVES * 64), 0, stream, a0, kch0, nkc0, b1, kch1);
+  else
+    hipLaunchKernelGGL((lora_t_part_kernel<RP>), dim3((a0.M + 15) / 16, nkc0 + nkc1), dim3(T_WAVES * 64), 0,
+                       stream, a0, kch0, nkc0, b1, kch1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // B serves as its own padded copy when its rows already are RP bf16, 16-byte

@@ -226,3 +226,17 @@ def test_group_prefill_layer_full_size(names, dev):
     for i, c in enumerate(group):
         so, sn = _run(c, dev)
         assert np.array_equal(go[i], so) and np.array_equal(gn[i], sn), c.name
+
+
+def test_opt13b_decode_rank128_group(dev):
+    """OPT-1.3b decode step: the generation batch of 6 rows through the four 2048 x 2048 attention projections at
+    rank 128, one group call, each member against the oracle and against its single call."""
+    cases = WL.make("opt13b_decode_r128")
+    say("opt13b decode r128", len(cases))
+    go, gn = _group_run(cases, dev)
+    for i, c in enumerate(cases):
+        e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+        assert_rel(go[i], e_off, f"{c.name} y_off")
+        assert_rel(gn[i], e_on, f"{c.name} y_on")
+        so, sn = _run(c, dev)
+        assert np.array_equal(go[i], so) and np.array_equal(gn[i], sn), c.name

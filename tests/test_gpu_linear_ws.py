@@ -83,3 +83,18 @@ def test_linear_ws_rank128_gate_projection_sampled_rows(dev):
     assert_rel(y_off[rows], e_off, "y_off")
     assert_rel(y_on[rows], e_on, "y_on")
     assert np.all(np.isfinite(y_off)) and np.all(np.isfinite(y_on))
+
+
+@pytest.mark.parametrize("proj", ["q", "fc1", "fc2"])
+def test_opt13b_layer_rank128_full_size(proj, dev):
+    """OPT-1.3b at the paper's rank 128 (App. B), mini-batch 8 x 512 = 4096 tokens: 2048 -> 2048, 2048 -> 8192 and
+    8192 -> 2048 through the pre-pass GEMM; the oracle checks sampled rows of both outputs."""
+    say("opt13b layer r128", proj)
+    c = {x.name: x for x in WL.make("opt13b_layer_r128")}[proj]
+    y_off, y_on = _run(c, dev)
+    rows = np.random.default_rng(8).choice(c.M, 24, replace=False)
+    rows[:2] = [0, c.M - 1]
+    e_off, e_on = lora_linear_ref(c.x[rows], c.W, c.A, c.B, c.s)
+    assert_rel(y_off[rows], e_off, "y_off rows")
+    assert_rel(y_on[rows], e_on, "y_on rows")
+    assert np.all(np.isfinite(y_off)) and np.all(np.isfinite(y_on))

@@ -180,3 +180,19 @@ def test_score_logits_identities(dev):
     ids2[1] = 2000
     gb = _score_logits(on, off, ids2, dev)
     assert gb["err"] == 1 and math.isnan(gb["lp_on"][1]) and not math.isnan(gb["lp_on"][0])
+
+
+def test_opt13b_score_rank128_sampled_rows(dev):
+    """OPT-1.3b's CLM head (K = 2048, V = 50272: a ragged last column tile) at rank 128 over 8 x 512 tokens, with the
+    reward head; the oracle checks sampled rows and every reward."""
+    c = WL.make("opt13b_score_r128")
+    say("opt13b score r128", c.M, c.K, c.V, c.r)
+    g = _score(c, dev)
+    rng = np.random.default_rng(9)
+    lasts = [b * c.seq_len + c.seq_len - 1 for b in range(c.n_seq)]
+    rows = np.unique(np.concatenate([[0, 255, 256], lasts, rng.integers(0, c.M, 24)]))
+    e = score_head_ref(c.h[rows], c.W_lm, c.A, c.B, c.s, c.ids[rows], c.w_rm, c.n_seq, c.seq_len, rows=rows)
+    for k in ("lp_on", "lp_off", "kl", "lse_on", "lse_off"):
+        assert_abs(g[k][rows], e[k], k)
+    assert_rel(g["reward"], e["reward"], "reward")
+    assert np.all(np.isfinite(g["lp_on"])) and g["err"] == 0

@@ -15,8 +15,9 @@ Storage conventions (the same ones the C-ABI uses):
 * token ids are ``int32``.
 
 Recipe (the paper's workload shapes are Llama-7B ones: hidden 4096, MLP 11008,
-vocabulary 32000, batch 4 per GPU and 512-token sequences; its datasets and
-weights are not available, so Gaussian stand-ins are drawn):
+vocabulary 32000, batch 4 per GPU and 512-token sequences, and OPT-1.3b ones:
+hidden 2048, MLP 8192, vocabulary 50272, generation batch 6 and mini-batch 8;
+its datasets and weights are not available, so Gaussian stand-ins are drawn):
 
 * one ``numpy.random.Generator(PCG64(seed))`` per workload, tensors drawn in
   the order listed by each generator, each as float64 standard normals in
@@ -55,6 +56,8 @@ __all__ = [
     "WORKLOADS",
     "DECODE_PROJ",
     "PREFILL_PROJ",
+    "OPT13B_DECODE_PROJ",
+    "OPT13B_PROJ",
 ]
 
 _CHUNK_ELEMS = 1 << 22
@@ -137,6 +140,10 @@ def gen_linear(seed: int, M: int, K: int, N: int, r: int, s: float = 2.0, name: 
 DECODE_PROJ = [("q", 4096, 4096), ("k", 4096, 4096), ("v", 4096, 4096), ("o", 4096, 4096)]
 # (name, K, N): every linear of one Llama-7B decoder layer.
 PREFILL_PROJ = DECODE_PROJ + [("gate", 4096, 11008), ("up", 4096, 11008), ("down", 11008, 4096)]
+# (name, K, N): every linear of one OPT-1.3b decoder layer (hidden 2048, MLP 8192); the attention projections
+# alone for its decode step.
+OPT13B_DECODE_PROJ = [("q", 2048, 2048), ("k", 2048, 2048), ("v", 2048, 2048), ("o", 2048, 2048)]
+OPT13B_PROJ = OPT13B_DECODE_PROJ + [("fc1", 2048, 8192), ("fc2", 8192, 2048)]
 
 
 def gen_linears(seed: int, M: int, proj, r: int, s: float = 2.0) -> List[LinearCase]:
@@ -335,6 +342,11 @@ WORKLOADS = {
     "decode_multi": dict(seed=6, M=4, K=4096, N=4096, r=16, n_on=2),
     # the update stage's backward through every linear of one layer (W frozen, rank-16 adapters trained)
     "backward_layer": dict(seed=7, M=2048, proj=PREFILL_PROJ, r=16, s=2.0),
+    # OPT-1.3b at the paper's LoRA rank 128: a layer over a mini-batch of 8 x 512 tokens, the CLM head (vocabulary
+    # 50272) with the reward head over the same tokens, and a decode step of the generation batch of 6
+    "opt13b_layer_r128": dict(seed=8, M=4096, proj=OPT13B_PROJ, r=128, s=2.0),
+    "opt13b_score_r128": dict(seed=9, n_seq=8, seq_len=512, K=2048, V=50272, r=128, s=2.0),
+    "opt13b_decode_r128": dict(seed=10, M=6, proj=OPT13B_DECODE_PROJ, r=128, s=2.0),
 }
 
 
@@ -345,9 +357,9 @@ def make(name: str, M: Optional[int] = None):
         return gen_linear(w["seed"], M or w["M"], w["K"], w["N"], w["r"], w["s"], name)
     if name == "score_logits":
         return gen_logits(w["seed"], M or w["n_seq"] * w["seq_len"], w["V"])
-    if name in ("decode_qkvo", "prefill_layer"):
+    if name in ("decode_qkvo", "prefill_layer", "opt13b_layer_r128", "opt13b_decode_r128"):
         return gen_linears(w["seed"], M or w["M"], w["proj"], w["r"], w["s"])
-    if name == "two_head_score":
+    if name in ("two_head_score", "opt13b_score_r128"):
         return gen_score_head(w["seed"], w["n_seq"], w["seq_len"], w["K"], w["V"], w["r"], w["s"])
     if name == "decode_multi":
         return gen_multi(w["seed"], M or w["M"], w["K"], w["N"], w["r"], w["n_on"], name=name)
