@@ -403,30 +403,41 @@ def bench_advantages(torch, H, WL, dev, iters=30):
         H.hydra_ppo_advantages(kl, rw, vals, adv.n_seq, adv.seq_len, a_out, ret_out, rewards=r_out, start=adv.start,
                                beta=adv.beta, gamma=adv.gamma, lam=adv.lam)
 
-    # launches queued back to back, one event pair per launch on the launch stream, one sync at the end
+    # PPO losses of the update stage on the same tokens (new log-probabilities a small step from the old ones)
+    rng = np.random.default_rng(5)
+    lp_old = torch.from_numpy(-rng.uniform(0.5, 6.0, M).astype(np.float32)).to(dev)
+    lp_new = lp_old + torch.from_numpy(rng.normal(0, 0.3, M).astype(np.float32)).to(dev)
+    losses, d_lp, d_v = torch.empty(3, device=dev), torch.empty(M, device=dev), torch.empty(M, device=dev)
+
+    def loss():
+        H.hydra_ppo_loss(lp_new, lp_old, a_out, vals, ret_out, adv.n_seq, adv.seq_len, losses, d_lp=d_lp, d_v=d_v)
+
+    # each launch repeated back to back between one pair of events on the launch stream
     stream = torch.cuda.current_stream()
-    for _ in range(3):
-        vh()
-        gae()
-    torch.cuda.synchronize()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(iters)]
-    for i in range(iters):
-        ev[i][0].record(stream)
-        vh()
-        ev[i][1].record(stream)
-        ev[i][2].record(stream)
-        gae()
-        ev[i][3].record(stream)
-    torch.cuda.synchronize()
-    t_vh = float(np.median([e[0].elapsed_time(e[1]) for e in ev])) * 1e3
-    t_gae = float(np.median([e[2].elapsed_time(e[3]) for e in ev])) * 1e3
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters * 1e3
+
+    vh()
+    gae()
+    t_vh, t_gae, t_loss = timed(vh), timed(gae), timed(loss)
     vh_bytes = 2.0 * M * K + 2.0 * K + 4.0 * M
     gae_bytes = 4.0 * M * 2 + 4.0 * adv.n_seq + 4.0 * M * 3
+    loss_bytes = 4.0 * M * 5 + 4.0 * M * 2 + 12.0
     return dict(tokens=M, K=K, value_head_us=round(t_vh, 2), value_head_gbps=round(vh_bytes / t_vh / 1e3, 1),
                 value_head_frac_hbm=round(vh_bytes / t_vh / 1e3 / PEAK_HBM_GBPS, 4), gae_us=round(t_gae, 2),
-                gae_bytes=int(gae_bytes),
-                note="median of per-launch HIP events over back-to-back launches; the 16 MB of hidden states "
-                     "stay in the last-level cache between iterations")
+                gae_bytes=int(gae_bytes), ppo_loss_us=round(t_loss, 2), ppo_loss_bytes=int(loss_bytes),
+                note="average over back-to-back launches (launch gaps included); the 16 MB of hidden states stay "
+                     "in the last-level cache between iterations")
 
 
 def bench_decode_multi(torch, H, WL, dev, iters=20, sets=3):
