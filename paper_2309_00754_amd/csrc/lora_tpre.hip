@@ -106,6 +106,7 @@ __global__ __launch_bounds__(T_WAVES * 64) void lora_t_part_kernel(TpreArgs a0, 
 // the x traffic at RP = 128).  Each wave holds the x slice and A pieces of
 // two sub-chunks in registers: the next one's loads are in flight while the
 // current one is staged and multiplied.
+constexpr int kWideFrom = 64;  // padded ranks from which the wide form runs
 constexpr int W_WAVES = 4;
 constexpr int W_ROWS = W_WAVES * 32;
 constexpr int W_SUB = 128;
@@ -123,11 +124,12 @@ inline void tpre_wide_chunks(int K, int& nkc, int& kch) {
 
 template <int RP>
 __device__ __forceinline__ void t_part_wide(const TpreArgs& a, int kch, int kc) {
-  constexpr int TJ = RP / 32;
+  constexpr int RA = RP < 32 ? 32 : RP;            // rows of A staged (rows RP.. read as zeros)
+  constexpr int TJ = RA / 32;
   constexpr int XS = W_SUB / 16;                   // 16-wide k-steps per sub-chunk
-  constexpr int AV = RP * (W_SUB / 8) / (W_WAVES * 64);  // 16-byte pieces of A per thread per sub-chunk
-  static_assert(AV * W_WAVES * 64 == RP * (W_SUB / 8), "the A sub-chunk splits evenly over the threads");
-  __shared__ uint16_t as[RP][W_LDA];
+  constexpr int AV = RA * (W_SUB / 8) / (W_WAVES * 64);  // 16-byte pieces of A per thread per sub-chunk
+  static_assert(AV * W_WAVES * 64 == RA * (W_SUB / 8), "the A sub-chunk splits evenly over the threads");
+  __shared__ uint16_t as[RA][W_LDA];
   const int M = a.M, K = a.K;
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -192,8 +194,9 @@ __device__ __forceinline__ void t_part_wide(const TpreArgs& a, int kch, int kc) 
   for (int j = 0; j < TJ; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<float4*>(out + 32 * j + 8 * i + 4 * lh) =
-          make_float4(acc[j][4 * i], acc[j][4 * i + 1], acc[j][4 * i + 2], acc[j][4 * i + 3]);
+      if (32 * j + 8 * i < RP)
+        *reinterpret_cast<float4*>(out + 32 * j + 8 * i + 4 * lh) =
+            make_float4(acc[j][4 * i], acc[j][4 * i + 1], acc[j][4 * i + 2], acc[j][4 * i + 3]);
 }
 
 template <int RP>
@@ -262,7 +265,7 @@ __global__ __launch_bounds__(256) void lora_t_finish_kernel(TpreArgs a0, int nkc
 
 template <int RP>
 hipError_t launch_rp(const TpreArgs& a0, const TpreArgs* a1, const uint16_t** bp_used, hipStream_t stream) {
-  constexpr bool wide = RP >= 64;
+  constexpr bool wide = RP >= kWideFrom;
   int nkc0, kch0, nkc1 = 0, kch1 = 0;
   (wide ? tpre_wide_chunks : tpre_chunks)(a0.K, nkc0, kch0);
   if (a1) (wide ? tpre_wide_chunks : tpre_chunks)(a1->K, nkc1, kch1);
