@@ -79,8 +79,8 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
-        print(f"bench.py: --gpus {max(args.gpus, world)} refused: this build runs and measures the path on one "
-              f"GPU only (the data-parallel sharding is described, not launched)", file=sys.stderr)
+        print(f"bench.py: --gpus {max(args.gpus, world)} refused: the path runs and is measured on one GPU "
+              f"(the data-parallel sharding is described, not launched)", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -55,7 +55,7 @@ typedef enum {
   HYDRA_ERR_NULL = -1,        /* a required pointer is NULL                         */
   HYDRA_ERR_SHAPE = -2,       /* a size is out of range or inconsistent             */
   HYDRA_ERR_ALIGN = -3,       /* a pointer is not aligned as required               */
-  HYDRA_ERR_UNSUPPORTED = -4, /* a valid request this build does not handle         */
+  HYDRA_ERR_UNSUPPORTED = -4, /* a valid request the library does not handle        */
   HYDRA_ERR_WORKSPACE = -5,   /* the workspace is missing or too small              */
   HYDRA_ERR_HIP = -6          /* the HIP runtime reported an error at launch        */
 } hydra_status;

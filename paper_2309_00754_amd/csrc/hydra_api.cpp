@@ -518,7 +518,7 @@ const char* hydra_status_string(hydra_status status) {
     case HYDRA_ERR_NULL: return "HYDRA_ERR_NULL: a required pointer is NULL";
     case HYDRA_ERR_SHAPE: return "HYDRA_ERR_SHAPE: a size is out of range or inconsistent";
     case HYDRA_ERR_ALIGN: return "HYDRA_ERR_ALIGN: a pointer is not aligned as required";
-    case HYDRA_ERR_UNSUPPORTED: return "HYDRA_ERR_UNSUPPORTED: request not handled by this build";
+    case HYDRA_ERR_UNSUPPORTED: return "HYDRA_ERR_UNSUPPORTED: valid request that the library does not handle";
     case HYDRA_ERR_WORKSPACE: return "HYDRA_ERR_WORKSPACE: workspace missing or too small";
     case HYDRA_ERR_HIP: return "HYDRA_ERR_HIP: the HIP runtime reported a launch error";
   }
