@@ -645,13 +645,15 @@ def cpu_baseline(target_s: float, host_inputs=None):
     b = max((t2 - t1) / 48.0, 1e-6)
     a = max(t1 - 16 * b, 0.0)
     rows = int(min(2048, max(64, (target_s - a) / b)))
-    # whole steps (all rows) are repeated until the sample holds about target_s of CPU work
-    reps = 1 if rows < 2048 else max(1, int(target_s / max(a + b * rows, 1e-3)))
-    fl = t = 0.0
-    for _ in range(reps):
+    # whole steps (all rows) are repeated until the sample holds about target_s of CPU work, the count taken
+    # from the first step's own time
+    fl, t = run(rows)
+    reps = 1
+    while rows == 2048 and t + t / reps <= target_s:
         f_, t_ = run(rows)
         fl += f_
         t += t_
+        reps += 1
     return dict(value=round(fl / t / 1e12, 5), unit="TFLOP/s", cores=int(threads), kind="oracle",
                 seconds=round(t, 2),
                 sample=f"float64 oracle on {reps} step(s) with the 2048-token parts cut to their first {rows} rows "
