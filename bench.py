@@ -61,8 +61,9 @@ def lin_bytes(M, K, N, r):
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=30,
+                   help="untimed steps first: the clock settles over the first few tens of milliseconds")
     p.add_argument("--parts", default="decode,prefill,score",
                    help="comma list of step parts to run (profiling aid; the metric needs all three; "
                         "'advantages' adds the PPO advantage step, which is also timed under aux)")
