@@ -14,12 +14,11 @@ decoder layer plus the heads:
     logits are never materialised).
 
 Inputs are synthetic (seeded Gaussians, see workloads/) and already resident
-in HBM when the timed region starts.  The timed region holds the K steps back
-to back between one pair of HIP events on the launch stream.  A part pass
-afterwards repeats the steps with an event at the start of each part (and at
-the step's end), so each part's time covers its launches back to back; a
-detail pass brackets every launch with its own pair of events (those figures
-include the events' own overhead, a few microseconds each).  The
+in HBM when the timed region starts.  Inside the timed region a HIP event on
+the launch stream marks the start of each part of the step (and the step's
+end), so each part's time covers its launches back to back; a separate detail
+pass afterwards brackets every launch with its own pair of events (those
+figures include the events' own overhead, a few microseconds each).  The
 decode step's two kernels (base stream, LoRA update) form one launch of
 hydra_lora_linear_group.  The standalone scoring epilogue over
 materialised logits (hydra_score_logits, 512 x 32000) is timed separately
@@ -199,24 +198,21 @@ def main():
     def new_event():
         return torch.cuda.Event(enable_timing=True)
 
+    # the timed region: K steps back to back, an event on the launch stream at each part boundary
+    evs = [[new_event() for _ in range(len(part_order) + 1)] for _ in range(K)]
     start, end = new_event(), new_event()
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     start.record(stream)
     for k in range(K):
-        step()
+        step(evs[k])
     end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / K
 
-    # part pass, outside the timed region: the same steps with an event at each part boundary; per-part
-    # durations (ms) averaged over the steps
-    evs = [[new_event() for _ in range(len(part_order) + 1)] for _ in range(K)]
-    for k in range(K):
-        step(evs[k])
-    torch.cuda.synchronize()
+    # per-part durations (ms) from the boundary events, averaged over the timed steps
     part_ms = {p: float(np.mean([evs[k][j].elapsed_time(evs[k][j + 1]) for k in range(K)]))
                for j, p in enumerate(part_order)}
 
