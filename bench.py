@@ -47,6 +47,7 @@ if ROOT not in sys.path:
 METRIC = "dual-path LoRA GEMM TFLOP/s + scoring tokens/s, % of MFMA/HBM roofline"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+AUX_NAMES = ("score_logits", "ppo_advantages", "decode_multi", "lora_backward_layer", "opt13b_r128")
 
 
 def lin_flops(M, K, N, r):
@@ -68,11 +69,17 @@ def parse():
                         "'advantages' adds the PPO advantage step, which is also timed under aux)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-aux", action="store_true")
+    p.add_argument("--aux", default=",".join(AUX_NAMES),
+                   help="comma list of the auxiliary measurements to run after the step (profiling aid)")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU oracle sample")
     p.add_argument("--copy-bytes", type=int, default=0,
                    help="run one plain device-to-device copy of this many bytes before the steps "
                         "(calibrates FETCH_SIZE / WRITE_SIZE counters in a profiling run)")
-    return p.parse_args()
+    a = p.parse_args()
+    unknown = [x for x in a.aux.split(",") if x and x not in AUX_NAMES]
+    if unknown:
+        p.error(f"unknown --aux entries {unknown}; known: {', '.join(AUX_NAMES)}")
+    return a
 
 
 def main():
@@ -93,6 +100,7 @@ def main():
     H.lib()  # fail loudly if the HIP library is missing
     dev = torch.device("cuda:0")
     parts = [p for p in args.parts.split(",") if p]
+    aux_names = [a for a in args.aux.split(",") if a]
 
     def bf(u):
         return torch.from_numpy(np.ascontiguousarray(u).view(np.int16)).to(dev)
@@ -293,11 +301,10 @@ def main():
     }
 
     if not args.no_aux:
-        out["aux"] = {"score_logits": bench_score_logits(torch, H, WL, dev),
-                      "ppo_advantages": bench_advantages(torch, H, WL, dev),
-                      "decode_multi": bench_decode_multi(torch, H, WL, dev),
-                      "lora_backward_layer": bench_backward(torch, H, WL, dev),
-                      "opt13b_r128": bench_opt13b(torch, H, WL, dev)}
+        aux_fns = {"score_logits": bench_score_logits, "ppo_advantages": bench_advantages,
+                   "decode_multi": bench_decode_multi, "lora_backward_layer": bench_backward,
+                   "opt13b_r128": bench_opt13b}
+        out["aux"] = {name: aux_fns[name](torch, H, WL, dev) for name in aux_names}
 
     if not args.no_cpu_baseline:
         hi = None

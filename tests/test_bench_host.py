@@ -44,3 +44,8 @@ def test_traffic_figure_only_for_the_measured_sources(monkeypatch):
     monkeypatch.setattr(bench, "kernel_source_digest", lambda: "0" * 64)
     assert bench.committed_traffic("prefill") is None
     assert bench.committed_traffic("no_such_part") is None
+
+
+def test_unknown_aux_entry_is_refused():
+    r = _run(["--aux", "score_logits,no_such_entry"])
+    assert r.returncode == 2 and "no_such_entry" in r.stderr
