@@ -147,3 +147,49 @@ def test_every_entry_point_runs_on_the_given_stream(dev):
         for k, v in got.items():
             g = host(v)
             assert np.array_equal(g.view(np.uint8), ref[k].view(np.uint8)), f"{name}: {k} differs on a second stream"
+
+
+def test_concurrent_calls_from_two_threads_on_two_streams(dev):
+    """The library keeps no mutable state between calls: two host threads, each calling entry points on its own
+    stream at the same time, get the bits of the calls made one after the other."""
+    import threading
+
+    import torch
+    cases = _cases(dev)
+    torch.cuda.synchronize()
+    groups = [["score", "linear_prefill", "group", "advantages_and_loss"],
+              ["transpose_and_backward", "linear_ws_r128", "multi", "score_logits", "value_head", "linear_decode"]]
+    ref = {}
+    for name in sum(groups, []):
+        o = cases[name](None)
+        torch.cuda.synchronize()
+        ref[name] = {k: host(v).copy() for k, v in o.items()}
+    say("two threads, two streams")
+    streams = [torch.cuda.Stream(device=dev) for _ in groups]
+    got = [dict() for _ in groups]
+    errors = []
+    start = threading.Barrier(len(groups))
+
+    def worker(i):
+        try:
+            torch.cuda.set_device(dev)
+            start.wait(timeout=30)
+            with torch.cuda.stream(streams[i]):
+                for _ in range(3):
+                    for name in groups[i]:
+                        got[i][name] = cases[name](streams[i])
+            streams[i].synchronize()
+        except BaseException as e:  # reported by the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(len(groups))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=60)
+    assert not any(t.is_alive() for t in threads), "a worker thread did not finish"
+    assert not errors, errors
+    for i, names in enumerate(groups):
+        for name in names:
+            for k, v in got[i][name].items():
+                assert np.array_equal(host(v).view(np.uint8), ref[name][k].view(np.uint8)), f"{name}: {k}"
