@@ -336,7 +336,11 @@ constexpr int URW = 8;   // rows of A per wave in the T pass
 // L2 hits once the first workgroup has touched them), reduces its partial
 // sums across its lanes, and the partials of the chunk groups are added in a
 // fixed order.  The rows of B and the current values of y_on are requested
-// first, so that their latency overlaps the T pass.
+// first, so that their latency overlaps the T pass.  The block of B is held in
+// LDS row by row ([column][j]) at padded ranks up to 32, and transposed with
+// padded rows ([j][column]) from rank 64 on: there the lanes of a wave, which
+// hold consecutive columns, would otherwise read LDS addresses 2 * RP bytes
+// apart, all in one bank at RP = 128.
 template <int MB, int RP>
 __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
   constexpr int NT = UW * 64;
@@ -349,7 +353,9 @@ __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
   static_assert(GR * GC == UW && VT <= 64 && BPT >= 1, "shape");
   __shared__ float part[UW][VT];      // per-wave partial T, index j_local * MB + m
   __shared__ float4 tsh[MB][RP / 4];  // T[m][j]
-  __shared__ uint16_t bsh[UNB][RP];
+  constexpr bool BT = RP >= 64;                    // B block transposed in LDS
+  constexpr int BLD = BT ? UNB + 2 : RP;           // u16 per LDS row of the block
+  __shared__ uint16_t bsh[BT ? RP : UNB][BLD];
   const int gi = blockIdx.y;
   const uint16_t* __restrict__ X = ga.x[gi];
   const uint16_t* __restrict__ At = ga.A[gi];
@@ -407,7 +413,10 @@ __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
 #pragma unroll
   for (int q = 0; q < BPT; ++q) {
     const int e = t + q * NT;
-    bsh[e / RP][e % RP] = (uint16_t)bv[q];
+    if constexpr (BT)
+      bsh[e % RP][e / RP] = (uint16_t)bv[q];
+    else
+      bsh[e / RP][e % RP] = (uint16_t)bv[q];
   }
   __syncthreads();
   // T[m][j] = sum over the chunk groups, in chunk-group order
@@ -423,14 +432,20 @@ __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
   for (int q = 0; q < OPT; ++q) {
     const int e = t + q * NT, m = e / UNB, nl = e % UNB;
     if (e < UNB * MB && m < M && nl < nb) {
+      auto b_at = [&](int j) __attribute__((always_inline)) {
+        if constexpr (BT)
+          return bf16_to_f32(bsh[j][nl]);
+        else
+          return bf16_to_f32(bsh[nl][j]);
+      };
       float d = 0.f;
 #pragma unroll
       for (int j4 = 0; j4 < RP / 4; ++j4) {
         const float4 tv = tsh[m][j4];
-        d = fmaf(tv.x, bf16_to_f32(bsh[nl][4 * j4 + 0]), d);
-        d = fmaf(tv.y, bf16_to_f32(bsh[nl][4 * j4 + 1]), d);
-        d = fmaf(tv.z, bf16_to_f32(bsh[nl][4 * j4 + 2]), d);
-        d = fmaf(tv.w, bf16_to_f32(bsh[nl][4 * j4 + 3]), d);
+        d = fmaf(tv.x, b_at(4 * j4 + 0), d);
+        d = fmaf(tv.y, b_at(4 * j4 + 1), d);
+        d = fmaf(tv.z, b_at(4 * j4 + 2), d);
+        d = fmaf(tv.w, b_at(4 * j4 + 3), d);
       }
       y_on[(size_t)m * N + n0 + nl] = yv[q] + s * d;
     }
