@@ -340,7 +340,10 @@ constexpr int URW = 8;   // rows of A per wave in the T pass
 // LDS row by row ([column][j]) at padded ranks up to 32, and transposed with
 // padded rows ([j][column]) from rank 64 on: there the lanes of a wave, which
 // hold consecutive columns, would otherwise read LDS addresses 2 * RP bytes
-// apart, all in one bank at RP = 128.
+// apart, all in one bank at RP = 128.  From rank 64 on the T pass also stages
+// the pieces of x in LDS once per workgroup: with one or two chunk groups the
+// 16 waves would otherwise each request all of x, as many bytes as their rows
+// of A.
 template <int MB, int RP>
 __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
   constexpr int NT = UW * 64;
@@ -353,9 +356,14 @@ __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
   static_assert(GR * GC == UW && VT <= 64 && BPT >= 1, "shape");
   __shared__ float part[UW][VT];      // per-wave partial T, index j_local * MB + m
   __shared__ float4 tsh[MB][RP / 4];  // T[m][j]
-  constexpr bool BT = RP >= 64;                    // B block transposed in LDS
+  constexpr bool BT = RP >= 64;                    // B block transposed in LDS (always when XS)
   constexpr int BLD = BT ? UNB + 2 : RP;           // u16 per LDS row of the block
   __shared__ uint16_t bsh[BT ? RP : UNB][BLD];
+  // from rank 64 on, x is staged in LDS per round of GC chunks ([chunk][m][lane])
+  constexpr bool XS = RP >= 64;
+  constexpr int XE = XS ? GC * MB * 64 : 1;        // 16-byte pieces of x per round
+  constexpr int XPT = (XE + NT - 1) / NT;
+  __shared__ uint4 xsh[XE];
   const int gi = blockIdx.y;
   const uint16_t* __restrict__ X = ga.x[gi];
   const uint16_t* __restrict__ At = ga.A[gi];
@@ -393,30 +401,75 @@ __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
   float acc[VT];
 #pragma unroll
   for (int q = 0; q < VT; ++q) acc[q] = 0.f;
-  for (int c = cg; c < nch; c += GC) {
-    const int k = c * DKC + lane * 8;
-    const bool kv = k < K;
-    uint4 av[URW], xv[MB];
+  if constexpr (XS) {
+    // Rounds of GC chunks: the workgroup stages the round's x pieces in LDS
+    // once (instead of every row group requesting them) while each wave's
+    // rows of A are in flight.  A wave whose chunk lies past K adds zeros.
+    const int nround = (nch + GC - 1) / GC;
+    for (int rd = 0; rd < nround; ++rd) {
+      const int c = rd * GC + cg;
+      const int k = c * DKC + lane * 8;
+      const bool kv = c < nch && k < K;
+      uint4 av[URW];
 #pragma unroll
-    for (int j = 0; j < URW; ++j) av[j] = buf_load16(ars, kv ? ((rg * URW + j) * K + k) * 2 : kOutOfRange);
+      for (int j = 0; j < URW; ++j) av[j] = buf_load16(ars, kv ? ((rg * URW + j) * K + k) * 2 : kOutOfRange);
+      uint4 xs[XPT];
 #pragma unroll
-    for (int m = 0; m < MB; ++m) xv[m] = buf_load16(xrs, kv ? (m * K + k) * 2 : kOutOfRange);
-    __builtin_amdgcn_sched_barrier(0);  // all of the chunk's loads in flight before the first use
+      for (int q = 0; q < XPT; ++q) {
+        const int e = t + q * NT, ch = e / (MB * 64), m = (e / 64) % MB;
+        const int cc = rd * GC + ch, kk = cc * DKC + (e % 64) * 8;
+        xs[q] = buf_load16(xrs, (e < XE && cc < nch && kk < K) ? (m * K + kk) * 2 : kOutOfRange);
+      }
+      if (rd == 0) {
+        // the block of B goes to LDS now (its loads were issued first, so only
+        // they are waited for), which frees its registers for the T pass
 #pragma unroll
-    for (int j = 0; j < URW; ++j)
+        for (int q = 0; q < BPT; ++q) {
+          const int e = t + q * NT;
+          bsh[e % RP][e / RP] = (uint16_t)bv[q];
+        }
+      }
+      if (rd > 0) __syncthreads();  // every wave is done with the previous round's x
 #pragma unroll
-      for (int m = 0; m < MB; ++m) acc[j * MB + m] = dot8(av[j], xv[m], acc[j * MB + m]);
-    __builtin_amdgcn_sched_barrier(0);
+      for (int q = 0; q < XPT; ++q)
+        if (t + q * NT < XE) xsh[t + q * NT] = xs[q];
+      __syncthreads();
+#pragma unroll
+      for (int m = 0; m < MB; ++m) {
+        const uint4 xv = xsh[(cg * MB + m) * 64 + lane];
+#pragma unroll
+        for (int j = 0; j < URW; ++j) acc[j * MB + m] = dot8(av[j], xv, acc[j * MB + m]);
+        __builtin_amdgcn_sched_barrier(0);  // one row of x in registers at a time
+      }
+    }
+  } else {
+    for (int c = cg; c < nch; c += GC) {
+      const int k = c * DKC + lane * 8;
+      const bool kv = k < K;
+      uint4 av[URW], xv[MB];
+#pragma unroll
+      for (int j = 0; j < URW; ++j) av[j] = buf_load16(ars, kv ? ((rg * URW + j) * K + k) * 2 : kOutOfRange);
+#pragma unroll
+      for (int m = 0; m < MB; ++m) xv[m] = buf_load16(xrs, kv ? (m * K + k) * 2 : kOutOfRange);
+      __builtin_amdgcn_sched_barrier(0);  // all of the chunk's loads in flight before the first use
+#pragma unroll
+      for (int j = 0; j < URW; ++j)
+#pragma unroll
+        for (int m = 0; m < MB; ++m) acc[j * MB + m] = dot8(av[j], xv[m], acc[j * MB + m]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
   wave_reduce_scatter<VT>(acc, lane);
   if (reduced_writer<VT>(lane)) part[wave][reduced_index<VT>(lane)] = acc[0];
+  if constexpr (!XS) {
 #pragma unroll
-  for (int q = 0; q < BPT; ++q) {
-    const int e = t + q * NT;
-    if constexpr (BT)
-      bsh[e % RP][e / RP] = (uint16_t)bv[q];
-    else
-      bsh[e / RP][e % RP] = (uint16_t)bv[q];
+    for (int q = 0; q < BPT; ++q) {
+      const int e = t + q * NT;
+      if constexpr (BT)
+        bsh[e % RP][e / RP] = (uint16_t)bv[q];
+      else
+        bsh[e / RP][e % RP] = (uint16_t)bv[q];
+    }
   }
   __syncthreads();
   // T[m][j] = sum over the chunk groups, in chunk-group order
