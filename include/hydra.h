@@ -103,8 +103,10 @@ hydra_status hydra_lora_linear_workspace_bytes(int64_t M, int64_t N, int64_t r, 
  * s x A^T is computed once per row (instead of once per 256-column tile) as
  * bf16 hi and lo parts, and added with B as 2 RP more k values of the GEMM
  * (RP = r rounded up to 16, 32, 64 or 128) after y_off has been stored.
- * This is the path for the paper's rank 128 (App. B) and the faster one at
- * every rank.  Defined by: the same passages as hydra_lora_linear.
+ * This is the path for the paper's rank 128 (App. B), and the faster one
+ * above rank 16, where the in-tile product of hydra_lora_linear adds RP / 256
+ * of the base GEMM's work; at rank 16 the pre-pass costs about what the GEMM
+ * saves.  Defined by: the same passages as hydra_lora_linear.
  *
  *   workspace, workspace_bytes   device memory of at least
  *       hydra_lora_linear_workspace_bytes(M, N, r) bytes, 16-byte aligned,
