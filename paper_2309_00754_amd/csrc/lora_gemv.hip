@@ -356,13 +356,14 @@ __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
   static_assert(GR * GC == UW && VT <= 64 && BPT >= 1, "shape");
   __shared__ float part[UW][VT];      // per-wave partial T, index j_local * MB + m
   __shared__ float4 tsh[MB][RP / 4];  // T[m][j]
-  constexpr bool BT = RP >= 64;                    // B block transposed in LDS (always when XS)
+  constexpr bool BT = RP >= 64;                    // B block transposed in LDS
   constexpr int BLD = BT ? UNB + 2 : RP;           // u16 per LDS row of the block
   __shared__ uint16_t bsh[BT ? RP : UNB][BLD];
   // from rank 64 on, x is staged in LDS per round of GC chunks ([chunk][m][lane])
   constexpr bool XS = RP >= 64;
   constexpr int XE = XS ? GC * MB * 64 : 1;        // 16-byte pieces of x per round
   constexpr int XPT = (XE + NT - 1) / NT;
+  static_assert(!XS || BT, "the staged T pass writes the B block in the transposed layout");
   __shared__ uint4 xsh[XE];
   const int gi = blockIdx.y;
   const uint16_t* __restrict__ X = ga.x[gi];
