@@ -47,7 +47,8 @@ if ROOT not in sys.path:
 METRIC = "dual-path LoRA GEMM TFLOP/s + scoring tokens/s, % of MFMA/HBM roofline"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
-AUX_NAMES = ("score_logits", "ppo_advantages", "decode_multi", "lora_backward_layer", "opt13b_r128")
+AUX_NAMES = ("score_logits", "single_linear", "ppo_advantages", "decode_multi", "lora_backward_layer",
+             "opt13b_r128")
 
 
 def lin_flops(M, K, N, r):
@@ -301,7 +302,8 @@ def main():
     }
 
     if not args.no_aux:
-        aux_fns = {"score_logits": bench_score_logits, "ppo_advantages": bench_advantages,
+        aux_fns = {"score_logits": bench_score_logits, "single_linear": bench_single_linear,
+                   "ppo_advantages": bench_advantages,
                    "decode_multi": bench_decode_multi, "lora_backward_layer": bench_backward,
                    "opt13b_r128": bench_opt13b}
         out["aux"] = {name: aux_fns[name](torch, H, WL, dev) for name in aux_names}
@@ -386,6 +388,55 @@ def bench_score_logits(torch, H, WL, dev, iters=20):
                 frac_hbm=round(by / us / 1e3 / PEAK_HBM_GBPS, 4), tokens_per_s=round(M / us * 1e6, 1),
                 note="average over blocks of 20 back-to-back launches (median of 5 blocks), 4 rotating input "
                      "sets (524 MB, more than the last-level cache)")
+
+
+def bench_single_linear(torch, H, WL, dev, iters=200):
+    """hydra_lora_linear on the small single linear (x [16 x 512], W [512 x 512], rank 8): launch-latency bound, so
+    it is reported for completeness (no roofline).  Eager back-to-back calls are bound by the host (the binding's
+    argument checks); the same calls captured in one HIP graph and replayed give the GPU-side time per call."""
+    c = WL.make("single_linear")
+    bf = (lambda u: torch.from_numpy(np.ascontiguousarray(u).view(np.int16)).to(dev))
+    x, W, A, B = bf(c.x), bf(c.W), bf(c.A), bf(c.B)
+    yo, yn = torch.empty(c.M, c.N, device=dev), torch.empty(c.M, c.N, device=dev)
+
+    def calls():
+        for _ in range(iters):
+            H.hydra_lora_linear(x, W, A, B, c.s, yo, yn)
+
+    stream = torch.cuda.current_stream()
+
+    def per_call_us(fn):
+        blocks = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            blocks.append(e0.elapsed_time(e1) / iters)
+        return float(np.median(blocks)) * 1e3
+
+    calls()
+    torch.cuda.synchronize()
+    eager = per_call_us(calls)
+    side = torch.cuda.Stream(device=dev)
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        calls()
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        calls()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    graph = per_call_us(g.replay)
+    fl = lin_flops(c.M, c.K, c.N, c.r)
+    return dict(M=c.M, K=c.K, N=c.N, r=c.r, us_graph=round(graph, 2), us_eager=round(eager, 2),
+                tflops_graph=round(fl / graph / 1e6, 3),
+                note="one call = one launch of the small-M MFMA kernel (8 < M <= 16); median of 5 blocks of 200 "
+                     "calls, eager (host-bound) and replayed from one captured HIP graph")
 
 
 def bench_advantages(torch, H, WL, dev, iters=30):
