@@ -136,8 +136,13 @@ def _ptr(t) -> Optional[int]:
 
 
 def _stream_handle(stream) -> Optional[int]:
+    """The hipStream_t of ``stream``, or of torch's current stream on the current device when None (read through
+    torch's raw-stream query when it has one: building a Stream object costs a few microseconds per call)."""
     torch = _torch()
     if stream is None:
+        raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+        if raw is not None:
+            return int(raw(torch.cuda.current_device()))
         stream = torch.cuda.current_stream()
     return int(stream.cuda_stream)
 
