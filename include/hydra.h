@@ -127,7 +127,7 @@ hydra_status hydra_lora_linear_ws(const uint16_t* x, const uint16_t* W, const ui
 /*
  * hydra_lora_linear_group -- G independent LoRA-switchable linears that share
  * M, N, K and r, in one launch (for instance the q/k/v/o projections of one
- * decode step, App. A Alg. 2 "generate"; each with its own adapter).
+ * decode step, App. A Alg. 2, generation step; each with its own adapter).
  * Defined by: the same passages as hydra_lora_linear.
  *
  *   G                     1 <= G <= HYDRA_MAX_GROUP
@@ -175,6 +175,9 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
  * pass reads W from HBM once for all its rows (M = 4 with the off input and
  * one adapter: one read of W instead of two); larger M runs one GEMM per input.
  * Every output has the bits of the corresponding hydra_lora_linear call.
+ * Above M = 16 with adapters, a padded rank above 64 (r > 64) returns
+ * HYDRA_ERR_WORKSPACE before anything is launched (the workspace call
+ * hydra_lora_linear_ws serves that rank).
  */
 hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, int64_t n_on,
                                      const uint16_t* const* x_on, const uint16_t* const* A,
@@ -192,8 +195,9 @@ hydra_status hydra_score_workspace_bytes(int64_t M, int64_t V, size_t* bytes);
 /*
  * hydra_score -- fused two-head PPO scoring pass.
  * Defined by: Sec. 3 (pi^hydra's CLM head and reward head on the same input),
- * App. A Alg. 1 / Alg. 2 ("turn LoRA off ... compute reward and reference log
- * probabilities"; the actor log-probability is the LoRA-on pass), App. B
+ * App. A Alg. 1 / Alg. 2 (the LoRA-off scoring step that yields the reward
+ * and the reference log-probabilities; the actor log-probability is the
+ * LoRA-on pass), App. B
  * (the KL penalty weight beta is applied by the caller, not here).
  *
  *   h        [M x K] bf16   final hidden states, M = n_seq * seq_len, sequence-major
@@ -240,9 +244,9 @@ hydra_status hydra_score_logits(const float* logits_on, const float* logits_off,
 /*
  * hydra_value_head -- the critic's scalar head on every token row.
  * Defined by: Sec. 2 Stage 3 (V(x, y) of the critic, used by generalized
- * advantage estimation), App. A Alg. 2 ("turn on the critic LoRA ... calculate
- * critic values on the generated sequence"; h is the critic pass's final
- * hidden state).  No bias.
+ * advantage estimation), App. A Alg. 2 (the critic-LoRA pass over the
+ * generated sequences that yields the values; h is that pass's final hidden
+ * state).  No bias.
  *
  *   h       [M x K] bf16   hidden states, row-major, 16-byte aligned
  *   w_v     [K] bf16       value head weight, 16-byte aligned
@@ -257,8 +261,9 @@ hydra_status hydra_value_head(const uint16_t* h, const uint16_t* w_v, int64_t M,
  * estimates for n_seq sequences of seq_len tokens (M = n_seq * seq_len,
  * sequence-major).
  * Defined by: Sec. 2 Stage 3 (GAE builds the advantage estimates from the
- * reward using V; V is trained on the returns), App. A Alg. 2 ("use reward and
- * reference log probability to calculate A-hat"), App. B (KL beta = 0.02,
+ * reward using V; V is trained on the returns), App. A Alg. 2 (the advantage
+ * step that combines the reward and the reference log-probabilities), App. B
+ * (KL beta = 0.02,
  * GAE gamma = 1.0, lambda = 0.95).
  *
  *   kl      [M] fp32       per-token KL estimate lp_on - lp_off (hydra_score)
@@ -273,8 +278,8 @@ hydra_status hydra_value_head(const uint16_t* h, const uint16_t* w_v, int64_t M,
  * Positions before `start` get advantage and return 0 (and reward 0).  No
  * output may be one of the inputs or another output (HYDRA_ERR_SHAPE);
  * partial overlaps are not detected and are not allowed.  Requires
- * n_seq, seq_len >= 1, n_seq below 2^26 and M below 2^31; buffers 4-byte
- * aligned.
+ * n_seq, seq_len >= 1 and M = n_seq * seq_len <= 2^20 (HYDRA_ERR_SHAPE
+ * otherwise, as for the other entry points' rows); buffers 4-byte aligned.
  */
 hydra_status hydra_ppo_advantages(const float* kl, const float* reward, const float* values, int64_t n_seq,
                                   int64_t seq_len, int64_t start, float beta, float gamma, float lam, float* rewards,
@@ -303,6 +308,7 @@ hydra_status hydra_ppo_advantages(const float* kl, const float* reward, const fl
  *   d_v [M] fp32              out, optional: d value loss / d V ((V - R) / n; 0 before start)
  * One workgroup sums in a fixed order (deterministic).  No output may be an
  * input or another output (HYDRA_ERR_SHAPE); buffers 4-byte aligned.
+ * Requires n_seq, seq_len >= 1 and M = n_seq * seq_len <= 2^20.
  */
 hydra_status hydra_ppo_loss(const float* lp_new, const float* lp_old, const float* advantages, const float* values,
                             const float* returns, int64_t n_seq, int64_t seq_len, int64_t start, float eps,

@@ -18,7 +18,7 @@ What is computed, and where the paper defines it
 * The two heads of pi^hydra: a causal-LM head over the vocabulary and a
   scalar reward head on the same input (Sec. 3, opening paragraph).
 * Reference log-probabilities and reward from the LoRA-off model
-  (App. A, Alg. 1 and Alg. 2, the "turn LoRA off" step); log-probability of
+  (App. A, Alg. 1 and Alg. 2, the LoRA-off scoring step); log-probability of
   the sampled token under a temperature-1 softmax; the per-token KL penalty
   estimate ``lp_on - lp_off`` whose weight beta = 0.02 (App. B, PPO common
   parameters) is applied downstream, not here.

@@ -9,13 +9,13 @@ What is computed, and where the paper defines it
 ------------------------------------------------
 * The critic's per-token values V(x, y) from its scalar head on the critic's
   hidden states (Sec. 2, "Stage 3: PPO": V is trained on the returns and used
-  by generalized advantage estimation; App. A, Alg. 2: "turn on the critic
-  LoRA ... calculate critic values on the generated sequence").  Reading: no
+  by generalized advantage estimation; App. A, Alg. 2: the critic-LoRA pass
+  over the generated sequences yields the values).  Reading: no
   bias, ``V[t] = <h_crit[t], w_v>``.
 * The per-token PPO reward: the KL penalty with weight beta (App. B: beta =
   0.02) on every scored token, plus the sequence's reward-model score on its
-  last token (App. A, Alg. 2: "use reward and reference log probability to
-  calculate A-hat").  Reading: ``r_t = -beta * KL_t`` for response tokens
+  last token (App. A, Alg. 2: the advantage step combines the reward and the
+  reference log-probabilities).  Reading: ``r_t = -beta * KL_t`` for response tokens
   ``t >= start``, ``r_{T-1} += reward``; tokens before ``start`` carry none.
 * Generalized advantage estimation with gamma and lambda (Sec. 2, "Stage 3:
   PPO", citing GAE; App. B: gamma = 1.0, lambda = 0.95): the TD residual

@@ -208,6 +208,10 @@ hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, i
     for (int64_t b = 0; b < a; ++b)
       if (y_on[b] == y_on[a]) return HYDRA_ERR_SHAPE;
   }
+  // Above the decode sizes the adapters run on the dual GEMM, which holds
+  // ranks up to 64 (hydra_lora_linear_ws serves rank 128 there): rejected
+  // here, before the LoRA-off output is launched.
+  if (M > kDecodeMaxRows && n_on > 0 && r > 0 && hydra::padded_rank(int(r)) > 64) return HYDRA_ERR_WORKSPACE;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   if (M > hydra::kStreamRows) {
     // One launch per input (the MFMA kernels are bound by arithmetic, not by reads of W).
@@ -362,7 +366,7 @@ hydra_status hydra_ppo_loss(const float* lp_new, const float* lp_old, const floa
                             const float* returns, int64_t n_seq, int64_t seq_len, int64_t start, float eps,
                             float* losses, float* d_lp, float* d_v, void* stream) {
   if (!lp_new || !lp_old || !advantages || !values || !returns || !losses) return HYDRA_ERR_NULL;
-  if (!dim_ok(n_seq) || !dim_ok(seq_len) || n_seq > kMaxDim / seq_len) return HYDRA_ERR_SHAPE;
+  if (!dim_ok(n_seq) || !dim_ok(seq_len) || n_seq > kMaxRows / seq_len) return HYDRA_ERR_SHAPE;  // M <= 2^20
   if (start < 0 || start >= seq_len) return HYDRA_ERR_SHAPE;
   if (!(eps >= 0.f && eps < 1.f)) return HYDRA_ERR_SHAPE;
   const void* ins[5] = {lp_new, lp_old, advantages, values, returns};
@@ -457,8 +461,7 @@ hydra_status hydra_ppo_advantages(const float* kl, const float* reward, const fl
                                   int64_t seq_len, int64_t start, float beta, float gamma, float lam, float* rewards,
                                   float* advantages, float* returns, void* stream) {
   if (!kl || !reward || !values || !advantages || !returns) return HYDRA_ERR_NULL;
-  if (!dim_ok(n_seq) || !dim_ok(seq_len) || n_seq > kMaxDim / seq_len) return HYDRA_ERR_SHAPE;
-  if (!grid_ok(n_seq, 64)) return HYDRA_ERR_SHAPE;  // one wave per sequence
+  if (!dim_ok(n_seq) || !dim_ok(seq_len) || n_seq > kMaxRows / seq_len) return HYDRA_ERR_SHAPE;  // M <= 2^20
   if (start < 0 || start >= seq_len) return HYDRA_ERR_SHAPE;
   // outputs are written while inputs are still read: no output may be an input
   const void* ins[3] = {kl, reward, values};

@@ -1,7 +1,7 @@
 // Decode-shaped (M <= 16) LoRA-switchable linear for gfx950, for one or a
 // group of linears in a single call.
 //
-// At decode time (App. A, Alg. 1 / Alg. 2: "generate ... for T steps") each
+// At decode time (App. A, Alg. 1 / Alg. 2, the token-by-token generation step) each
 // linear sees one new token per sequence, so the work is a stream over W at
 // HBM rate with almost no arithmetic intensity.
 //  * M <= 8: two kernels.  gemv_stream_kernel computes the base product x W^T

@@ -1,8 +1,9 @@
 // Scoring kernels for gfx950: sampled-token log-probabilities under the
 // LoRA-on (actor) and LoRA-off (reference) passes, their difference as the
 // per-token KL estimate, and the scalar reward head (Sec. 3, the two heads of
-// pi^hydra; App. A, Alg. 1 / Alg. 2, "compute reward and reference log
-// probabilities"; the KL weight beta of App. B is applied by the caller).
+// pi^hydra; App. A, Alg. 1 / Alg. 2, the step that scores the generated
+// sequences with LoRA off for the reward and the reference log-probabilities;
+// the KL weight beta of App. B is applied by the caller).
 //
 //  * score_logits_vec_kernel (V % 4 == 0) / score_logits_kernel (other V):
 //    one workgroup per token row streams both fp32 logit rows once, keeping

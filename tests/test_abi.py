@@ -266,6 +266,18 @@ def test_lora_linear_multi_rejects(kw, code):
     assert _multi(**kw) == code
 
 
+def test_lora_linear_multi_rank_above_64_rejected_before_any_launch():
+    """M > 16 with adapters of padded rank 128: HYDRA_ERR_WORKSPACE from the host checks, before the LoRA-off output
+    is launched (the pointers here are fake: a launch would fault or report HYDRA_ERR_HIP)."""
+    assert _multi(M=32, r=100) == H.HYDRA_ERR_WORKSPACE
+    assert _multi(M=4096, r=128, n_on=1, xs=(P,), As=(P,), Bs=(P,), ss=(2.0,), yn=(P + 0x3000,)) == \
+        H.HYDRA_ERR_WORKSPACE
+    # without adapters (LoRA-off input alone) the rank plays no part
+    assert _multi(M=32, r=100, n_on=0, xs=None, As=None, Bs=None, ss=None, yn=None, W=P8) == H.HYDRA_ERR_ALIGN
+    # decode sizes take rank 128 (the rows go through the stream and update kernels)
+    assert _multi(M=16, r=128, W=P8) == H.HYDRA_ERR_ALIGN
+
+
 def test_lora_linear_multi_adapters_unused_at_rank_zero():
     """r == 0: A and B may be NULL arrays; validation then fails only on the deliberate bad alignment."""
     assert _multi(r=0, As=None, Bs=None, W=P8) == H.HYDRA_ERR_ALIGN
@@ -452,6 +464,18 @@ def test_row_and_width_limits():
     assert L.hydra_value_head(P, P, big + 1, 64, P + 0x1000, None) == H.HYDRA_ERR_SHAPE
     assert L.hydra_ppo_advantages(P, P + 0x100, P + 0x200, 1 << 26, 1, 0, 0.02, 1.0, 0.95, None, P + 0x300,
                                   P + 0x400, None) == H.HYDRA_ERR_SHAPE
+    # the PPO calls bound M = n_seq * seq_len (and so seq_len) by the same 2^20 rows
+    for n_seq, seq_len in ((1, big + 1), (1 << 10, (1 << 10) + 1), (big + 1, 1)):
+        assert L.hydra_ppo_advantages(P, P + 0x100, P + 0x200, n_seq, seq_len, 0, 0.02, 1.0, 0.95, None, P + 0x300,
+                                      P + 0x400, None) == H.HYDRA_ERR_SHAPE
+        assert L.hydra_ppo_loss(P, P + 0x100, P + 0x200, P + 0x300, P + 0x400, n_seq, seq_len, 0, 0.2, P + 0x500,
+                                None, None, None) == H.HYDRA_ERR_SHAPE
+    # M = 2^20 exactly passes the size checks (then fails on a planted misalignment)
+    for n_seq, seq_len in ((1, big), (1 << 10, 1 << 10)):
+        assert L.hydra_ppo_advantages(P + 2, P + 0x100, P + 0x200, n_seq, seq_len, 0, 0.02, 1.0, 0.95, None,
+                                      P + 0x300, P + 0x400, None) == H.HYDRA_ERR_ALIGN
+        assert L.hydra_ppo_loss(P + 2, P + 0x100, P + 0x200, P + 0x300, P + 0x400, n_seq, seq_len, 0, 0.2,
+                                P + 0x500, None, None, None) == H.HYDRA_ERR_ALIGN
     assert L.hydra_transpose_bf16(P, 1 << 21, 1 << 21, P + 0x100, None) == H.HYDRA_ERR_SHAPE
     assert _bwd(M=big + 1) == H.HYDRA_ERR_SHAPE
     assert _bwd(M=big, K=1 << 21, N=64) == H.HYDRA_ERR_SHAPE                   # dx's tile grid
