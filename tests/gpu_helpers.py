@@ -21,6 +21,12 @@ def say(*a):
     sys.stdout.flush()
 
 
+def row_chunks(M, size=512):
+    """Row blocks [i, i + size) covering 0..M: the oracle is evaluated block by block on full-size cases so that
+    its float64 intermediates stay small."""
+    return [np.arange(i, min(i + size, M)) for i in range(0, M, size)]
+
+
 def dev_bf16(u16, device):
     import torch
     return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).to(device)

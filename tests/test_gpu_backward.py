@@ -103,17 +103,13 @@ def test_backward_b_zero(dev):
 
 @pytest.mark.parametrize("proj", ["q", "gate", "down"])
 def test_backward_llama_layer_full_size(proj, dev):
-    """The Llama-7B layer's backward at M = 2048, rank 16 (the bench's shapes): dA and dB whole, dx on
-    sampled rows (each row of dx depends on its own row of dy only)."""
+    """The Llama-7B layer's backward at M = 2048, rank 16 (the bench's shapes): dx, dA and dB compared whole."""
     say("backward full size", proj)
     cases = {b.lin.name: b for b in WL.make("backward_layer")}
     case = cases[proj]
     c = case.lin
     dx, dA, dB = _run(case, dev)
-    rows = np.random.Generator(np.random.PCG64(11)).choice(c.M, 24, replace=False)
-    rows[:2] = [0, c.M - 1]
-    e_dx, _, _ = lora_linear_backward_ref(c.x[rows], c.W, c.A, c.B, c.s, case.dy[rows])
-    assert_rel(dx[rows], e_dx, "dx rows")
-    _, e_dA, e_dB = lora_linear_backward_ref(c.x, c.W, c.A, c.B, c.s, case.dy)
+    e_dx, e_dA, e_dB = lora_linear_backward_ref(c.x, c.W, c.A, c.B, c.s, case.dy)
+    assert_rel(dx, e_dx, "dx")
     assert_rel(dA, e_dA, "dA")
     assert_rel(dB, e_dB, "dB")

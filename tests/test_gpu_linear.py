@@ -103,22 +103,16 @@ def test_decode_qkvo_full(dev):
         assert_rel(y_on, e_on, f"{c.name} y_on")
 
 
-def test_prefill_layer_full_size_sampled_rows(dev):
-    """Prefill, M = 2048: all seven linears of one Llama-7B layer, r = 16.
-
-    The GPU computes every row in the launch configuration the bench times;
-    the oracle checks 40 sampled rows (first, last, and random) of each.
-    """
+def test_prefill_layer_full_size_every_row(dev):
+    """Prefill, M = 2048: all seven linears of one Llama-7B layer, r = 16, in the launch configuration the bench
+    times; every row of both outputs is compared with the oracle."""
     cases = WL.make("prefill_layer")
-    rng = np.random.default_rng(3)
-    rows = np.unique(np.concatenate([[0, 1, 127, 128, 2047], rng.integers(0, 2048, 35)]))
     for c in cases:
         say("prefill", c.name, c.M, c.K, c.N, c.r)
         y_off, y_on = _run(c, dev)
-        e_off, e_on = lora_linear_ref(c.x[rows], c.W, c.A, c.B, c.s)
-        assert_rel(y_off[rows], e_off, f"{c.name} y_off")
-        assert_rel(y_on[rows], e_on, f"{c.name} y_on")
-        assert np.all(np.isfinite(y_off)) and np.all(np.isfinite(y_on))
+        e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+        assert_rel(y_off, e_off, f"{c.name} y_off")
+        assert_rel(y_on, e_on, f"{c.name} y_on")
 
 
 def _group_run(cases, device, want_on=None):

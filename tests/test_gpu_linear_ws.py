@@ -72,29 +72,23 @@ def test_linear_ws_b_zero_is_lora_off(dev):
     assert np.array_equal(y_off, y_on)
 
 
-def test_linear_ws_rank128_gate_projection_sampled_rows(dev):
-    """The Llama-7B gate projection (4096 -> 11008) over 2048 tokens at the paper's rank 128, sampled rows."""
+def test_linear_ws_rank128_gate_projection_every_row(dev):
+    """The Llama-7B gate projection (4096 -> 11008) over 2048 tokens at the paper's rank 128, every row."""
     say("linear_ws gate r=128 full size")
     c = WL.gen_linear(952, 2048, 4096, 11008, 128)
     y_off, y_on = _run(c, dev)
-    rng = np.random.default_rng(5)
-    rows = np.unique(np.concatenate([[0, 127, 128, 2047], rng.integers(0, 2048, 28)]))
-    e_off, e_on = lora_linear_ref(c.x[rows], c.W, c.A, c.B, c.s)
-    assert_rel(y_off[rows], e_off, "y_off")
-    assert_rel(y_on[rows], e_on, "y_on")
-    assert np.all(np.isfinite(y_off)) and np.all(np.isfinite(y_on))
+    e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+    assert_rel(y_off, e_off, "y_off")
+    assert_rel(y_on, e_on, "y_on")
 
 
 @pytest.mark.parametrize("proj", ["q", "fc1", "fc2"])
 def test_opt13b_layer_rank128_full_size(proj, dev):
     """OPT-1.3b at the paper's rank 128 (App. B), mini-batch 8 x 512 = 4096 tokens: 2048 -> 2048, 2048 -> 8192 and
-    8192 -> 2048 through the pre-pass GEMM; the oracle checks sampled rows of both outputs."""
+    8192 -> 2048 through the pre-pass GEMM; every row of both outputs is compared with the oracle."""
     say("opt13b layer r128", proj)
     c = {x.name: x for x in WL.make("opt13b_layer_r128")}[proj]
     y_off, y_on = _run(c, dev)
-    rows = np.random.default_rng(8).choice(c.M, 24, replace=False)
-    rows[:2] = [0, c.M - 1]
-    e_off, e_on = lora_linear_ref(c.x[rows], c.W, c.A, c.B, c.s)
-    assert_rel(y_off[rows], e_off, "y_off rows")
-    assert_rel(y_on[rows], e_on, "y_on rows")
-    assert np.all(np.isfinite(y_off)) and np.all(np.isfinite(y_on))
+    e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+    assert_rel(y_off, e_off, "y_off")
+    assert_rel(y_on, e_on, "y_on")

@@ -8,7 +8,7 @@ import pytest
 import paper_2309_00754_amd as H
 import workloads as WL
 from oracle import reward_ref, score_head_ref, score_logits_ref
-from gpu_helpers import assert_abs, assert_rel, dev, dev_bf16, host, say
+from gpu_helpers import assert_abs, assert_rel, dev, dev_bf16, host, row_chunks, say
 
 pytestmark = pytest.mark.gpu
 
@@ -112,20 +112,22 @@ def test_score_workspace_contents_do_not_matter(dev):
         assert np.array_equal(host(out[k]), clean[k]), k
 
 
-def test_two_head_score_full_size_sampled_rows(dev):
-    """M = 2048 tokens (4 x 512), K = 4096, V = 32000, r = 16: the full CLM head on
-    every row in the bench's launch configuration; the oracle checks 48 sampled
-    rows including each sequence's last row, and the reward exactly."""
+def _assert_score_every_row(c, g):
+    """Every row of lp_on, lp_off, kl and both lse against the oracle (evaluated in row blocks), and every reward."""
+    for rows in row_chunks(c.M):
+        e = score_head_ref(c.h[rows], c.W_lm, c.A, c.B, c.s, c.ids[rows])
+        for k in ("lp_on", "lp_off", "kl", "lse_on", "lse_off"):
+            assert_abs(g[k][rows], e[k], f"{k} rows {rows[0]}..{rows[-1]}")
+    assert_rel(g["reward"], reward_ref(c.h, c.w_rm, c.n_seq, c.seq_len), "reward")
+
+
+def test_two_head_score_full_size_every_row(dev):
+    """M = 2048 tokens (4 x 512), K = 4096, V = 32000, r = 16: the full CLM head in the bench's launch
+    configuration; every row and every reward compared with the oracle."""
     c = WL.make("two_head_score")
     say("two_head_score full", c.M, c.K, c.V, c.r)
     g = _score(c, dev)
-    rng = np.random.default_rng(4)
-    lasts = [b * c.seq_len + c.seq_len - 1 for b in range(c.n_seq)]
-    rows = np.unique(np.concatenate([[0, 1, 127, 128], lasts, rng.integers(0, c.M, 40)]))
-    e = score_head_ref(c.h[rows], c.W_lm, c.A, c.B, c.s, c.ids[rows], c.w_rm, c.n_seq, c.seq_len, rows=rows)
-    for k in ("lp_on", "lp_off", "kl", "lse_on", "lse_off"):
-        assert_abs(g[k][rows], e[k], k)
-    assert_rel(g["reward"], e["reward"], "reward")
+    _assert_score_every_row(c, g)
     assert np.all(np.isfinite(g["lp_on"])) and np.all(np.isfinite(g["kl"]))
     # every row: the log-sum-exp dominates the sampled logit, so lp <= 0
     assert np.all(g["lp_on"] <= 1e-6) and np.all(g["lp_off"] <= 1e-6)
@@ -182,17 +184,11 @@ def test_score_logits_identities(dev):
     assert gb["err"] == 1 and math.isnan(gb["lp_on"][1]) and not math.isnan(gb["lp_on"][0])
 
 
-def test_opt13b_score_rank128_sampled_rows(dev):
+def test_opt13b_score_rank128_every_row(dev):
     """OPT-1.3b's CLM head (K = 2048, V = 50272: a ragged last column tile) at rank 128 over 8 x 512 tokens, with the
-    reward head; the oracle checks sampled rows and every reward."""
+    reward head; every row and every reward compared with the oracle."""
     c = WL.make("opt13b_score_r128")
     say("opt13b score r128", c.M, c.K, c.V, c.r)
     g = _score(c, dev)
-    rng = np.random.default_rng(9)
-    lasts = [b * c.seq_len + c.seq_len - 1 for b in range(c.n_seq)]
-    rows = np.unique(np.concatenate([[0, 255, 256], lasts, rng.integers(0, c.M, 24)]))
-    e = score_head_ref(c.h[rows], c.W_lm, c.A, c.B, c.s, c.ids[rows], c.w_rm, c.n_seq, c.seq_len, rows=rows)
-    for k in ("lp_on", "lp_off", "kl", "lse_on", "lse_off"):
-        assert_abs(g[k][rows], e[k], k)
-    assert_rel(g["reward"], e["reward"], "reward")
-    assert np.all(np.isfinite(g["lp_on"])) and g["err"] == 0
+    _assert_score_every_row(c, g)
+    assert g["err"] == 0
