@@ -225,6 +225,37 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
                          float* lp_on, float* lp_off, float* kl, float* reward, float* lse_on, float* lse_off,
                          void* workspace, size_t workspace_bytes, int32_t* err_flag, void* stream);
 
+/* Largest workspace that hydra_score_noalloc serves from its own device scratch (48 MiB). */
+#define HYDRA_SCORE_NOALLOC_MAX_BYTES (48u << 20)
+
+/*
+ * hydra_score_noalloc -- hydra_score without a caller workspace, for callers
+ * that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  The call itself allocates
+ * nothing (no hipMalloc, hipFree or allocating library routine): the
+ * workspace lives in a file-scope device array of the library,
+ * HYDRA_SCORE_NOALLOC_MAX_BYTES long, one copy on each GPU the library runs
+ * on, held until the process ends.  Its device address is looked up once per
+ * device (on the first call there) and kept.
+ *
+ * Arguments, outputs and errors as in hydra_score, less `workspace` and
+ * `workspace_bytes`; the caller still passes every input and output.
+ * Returns HYDRA_ERR_WORKSPACE (before any HIP call) when
+ * hydra_score_workspace_bytes(n_seq * seq_len, V) exceeds
+ * HYDRA_SCORE_NOALLOC_MAX_BYTES (for example M = 2048, V = 32000 needs 21.5 MB
+ * and fits; M = 4096, V = 50272 needs 44.6 MB and fits), and HYDRA_ERR_HIP if
+ * the scratch's address cannot be found.  Results have the bits of hydra_score.
+ * Every call on one GPU shares that GPU's scratch: calls that overlap in time
+ * on one GPU (two streams, two host threads) race and give undefined results;
+ * serialise them.  The scratch keeps the last call's contents; no call needs
+ * it cleared.
+ */
+hydra_status hydra_score_noalloc(const uint16_t* h, const uint16_t* W_lm, const uint16_t* A, const uint16_t* B,
+                                 float s, const int32_t* tokens, const uint16_t* w_rm,
+                                 int64_t n_seq, int64_t seq_len, int64_t K, int64_t V, int64_t r,
+                                 float* lp_on, float* lp_off, float* kl, float* reward, float* lse_on,
+                                 float* lse_off, int32_t* err_flag, void* stream);
+
 /*
  * hydra_score_logits -- the scoring epilogue alone, from materialised logits.
  * Defined by: App. A Alg. 2 (reference log-probabilities), Sec. 2 Stage 3

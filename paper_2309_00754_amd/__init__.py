@@ -14,6 +14,7 @@ from ._binding import (  # noqa: F401
     HYDRA_MAX_ADAPTERS,
     HYDRA_MAX_GROUP,
     HYDRA_MAX_RANK,
+    HYDRA_SCORE_NOALLOC_MAX_BYTES,
     HYDRA_OK,
     HydraError,
     HydraLibraryMissing,
@@ -28,6 +29,7 @@ from ._binding import (  # noqa: F401
     hydra_ppo_advantages,
     hydra_ppo_loss,
     hydra_score,
+    hydra_score_noalloc,
     hydra_score_logits,
     hydra_score_workspace_bytes,
     hydra_transpose_bf16,

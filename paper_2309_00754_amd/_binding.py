@@ -25,6 +25,7 @@ HYDRA_ERR_HIP = -6
 HYDRA_MAX_RANK = 128
 HYDRA_MAX_GROUP = 8
 HYDRA_MAX_ADAPTERS = 4
+HYDRA_SCORE_NOALLOC_MAX_BYTES = 48 << 20
 
 # Every symbol include/hydra.h declares.
 EXPORTED = (
@@ -35,6 +36,7 @@ EXPORTED = (
     "hydra_lora_linear_multi",
     "hydra_score_workspace_bytes",
     "hydra_score",
+    "hydra_score_noalloc",
     "hydra_score_logits",
     "hydra_value_head",
     "hydra_ppo_advantages",
@@ -92,6 +94,9 @@ def lib() -> ctypes.CDLL:
     L.hydra_score.argtypes = [_vp, _vp, _vp, _vp, _f32, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
                               _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _vp]
     L.hydra_score.restype = ctypes.c_int
+    L.hydra_score_noalloc.argtypes = [_vp, _vp, _vp, _vp, _f32, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
+                                      _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+    L.hydra_score_noalloc.restype = ctypes.c_int
     L.hydra_score_logits.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
     L.hydra_score_logits.restype = ctypes.c_int
     L.hydra_value_head.argtypes = [_vp, _vp, _i64, _i64, _vp, _vp]
@@ -329,6 +334,33 @@ def hydra_score(h, W_lm, A, B, s: float, tokens, w_rm, n_seq: int, seq_len: int,
                            _ptr(lse_on), _ptr(lse_off), _ptr(workspace), workspace.numel(), _ptr(err_flag),
                            _stream_handle(stream))
     _check(st, "hydra_score")
+
+
+def hydra_score_noalloc(h, W_lm, A, B, s: float, tokens, w_rm, n_seq: int, seq_len: int,
+                        lp_on, lp_off, kl, reward=None, lse_on=None, lse_off=None, err_flag=None,
+                        stream=None) -> None:
+    """hydra_score with its workspace in the library's own device scratch (no allocation by the call)."""
+    torch = _torch()
+    bf = _bf16_types()
+    M, K = h.shape
+    V = W_lm.shape[0]
+    r = 0 if A is None else A.shape[0]
+    if M != n_seq * seq_len:
+        raise ValueError("h rows must equal n_seq * seq_len")
+    _need(h, "h", bf)
+    _need(W_lm, "W_lm", bf, (V, K))
+    _need(A, "A", bf, (r, K))
+    _need(B, "B", bf, (V, r))
+    _need(tokens, "tokens", (torch.int32,), (M,))
+    _need(w_rm, "w_rm", bf, (K,))
+    for name, t in (("lp_on", lp_on), ("lp_off", lp_off), ("kl", kl), ("lse_on", lse_on), ("lse_off", lse_off)):
+        _need(t, name, (torch.float32,), (M,))
+    _need(reward, "reward", (torch.float32,), (n_seq,))
+    _need(err_flag, "err_flag", (torch.int32,), (1,))
+    st = lib().hydra_score_noalloc(_ptr(h), _ptr(W_lm), _ptr(A), _ptr(B), float(s), _ptr(tokens), _ptr(w_rm),
+                                   int(n_seq), int(seq_len), K, V, r, _ptr(lp_on), _ptr(lp_off), _ptr(kl),
+                                   _ptr(reward), _ptr(lse_on), _ptr(lse_off), _ptr(err_flag), _stream_handle(stream))
+    _check(st, "hydra_score_noalloc")
 
 
 def hydra_score_logits(logits_on, logits_off, tokens, lp_on, lp_off, kl,

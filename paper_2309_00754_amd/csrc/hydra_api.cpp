@@ -5,6 +5,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "hydra_internal.h"
 
 namespace {
@@ -275,11 +277,15 @@ hydra_status hydra_score_workspace_bytes(int64_t M, int64_t V, size_t* bytes) {
   return HYDRA_OK;
 }
 
-hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t* A, const uint16_t* B, float s,
+}  // extern "C"
+
+namespace {
+
+// Argument checks of the fused scoring pass, except the workspace (host only).
+hydra_status score_check(const uint16_t* h, const uint16_t* W_lm, const uint16_t* A, const uint16_t* B,
                          const int32_t* tokens, const uint16_t* w_rm, int64_t n_seq, int64_t seq_len, int64_t K,
                          int64_t V, int64_t r, float* lp_on, float* lp_off, float* kl, float* reward,
-                         float* lse_on, float* lse_off, void* workspace, size_t workspace_bytes, int32_t* err_flag,
-                         void* stream) {
+                         float* lse_on, float* lse_off, int32_t* err_flag) {
   if (!h || !W_lm || !tokens || !lp_on || !lp_off || !kl) return HYDRA_ERR_NULL;
   if (!dim_ok(n_seq) || !dim_ok(seq_len) || !dim_ok(K) || !dim_ok(V) || (K % 8) != 0 || K > kMaxK)
     return HYDRA_ERR_SHAPE;
@@ -290,16 +296,22 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
     return HYDRA_ERR_SHAPE;
   if (r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
   if (r > 0 && (!A || !B)) return HYDRA_ERR_NULL;
-  if (!workspace) return HYDRA_ERR_WORKSPACE;
-  if (workspace_bytes < score_ws_bytes(M, V)) return HYDRA_ERR_WORKSPACE;
-  if (!aligned(h, 16) || !aligned(W_lm, 16) || !aligned(workspace, 16)) return HYDRA_ERR_ALIGN;
+  if (!aligned(h, 16) || !aligned(W_lm, 16)) return HYDRA_ERR_ALIGN;
   if (r > 0 && (!aligned(A, 16) || !aligned(B, 2))) return HYDRA_ERR_ALIGN;
   if (!aligned(tokens, 4) || !aligned(lp_on, 4) || !aligned(lp_off, 4) || !aligned(kl, 4)) return HYDRA_ERR_ALIGN;
   if ((reward && !aligned(reward, 4)) || (lse_on && !aligned(lse_on, 4)) || (lse_off && !aligned(lse_off, 4)) ||
       (err_flag && !aligned(err_flag, 4)) || (w_rm && !aligned(w_rm, 2)))
     return HYDRA_ERR_ALIGN;
+  return HYDRA_OK;
+}
 
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+// The fused scoring pass's launches over a checked workspace of at least
+// score_ws_bytes(M, V) bytes, 16-byte aligned.
+hydra_status score_launch(const uint16_t* h, const uint16_t* W_lm, const uint16_t* A, const uint16_t* B, float s,
+                          const int32_t* tokens, const uint16_t* w_rm, int64_t n_seq, int64_t seq_len, int64_t K,
+                          int64_t V, int64_t r, float* lp_on, float* lp_off, float* kl, float* reward,
+                          float* lse_on, float* lse_off, void* workspace, int32_t* err_flag, hipStream_t st) {
+  const int64_t M = n_seq * seq_len;
   float4* part = reinterpret_cast<float4*>(workspace);
   float* zt = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + score_zt_offset(M, V));
   uint16_t* ts = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(workspace) + score_ts_offset(M, V));
@@ -346,6 +358,85 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
   c.seq_len = int(seq_len);
   c.K = int(K);
   return from_hip(hydra::launch_score_combine(c, st));
+}
+
+// Device scratch of hydra_score_noalloc: a file-scope device array, one copy
+// on every GPU the library runs on, held until the process ends.  Host code
+// never passes the array's name to a kernel (on the host it is only a
+// stand-in for the symbol): the device address comes from
+// hipGetSymbolAddress, taken once per device with that device current, and
+// only that address is used.
+__device__ __align__(256) uint8_t scratch[HYDRA_SCORE_NOALLOC_MAX_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+// Device address of `scratch` on the device of `stream` (the current device for
+// the null stream).
+hipError_t scratch_address(hipStream_t stream, void** out) {
+  int cur = -1;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return e;
+  int dev = cur;
+  if (stream != nullptr) {
+    hipDevice_t d = 0;
+    e = hipStreamGetDevice(stream, &d);
+    if (e != hipSuccess) return e;
+    dev = int(d);
+  }
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::call_once(g_scratch_once[dev], [dev, cur]() {
+    hipError_t err = hipSuccess;
+    if (dev != cur) err = hipSetDevice(dev);
+    void* p = nullptr;
+    if (err == hipSuccess) err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) {
+      const hipError_t back = hipSetDevice(cur);
+      if (err == hipSuccess) err = back;
+    }
+    g_scratch_ptr[dev] = err == hipSuccess ? p : nullptr;
+    g_scratch_err[dev] = err;
+  });
+  if (g_scratch_err[dev] != hipSuccess) return g_scratch_err[dev];
+  *out = g_scratch_ptr[dev];
+  return *out != nullptr ? hipSuccess : hipErrorInvalidSymbol;
+}
+
+}  // namespace
+
+extern "C" {
+
+hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t* A, const uint16_t* B, float s,
+                         const int32_t* tokens, const uint16_t* w_rm, int64_t n_seq, int64_t seq_len, int64_t K,
+                         int64_t V, int64_t r, float* lp_on, float* lp_off, float* kl, float* reward,
+                         float* lse_on, float* lse_off, void* workspace, size_t workspace_bytes, int32_t* err_flag,
+                         void* stream) {
+  const hydra_status chk = score_check(h, W_lm, A, B, tokens, w_rm, n_seq, seq_len, K, V, r, lp_on, lp_off, kl,
+                                       reward, lse_on, lse_off, err_flag);
+  if (chk != HYDRA_OK) return chk;
+  if (!workspace) return HYDRA_ERR_WORKSPACE;
+  if (workspace_bytes < score_ws_bytes(n_seq * seq_len, V)) return HYDRA_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return HYDRA_ERR_ALIGN;
+  return score_launch(h, W_lm, A, B, s, tokens, w_rm, n_seq, seq_len, K, V, r, lp_on, lp_off, kl, reward, lse_on,
+                      lse_off, workspace, err_flag, reinterpret_cast<hipStream_t>(stream));
+}
+
+hydra_status hydra_score_noalloc(const uint16_t* h, const uint16_t* W_lm, const uint16_t* A, const uint16_t* B,
+                                 float s, const int32_t* tokens, const uint16_t* w_rm, int64_t n_seq,
+                                 int64_t seq_len, int64_t K, int64_t V, int64_t r, float* lp_on, float* lp_off,
+                                 float* kl, float* reward, float* lse_on, float* lse_off, int32_t* err_flag,
+                                 void* stream) {
+  const hydra_status chk = score_check(h, W_lm, A, B, tokens, w_rm, n_seq, seq_len, K, V, r, lp_on, lp_off, kl,
+                                       reward, lse_on, lse_off, err_flag);
+  if (chk != HYDRA_OK) return chk;
+  if (score_ws_bytes(n_seq * seq_len, V) > size_t(HYDRA_SCORE_NOALLOC_MAX_BYTES)) return HYDRA_ERR_WORKSPACE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  void* ws = nullptr;
+  if (scratch_address(st, &ws) != hipSuccess) return HYDRA_ERR_HIP;
+  return score_launch(h, W_lm, A, B, s, tokens, w_rm, n_seq, seq_len, K, V, r, lp_on, lp_off, kl, reward, lse_on,
+                      lse_off, ws, err_flag, st);
 }
 
 hydra_status hydra_value_head(const uint16_t* h, const uint16_t* w_v, int64_t M, int64_t K, float* values,

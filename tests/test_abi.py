@@ -106,6 +106,41 @@ def test_score_rejects(kw, code):
     assert _score(**kw) == code
 
 
+def _score_na(h=P, W=P, A=P, B=P, tok=P, w_rm=P, n_seq=4, seq_len=8, K=64, V=1000, r=8,
+              lp_on=P, lp_off=P, kl=P, reward=P, lse_on=None, lse_off=None, err=None):
+    return H.lib().hydra_score_noalloc(h, W, A, B, 2.0, tok, w_rm, n_seq, seq_len, K, V, r, lp_on, lp_off, kl,
+                                       reward, lse_on, lse_off, err, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(h=None), H.HYDRA_ERR_NULL),
+    (dict(tok=None), H.HYDRA_ERR_NULL),
+    (dict(A=None), H.HYDRA_ERR_NULL),
+    (dict(n_seq=0), H.HYDRA_ERR_SHAPE),
+    (dict(K=12), H.HYDRA_ERR_SHAPE),
+    (dict(r=129), H.HYDRA_ERR_SHAPE),
+    (dict(h=P8), H.HYDRA_ERR_ALIGN),
+    (dict(lp_on=P + 2), H.HYDRA_ERR_ALIGN),
+    # beyond the scratch: 8192 tokens over a 50272-entry vocabulary need 86 MB of workspace
+    (dict(n_seq=16, seq_len=512, V=50272, K=2048), H.HYDRA_ERR_WORKSPACE),
+    (dict(n_seq=16, seq_len=512, V=50272, K=2048, h=P8), H.HYDRA_ERR_ALIGN),   # argument errors come first
+])
+def test_score_noalloc_rejects(kw, code):
+    """Every argument error and the scratch limit are reported before any HIP call (the pointers are fake)."""
+    assert _score_na(**kw) == code
+
+
+def test_score_noalloc_limit_covers_the_scoring_workloads():
+    """The scratch holds the workspace of the Llama-7B (2048 x 32000) and OPT-1.3b (4096 x 50272) scoring passes;
+    calls up to the limit pass the size check (then fail on a planted misalignment)."""
+    cap = H.HYDRA_SCORE_NOALLOC_MAX_BYTES
+    assert cap == 48 << 20
+    assert H.hydra_score_workspace_bytes(2048, 32000) <= cap
+    assert H.hydra_score_workspace_bytes(4096, 50272) <= cap
+    assert _score_na(n_seq=8, seq_len=512, V=50272, K=2048, h=P8) == H.HYDRA_ERR_ALIGN
+    assert H.hydra_score_workspace_bytes(8192, 50272) > cap
+
+
 def _ws(M, V):
     # one float4 partial per (row, 256-column tile), two floats per row (the
     # gathered token logits), then, 16-byte aligned, 2 x 128 bf16 per row (the
