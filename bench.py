@@ -123,17 +123,29 @@ def main():
         launches.append(("decode", "qkvo", fn, sum(lin_flops(c.M, c.K, c.N, c.r) for c in dec),
                          sum(lin_bytes(c.M, c.K, c.N, c.r) for c in dec)))
     if "prefill" in parts:
+        # the seven linears as a layer issues them: q/k/v share their input (one group call), then o, then
+        # gate/up (one group call), then down; every call computes both outputs of each of its linears
         xs = {}
         host["prefill"] = WL.make("prefill_layer")
+        dev_in = {}
         for c in host["prefill"]:
             if id(c.x) not in xs:
                 xs[id(c.x)] = bf(c.x)
-            x = xs[id(c.x)]
-            W, A, B = bf(c.W), bf(c.A), bf(c.B)
-            yo = torch.empty(c.M, c.N, device=dev)
-            yn = torch.empty(c.M, c.N, device=dev)
-            fn = (lambda x=x, W=W, A=A, B=B, s=c.s, yo=yo, yn=yn: H.hydra_lora_linear(x, W, A, B, s, yo, yn))
-            launches.append(("prefill", c.name, fn, lin_flops(c.M, c.K, c.N, c.r), lin_bytes(c.M, c.K, c.N, c.r)))
+            dev_in[c.name] = (c, xs[id(c.x)], bf(c.W), bf(c.A), bf(c.B), torch.empty(c.M, c.N, device=dev),
+                              torch.empty(c.M, c.N, device=dev))
+        for names in (("q", "k", "v"), ("o",), ("gate", "up"), ("down",)):
+            mem = [dev_in[n] for n in names]
+            if len(mem) == 1:
+                c, x, W, A, B, yo, yn = mem[0]
+                fn = (lambda x=x, W=W, A=A, B=B, s=c.s, yo=yo, yn=yn: H.hydra_lora_linear(x, W, A, B, s, yo, yn))
+            else:
+                fn = (lambda mem=mem: H.hydra_lora_linear_group([m[1] for m in mem], [m[2] for m in mem],
+                                                                [m[3] for m in mem], [m[4] for m in mem],
+                                                                [m[0].s for m in mem], [m[5] for m in mem],
+                                                                [m[6] for m in mem]))
+            launches.append(("prefill", "_".join(names), fn,
+                             sum(lin_flops(m[0].M, m[0].K, m[0].N, m[0].r) for m in mem),
+                             sum(lin_bytes(m[0].M, m[0].K, m[0].N, m[0].r) for m in mem)))
     sc = None
     if "score" in parts:
         sc = host["score"] = WL.make("two_head_score")

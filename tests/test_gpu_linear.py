@@ -211,8 +211,9 @@ def test_group_gemm_lora_off_member(dev):
 
 @pytest.mark.parametrize("names", [("q", "k", "v"), ("gate", "up")])
 def test_group_prefill_layer_full_size(names, dev):
-    """The prefill layer's linears that share an input (q/k/v; gate/up) as one group call: each member has the bits
-    of its single call at the full Llama-7B size."""
+    """The prefill layer's linears that share an input (q/k/v: 768 tiles, three rounds of the persistent launch;
+    gate/up: 1376 tiles, a last round of 96) as one group call: each member has the bits of its single call, and
+    every row of both outputs matches the oracle."""
     say("group prefill", names)
     cases = {c.name: c for c in WL.make("prefill_layer")}
     group = [cases[n] for n in names]
@@ -220,6 +221,30 @@ def test_group_prefill_layer_full_size(names, dev):
     for i, c in enumerate(group):
         so, sn = _run(c, dev)
         assert np.array_equal(go[i], so) and np.array_equal(gn[i], sn), c.name
+        e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+        assert_rel(go[i], e_off, f"group {c.name} y_off")
+        assert_rel(gn[i], e_on, f"group {c.name} y_on")
+
+
+@pytest.mark.parametrize("M,K,N,r,G", [
+    (1000, 136, 1040, 16, 8),   # 320 tiles: two rounds, the second of 64 (eight per XCD)
+    (2050, 72, 1300, 9, 3),     # 306 tiles, a one-row last row tile; last round of 50 (not a multiple of 8)
+    (520, 200, 2100, 32, 7),    # rank 32, 315 tiles
+])
+def test_group_gemm_several_rounds(M, K, N, r, G, dev):
+    """More tiles than CUs: the persistent workgroups run several rounds, each one streaming the next tile's slabs
+    through the ring while the current tile's epilogue runs; members alternate scales and one has no adapter."""
+    say("group gemm rounds", M, K, N, r, G)
+    cases = [WL.gen_linear(700 + 10 * G + i, M, K, N, r, s=[2.0, -0.5, 1.5][i % 3]) for i in range(G)]
+    want_on = [i != 1 for i in range(G)]
+    go, gn = _group_run(cases, dev, want_on=want_on)
+    for i, c in enumerate(cases):
+        e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+        assert_rel(go[i], e_off, f"member {i} y_off")
+        if want_on[i]:
+            assert_rel(gn[i], e_on, f"member {i} y_on")
+        else:
+            assert gn[i] is None
 
 
 def test_opt13b_decode_rank128_group(dev):
