@@ -6,7 +6,7 @@ rank 16, scale 2), i.e. the inference stage of one PPO iteration for one
 decoder layer plus the heads:
 
   * decode: one generation step of the four attention projections, M = 4
-    (hydra_lora_linear_group, bandwidth-bound kernels), both LoRA-off and LoRA-on outputs;
+    (hydra_lora_linear_group_ws: one bandwidth-bound launch), both LoRA-off and LoRA-on outputs;
   * prefill: the seven LoRA linears of a layer over all 2048 tokens
     (hydra_lora_linear, dual-output MFMA GEMM), both outputs;
   * score: the CLM head with LoRA on and off, sampled-token log-probabilities,
@@ -19,8 +19,8 @@ the launch stream marks the start of each part of the step (and the step's
 end), so each part's time covers its launches back to back; a separate detail
 pass afterwards brackets every launch with its own pair of events (those
 figures include the events' own overhead, a few microseconds each).  The
-decode step's two kernels (base stream, LoRA update) form one launch of
-hydra_lora_linear_group.  The standalone scoring epilogue over
+decode step is one launch of hydra_lora_linear_group_ws (T = x A^T published by
+its first workgroups, the LoRA update added by the workgroups that stream W).  The standalone scoring epilogue over
 materialised logits (hydra_score_logits, 512 x 32000) is timed separately
 (rotating four input sets so that the 256 MB last-level cache does not serve
 it) and reported under "aux"; it is not part of the step.  So is the PPO
@@ -119,7 +119,9 @@ def main():
         gB = [bf(c.B) for c in dec]
         gyo = [torch.empty(c.M, c.N, device=dev) for c in dec]
         gyn = [torch.empty(c.M, c.N, device=dev) for c in dec]
-        fn = (lambda: H.hydra_lora_linear_group([xd] * len(dec), gW, gA, gB, [c.s for c in dec], gyo, gyn))
+        dws = H.hydra_lora_linear_group_workspace(len(dec), dec[0].M, dec[0].N, dec[0].r, dev)
+        fn = (lambda: H.hydra_lora_linear_group_ws([xd] * len(dec), gW, gA, gB, [c.s for c in dec], gyo, gyn,
+                                                   workspace=dws))
         launches.append(("decode", "qkvo", fn, sum(lin_flops(c.M, c.K, c.N, c.r) for c in dec),
                          sum(lin_bytes(c.M, c.K, c.N, c.r) for c in dec)))
     if "prefill" in parts:
@@ -279,7 +281,7 @@ def main():
     roof["kernel"] = {"prefill": "lora_gemm_kernel<16,false> (4 copy + 4 MFMA waves, 128x256 tiles)",
                       "score": "lora_t_part_kernel<16> + lora_t_finish_kernel<16> + score_gemm_kernel<16,false> + "
                                "score_combine_kernel",
-                      "decode": "gemv_stream_kernel<4> + lora_update_kernel<4,16> (grouped q/k/v/o)",
+                      "decode": "gemv_fused_kernel<4,16> (q/k/v/o in one launch)",
                       "advantages": "value_head_kernel + gae_kernel"}[dom]
     tr = committed_traffic(dom)
     roof["traffic"] = None if tr is None else tr["bytes_per_launch"]
@@ -667,13 +669,16 @@ def bench_opt13b(torch, H, WL, dev, iters=5):
     gen.manual_seed(1310)
     sets = [gW] + [[(torch.randn(c.N, c.K, generator=gen, device=dev) / np.sqrt(c.K)).to(torch.bfloat16)
                     .view(torch.int16) for c in dec] for _ in range(9)]
-    calls = [lambda Ws=Ws: H.hydra_lora_linear_group([xd] * len(dec), Ws, gA, gB, [c.s for c in dec], gyo, gyn)
+    dws = H.hydra_lora_linear_group_workspace(len(dec), dec[0].M, dec[0].N, dec[0].r, dev)
+    calls = [lambda Ws=Ws: H.hydra_lora_linear_group_ws([xd] * len(dec), Ws, gA, gB, [c.s for c in dec], gyo, gyn,
+                                                        workspace=dws)
              for Ws in sets]
     t_dec = timed(calls) / len(calls)
     by = sum(lin_bytes(c.M, c.K, c.N, c.r) for c in dec)
     out["decode"] = dict(M=dec[0].M, r=dec[0].r, us=round(t_dec, 2), gbps=round(by / t_dec / 1e3, 1),
                          frac_hbm=round(by / t_dec / 1e3 / PEAK_HBM_GBPS, 4),
-                         note="four 2048 x 2048 projections per call, ten weight sets rotating (336 MB)")
+                         note="four 2048 x 2048 projections per call (hydra_lora_linear_group_ws, one launch), ten "
+                              "weight sets rotating (336 MB)")
     return out
 
 

@@ -147,6 +147,59 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
                                      int64_t M, int64_t N, int64_t K, int64_t r,
                                      float* const* y_off, float* const* y_on, void* stream);
 
+/*
+ * hydra_lora_linear_group_workspace_bytes -- device workspace that
+ * hydra_lora_linear_group_ws needs for G linears of M rows, N outputs and
+ * rank r (writes *bytes).  HYDRA_ERR_NULL for a NULL `bytes`, HYDRA_ERR_SHAPE
+ * for G, M, N or r outside the limits of hydra_lora_linear_group.
+ */
+hydra_status hydra_lora_linear_group_workspace_bytes(int64_t G, int64_t M, int64_t N, int64_t r, size_t* bytes);
+
+/* Control area at the start of a hydra_lora_linear_group_ws workspace, and its caller-owned wait-bound word. */
+#define HYDRA_GROUP_WS_CONTROL_BYTES 4352
+#define HYDRA_GROUP_WS_BOUND_WORD 8
+
+/*
+ * hydra_lora_linear_group_ws -- hydra_lora_linear_group with a caller
+ * workspace, which lets a decode step (M <= 8 rows, App. A Alg. 1 / Alg. 2,
+ * generation step) run as a single launch: the first workgroups form
+ * T = x A^T of every member once and publish it in the workspace, and the
+ * workgroups that stream the rows of W add s T B^T to their own rows of y_on
+ * (no second launch, no T recomputed per column block).  Defined by: the
+ * same passages as hydra_lora_linear.
+ *
+ *   G, x, W, A, B, s, M, N, K, r, y_off, y_on   as in hydra_lora_linear_group
+ *   workspace, workspace_bytes   device, 16-byte aligned, at least
+ *                         hydra_lora_linear_group_workspace_bytes(G, M, N, r)
+ *                         bytes.  Its first HYDRA_GROUP_WS_CONTROL_BYTES bytes
+ *                         are control words: they must be zero before the
+ *                         first call (fill the buffer with zeros once after
+ *                         allocating it), and every call leaves them zero
+ *                         again, so the buffer is reused as it is.  One
+ *                         workspace serves one stream at a time: calls that
+ *                         overlap in time must not share it.  The 32-bit word
+ *                         HYDRA_GROUP_WS_BOUND_WORD of the control area is the
+ *                         caller's: 0 selects the default bound of the wait
+ *                         for T (about 10 ms); another value bounds it to that
+ *                         many polls (a workgroup that gives up forms T
+ *                         itself, with the same bits).
+ * By rows: M <= 8 one launch; 8 < M <= 16 as hydra_lora_linear_group, but at
+ * rank above 64 the two row halves each take the single launch; M > 16 as
+ * hydra_lora_linear_group, and at rank above 64 each member runs the pre-pass
+ * GEMM of hydra_lora_linear_ws in turn over the workspace (rank 128 is
+ * accepted at every M).  Errors as in hydra_lora_linear_group, plus
+ * HYDRA_ERR_NULL for a NULL workspace, HYDRA_ERR_WORKSPACE when it is too
+ * small, HYDRA_ERR_ALIGN when it is not 16-byte aligned.  Results: the
+ * oracle's tolerances; the bits may differ from hydra_lora_linear_group's in
+ * y_on (another summation order of the LoRA update); repeated calls give the
+ * same bits.
+ */
+hydra_status hydra_lora_linear_group_ws(int64_t G, const uint16_t* const* x, const uint16_t* const* W,
+                                        const uint16_t* const* A, const uint16_t* const* B, const float* s,
+                                        int64_t M, int64_t N, int64_t K, int64_t r,
+                                        float* const* y_off, float* const* y_on,
+                                        void* workspace, size_t workspace_bytes, void* stream);
+
 /* Largest number of LoRA-on inputs in one hydra_lora_linear_multi call. */
 #define HYDRA_MAX_ADAPTERS 4
 

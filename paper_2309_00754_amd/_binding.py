@@ -26,6 +26,8 @@ HYDRA_MAX_RANK = 128
 HYDRA_MAX_GROUP = 8
 HYDRA_MAX_ADAPTERS = 4
 HYDRA_SCORE_NOALLOC_MAX_BYTES = 48 << 20
+HYDRA_GROUP_WS_CONTROL_BYTES = 4352
+HYDRA_GROUP_WS_BOUND_WORD = 8
 
 # Every symbol include/hydra.h declares.
 EXPORTED = (
@@ -33,6 +35,8 @@ EXPORTED = (
     "hydra_lora_linear_workspace_bytes",
     "hydra_lora_linear_ws",
     "hydra_lora_linear_group",
+    "hydra_lora_linear_group_workspace_bytes",
+    "hydra_lora_linear_group_ws",
     "hydra_lora_linear_multi",
     "hydra_score_workspace_bytes",
     "hydra_score",
@@ -81,6 +85,11 @@ def lib() -> ctypes.CDLL:
     L.hydra_lora_linear_group.argtypes = [_i64, _pp, _pp, _pp, _pp, ctypes.POINTER(ctypes.c_float), _i64, _i64, _i64,
                                           _i64, _pp, _pp, _vp]
     L.hydra_lora_linear_group.restype = ctypes.c_int
+    L.hydra_lora_linear_group_workspace_bytes.argtypes = [_i64, _i64, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]
+    L.hydra_lora_linear_group_workspace_bytes.restype = ctypes.c_int
+    L.hydra_lora_linear_group_ws.argtypes = [_i64, _pp, _pp, _pp, _pp, ctypes.POINTER(ctypes.c_float), _i64, _i64,
+                                             _i64, _i64, _pp, _pp, _vp, ctypes.c_size_t, _vp]
+    L.hydra_lora_linear_group_ws.restype = ctypes.c_int
     L.hydra_lora_linear_workspace_bytes.argtypes = [_i64, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]
     L.hydra_lora_linear_workspace_bytes.restype = ctypes.c_int
     L.hydra_lora_linear_ws.argtypes = [_vp, _vp, _vp, _vp, _f32, _i64, _i64, _i64, _i64, _vp, _vp, _vp,
@@ -261,6 +270,51 @@ def hydra_lora_linear_group(xs, Ws, As, Bs, ss, y_offs=None, y_ons=None, stream=
     st = lib().hydra_lora_linear_group(G, _ptr_array(xs), _ptr_array(Ws), _ptr_array(As), _ptr_array(Bs), svals,
                                        M, N, K, r, _ptr_array(y_offs), _ptr_array(y_ons), _stream_handle(stream))
     _check(st, "hydra_lora_linear_group")
+
+
+def hydra_lora_linear_group_workspace_bytes(G: int, M: int, N: int, r: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().hydra_lora_linear_group_workspace_bytes(int(G), int(M), int(N), int(r), ctypes.byref(out)),
+           "hydra_lora_linear_group_workspace_bytes")
+    return int(out.value)
+
+
+def hydra_lora_linear_group_workspace(G: int, M: int, N: int, r: int, device):
+    """A zero-filled workspace for hydra_lora_linear_group_ws (the calls leave its control words zero, so it is
+    reused as it is)."""
+    torch = _torch()
+    return torch.zeros(hydra_lora_linear_group_workspace_bytes(G, M, N, r), dtype=torch.uint8, device=device)
+
+
+def hydra_lora_linear_group_ws(xs, Ws, As, Bs, ss, y_offs=None, y_ons=None, workspace=None, stream=None) -> None:
+    """hydra_lora_linear_group with a caller workspace: a decode step (M <= 8) in one launch (see include/hydra.h).
+
+    workspace: a uint8 tensor from hydra_lora_linear_group_workspace (zero before its first use)."""
+    torch = _torch()
+    bf = _bf16_types()
+    G = len(Ws)
+    if not (len(xs) == len(As) == len(Bs) == len(ss) == G):
+        raise ValueError("all per-member sequences must have the same length")
+    y_offs = list(y_offs) if y_offs is not None else [None] * G
+    y_ons = list(y_ons) if y_ons is not None else [None] * G
+    M, K = xs[0].shape
+    N = Ws[0].shape[0]
+    r = next((a.shape[0] for a in As if a is not None), 0)
+    for i in range(G):
+        _need(xs[i], "x", bf, (M, K))
+        _need(Ws[i], "W", bf, (N, K))
+        _need(As[i], "A", bf, (r, K))
+        _need(Bs[i], "B", bf, (N, r))
+        _need(y_offs[i], "y_off", (torch.float32,), (M, N))
+        _need(y_ons[i], "y_on", (torch.float32,), (M, N))
+    if workspace is None:
+        raise ValueError("hydra_lora_linear_group_ws needs a workspace from hydra_lora_linear_group_workspace")
+    _need(workspace, "workspace", (torch.uint8,))
+    svals = (ctypes.c_float * G)(*[float(v) for v in ss])
+    st = lib().hydra_lora_linear_group_ws(G, _ptr_array(xs), _ptr_array(Ws), _ptr_array(As), _ptr_array(Bs), svals,
+                                          M, N, K, r, _ptr_array(y_offs), _ptr_array(y_ons), _ptr(workspace),
+                                          workspace.numel(), _stream_handle(stream))
+    _check(st, "hydra_lora_linear_group_ws")
 
 
 def hydra_lora_linear_multi(x_off, W, x_ons, As, Bs, ss, y_off=None, y_ons=None, stream=None) -> None:

@@ -79,22 +79,26 @@ hydra_status hydra_lora_linear(const uint16_t* x, const uint16_t* W, const uint1
   return hydra_lora_linear_group(1, &x, &W, &A, &B, &s, M, N, K, r, &y_off, &y_on, stream);
 }
 
-hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const uint16_t* const* W,
-                                     const uint16_t* const* A, const uint16_t* const* B, const float* s, int64_t M,
-                                     int64_t N, int64_t K, int64_t r, float* const* y_off, float* const* y_on,
-                                     void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks of a group call (host only); fills g and any_on.
+hydra_status group_check(int64_t G, const uint16_t* const* x, const uint16_t* const* W, const uint16_t* const* A,
+                         const uint16_t* const* B, const float* s, int64_t M, int64_t N, int64_t K, int64_t r,
+                         float* const* y_off, float* const* y_on, hydra::GroupArgs& g, bool& any_on) {
   if (G < 1 || G > HYDRA_MAX_GROUP) return HYDRA_ERR_SHAPE;
   if (!x || !W || !s) return HYDRA_ERR_NULL;
   if (!y_off && !y_on) return HYDRA_ERR_NULL;
   if (!linear_shape_ok(M, N, K)) return HYDRA_ERR_SHAPE;
   if (r < 0 || r > HYDRA_MAX_RANK) return HYDRA_ERR_SHAPE;
-  hydra::GroupArgs g{};
+  g = hydra::GroupArgs{};
   g.G = int(G);
   g.M = int(M);
   g.N = int(N);
   g.K = int(K);
   g.r = int(r);
-  bool any_on = false;
+  any_on = false;
   for (int64_t i = 0; i < G; ++i) {
     float* yo = y_off ? y_off[i] : nullptr;
     float* yn = y_on ? y_on[i] : nullptr;
@@ -117,14 +121,11 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
     g.s[i] = s[i];
     any_on = any_on || lora;
   }
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (M <= kDecodeMaxRows) {
-    // y_on of a member without an adapter equals its y_off: the kernel's
-    // update adds s * 0 there, because that member's A and B read as zeros.
-    if (!any_on) g.r = 0;
-    return from_hip(hydra::launch_lora_gemv_group(g, st));
-  }
-  if (any_on && hydra::padded_rank(g.r) > 64) return HYDRA_ERR_WORKSPACE;  // see hydra_lora_linear_ws
+  return HYDRA_OK;
+}
+
+// M > 16, padded rank <= 64: one dual GEMM per member.
+hydra_status group_gemm(const hydra::GroupArgs& g, hipStream_t st) {
   for (int i = 0; i < g.G; ++i) {
     hydra::LinearArgs a{};
     a.x = g.x[i];
@@ -139,6 +140,108 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
     a.y_off = g.y_off[i];
     a.y_on = g.y_on[i];
     const hipError_t e = hydra::launch_lora_gemm(a, st);
+    if (e != hipSuccess) return HYDRA_ERR_HIP;
+  }
+  return HYDRA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const uint16_t* const* W,
+                                     const uint16_t* const* A, const uint16_t* const* B, const float* s, int64_t M,
+                                     int64_t N, int64_t K, int64_t r, float* const* y_off, float* const* y_on,
+                                     void* stream) {
+  hydra::GroupArgs g{};
+  bool any_on = false;
+  const hydra_status chk = group_check(G, x, W, A, B, s, M, N, K, r, y_off, y_on, g, any_on);
+  if (chk != HYDRA_OK) return chk;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (M <= kDecodeMaxRows) {
+    // y_on of a member without an adapter equals its y_off: the kernel's
+    // update adds s * 0 there, because that member's A and B read as zeros.
+    if (!any_on) g.r = 0;
+    return from_hip(hydra::launch_lora_gemv_group(g, st));
+  }
+  if (any_on && hydra::padded_rank(g.r) > 64) return HYDRA_ERR_WORKSPACE;  // see hydra_lora_linear_ws
+  return group_gemm(g, st);
+}
+
+}  // extern "C"
+
+namespace {
+// Workspace of hydra_lora_linear_group_ws: kFusedCtlBytes of control words
+// (zero between calls), then per M: up to 16 rows the published T of every
+// member ([G][8][RP] fp32), above 16 rows at padded rank 128 the pre-pass
+// workspace of hydra_lora_linear_ws (shared by the members in turn).
+size_t group_ws_body(int64_t G, int64_t M, int64_t N, int rp) {
+  if (M <= kDecodeMaxRows) return hydra::fused_ws_bytes(int(G), rp) - hydra::kFusedCtlBytes;
+  return rp > 64 ? linear_ws_bytes(M, N, rp) : 0;
+}
+}  // namespace
+
+extern "C" {
+
+hydra_status hydra_lora_linear_group_workspace_bytes(int64_t G, int64_t M, int64_t N, int64_t r, size_t* bytes) {
+  if (!bytes) return HYDRA_ERR_NULL;
+  if (G < 1 || G > HYDRA_MAX_GROUP || M < 1 || M > kMaxRows || N < 1 || N > kMaxCols || r < 0 ||
+      r > HYDRA_MAX_RANK)
+    return HYDRA_ERR_SHAPE;
+  *bytes = hydra::kFusedCtlBytes + group_ws_body(G, M, N, hydra::padded_rank(int(r)));
+  return HYDRA_OK;
+}
+
+hydra_status hydra_lora_linear_group_ws(int64_t G, const uint16_t* const* x, const uint16_t* const* W,
+                                        const uint16_t* const* A, const uint16_t* const* B, const float* s,
+                                        int64_t M, int64_t N, int64_t K, int64_t r, float* const* y_off,
+                                        float* const* y_on, void* workspace, size_t workspace_bytes,
+                                        void* stream) {
+  hydra::GroupArgs g{};
+  bool any_on = false;
+  const hydra_status chk = group_check(G, x, W, A, B, s, M, N, K, r, y_off, y_on, g, any_on);
+  if (chk != HYDRA_OK) return chk;
+  const int rp = any_on ? hydra::padded_rank(int(r)) : 0;
+  if (!workspace) return HYDRA_ERR_NULL;
+  if (workspace_bytes < hydra::kFusedCtlBytes + group_ws_body(G, M, N, hydra::padded_rank(int(r))))
+    return HYDRA_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return HYDRA_ERR_ALIGN;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (!any_on) g.r = 0;
+  if (M <= hydra::kStreamRows) return from_hip(hydra::launch_gemv_fused(g, workspace, st));
+  if (M <= kDecodeMaxRows) {
+    if (rp <= 64) return from_hip(hydra::launch_lora_gemv_group(g, st));
+    // rank 128 above 8 rows: the two row halves in turn
+    hydra::GroupArgs lo = g, hi = g;
+    lo.M = hydra::kStreamRows;
+    hi.M = g.M - hydra::kStreamRows;
+    for (int i = 0; i < g.G; ++i) {
+      hi.x[i] = g.x[i] + size_t(hydra::kStreamRows) * g.K;
+      hi.y_off[i] = g.y_off[i] ? g.y_off[i] + size_t(hydra::kStreamRows) * g.N : nullptr;
+      hi.y_on[i] = g.y_on[i] ? g.y_on[i] + size_t(hydra::kStreamRows) * g.N : nullptr;
+    }
+    const hipError_t e = hydra::launch_gemv_fused(lo, workspace, st);
+    return from_hip(e != hipSuccess ? e : hydra::launch_gemv_fused(hi, workspace, st));
+  }
+  if (rp <= 64) return group_gemm(g, st);
+  // rank 128 above 16 rows: each member through the pre-pass GEMM, sharing the workspace body
+  uint8_t* body = static_cast<uint8_t*>(workspace) + hydra::kFusedCtlBytes;
+  for (int i = 0; i < g.G; ++i) {
+    hydra::LinearArgs a{};
+    a.x = g.x[i];
+    a.W = g.W[i];
+    a.A = g.A[i];
+    a.B = g.B[i];
+    a.s = g.s[i];
+    a.M = g.M;
+    a.N = g.N;
+    a.K = g.K;
+    a.r = g.A[i] ? g.r : 0;
+    a.y_off = g.y_off[i];
+    a.y_on = g.y_on[i];
+    const hipError_t e = hydra::launch_lora_gemm_tpre(
+        a, reinterpret_cast<uint16_t*>(body), reinterpret_cast<uint16_t*>(body + linear_bp_offset(M, rp)),
+        reinterpret_cast<float*>(body + linear_part_offset(M, N, rp)), st);
     if (e != hipSuccess) return HYDRA_ERR_HIP;
   }
   return HYDRA_OK;

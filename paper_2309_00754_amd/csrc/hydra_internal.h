@@ -109,6 +109,10 @@ struct ScoreGemmArgs {
   float* tpart;            // LoRA pre-pass partial sums over K chunks
   int ntn;                 // number of column tiles
   int ntm;                 // number of row tiles (set by the launcher)
+  // Two inputs (the actor pass and the LoRA-off pass have their own hidden
+  // states): lin.x holds the LoRA-off rows, x_act the rows scored with the
+  // head's LoRA; each row tile of either input is its own GEMM tile.
+  const uint16_t* x_act;   // nullptr: one input (lin.x) for both passes
 };
 
 struct CombineArgs {
@@ -221,6 +225,13 @@ hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream);
 hipError_t launch_gemv_stream(const StreamArgs& a, hipStream_t stream);
 // y_on += s (x A^T) B^T for the members of g with an adapter (M <= 8 rows).
 hipError_t launch_lora_update(const GroupArgs& g, hipStream_t stream);
+// The decode step of a group (M <= 8) in one launch.  ws: kFusedCtlBytes of
+// control words (zero between calls; the kernel leaves them zero), then fp32
+// T [G][kStreamRows][padded rank], 16-byte aligned.
+constexpr int kFusedBuckets = 32;
+constexpr size_t kFusedCtlBytes = size_t(2 + kFusedBuckets) * 128;
+inline size_t fused_ws_bytes(int G, int rp) { return kFusedCtlBytes + size_t(G) * kStreamRows * size_t(rp) * 4; }
+hipError_t launch_gemv_fused(const GroupArgs& g, void* ws, hipStream_t stream);
 hipError_t launch_score_gemm(const ScoreGemmArgs& a, hipStream_t stream);
 hipError_t launch_value_head(const ValueHeadArgs& a, hipStream_t stream);
 hipError_t launch_gae(const GaeArgs& a, hipStream_t stream);

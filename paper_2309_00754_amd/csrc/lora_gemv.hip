@@ -21,6 +21,7 @@
 //    and their partial tiles are combined in LDS in a fixed order.
 // Every reduction runs in a fixed order (results are deterministic and the
 // same for a linear called alone or inside a group).
+#include "../../include/hydra.h"
 #include "hydra_device.h"
 #include "hydra_internal.h"
 
@@ -187,6 +188,15 @@ __device__ __forceinline__ int reduced_index(int lane) {
 #pragma unroll
   for (int half = V / 2; half >= 1; half >>= 1, o >>= 1) idx += (lane & o) ? half : 0;
   return idx;
+}
+// a lane that holds reduced index v after wave_reduce_scatter<V>: the index
+// bits are the lane bits o = 32, 16, ... (v's most significant bit first)
+template <int V>
+__device__ __forceinline__ int reduced_lane(int v) {
+  int lane = 0, o = 32;
+#pragma unroll
+  for (int half = V / 2; half >= 1; half >>= 1, o >>= 1) lane |= (v & half) ? o : 0;
+  return lane;
 }
 // lanes that write a reduced value: one per index (the low lane bits that
 // were summed in full are zero)
@@ -538,6 +548,359 @@ hipError_t launch_nb(const GroupArgs& g, int rp, hipStream_t stream) {
   }
 }
 
+
+// ---------------------------------------------------------------- decode in one launch
+// The decode step of a group (M <= 8 rows per member) in a single launch,
+// with a small caller workspace.  The first workgroups of the grid form T =
+// x A^T of every member with an adapter (one wave per row of A, the same
+// routine as a row of W) and publish it in the workspace; the other
+// workgroups stream the rows of W, write y_off, then wait for their member's
+// T and add s T B^T to their own rows to write y_on.  The hardware dispatches
+// workgroups in grid order, so the T workgroups run first and the wait is
+// short; it is bounded, and a workgroup that runs out of patience forms T
+// itself through the same routine (same bits).  T is written and read with
+// device-coherent loads and stores, so no cache flush is needed.  The last
+// workgroup to finish clears the counters.
+struct FusedArgs {
+  GroupArgs ga;
+  uint32_t* ctl;  // control words (layout below), zero between calls
+  float* tbuf;    // T [G][kStreamRows][RP]
+  int nT;         // T workgroups per member (RP / 4)
+  int nWB;        // W workgroups per member (ceil(N / 16))
+  int total;      // workgroups of the launch
+  int nbk;        // buckets of the completion count
+};
+// Control words, one 128-byte line each where many workgroups update them
+// (atomics on one address serialise at the memory side, ~15 ns each): line 0
+// holds the per-member T counters and the wait bound, line 1 is spare, lines
+// 2 .. 2 + kFusedBuckets count the completed workgroups of each bucket
+// (bucket = workgroup id mod nbk).
+constexpr int kCtlLine = 32;  // words per line
+constexpr int kCtlBound = kMaxGroup;
+constexpr int kCtlBucket0 = 2 * kCtlLine;
+static_assert(kFusedCtlBytes == HYDRA_GROUP_WS_CONTROL_BYTES && kCtlBound == HYDRA_GROUP_WS_BOUND_WORD,
+              "control area as documented in hydra.h");
+constexpr uint32_t kDefaultWaitBound = 1u << 18;  // s_sleep(1) rounds (~10 ms)
+constexpr uint32_t kFinalWaitBound = 1u << 24;    // s_sleep(1) rounds (~1 s)
+
+__device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// this wave's vector-memory operations complete
+__device__ __forceinline__ void wait_vm_all() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), expcnt / lgkmcnt untouched
+  asm volatile("" ::: "memory");
+}
+
+// acc[m] = <x[m], row> for the MB rows of x (rows past M and k past K read as
+// zeros), one wave per row, the workgroup's x staged in LDS by all its waves
+// together (every wave of the workgroup must call this).  Afterwards lane l
+// holds in acc[0] the total of row reduced_index<MB>(l).
+template <int MB>
+__device__ __forceinline__ void wave_row_dot(const uint16_t* row, bool row_ok, const uint16_t* X, int M, int K,
+                                             uint4* xsh, int t, int lane, float (&acc)[MB]) {
+  constexpr int SEG = XSeg<MB>::SEG;
+  const __amdgpu_buffer_rsrc_t wrs = make_rsrc(row_ok ? row : nullptr, row_ok ? (uint32_t)K * 2u : 0u);
+  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(X, (uint32_t)M * K * 2u);
+  const int nch = (K + DKC - 1) / DKC;
+#pragma unroll
+  for (int m = 0; m < MB; ++m) acc[m] = 0.f;
+  for (int c0 = 0; c0 < nch; c0 += SEG) {
+    uint4 wb[SEG];
+#pragma unroll
+    for (int u = 0; u < SEG; ++u) {
+      const int c = c0 + u, k = c * DKC + lane * 8;
+      wb[u] = buf_load16(wrs, (c < nch && k < K) ? k * 2 : kOutOfRange);
+    }
+    if (c0 > 0) __syncthreads();  // every wave is done with the previous x segment
+    stage_x<MB, SW * 64>(xsh, xrs, c0, nch, K, t);
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < SEG; ++u)
+#pragma unroll
+      for (int m = 0; m < MB; ++m) acc[m] = dot8(wb[u], xsh[(m * SEG + u) * 64 + lane], acc[m]);
+  }
+  wave_reduce_scatter<MB>(acc, lane);
+}
+
+// T rows j0 .. j0 + 3 of one member: T[m][j] = <x[m], A[j]> for rows j < r
+// (zero otherwise), written to dst[m * ld + j] for m < M.  Wave w takes row
+// j0 + w / 4 and the chunks c with c % 4 == w % 4 of every x segment, so a
+// block of four rows costs each wave a quarter of a row; the four partial
+// sums of a row are added in chunk-class order through LDS.  Every wave of
+// the workgroup must call this; it ends with a workgroup barrier.
+constexpr int kTRows = 4;   // rows of A per T block
+constexpr int kTSplit = SW / kTRows;
+template <int MB, bool COHERENT>
+__device__ __forceinline__ void t_rows_dot(const uint16_t* A, int r, int j0, const uint16_t* X, int M, int K,
+                                           uint4* xsh, float (*tpart)[MB], float* dst, int ld, int t, int lane,
+                                           int wave) {
+  constexpr int SEG = XSeg<MB>::SEG;
+  static_assert(SEG % kTSplit == 0, "every wave takes whole chunks of each segment");
+  const int j = j0 + wave / kTSplit;
+  const int cls = wave % kTSplit;
+  const bool ok = j < r;
+  const __amdgpu_buffer_rsrc_t ars = make_rsrc(ok ? A + (size_t)j * K : nullptr, ok ? (uint32_t)K * 2u : 0u);
+  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(X, (uint32_t)M * K * 2u);
+  const int nch = (K + DKC - 1) / DKC;
+  float acc[MB];
+#pragma unroll
+  for (int m = 0; m < MB; ++m) acc[m] = 0.f;
+  for (int c0 = 0; c0 < nch; c0 += SEG) {
+    uint4 ab[SEG / kTSplit];
+#pragma unroll
+    for (int u = 0; u < SEG / kTSplit; ++u) {
+      const int c = c0 + u * kTSplit + cls, k = c * DKC + lane * 8;
+      ab[u] = buf_load16(ars, (c < nch && k < K) ? k * 2 : kOutOfRange);
+    }
+    __syncthreads();  // every wave is done with the previous contents of xsh
+    stage_x<MB, SW * 64>(xsh, xrs, c0, nch, K, t);
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < SEG / kTSplit; ++u)
+#pragma unroll
+      for (int m = 0; m < MB; ++m) acc[m] = dot8(ab[u], xsh[(m * SEG + u * kTSplit + cls) * 64 + lane], acc[m]);
+  }
+  wave_reduce_scatter<MB>(acc, lane);
+  if (reduced_writer<MB>(lane)) tpart[wave][reduced_index<MB>(lane)] = acc[0];
+  __syncthreads();
+  if (t < kTRows * MB) {
+    const int q = t / MB, m = t % MB;
+    float v = tpart[q * kTSplit][m];
+#pragma unroll
+    for (int c = 1; c < kTSplit; ++c) v += tpart[q * kTSplit + c][m];
+    if (m < M) {
+      if constexpr (COHERENT)
+        st_dev(&dst[m * ld + j0 + q], v);
+      else
+        dst[m * ld + j0 + q] = v;
+    }
+  }
+  __syncthreads();
+}
+
+template <int MB, int RP>
+__global__ __launch_bounds__(SW * 64, 8) void gemv_fused_kernel(FusedArgs fa) {
+  constexpr int TS = RP > 0 ? RP : 1;
+  __shared__ uint4 xsh[XSeg<MB>::ELEMS];
+  const GroupArgs& ga = fa.ga;
+  const int M = ga.M, N = ga.N, K = ga.K, r = ga.r;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int bid = blockIdx.x;
+  const int nTall = ga.G * fa.nT;
+  float acc[MB];
+  if (bid < nTall) {
+    // ---------------------------------------------- rows of A: T of one member
+    const int gi = bid / fa.nT, jb = bid - (bid / fa.nT) * fa.nT;
+    const bool on = ga.y_on[gi] != nullptr && ga.A[gi] != nullptr && ga.B[gi] != nullptr;
+    if (on) {
+      __shared__ float tpart[SW][MB];
+      t_rows_dot<MB, true>(ga.A[gi], r, jb * kTRows, ga.x[gi], M, K, xsh, tpart, fa.tbuf + gi * kStreamRows * TS, TS,
+                           t, lane, wave);
+      wait_vm_all();  // this thread's T values are stored
+    }
+    __syncthreads();
+    if (t == 0) {
+      __hip_atomic_fetch_add(&fa.ctl[gi], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      wait_vm_all();  // the count has landed before this workgroup reports completion
+    }
+  } else {
+    // ---------------------------------------------- rows of W
+    // Wave 0 reads the member's T counter before it requests its row of W
+    // and, when the counter is complete, requests T (device-coherent loads:
+    // a handful of requests per workgroup); every wave requests its row of B
+    // next to its row of W.  After the dot products wave 0 shares T through
+    // LDS.  A workgroup that started before T was published (only the first
+    // ones, which run next to the T workgroups) polls the counter after its
+    // dot products (bounded), or forms T itself.
+    constexpr int SEG = XSeg<MB>::SEG;
+    constexpr int RPL = (TS + 63) / 64;  // j values per lane
+    __shared__ float tsh[MB][TS];
+    __shared__ uint32_t seen_sh;
+    const int idx = bid - nTall;
+    const int gi = idx / fa.nWB, nb = idx - (idx / fa.nWB) * fa.nWB;
+    const int n = nb * 16 + wave;
+    const bool row_ok = n < N;
+    float* const yo = ga.y_off[gi];
+    float* const yn = ga.y_on[gi];
+    const bool on = RP > 0 && yn != nullptr && ga.A[gi] != nullptr && ga.B[gi] != nullptr;
+    const __amdgpu_buffer_rsrc_t wrs =
+        make_rsrc(row_ok ? ga.W[gi] + (size_t)n * K : nullptr, row_ok ? (uint32_t)K * 2u : 0u);
+    const __amdgpu_buffer_rsrc_t xrs = make_rsrc(ga.x[gi], (uint32_t)M * K * 2u);
+    const int nch = (K + DKC - 1) / DKC;
+#pragma unroll
+    for (int m = 0; m < MB; ++m) acc[m] = 0.f;
+    float bv[RPL], tv[MB][RPL];
+#pragma unroll
+    for (int q = 0; q < RPL; ++q) {
+      bv[q] = 0.f;
+#pragma unroll
+      for (int mm = 0; mm < MB; ++mm) tv[mm][q] = 0.f;
+    }
+    // T of the member into tv, read by the lanes j % 64 of this wave
+    auto load_t = [&]() __attribute__((always_inline)) {
+#pragma unroll
+      for (int q = 0; q < RPL; ++q) {
+        const int jj = q * 64 + lane;
+#pragma unroll
+        for (int mm = 0; mm < MB; ++mm)
+          tv[mm][q] = (jj < TS && mm < M) ? ld_dev(&fa.tbuf[(gi * kStreamRows + mm) * TS + jj]) : 0.f;
+      }
+    };
+    uint32_t seen = 0u;
+    if (on && wave == 0) seen = ld_dev(&fa.ctl[gi]);
+    for (int c0 = 0; c0 < nch; c0 += SEG) {
+      uint4 wb[SEG];
+#pragma unroll
+      for (int u = 0; u < SEG; ++u) {
+        const int c = c0 + u, k = c * DKC + lane * 8;
+        wb[u] = buf_load16(wrs, (c < nch && k < K) ? k * 2 : kOutOfRange);
+      }
+      if (c0 == 0 && on) {
+        const __amdgpu_buffer_rsrc_t brs =
+            make_rsrc(row_ok ? ga.B[gi] + (size_t)n * r : nullptr, row_ok ? (uint32_t)r * 2u : 0u);
+#pragma unroll
+        for (int q = 0; q < RPL; ++q) {
+          const int jj = q * 64 + lane;
+          bv[q] = bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(brs, jj < r ? jj * 2 : kOutOfRange, 0, 0));
+        }
+        if (wave == 0) {
+          if (seen >= (uint32_t)fa.nT) load_t();
+          if (lane == 0) seen_sh = seen;
+        }
+      }
+      if (c0 > 0) __syncthreads();  // every wave is done with the previous x segment
+      stage_x<MB, SW * 64>(xsh, xrs, c0, nch, K, t);
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < SEG; ++u)
+#pragma unroll
+        for (int m = 0; m < MB; ++m) acc[m] = dot8(wb[u], xsh[(m * SEG + u) * 64 + lane], acc[m]);
+    }
+    wave_reduce_scatter<MB>(acc, lane);
+    const int m = reduced_index<MB>(lane);
+    const bool writer = reduced_writer<MB>(lane) && m < M && row_ok;
+    if (writer && yo) yo[(size_t)m * N + n] = acc[0];
+    if (on) {
+      if (seen_sh < (uint32_t)fa.nT) {
+        // T was not published when this workgroup started
+        if (wave == 0) {
+          uint32_t bound = ld_dev(&fa.ctl[kCtlBound]);
+          if (bound == 0u) bound = kDefaultWaitBound;
+          uint32_t it = 0;
+          seen = ld_dev(&fa.ctl[gi]);
+          while (seen < (uint32_t)fa.nT && ++it < bound) {
+            __builtin_amdgcn_s_sleep(1);
+            seen = ld_dev(&fa.ctl[gi]);
+          }
+          if (seen >= (uint32_t)fa.nT) load_t();
+        }
+        __syncthreads();  // every wave has read seen_sh
+        if (wave == 0 && lane == 0) seen_sh = seen;
+        __syncthreads();
+        if (seen_sh < (uint32_t)fa.nT) {
+          // T formed here, block by block as the T workgroups do
+          __shared__ float tpart2[SW][MB];
+          for (int q = t; q < MB * TS; q += SW * 64) tsh[q / TS][q % TS] = 0.f;
+          for (int jb = 0; jb < fa.nT; ++jb)
+            t_rows_dot<MB, false>(ga.A[gi], r, jb * kTRows, ga.x[gi], M, K, xsh, tpart2, &tsh[0][0], TS, t, lane,
+                                  wave);
+#pragma unroll
+          for (int q = 0; q < RPL; ++q) {
+            const int jj = q * 64 + lane;
+#pragma unroll
+            for (int mm = 0; mm < MB; ++mm) tv[mm][q] = jj < TS ? tsh[mm][jj] : 0.f;
+          }
+        }
+      }
+      if (seen_sh >= (uint32_t)fa.nT) {
+        // wave 0 shares the T it read
+        if (wave == 0) {
+#pragma unroll
+          for (int q = 0; q < RPL; ++q) {
+            const int jj = q * 64 + lane;
+            if (jj < TS) {
+#pragma unroll
+              for (int mm = 0; mm < MB; ++mm) tsh[mm][jj] = tv[mm][q];
+            }
+          }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < RPL; ++q) {
+          const int jj = q * 64 + lane;
+#pragma unroll
+          for (int mm = 0; mm < MB; ++mm) tv[mm][q] = jj < TS ? tsh[mm][jj] : 0.f;
+        }
+      }
+      // d[m] = sum_j T[m][j] B[n][j]: lane l holds j = l, l + 64
+      float part[MB];
+#pragma unroll
+      for (int mm = 0; mm < MB; ++mm) {
+        part[mm] = 0.f;
+#pragma unroll
+        for (int q = 0; q < RPL; ++q) part[mm] = fmaf(tv[mm][q], bv[q], part[mm]);
+      }
+      wave_reduce_scatter<MB>(part, lane);
+      if (writer) yn[(size_t)m * N + n] = acc[0] + ga.s[gi] * part[0];
+    } else if (writer && yn) {
+      yn[(size_t)m * N + n] = acc[0];
+    }
+  }
+  // Completion: every workgroup but the last one dispatched adds one to its
+  // bucket (no return value, so nothing waits for it); the last one, which
+  // starts after every other has started, waits until every bucket is full
+  // (every other workgroup is past its reads of the counters) and clears the
+  // counters for the next call.  Its wait is bounded too; past the bound it
+  // clears them anyway (a workgroup that still had to read them would find
+  // its member's T counter at zero and form T itself).
+  if constexpr (RP > 0) {
+    if (fa.nT > 0 && wave == 0) {
+      if (bid != fa.total - 1) {
+        if (lane == 0)
+          __hip_atomic_fetch_add(&fa.ctl[kCtlBucket0 + (bid % fa.nbk) * kCtlLine], 1u, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+      } else {
+        // lane q < nbk watches bucket q: one load per poll for all buckets
+        const int q = lane;
+        const bool mine = q < fa.nbk;
+        const uint32_t want =
+            mine ? (uint32_t)((fa.total - q + fa.nbk - 1) / fa.nbk) - (q == bid % fa.nbk ? 1u : 0u) : 0u;
+        uint32_t it = 0;
+        while (__builtin_amdgcn_ballot_w64(mine && ld_dev(&fa.ctl[kCtlBucket0 + (mine ? q : 0) * kCtlLine]) < want) !=
+                   0ull &&
+               ++it < kFinalWaitBound)
+          __builtin_amdgcn_s_sleep(1);
+        if (lane < ga.G) st_dev(&fa.ctl[lane], 0u);
+        if (mine) st_dev(&fa.ctl[kCtlBucket0 + q * kCtlLine], 0u);
+      }
+    }
+  }
+}
+
+template <int MB>
+hipError_t launch_fused_mb(const FusedArgs& fa, int rp, hipStream_t stream) {
+  const dim3 grid(fa.total), block(SW * 64);
+  switch (rp) {
+    case 0: hipLaunchKernelGGL((gemv_fused_kernel<MB, 0>), grid, block, 0, stream, fa); break;
+    case 16: hipLaunchKernelGGL((gemv_fused_kernel<MB, 16>), grid, block, 0, stream, fa); break;
+    case 32: hipLaunchKernelGGL((gemv_fused_kernel<MB, 32>), grid, block, 0, stream, fa); break;
+    case 64: hipLaunchKernelGGL((gemv_fused_kernel<MB, 64>), grid, block, 0, stream, fa); break;
+    default: hipLaunchKernelGGL((gemv_fused_kernel<MB, 128>), grid, block, 0, stream, fa); break;
+  }
+  return hipGetLastError();
+}
 }  // namespace
 
 hipError_t launch_gemv_stream(const StreamArgs& a_in, hipStream_t stream) {
@@ -551,6 +914,24 @@ hipError_t launch_gemv_stream(const StreamArgs& a_in, hipStream_t stream) {
   else if (rows <= 4) hipLaunchKernelGGL((gemv_stream_kernel<4>), grid, block, 0, stream, a);
   else hipLaunchKernelGGL((gemv_stream_kernel<8>), grid, block, 0, stream, a);
   return hipGetLastError();
+}
+
+hipError_t launch_gemv_fused(const GroupArgs& g, void* ws, hipStream_t stream) {
+  bool any_on = false;
+  for (int i = 0; i < g.G; ++i) any_on = any_on || (g.y_on[i] && g.A[i] && g.B[i]);
+  const int rp = any_on ? padded_rank(g.r) : 0;
+  FusedArgs fa{};
+  fa.ga = g;
+  fa.ctl = static_cast<uint32_t*>(ws);
+  fa.tbuf = reinterpret_cast<float*>(static_cast<char*>(ws) + kFusedCtlBytes);
+  fa.nT = rp / kTRows;
+  fa.nWB = (g.N + SW - 1) / SW;
+  fa.total = g.G * (fa.nT + fa.nWB);
+  fa.nbk = fa.total < kFusedBuckets ? fa.total : kFusedBuckets;
+  if (g.M <= 1) return launch_fused_mb<1>(fa, rp, stream);
+  if (g.M <= 2) return launch_fused_mb<2>(fa, rp, stream);
+  if (g.M <= 4) return launch_fused_mb<4>(fa, rp, stream);
+  return launch_fused_mb<8>(fa, rp, stream);
 }
 
 hipError_t launch_lora_update(const GroupArgs& g, hipStream_t stream) {

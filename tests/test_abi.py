@@ -259,6 +259,60 @@ def test_rank_above_64_needs_the_workspace_in_the_gemm():
     assert _grp(M=64, r=100, G=2) == H.HYDRA_ERR_WORKSPACE
 
 
+def _grp_ws(G=2, xs=(P, P), Ws=(P, P), As=(P, P), Bs=(P, P), ss=(2.0, 2.0), M=4, N=64, K=64, r=8,
+            yo=(P + 0x1000, P + 0x2000), yn=(P + 0x3000, P + 0x4000), ws=P + 0x10000, nbytes=None):
+    def arr(v):
+        if v is None:
+            return None
+        a = (ctypes.c_void_p * len(v))()
+        for i, p in enumerate(v):
+            a[i] = p
+        return a
+    if nbytes is None:
+        nbytes = H.hydra_lora_linear_group_workspace_bytes(min(max(G, 1), 8), min(max(M, 1), 1 << 20), max(N, 1),
+                                                            min(max(r, 0), 128))
+    svals = None if ss is None else (ctypes.c_float * len(ss))(*ss)
+    return H.lib().hydra_lora_linear_group_ws(G, arr(xs), arr(Ws), arr(As), arr(Bs), svals, M, N, K, r,
+                                              arr(yo), arr(yn), ws, nbytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(G=0), H.HYDRA_ERR_SHAPE),
+    (dict(G=9), H.HYDRA_ERR_SHAPE),
+    (dict(xs=None), H.HYDRA_ERR_NULL),
+    (dict(As=(P, None)), H.HYDRA_ERR_NULL),
+    (dict(K=20), H.HYDRA_ERR_SHAPE),
+    (dict(r=129), H.HYDRA_ERR_SHAPE),
+    (dict(M=(1 << 20) + 1), H.HYDRA_ERR_SHAPE),
+    (dict(xs=(P, P8)), H.HYDRA_ERR_ALIGN),
+    (dict(ws=None), H.HYDRA_ERR_NULL),
+    (dict(nbytes=H.HYDRA_GROUP_WS_CONTROL_BYTES - 1, r=0), H.HYDRA_ERR_WORKSPACE),
+    (dict(ws=P + 8), H.HYDRA_ERR_ALIGN),
+    (dict(M=2048, r=128, nbytes=4096), H.HYDRA_ERR_WORKSPACE),     # rank 128 above 16 rows: the pre-pass body
+])
+def test_group_ws_rejects(kw, code):
+    """Argument and workspace errors of the workspace group call, all before any HIP call (fake pointers)."""
+    assert _grp_ws(**kw) == code
+
+
+def test_group_ws_workspace_bytes():
+    """The control words, then the published T (G x 8 rows x padded rank fp32) up to 16 rows, or above 16
+    rows at padded rank 128 the pre-pass workspace of hydra_lora_linear_ws."""
+    gb = H.hydra_lora_linear_group_workspace_bytes
+    C = H.HYDRA_GROUP_WS_CONTROL_BYTES
+    assert C == 34 * 128  # a line of T counters, a line of completed buckets, 32 bucket lines
+    assert gb(4, 4, 4096, 16) == C + 4 * 8 * 16 * 4
+    assert gb(4, 6, 2048, 128) == C + 4 * 8 * 128 * 4
+    assert gb(1, 1, 10, 0) == C
+    assert gb(8, 16, 100, 9) == C + 8 * 8 * 16 * 4
+    assert gb(3, 2048, 4096, 16) == C                                         # rank <= 64 above 16 rows: no body
+    assert gb(3, 2048, 4096, 128) == C + H.hydra_lora_linear_workspace_bytes(2048, 4096, 128)
+    out = ctypes.c_size_t(0)
+    assert H.lib().hydra_lora_linear_group_workspace_bytes(9, 4, 10, 0, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
+    assert H.lib().hydra_lora_linear_group_workspace_bytes(1, 4, 10, 129, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
+    assert H.lib().hydra_lora_linear_group_workspace_bytes(1, 4, 10, 8, None) == H.HYDRA_ERR_NULL
+
+
 def _multi(x_off=P, W=P, n_on=2, xs=(P, P), As=(P, P), Bs=(P, P), ss=(2.0, 2.0), M=4, N=64, K=64, r=8,
            y_off=P + 0x2000, yn=(P + 0x3000, P + 0x4000)):
     def arr(v):

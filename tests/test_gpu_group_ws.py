@@ -1,0 +1,170 @@
+"""GPU parity of hydra_lora_linear_group_ws: the decode step in one launch (T = x A^T published by the first
+workgroups, the LoRA update added by the workgroups that stream W), and the workspace group call at every row
+class, against the oracle."""
+import numpy as np
+import pytest
+
+import paper_2309_00754_amd as H
+import workloads as WL
+from oracle import lora_linear_ref
+from gpu_helpers import assert_rel, dev_bf16, host, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(cases, device, want_on=None):
+    import torch
+    G = len(cases)
+    want_on = want_on or [True] * G
+    t = dict(
+        xs=[dev_bf16(c.x, device) for c in cases],
+        Ws=[dev_bf16(c.W, device) for c in cases],
+        As=[dev_bf16(c.A, device) if (c.r and want_on[i]) else None for i, c in enumerate(cases)],
+        Bs=[dev_bf16(c.B, device) if (c.r and want_on[i]) else None for i, c in enumerate(cases)],
+        ss=[c.s for c in cases],
+        yo=[torch.full((c.M, c.N), float("nan"), device=device) for c in cases],
+        yn=[torch.full((c.M, c.N), float("nan"), device=device) if want_on[i] else None
+            for i, c in enumerate(cases)],
+    )
+    return t
+
+
+def _call(t, ws):
+    import torch
+    H.hydra_lora_linear_group_ws(t["xs"], t["Ws"], t["As"], t["Bs"], t["ss"], t["yo"], t["yn"], workspace=ws)
+    torch.cuda.synchronize()
+    return [host(v).copy() for v in t["yo"]], [None if v is None else host(v).copy() for v in t["yn"]]
+
+
+def _check(cases, go, gn, want_on=None):
+    want_on = want_on or [True] * len(cases)
+    for i, c in enumerate(cases):
+        e_off, e_on = lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
+        assert_rel(go[i], e_off, f"member {i} y_off")
+        if want_on[i]:
+            assert_rel(gn[i], e_on, f"member {i} y_on")
+        else:
+            assert gn[i] is None
+
+
+@pytest.mark.parametrize("M,K,N,r,G", [
+    (1, 512, 256, 16, 1), (2, 1032, 200, 8, 3), (4, 4096, 520, 16, 4), (3, 8200, 130, 32, 2),
+    (6, 2048, 300, 128, 4), (8, 1000, 64, 64, 2), (5, 264, 33, 1, 8), (4, 520, 100, 0, 2),
+])
+def test_group_ws_decode_matches_oracle(M, K, N, r, G, dev):
+    """One launch per call at M <= 8: every rank class (0, 1, 8, 16, 32, 64, 128), ragged K (segments of x
+    past 4096, a K tail inside a chunk) and N (a partial 16-row block), up to 8 members."""
+    say("group_ws decode", M, K, N, r, G)
+    cases = [WL.gen_linear(1100 + 10 * G + i, M, K, N, r, s=[2.0, -0.5, 1.5][i % 3]) for i in range(G)]
+    t = _inputs(cases, dev)
+    ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
+    go, gn = _call(t, ws)
+    _check(cases, go, gn)
+    # the control words are zero again after the call
+    assert int(host(ws[:H.HYDRA_GROUP_WS_CONTROL_BYTES]).astype(np.int64).sum()) == 0
+
+
+def test_group_ws_repeated_calls_reuse_the_workspace(dev):
+    """Ten calls in a row on one workspace with changing inputs: each gives the oracle's result, and a repeated
+    input gives the same bits."""
+    import torch
+    say("group_ws repeated")
+    M, K, N, r, G = 4, 2048, 400, 16, 4
+    ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
+    first = None
+    for it in range(10):
+        seed = 1200 + (it % 3)
+        cases = [WL.gen_linear(seed * 10 + i, M, K, N, r) for i in range(G)]
+        go, gn = _call(_inputs(cases, dev), ws)
+        if it in (0, 1, 2):
+            _check(cases, go, gn)
+        if it == 0:
+            first = (go, gn)
+        if it in (3, 6, 9):  # seed 1200 again
+            for i in range(G):
+                assert np.array_equal(go[i], first[0][i]) and np.array_equal(gn[i], first[1][i])
+    assert int(host(ws[:H.HYDRA_GROUP_WS_CONTROL_BYTES]).astype(np.int64).sum()) == 0
+
+
+def test_group_ws_members_without_adapter(dev):
+    """A LoRA-off member (no y_on, no adapter) between members with adapters, and a member whose y_on has no
+    adapter's update to wait for."""
+    say("group_ws mixed members")
+    cases = [WL.gen_linear(1300 + i, 4, 1024, 260, 16) for i in range(3)]
+    want_on = [True, False, True]
+    t = _inputs(cases, dev, want_on)
+    ws = H.hydra_lora_linear_group_workspace(3, 4, 260, 16, dev)
+    go, gn = _call(t, ws)
+    _check(cases, go, gn, want_on)
+
+
+def test_group_ws_wait_bound_fallback_same_bits(dev):
+    """With the wait bound word set to one round, workgroups that find T not yet published form it themselves
+    through the same routine: the bits are those of the default bound."""
+    import torch
+    say("group_ws wait bound")
+    M, K, N, r, G = 6, 4096, 2048, 128, 4
+    cases = [WL.gen_linear(1400 + i, M, K, N, r) for i in range(G)]
+    t = _inputs(cases, dev)
+    ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
+    go, gn = _call(t, ws)
+    _check(cases, go, gn)
+    bw = 4 * H.HYDRA_GROUP_WS_BOUND_WORD
+    bound = ws[bw:bw + 4].view(torch.int32)  # the caller's wait bound word (0 selects the default)
+    bound.fill_(1)
+    go1, gn1 = _call(t, ws)
+    for i in range(G):
+        assert np.array_equal(go[i], go1[i]) and np.array_equal(gn[i], gn1[i]), i
+    assert int(host(ws[bw:bw + 4].view(torch.int32))[0]) == 1  # the bound word is the caller's, not reset
+    bound.fill_(0)
+    assert int(host(ws[:H.HYDRA_GROUP_WS_CONTROL_BYTES]).astype(np.int64).sum()) == 0
+
+
+@pytest.mark.parametrize("M,r", [(12, 16), (16, 128), (130, 16), (130, 128)])
+def test_group_ws_above_decode_rows(M, r, dev):
+    """9..16 rows (the small-M MFMA kernel; at rank 128 two single-launch halves) and the GEMM rows (rank 128 per
+    member through the pre-pass GEMM, sharing the workspace)."""
+    say("group_ws rows", M, r)
+    K, N, G = 520, 300, 3
+    cases = [WL.gen_linear(1500 + 7 * M + i, M, K, N, r, s=1.0 + i) for i in range(G)]
+    t = _inputs(cases, dev)
+    ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
+    go, gn = _call(t, ws)
+    _check(cases, go, gn)
+    assert int(host(ws[:H.HYDRA_GROUP_WS_CONTROL_BYTES]).astype(np.int64).sum()) == 0
+
+
+def test_group_ws_decode_qkvo_full(dev):
+    """The decode step of the Llama-7B attention projections (batch 4, 4096 x 4096, r = 16) as one call."""
+    say("group_ws decode_qkvo")
+    cases = WL.make("decode_qkvo")
+    t = _inputs(cases, dev)
+    ws = H.hydra_lora_linear_group_workspace(len(cases), 4, 4096, 16, dev)
+    go, gn = _call(t, ws)
+    _check(cases, go, gn)
+
+
+def test_group_ws_graph_replays(dev):
+    """Captured in a HIP graph and replayed three times with eager work between the replays: every replay has the
+    bits of the eager call (each call leaves the control words zero for the next)."""
+    import torch
+    say("group_ws graph")
+    M, K, N, r, G = 4, 1024, 512, 16, 4
+    cases = [WL.gen_linear(1600 + i, M, K, N, r) for i in range(G)]
+    t = _inputs(cases, dev)
+    ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
+    eo, en = _call(t, ws)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        H.hydra_lora_linear_group_ws(t["xs"], t["Ws"], t["As"], t["Bs"], t["ss"], t["yo"], t["yn"], workspace=ws)
+    torch.cuda.synchronize()
+    other = [WL.gen_linear(1700 + i, M, K, N, r) for i in range(G)]
+    to = _inputs(other, dev)
+    for rep in range(3):
+        for v in t["yo"] + t["yn"]:
+            v.fill_(float("nan"))
+        _call(to, ws)  # eager work on the same workspace between the replays
+        g.replay()
+        torch.cuda.synchronize()
+        for i in range(G):
+            assert np.array_equal(host(t["yo"][i]), eo[i]) and np.array_equal(host(t["yn"][i]), en[i]), (rep, i)
