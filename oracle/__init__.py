@@ -8,6 +8,7 @@ from .hydra_oracle import (  # noqa: F401
     score_logits_ref,
     reward_ref,
     score_head_ref,
+    score_head_two_input_ref,
 )
 from .ppo_oracle import (  # noqa: F401
     gae_ref,

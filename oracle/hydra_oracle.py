@@ -47,6 +47,7 @@ __all__ = [
     "score_logits_ref",
     "reward_ref",
     "score_head_ref",
+    "score_head_two_input_ref",
 ]
 
 _ROW_BLOCK = 256
@@ -197,4 +198,22 @@ def score_head_ref(h, W_lm, A, B, s: float, ids, w_rm=None, n_seq: int = 0, seq_
         lasts = [b * seq_len + seq_len - 1 for b in range(n_seq)]
         if rows is None or all(l in set(int(v) for v in rows) for l in lasts):
             res["reward"] = reward_ref(h, w_rm, n_seq, seq_len, rows)
+    return res
+
+
+def score_head_two_input_ref(h_act, h_off, W_lm, A, B, s: float, ids, w_rm=None, n_seq: int = 0, seq_len: int = 0):
+    """Two-head scoring with each pass's own final hidden states (App. A, Alg. 2: the actor pass runs with the
+    actor's adapter and the reference / reward pass with LoRA off, over the same sequences; in a multi-layer
+    model their hidden states differ; Sec. 3 Dynamic LoRA: the reward model is the LoRA-off network).
+
+      z_on  = H_act W_lm^T + s (H_act A^T) B^T   (the actor's logits: LoRA on the CLM head too)
+      z_off = H_off W_lm^T                        (the reference logits: LoRA off)
+      lp_on, lp_off, lse_on, lse_off, kl = lp_on - lp_off as in score_logits_ref;
+      reward[b] = <H_off[b*seq_len + seq_len - 1], w_rm>  (the reward head on the LoRA-off pass).
+    """
+    _, z_on = lora_linear_ref(h_act, W_lm, A, B, s)
+    z_off = _mm(bf16_to_f64(h_off), bf16_to_f64(W_lm))
+    res = score_logits_ref(z_on, z_off, ids)
+    if w_rm is not None and n_seq > 0:
+        res["reward"] = reward_ref(h_off, w_rm, n_seq, seq_len)
     return res

@@ -402,6 +402,90 @@ def test_score_head_is_linear_then_log_softmax():
     assert np.allclose(rs["reward"], r["reward"], rtol=0, atol=0)
 
 
+# ---------------------------------------------------------------- two-input scoring head
+
+def _two_input_case(seed, n_seq=2, seq_len=3, K=8, V=6, r=2):
+    rng = np.random.default_rng(seed)
+    M = n_seq * seq_len
+    h_act = _int_bf16(rng, (M, K), -3, 3)
+    h_off = _int_bf16(rng, (M, K), -3, 3)
+    W = _int_bf16(rng, (V, K), -2, 2)
+    A = _int_bf16(rng, (r, K), -2, 2)
+    B = _int_bf16(rng, (V, r), -2, 2)
+    w = _int_bf16(rng, (K,))
+    ids = rng.integers(0, V, size=M)
+    return h_act, h_off, W, A, B, w, ids, n_seq, seq_len
+
+
+def _two_input_pins_hold(fn):
+    """True when fn matches the brute force: exact Fraction logits of each pass from its own input (LoRA on the
+    actor pass only), the log-softmax of each row from math.fsum over those exact logits, the exact reward from
+    the LoRA-off input's last rows."""
+    s = 0.5
+    for seed in (51, 52):
+        h_act, h_off, W, A, B, w, ids, n_seq, seq_len = _two_input_case(seed)
+        res = fn(h_act[0], h_off[0], W[0], A[0], B[0], s, ids, w[0], n_seq, seq_len)
+        _, z_on = _frac_lora(h_act[1], W[1], A[1], B[1], s)
+        z_off, _ = _frac_lora(h_off[1], W[1], A[1], B[1], s)
+        for i in range(len(ids)):
+            for z, key in ((z_on, "on"), (z_off, "off")):
+                row = [float(v) for v in z[i]]
+                m = max(row)
+                lse = m + math.log(math.fsum(math.exp(v - m) for v in row))
+                if abs(res["lse_" + key][i] - lse) > 1e-12 or abs(res["lp_" + key][i] - (row[ids[i]] - lse)) > 1e-12:
+                    return False
+            if abs(res["kl"][i] - (res["lp_on"][i] - res["lp_off"][i])) > 0:
+                return False
+        for b in range(n_seq):
+            last = b * seq_len + seq_len - 1
+            if Fraction(res["reward"][b]) != sum(Fraction(int(h_off[1][last, k])) * int(w[1][k]) for k in range(8)):
+                return False
+    return True
+
+
+def test_score_two_input_bruteforce():
+    """The actor pass's logits come from h_act with the head's LoRA, the reference logits and the reward from h_off
+    without it (App. A, Alg. 2): exact per-pass brute force."""
+    assert _two_input_pins_hold(O.score_head_two_input_ref)
+
+
+def test_score_two_input_equal_inputs_is_the_one_input_head():
+    """With h_act == h_off the two-input head is the one-input head of score_head_ref."""
+    c = gen_score_head(53, 2, 8, 64, 500, 8)
+    a = O.score_head_two_input_ref(c.h, c.h, c.W_lm, c.A, c.B, c.s, c.ids, c.w_rm, 2, 8)
+    b = O.score_head_ref(c.h, c.W_lm, c.A, c.B, c.s, c.ids, c.w_rm, 2, 8)
+    for k in ("lp_on", "lp_off", "kl", "lse_on", "lse_off", "reward"):
+        assert np.array_equal(a[k], b[k]), k
+
+
+def _mut_two_lora_on_off_pass(h_act, h_off, W, A, B, s, ids, w, n_seq, seq_len):
+    _, z_on = O.lora_linear_ref(h_act, W, A, B, s)
+    _, z_off = O.lora_linear_ref(h_off, W, A, B, s)
+    res = O.score_logits_ref(z_on, z_off, ids)
+    res["reward"] = O.reward_ref(h_off, w, n_seq, seq_len)
+    return res
+
+
+def _mut_two_swapped_inputs(h_act, h_off, W, A, B, s, ids, w, n_seq, seq_len):
+    return O.score_head_two_input_ref(h_off, h_act, W, A, B, s, ids, w, n_seq, seq_len)
+
+
+def _mut_two_reward_from_actor(h_act, h_off, W, A, B, s, ids, w, n_seq, seq_len):
+    res = O.score_head_two_input_ref(h_act, h_off, W, A, B, s, ids, w, n_seq, seq_len)
+    res["reward"] = O.reward_ref(h_act, w, n_seq, seq_len)
+    return res
+
+
+def _mut_two_one_input(h_act, h_off, W, A, B, s, ids, w, n_seq, seq_len):
+    return O.score_head_ref(h_act, W, A, B, s, ids, w, n_seq, seq_len)
+
+
+@pytest.mark.parametrize("mut", [_mut_two_lora_on_off_pass, _mut_two_swapped_inputs, _mut_two_reward_from_actor,
+                                 _mut_two_one_input])
+def test_pins_catch_two_input_mutations(mut):
+    assert not _two_input_pins_hold(mut)
+
+
 # ---------------------------------------------------------------- mutation checks
 
 def _pins_for_linear(fn):
