@@ -48,7 +48,7 @@ METRIC = "dual-path LoRA GEMM TFLOP/s + scoring tokens/s, % of MFMA/HBM roofline
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
 AUX_NAMES = ("score_logits", "single_linear", "ppo_advantages", "decode_multi", "lora_backward_layer",
-             "opt13b_r128")
+             "opt13b_r128", "score_two_input")
 
 
 def lin_flops(M, K, N, r):
@@ -319,7 +319,7 @@ def main():
         aux_fns = {"score_logits": bench_score_logits, "single_linear": bench_single_linear,
                    "ppo_advantages": bench_advantages,
                    "decode_multi": bench_decode_multi, "lora_backward_layer": bench_backward,
-                   "opt13b_r128": bench_opt13b}
+                   "opt13b_r128": bench_opt13b, "score_two_input": bench_score_two_input}
         out["aux"] = {name: aux_fns[name](torch, H, WL, dev) for name in aux_names}
 
     if not args.no_cpu_baseline:
@@ -680,6 +680,47 @@ def bench_opt13b(torch, H, WL, dev, iters=5):
                          note="four 2048 x 2048 projections per call (hydra_lora_linear_group_ws, one launch), ten "
                               "weight sets rotating (336 MB)")
     return out
+
+
+def bench_score_two_input(torch, H, WL, dev, iters=5):
+    """The two-head scoring with each pass's own hidden states (hydra_score_two_input: the actor's rows with the
+    head's LoRA, the LoRA-off rows for the reference log-probabilities and the reward) on the Llama-7B heads,
+    2048 tokens, V = 32000, r = 16, beside the one-input call (hydra_score) on the same sizes.  The two-input call
+    does the base product twice (once per input), so its FLOPs are about twice the one-input call's; the W_lm
+    tiles are still read once per pair of row tiles.  Each figure is the average over a block of back-to-back
+    calls between one pair of events."""
+    bf = (lambda u: torch.from_numpy(np.ascontiguousarray(u).view(np.int16)).to(dev))
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters * 1e3
+
+    c = WL.make("two_input_score")
+    ha, ho, Wl, A, B, w_rm = bf(c.h_act), bf(c.h), bf(c.W_lm), bf(c.A), bf(c.B), bf(c.w_rm)
+    ids = torch.from_numpy(c.ids).to(dev)
+    lp_on, lp_off, kl = (torch.empty(c.M, device=dev) for _ in range(3))
+    reward = torch.empty(c.n_seq, device=dev)
+    ws = torch.empty(H.hydra_score_workspace_bytes(c.M, c.V), dtype=torch.uint8, device=dev)
+    t2 = timed(lambda: H.hydra_score_two_input(ha, ho, Wl, A, B, c.s, ids, w_rm, c.n_seq, c.seq_len, lp_on, lp_off,
+                                               kl, reward=reward, workspace=ws))
+    t1 = timed(lambda: H.hydra_score(ho, Wl, A, B, c.s, ids, w_rm, c.n_seq, c.seq_len, lp_on, lp_off, kl,
+                                     reward=reward, workspace=ws))
+    fl2 = 2 * 2.0 * c.M * c.K * c.V + 2.0 * c.M * c.K * c.r + 2.0 * c.M * c.r * c.V + 2.0 * c.n_seq * c.K
+    fl1 = lin_flops(c.M, c.K, c.V, c.r) + 2.0 * c.n_seq * c.K
+    return dict(M=c.M, K=c.K, V=c.V, r=c.r,
+                two_input=dict(us=round(t2, 2), tflops=round(fl2 / t2 / 1e6, 2),
+                               frac_bf16_peak=round(fl2 / t2 / 1e6 / PEAK_BF16_TFLOPS, 4),
+                               tokens_per_s=round(c.M / (t2 * 1e-6), 1)),
+                one_input=dict(us=round(t1, 2), tflops=round(fl1 / t1 / 1e6, 2),
+                               frac_bf16_peak=round(fl1 / t1 / 1e6 / PEAK_BF16_TFLOPS, 4)))
 
 
 def cpu_baseline(target_s: float, host_inputs=None):

@@ -278,6 +278,37 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
                          float* lp_on, float* lp_off, float* kl, float* reward, float* lse_on, float* lse_off,
                          void* workspace, size_t workspace_bytes, int32_t* err_flag, void* stream);
 
+/*
+ * hydra_score_two_input -- the scoring pass when the actor pass and the
+ * LoRA-off pass have their own final hidden states, as in a multi-layer model
+ * (their activations differ after the first layer).
+ * Defined by: App. A Alg. 2 (the actor pass runs with the actor's adapter, the
+ * reference / reward pass with LoRA off, over the same sequences), Sec. 3
+ * "Dynamic LoRA" (the reward model is the LoRA-off network), Sec. 3 (the two
+ * heads of pi^hydra).
+ *
+ *   h_act    [M x K] bf16   final hidden states of the actor pass
+ *   h_off    [M x K] bf16   final hidden states of the LoRA-off pass
+ *   lp_on    [M] fp32       out: log softmax(z_on)[token],  z_on  = h_act W^T + s (h_act A^T) B^T
+ *   lp_off   [M] fp32       out: log softmax(z_off)[token], z_off = h_off W^T
+ *   kl       [M] fp32       out: lp_on - lp_off
+ *   reward   [n_seq] fp32   out: <h_off[b*seq_len + seq_len - 1], w_rm> (NULL: skipped)
+ *   every other argument    as in hydra_score (the same workspace size:
+ *                           hydra_score_workspace_bytes(M, V))
+ * One launch covers both inputs: the LoRA-off tile and the actor tile of a row
+ * block run next to each other, so each block of W_lm is read from HBM once
+ * for both.  The [M x V] logits are never written.  Errors as in hydra_score
+ * (h_act is checked like h), plus HYDRA_ERR_SHAPE when
+ * 2 * ceil(M / 256) * ceil(V / 256) >= 2^24.  With h_act and h_off equal the
+ * results have the bits of hydra_score.
+ */
+hydra_status hydra_score_two_input(const uint16_t* h_act, const uint16_t* h_off, const uint16_t* W_lm,
+                                   const uint16_t* A, const uint16_t* B, float s, const int32_t* tokens,
+                                   const uint16_t* w_rm, int64_t n_seq, int64_t seq_len, int64_t K, int64_t V,
+                                   int64_t r, float* lp_on, float* lp_off, float* kl, float* reward, float* lse_on,
+                                   float* lse_off, void* workspace, size_t workspace_bytes, int32_t* err_flag,
+                                   void* stream);
+
 /* Largest workspace that hydra_score_noalloc serves from its own device scratch (48 MiB). */
 #define HYDRA_SCORE_NOALLOC_MAX_BYTES (48u << 20)
 

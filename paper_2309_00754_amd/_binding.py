@@ -41,6 +41,7 @@ EXPORTED = (
     "hydra_score_workspace_bytes",
     "hydra_score",
     "hydra_score_noalloc",
+    "hydra_score_two_input",
     "hydra_score_logits",
     "hydra_value_head",
     "hydra_ppo_advantages",
@@ -106,6 +107,9 @@ def lib() -> ctypes.CDLL:
     L.hydra_score_noalloc.argtypes = [_vp, _vp, _vp, _vp, _f32, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
                                       _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
     L.hydra_score_noalloc.restype = ctypes.c_int
+    L.hydra_score_two_input.argtypes = [_vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
+                                        _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _vp]
+    L.hydra_score_two_input.restype = ctypes.c_int
     L.hydra_score_logits.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
     L.hydra_score_logits.restype = ctypes.c_int
     L.hydra_value_head.argtypes = [_vp, _vp, _i64, _i64, _vp, _vp]
@@ -388,6 +392,39 @@ def hydra_score(h, W_lm, A, B, s: float, tokens, w_rm, n_seq: int, seq_len: int,
                            _ptr(lse_on), _ptr(lse_off), _ptr(workspace), workspace.numel(), _ptr(err_flag),
                            _stream_handle(stream))
     _check(st, "hydra_score")
+
+
+def hydra_score_two_input(h_act, h_off, W_lm, A, B, s: float, tokens, w_rm, n_seq: int, seq_len: int,
+                          lp_on, lp_off, kl, reward=None, lse_on=None, lse_off=None,
+                          workspace=None, err_flag=None, stream=None) -> None:
+    """Scoring with the actor pass's own hidden states (h_act, with the head's LoRA) and the LoRA-off pass's (h_off:
+    reference log-probabilities and reward), one launch over both (see include/hydra.h)."""
+    torch = _torch()
+    bf = _bf16_types()
+    M, K = h_off.shape
+    V = W_lm.shape[0]
+    r = 0 if A is None else A.shape[0]
+    if M != n_seq * seq_len:
+        raise ValueError("h rows must equal n_seq * seq_len")
+    _need(h_act, "h_act", bf, (M, K))
+    _need(h_off, "h_off", bf, (M, K))
+    _need(W_lm, "W_lm", bf, (V, K))
+    _need(A, "A", bf, (r, K))
+    _need(B, "B", bf, (V, r))
+    _need(tokens, "tokens", (torch.int32,), (M,))
+    _need(w_rm, "w_rm", bf, (K,))
+    for name, t in (("lp_on", lp_on), ("lp_off", lp_off), ("kl", kl), ("lse_on", lse_on), ("lse_off", lse_off)):
+        _need(t, name, (torch.float32,), (M,))
+    _need(reward, "reward", (torch.float32,), (n_seq,))
+    _need(err_flag, "err_flag", (torch.int32,), (1,))
+    if workspace is None:
+        workspace = torch.empty(hydra_score_workspace_bytes(M, V), dtype=torch.uint8, device=h_off.device)
+    _need(workspace, "workspace", (torch.uint8,))
+    st = lib().hydra_score_two_input(_ptr(h_act), _ptr(h_off), _ptr(W_lm), _ptr(A), _ptr(B), float(s), _ptr(tokens),
+                                     _ptr(w_rm), int(n_seq), int(seq_len), K, V, r, _ptr(lp_on), _ptr(lp_off),
+                                     _ptr(kl), _ptr(reward), _ptr(lse_on), _ptr(lse_off), _ptr(workspace),
+                                     workspace.numel(), _ptr(err_flag), _stream_handle(stream))
+    _check(st, "hydra_score_two_input")
 
 
 def hydra_score_noalloc(h, W_lm, A, B, s: float, tokens, w_rm, n_seq: int, seq_len: int,

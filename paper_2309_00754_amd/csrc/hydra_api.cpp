@@ -413,7 +413,8 @@ hydra_status score_check(const uint16_t* h, const uint16_t* W_lm, const uint16_t
 hydra_status score_launch(const uint16_t* h, const uint16_t* W_lm, const uint16_t* A, const uint16_t* B, float s,
                           const int32_t* tokens, const uint16_t* w_rm, int64_t n_seq, int64_t seq_len, int64_t K,
                           int64_t V, int64_t r, float* lp_on, float* lp_off, float* kl, float* reward,
-                          float* lse_on, float* lse_off, void* workspace, int32_t* err_flag, hipStream_t st) {
+                          float* lse_on, float* lse_off, void* workspace, int32_t* err_flag, hipStream_t st,
+                          const uint16_t* h_act = nullptr) {
   const int64_t M = n_seq * seq_len;
   float4* part = reinterpret_cast<float4*>(workspace);
   float* zt = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + score_zt_offset(M, V));
@@ -438,6 +439,7 @@ hydra_status score_launch(const uint16_t* h, const uint16_t* W_lm, const uint16_
   g.bp_buf = bp;
   g.tpart = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + score_part_offset(M, V));
   g.ntn = int(score_tiles(V));
+  g.x_act = h_act;
   hipError_t e = hydra::launch_score_gemm(g, st);
   if (e != hipSuccess) return HYDRA_ERR_HIP;
 
@@ -524,6 +526,28 @@ hydra_status hydra_score(const uint16_t* h, const uint16_t* W_lm, const uint16_t
   if (!aligned(workspace, 16)) return HYDRA_ERR_ALIGN;
   return score_launch(h, W_lm, A, B, s, tokens, w_rm, n_seq, seq_len, K, V, r, lp_on, lp_off, kl, reward, lse_on,
                       lse_off, workspace, err_flag, reinterpret_cast<hipStream_t>(stream));
+}
+
+hydra_status hydra_score_two_input(const uint16_t* h_act, const uint16_t* h_off, const uint16_t* W_lm,
+                                   const uint16_t* A, const uint16_t* B, float s, const int32_t* tokens,
+                                   const uint16_t* w_rm, int64_t n_seq, int64_t seq_len, int64_t K, int64_t V,
+                                   int64_t r, float* lp_on, float* lp_off, float* kl, float* reward, float* lse_on,
+                                   float* lse_off, void* workspace, size_t workspace_bytes, int32_t* err_flag,
+                                   void* stream) {
+  if (!h_act) return HYDRA_ERR_NULL;
+  const hydra_status chk = score_check(h_off, W_lm, A, B, tokens, w_rm, n_seq, seq_len, K, V, r, lp_on, lp_off, kl,
+                                       reward, lse_on, lse_off, err_flag);
+  if (chk != HYDRA_OK) return chk;
+  const int64_t M = n_seq * seq_len;
+  // twice the row tiles of the one-input pass
+  if (!grid_ok(2 * cdiv(M, hydra::kScoreTileM) * cdiv(V, hydra::kScoreTileN), hydra::kScoreThreads))
+    return HYDRA_ERR_SHAPE;
+  if (!aligned(h_act, 16)) return HYDRA_ERR_ALIGN;
+  if (!workspace) return HYDRA_ERR_WORKSPACE;
+  if (workspace_bytes < score_ws_bytes(M, V)) return HYDRA_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return HYDRA_ERR_ALIGN;
+  return score_launch(h_off, W_lm, A, B, s, tokens, w_rm, n_seq, seq_len, K, V, r, lp_on, lp_off, kl, reward, lse_on,
+                      lse_off, workspace, err_flag, reinterpret_cast<hipStream_t>(stream), h_act);
 }
 
 hydra_status hydra_score_noalloc(const uint16_t* h, const uint16_t* W_lm, const uint16_t* A, const uint16_t* B,

@@ -31,6 +31,14 @@
 //    tile) goes to the workspace for score_combine_kernel.
 // With B = 0 or s = 0 the LoRA update adds exact zeros, so the on and off
 // statistics (computed by the same code) are bit-identical and KL == 0.
+//
+// Two inputs (the actor pass and the LoRA-off pass each with their own final
+// hidden states, App. A, Alg. 2): the grid holds twice the row tiles, the
+// LoRA-off tile and the actor tile of each row block next to each other in
+// the tile order (so both read a column block of W while it is in L2).  A
+// LoRA-off tile takes only the LoRA-off statistics and runs no LoRA slabs;
+// an actor tile runs the LoRA slabs over its own T and takes only the LoRA-on
+// statistics.  Each writes its half of the (row, column tile) partial.
 #include "hydra_device.h"
 #include "hydra_internal.h"
 
@@ -95,7 +103,7 @@ struct IC {
 
 // RAGGED: the vocabulary is not a multiple of the column tile, so the last
 // column tile masks the columns past N.
-template <int RP, bool RAGGED>
+template <int RP, bool RAGGED, bool DUAL>
 __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
   __shared__ uint4 sm[NS][STAGE];
 
@@ -110,8 +118,14 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
   const int l32 = lane & 31;
   const int lh = lane >> 5;
 
+  constexpr bool dual = DUAL;
   int tmi, tni;
-  tile_of(blockIdx.x, g.ntm, g.ntn, tmi, tni);
+  tile_of(blockIdx.x, dual ? 2 * g.ntm : g.ntm, g.ntn, tmi, tni);
+  // two inputs: row tile 2 i is the LoRA-off tile of row block i, 2 i + 1 its actor tile
+  const bool is_act = dual && (tmi & 1) != 0;
+  if (dual) tmi >>= 1;
+  const bool do_off = !dual || !is_act;  // this tile takes the LoRA-off statistics
+  const bool do_on = !dual || is_act;    // ... and / or the LoRA-on ones
   // (tile coordinates are made provably wave-uniform, so that everything
   // derived from them -- buffer descriptors, LDS bases -- lives in SGPRs)
   const int m0 = __builtin_amdgcn_readfirstlane(tmi * BM);
@@ -123,7 +137,7 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
   // (B zero padded to RP).  Those run as LS more slabs of the same ring,
   // after the LoRA-off statistics have been taken from the accumulators.
   constexpr int LS = 2 * RP / BK;
-  const int nsl = nkt + LS;
+  const int nsl = nkt + (do_on ? LS : 0);
 
   // the sampled tokens of this lane's four rows, fetched early
   int tk[MT];
@@ -141,7 +155,7 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
   // of the slabs past the last one, which land in stages that are not read
   // again.  Wave w copies 16-row blocks w, w + 4, w + 8, w + 12 of the x side
   // (j < 4) and of the W side (j >= 4) of every slab.
-  const i32x4_t xr = make_rsrc_raw(a.x + (size_t)m0 * K, (uint32_t)min(BM, M - m0) * K * 2u);
+  const i32x4_t xr = make_rsrc_raw((is_act ? g.x_act : a.x) + (size_t)m0 * K, (uint32_t)min(BM, M - m0) * K * 2u);
   const i32x4_t wrs = make_rsrc_raw(a.W + (size_t)n0 * K, (uint32_t)min(BN, N - n0) * K * 2u);
   const i32x4_t tsr = make_rsrc_raw(g.ts + (size_t)m0 * 2 * RP, (uint32_t)min(BM, M - m0) * 2 * RP * 2u);
   const i32x4_t bpr = make_rsrc_raw(g.bp + (size_t)n0 * RP, (uint32_t)min(BN, N - n0) * RP * 2u);
@@ -286,12 +300,16 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
   };
 
   float st_off[MT][2], st_on[MT][2];
+  if (do_off) {
 #pragma unroll
-  for (int mi = 0; mi < MT; ++mi) {
-    __builtin_amdgcn_sched_barrier(0);
-    row_stats(mi, 0, st_off[mi][0], st_off[mi][1]);  // LoRA off
+    for (int mi = 0; mi < MT; ++mi) {
+      __builtin_amdgcn_sched_barrier(0);
+      row_stats(mi, 0, st_off[mi][0], st_off[mi][1]);  // LoRA off
+    }
   }
-  if constexpr (LS > 0) {
+  if (!do_on) {
+    // a LoRA-off tile of two inputs: nothing more
+  } else if constexpr (LS > 0) {
     // The LoRA slabs nkt .. nkt + LS - 1 (stage (nkt + q) % NS; the last main
     // slab already read the first k-step of slab nkt into F0).
 #pragma unroll
@@ -303,6 +321,13 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
     for (int mi = 0; mi < MT; ++mi) {
       __builtin_amdgcn_sched_barrier(0);
       row_stats(mi, 1, st_on[mi][0], st_on[mi][1]);  // LoRA on
+    }
+  } else if constexpr (DUAL) {
+    // an actor tile without an adapter: its logits are the LoRA-on logits
+#pragma unroll
+    for (int mi = 0; mi < MT; ++mi) {
+      __builtin_amdgcn_sched_barrier(0);
+      row_stats(mi, 1, st_on[mi][0], st_on[mi][1]);
     }
   } else {
     // no adapter: the LoRA-on logits are the LoRA-off logits
@@ -325,8 +350,10 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
 #pragma unroll
     for (int mi = 0; mi < MT; ++mi) {
       const int rloc = wr * WM + mi * 32 + l32;
+      // (a tile of two inputs fills only its own half; the other half is never read)
       *reinterpret_cast<float4*>(red + (wc * BM + rloc) * 4) =
-          make_float4(st_off[mi][0], st_off[mi][1], st_on[mi][0], st_on[mi][1]);
+          make_float4(do_off ? st_off[mi][0] : 0.f, do_off ? st_off[mi][1] : 0.f, do_on ? st_on[mi][0] : 0.f,
+                      do_on ? st_on[mi][1] : 0.f);
     }
   }
   __syncthreads();
@@ -338,7 +365,13 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
       float mo = p0.x, so = p0.y, mn = p0.z, sn = p0.w;
       lse_merge(mo, so, p1.x, p1.y);
       lse_merge(mn, sn, p1.z, p1.w);
-      g.part[(size_t)row * g.ntn + tni] = make_float4(mo, so, mn, sn);
+      float4* dst = g.part + (size_t)row * g.ntn + tni;
+      if constexpr (!DUAL)
+        *dst = make_float4(mo, so, mn, sn);
+      else if (do_off)
+        reinterpret_cast<float2*>(dst)[0] = make_float2(mo, so);
+      else
+        reinterpret_cast<float2*>(dst)[1] = make_float2(mn, sn);
     }
   }
 }
@@ -352,7 +385,7 @@ hipError_t launch_rp(const ScoreGemmArgs& s_in, hipStream_t stream) {
   const bool ragged = s.lin.N % BN != 0;
   if constexpr (RP > 0) {
     TpreArgs t{};
-    t.x = s.lin.x;
+    t.x = s.x_act ? s.x_act : s.lin.x;
     t.A = s.lin.A;
     t.B = s.lin.B;
     t.s = s.lin.s;
@@ -366,10 +399,17 @@ hipError_t launch_rp(const ScoreGemmArgs& s_in, hipStream_t stream) {
     const hipError_t e = launch_lora_tpre(t, RP, &s.bp, stream);
     if (e != hipSuccess) return e;
   }
-  if (ragged)
-    hipLaunchKernelGGL((score_gemm_kernel<RP, true>), dim3(s.ntm * s.ntn), dim3(NT), 0, stream, s);
-  else
-    hipLaunchKernelGGL((score_gemm_kernel<RP, false>), dim3(s.ntm * s.ntn), dim3(NT), 0, stream, s);
+  const dim3 grid((s.x_act ? 2 : 1) * s.ntm * s.ntn);
+  if (s.x_act) {
+    if (ragged)
+      hipLaunchKernelGGL((score_gemm_kernel<RP, true, true>), grid, dim3(NT), 0, stream, s);
+    else
+      hipLaunchKernelGGL((score_gemm_kernel<RP, false, true>), grid, dim3(NT), 0, stream, s);
+  } else if (ragged) {
+    hipLaunchKernelGGL((score_gemm_kernel<RP, true, false>), grid, dim3(NT), 0, stream, s);
+  } else {
+    hipLaunchKernelGGL((score_gemm_kernel<RP, false, false>), grid, dim3(NT), 0, stream, s);
+  }
   return hipGetLastError();
 }
 

@@ -106,6 +106,40 @@ def test_score_rejects(kw, code):
     assert _score(**kw) == code
 
 
+def _score2(h_act=P, **kw):
+    a = dict(h=P, W=P, A=P, B=P, tok=P, w_rm=P, n_seq=4, seq_len=8, K=64, V=1000, r=8, lp_on=P, lp_off=P, kl=P,
+             reward=P, lse_on=None, lse_off=None, ws=P, ws_bytes=None, err=None)
+    a.update(kw)
+    if a["ws_bytes"] is None:
+        a["ws_bytes"] = H.hydra_score_workspace_bytes(a["n_seq"] * a["seq_len"], a["V"])
+    return H.lib().hydra_score_two_input(h_act, a["h"], a["W"], a["A"], a["B"], 2.0, a["tok"], a["w_rm"], a["n_seq"],
+                                         a["seq_len"], a["K"], a["V"], a["r"], a["lp_on"], a["lp_off"], a["kl"],
+                                         a["reward"], a["lse_on"], a["lse_off"], a["ws"], a["ws_bytes"], a["err"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(h_act=None), H.HYDRA_ERR_NULL),
+    (dict(h=None), H.HYDRA_ERR_NULL),
+    (dict(A=None), H.HYDRA_ERR_NULL),
+    (dict(K=12), H.HYDRA_ERR_SHAPE),
+    (dict(h_act=P8), H.HYDRA_ERR_ALIGN),
+    (dict(h=P8), H.HYDRA_ERR_ALIGN),
+    (dict(ws=None), H.HYDRA_ERR_WORKSPACE),
+    (dict(ws_bytes=16), H.HYDRA_ERR_WORKSPACE),
+    # twice the one-input tile grid: 2048 x 4096 row x column tiles of 256 would reach 2^24 x 256 work-items
+    (dict(n_seq=1 << 11, seq_len=1 << 8, V=1 << 20, K=64, ws_bytes=1 << 40), H.HYDRA_ERR_SHAPE),
+])
+def test_score_two_input_rejects(kw, code):
+    assert _score2(**kw) == code
+
+
+def test_score_two_input_grid_limit_is_twice_the_one_input_one():
+    """The same sizes that the one-input call accepts up to its grid limit are halved here (fake pointers; the call
+    then fails only on a planted misalignment)."""
+    assert _score(n_seq=1 << 11, seq_len=1 << 8, V=1 << 20, K=64, ws_bytes=1 << 40, h=P8) == H.HYDRA_ERR_ALIGN
+    assert _score2(n_seq=1 << 10, seq_len=1 << 8, V=1 << 20, K=64, ws_bytes=1 << 40, h=P8) == H.HYDRA_ERR_ALIGN
+
+
 def _score_na(h=P, W=P, A=P, B=P, tok=P, w_rm=P, n_seq=4, seq_len=8, K=64, V=1000, r=8,
               lp_on=P, lp_off=P, kl=P, reward=P, lse_on=None, lse_off=None, err=None):
     return H.lib().hydra_score_noalloc(h, W, A, B, 2.0, tok, w_rm, n_seq, seq_len, K, V, r, lp_on, lp_off, kl,

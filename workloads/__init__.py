@@ -295,6 +295,22 @@ def gen_score_head(seed: int, n_seq: int, seq_len: int, K: int, V: int, r: int, 
 
 
 @dataclasses.dataclass
+class TwoInputScoreCase(ScoreCase):
+    """Scoring with the actor pass's own final hidden states: h (inherited) is the LoRA-off pass's, h_act the actor
+    pass's [M x K] bf16."""
+    h_act: np.ndarray = None
+
+
+def gen_score_two_input(seed: int, n_seq: int, seq_len: int, K: int, V: int, r: int,
+                        s: float = 2.0) -> TwoInputScoreCase:
+    """Draw order: the inputs of gen_score_head (h, W_lm, A, B, w_rm, ids), then h_act ~ N(0, 1)."""
+    c = gen_score_head(seed, n_seq, seq_len, K, V, r, s)
+    rng = np.random.Generator(np.random.PCG64(seed + (1 << 20)))
+    h_act = _normal_bf16(rng, (c.M, K), 1.0)
+    return TwoInputScoreCase(c.h, c.W_lm, c.A, c.B, c.w_rm, c.ids, c.s, c.n_seq, c.seq_len, h_act)
+
+
+@dataclasses.dataclass
 class AdvantageCase:
     """PPO advantage-step input: per-token KL kl[M] and sequence rewards reward[n_seq] (fp32), the critic's
     hidden states h[M x K] and value head w_v[K] (bf16); M = n_seq * seq_len, sequence-major."""
@@ -347,6 +363,8 @@ WORKLOADS = {
     "opt13b_layer_r128": dict(seed=8, M=4096, proj=OPT13B_PROJ, r=128, s=2.0),
     "opt13b_score_r128": dict(seed=9, n_seq=8, seq_len=512, K=2048, V=50272, r=128, s=2.0),
     "opt13b_decode_r128": dict(seed=10, M=6, proj=OPT13B_DECODE_PROJ, r=128, s=2.0),
+    # the Llama-7B two-head scoring pass with the actor pass's and the LoRA-off pass's own final hidden states
+    "two_input_score": dict(seed=11, n_seq=4, seq_len=512, K=4096, V=32000, r=16, s=2.0),
 }
 
 
@@ -361,6 +379,8 @@ def make(name: str, M: Optional[int] = None):
         return gen_linears(w["seed"], M or w["M"], w["proj"], w["r"], w["s"])
     if name in ("two_head_score", "opt13b_score_r128"):
         return gen_score_head(w["seed"], w["n_seq"], w["seq_len"], w["K"], w["V"], w["r"], w["s"])
+    if name == "two_input_score":
+        return gen_score_two_input(w["seed"], w["n_seq"], w["seq_len"], w["K"], w["V"], w["r"], w["s"])
     if name == "decode_multi":
         return gen_multi(w["seed"], M or w["M"], w["K"], w["N"], w["r"], w["n_on"], name=name)
     if name == "backward_layer":
