@@ -155,9 +155,11 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
  */
 hydra_status hydra_lora_linear_group_workspace_bytes(int64_t G, int64_t M, int64_t N, int64_t r, size_t* bytes);
 
-/* Control area at the start of a hydra_lora_linear_group_ws workspace, and its caller-owned wait-bound word. */
+/* Control area at the start of a hydra_lora_linear_group_ws workspace, its caller-owned wait-bound word, and the
+ * size of the region of published T values that follows it. */
 #define HYDRA_GROUP_WS_CONTROL_BYTES 4352
 #define HYDRA_GROUP_WS_BOUND_WORD 8
+#define HYDRA_GROUP_WS_T_BYTES 65536
 
 /*
  * hydra_lora_linear_group_ws -- hydra_lora_linear_group with a caller
@@ -171,18 +173,27 @@ hydra_status hydra_lora_linear_group_workspace_bytes(int64_t G, int64_t M, int64
  *   G, x, W, A, B, s, M, N, K, r, y_off, y_on   as in hydra_lora_linear_group
  *   workspace, workspace_bytes   device, 16-byte aligned, at least
  *                         hydra_lora_linear_group_workspace_bytes(G, M, N, r)
- *                         bytes.  Its first HYDRA_GROUP_WS_CONTROL_BYTES bytes
- *                         are control words: they must be zero before the
- *                         first call (fill the buffer with zeros once after
- *                         allocating it), and every call leaves them zero
- *                         again, so the buffer is reused as it is.  One
- *                         workspace serves one stream at a time: calls that
- *                         overlap in time must not share it.  The 32-bit word
+ *                         bytes.  Fill the whole buffer with zeros once after
+ *                         allocating it; after that the library keeps its
+ *                         state there (HYDRA_GROUP_WS_CONTROL_BYTES of control
+ *                         words holding a call generation, then
+ *                         HYDRA_GROUP_WS_T_BYTES of published T values tagged
+ *                         with it), so the buffer is reused as it is and
+ *                         serves calls of any shape.  To reset it, zero all of
+ *                         it (the control words alone are not enough), and
+ *                         zero it again before its next use here after lending
+ *                         it to another entry point.  One workspace serves one
+ *                         stream at a time: calls that overlap in time must
+ *                         not share it.  The 32-bit word
  *                         HYDRA_GROUP_WS_BOUND_WORD of the control area is the
- *                         caller's: 0 selects the default bound of the wait
- *                         for T (about 10 ms); another value bounds it to that
- *                         many polls (a workgroup that gives up forms T
- *                         itself, with the same bits).
+ *                         caller's: 0 selects the default bounds of the
+ *                         launch's two waits (for T, about 10 ms; for every
+ *                         workgroup to have read the generation, about 1 s);
+ *                         another value bounds each to that many polls.  A
+ *                         workgroup that gives up waiting for T forms it
+ *                         itself, with the same bits; if the second wait runs
+ *                         out, every later call forms T in every workgroup
+ *                         (same bits, slower) until the workspace is zeroed.
  * By rows: M <= 8 one launch; 8 < M <= 16 as hydra_lora_linear_group, but at
  * rank above 64 the two row halves each take the single launch; M > 16 as
  * hydra_lora_linear_group, and at rank above 64 each member runs the pre-pass

@@ -171,13 +171,13 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
 }  // extern "C"
 
 namespace {
-// Workspace of hydra_lora_linear_group_ws: kFusedCtlBytes of control words
-// (zero between calls), then per M: up to 16 rows the published T of every
-// member ([G][8][RP] fp32), above 16 rows at padded rank 128 the pre-pass
-// workspace of hydra_lora_linear_ws (shared by the members in turn).
-size_t group_ws_body(int64_t G, int64_t M, int64_t N, int rp) {
-  if (M <= kDecodeMaxRows) return hydra::fused_ws_bytes(int(G), rp) - hydra::kFusedCtlBytes;
-  return rp > 64 ? linear_ws_bytes(M, N, rp) : 0;
+// Workspace of hydra_lora_linear_group_ws: the control words and the tagged
+// T slots of the single-launch decode (a fixed size, whatever the shape),
+// then above 16 rows at padded rank 128 the pre-pass workspace of
+// hydra_lora_linear_ws (shared by the members in turn), which therefore never
+// overwrites the T slots.
+size_t group_ws_bytes(int64_t M, int64_t N, int rp) {
+  return hydra::kFusedWsBytes + (M > kDecodeMaxRows && rp > 64 ? linear_ws_bytes(M, N, rp) : 0);
 }
 }  // namespace
 
@@ -188,7 +188,7 @@ hydra_status hydra_lora_linear_group_workspace_bytes(int64_t G, int64_t M, int64
   if (G < 1 || G > HYDRA_MAX_GROUP || M < 1 || M > kMaxRows || N < 1 || N > kMaxCols || r < 0 ||
       r > HYDRA_MAX_RANK)
     return HYDRA_ERR_SHAPE;
-  *bytes = hydra::kFusedCtlBytes + group_ws_body(G, M, N, hydra::padded_rank(int(r)));
+  *bytes = group_ws_bytes(M, N, hydra::padded_rank(int(r)));
   return HYDRA_OK;
 }
 
@@ -203,7 +203,7 @@ hydra_status hydra_lora_linear_group_ws(int64_t G, const uint16_t* const* x, con
   if (chk != HYDRA_OK) return chk;
   const int rp = any_on ? hydra::padded_rank(int(r)) : 0;
   if (!workspace) return HYDRA_ERR_NULL;
-  if (workspace_bytes < hydra::kFusedCtlBytes + group_ws_body(G, M, N, hydra::padded_rank(int(r))))
+  if (workspace_bytes < group_ws_bytes(M, N, hydra::padded_rank(int(r))))
     return HYDRA_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return HYDRA_ERR_ALIGN;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
@@ -225,7 +225,7 @@ hydra_status hydra_lora_linear_group_ws(int64_t G, const uint16_t* const* x, con
   }
   if (rp <= 64) return group_gemm(g, st);
   // rank 128 above 16 rows: each member through the pre-pass GEMM, sharing the workspace body
-  uint8_t* body = static_cast<uint8_t*>(workspace) + hydra::kFusedCtlBytes;
+  uint8_t* body = static_cast<uint8_t*>(workspace) + hydra::kFusedWsBytes;
   for (int i = 0; i < g.G; ++i) {
     hydra::LinearArgs a{};
     a.x = g.x[i];

@@ -225,12 +225,15 @@ hipError_t launch_lora_gemv_group(const GroupArgs& g, hipStream_t stream);
 hipError_t launch_gemv_stream(const StreamArgs& a, hipStream_t stream);
 // y_on += s (x A^T) B^T for the members of g with an adapter (M <= 8 rows).
 hipError_t launch_lora_update(const GroupArgs& g, hipStream_t stream);
-// The decode step of a group (M <= 8) in one launch.  ws: kFusedCtlBytes of
-// control words (zero between calls; the kernel leaves them zero), then fp32
-// T [G][kStreamRows][padded rank], 16-byte aligned.
+// The decode step of a group (M <= 8) in one launch.  ws (16-byte aligned,
+// zero before its first use): kFusedCtlBytes of control words (the kernel
+// keeps a call generation there), then kFusedTSlotBytes of tagged T slots
+// (64-bit entries, [G][kStreamRows][padded rank]), a region of fixed size so
+// that calls of any shape find only their own or older tags there.
 constexpr int kFusedBuckets = 32;
 constexpr size_t kFusedCtlBytes = size_t(2 + kFusedBuckets) * 128;
-inline size_t fused_ws_bytes(int G, int rp) { return kFusedCtlBytes + size_t(G) * kStreamRows * size_t(rp) * 4; }
+constexpr size_t kFusedTSlotBytes = size_t(kMaxGroup) * kStreamRows * 128 * 8;
+constexpr size_t kFusedWsBytes = kFusedCtlBytes + kFusedTSlotBytes;
 hipError_t launch_gemv_fused(const GroupArgs& g, void* ws, hipStream_t stream);
 hipError_t launch_score_gemm(const ScoreGemmArgs& a, hipStream_t stream);
 hipError_t launch_value_head(const ValueHeadArgs& a, hipStream_t stream);

@@ -218,10 +218,10 @@ struct XSeg {
 // Stage x[m][c0 * 512 ... (c0 + SEG) * 512) for m < MB in LDS: element
 // (m, u, lane) holds the 8 k values that lane `lane` of any wave uses in chunk
 // c0 + u.  Rows past M and k past K read as zeros.
-template <int MB, int NT>
+template <int MB, int NT, int SEG = XSeg<MB>::SEG>
 __device__ __forceinline__ void stage_x(uint4* xsh, __amdgpu_buffer_rsrc_t xrs, int c0, int nch, int K, int t) {
-  constexpr int SEG = XSeg<MB>::SEG;
-  for (int e = t; e < XSeg<MB>::ELEMS; e += NT) {
+  static_assert(SEG <= XSeg<MB>::SEG, "a segment fits the staging buffer");
+  for (int e = t; e < MB * SEG * 64; e += NT) {
     const int m = e / (SEG * 64), u = (e / 64) % SEG, l = e % 64;
     const int c = c0 + u, k = c * DKC + l * 8;
     xsh[e] = buf_load16(xrs, (c < nch && k < K) ? (m * K + k) * 2 : kOutOfRange);
@@ -554,99 +554,90 @@ hipError_t launch_nb(const GroupArgs& g, int rp, hipStream_t stream) {
 // with a small caller workspace.  The first workgroups of the grid form T =
 // x A^T of every member with an adapter (one wave per row of A, the same
 // routine as a row of W) and publish it in the workspace; the other
-// workgroups stream the rows of W, write y_off, then wait for their member's
-// T and add s T B^T to their own rows to write y_on.  The hardware dispatches
-// workgroups in grid order, so the T workgroups run first and the wait is
-// short; it is bounded, and a workgroup that runs out of patience forms T
-// itself through the same routine (same bits).  T is written and read with
-// device-coherent loads and stores, so no cache flush is needed.  The last
-// workgroup to finish clears the counters.
+// workgroups stream the rows of W, write y_off, and add s T B^T to their own
+// rows to write y_on.
+//
+// Publishing without a flush or a second round trip: every T value is stored
+// together with a 32-bit tag in one 64-bit device-coherent store, and a
+// reader accepts T only when every tag it loaded equals the tag of the
+// current call.  The tag of a call is derived from a generation word in the
+// workspace: each workgroup reads it with the same returning atomic that
+// reports the read (the atomic adds one to a count in the low half of a
+// 64-bit word whose high half is the generation), and one extra workgroup at
+// the end of the grid, the keeper, waits until every count is complete and
+// then advances the generation and clears the counts.  Every workgroup of a
+// call therefore sees the same generation, every T value carrying the next
+// tag was computed by this call, and values left by earlier calls carry
+// older tags.  The keeper starts after every other workgroup has started
+// (the hardware dispatches in grid order), so its wait is short and runs
+// beside the W stream instead of after it.
+//
+// A W workgroup loads its member's T right at its start next to its rows of
+// W (one entry per thread); if T was not complete yet (only the first
+// workgroups, which run next to the T workgroups), it loads it again after
+// its dot products, in a bounded loop, and past the bound forms T itself
+// through the same routine (same bits).  If the keeper's own bounded wait
+// runs out, it sets the poison bit of the generation word instead of leaving
+// a generation that a late reader could share with the next call: from then
+// on every W workgroup forms T itself (same bits, slower) until the caller
+// zeroes the workspace again.  The caller's bound word, when set, bounds
+// both waits.
 struct FusedArgs {
   GroupArgs ga;
-  uint32_t* ctl;  // control words (layout below), zero between calls
-  float* tbuf;    // T [G][kStreamRows][RP]
-  int nT;         // T workgroups per member (RP / 4)
-  int nWB;        // W workgroups per member (ceil(N / 16))
-  int total;      // workgroups of the launch
-  int nbk;        // buckets of the completion count
+  uint32_t* ctl;   // control words (layout below)
+  uint64_t* tsl;   // tagged T [G][kStreamRows][RP]: (tag << 32) | value bits
+  int nT;          // T workgroups per member (RP / 4)
+  int nWB;         // W workgroups per member (ceil(N / 16))
+  int total;       // T and W workgroups; workgroup `total` is the keeper
+  int nbk;         // count buckets in use
 };
-// Control words, one 128-byte line each where many workgroups update them
-// (atomics on one address serialise at the memory side, ~15 ns each): line 0
-// holds the per-member T counters and the wait bound, line 1 is spare, lines
-// 2 .. 2 + kFusedBuckets count the completed workgroups of each bucket
-// (bucket = workgroup id mod nbk).
-constexpr int kCtlLine = 32;  // words per line
+// Control words.  Line 0 holds the caller's wait bound (word kCtlBound);
+// line 1 is spare; line 2 + q (q < kFusedBuckets) holds the 64-bit word of
+// bucket q: low half the count of workgroups b with b % nbk == q that have
+// read the generation in this call, high half a copy of the generation word
+// (every line holds the same copy: the reads spread over the lines).
+constexpr int kCtlLine = 32;  // 32-bit words per 128-byte line
 constexpr int kCtlBound = kMaxGroup;
 constexpr int kCtlBucket0 = 2 * kCtlLine;
 static_assert(kFusedCtlBytes == HYDRA_GROUP_WS_CONTROL_BYTES && kCtlBound == HYDRA_GROUP_WS_BOUND_WORD,
               "control area as documented in hydra.h");
+static_assert(kFusedCtlBytes == size_t(kCtlBucket0 / kCtlLine + kFusedBuckets) * 128, "bucket lines");
+static_assert(kFusedTSlotBytes == HYDRA_GROUP_WS_T_BYTES, "T region as documented in hydra.h");
+constexpr uint32_t kPoison = 1u << 31;
+constexpr uint32_t kGenMask = kPoison - 1;
 constexpr uint32_t kDefaultWaitBound = 1u << 18;  // s_sleep(1) rounds (~10 ms)
 constexpr uint32_t kFinalWaitBound = 1u << 24;    // s_sleep(1) rounds (~1 s)
 
 __device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ float ld_dev(const float* p) {
+__device__ __forceinline__ uint64_t ld_dev(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void st_dev(float* p, float v) {
+__device__ __forceinline__ void st_dev(uint64_t* p, uint64_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void st_dev(uint32_t* p, uint32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ uint64_t* bucket_word(uint32_t* ctl, int q) {
+  return reinterpret_cast<uint64_t*>(ctl + kCtlBucket0 + q * kCtlLine);
 }
-// this wave's vector-memory operations complete
-__device__ __forceinline__ void wait_vm_all() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), expcnt / lgkmcnt untouched
-  asm volatile("" ::: "memory");
-}
-
-// acc[m] = <x[m], row> for the MB rows of x (rows past M and k past K read as
-// zeros), one wave per row, the workgroup's x staged in LDS by all its waves
-// together (every wave of the workgroup must call this).  Afterwards lane l
-// holds in acc[0] the total of row reduced_index<MB>(l).
-template <int MB>
-__device__ __forceinline__ void wave_row_dot(const uint16_t* row, bool row_ok, const uint16_t* X, int M, int K,
-                                             uint4* xsh, int t, int lane, float (&acc)[MB]) {
-  constexpr int SEG = XSeg<MB>::SEG;
-  const __amdgpu_buffer_rsrc_t wrs = make_rsrc(row_ok ? row : nullptr, row_ok ? (uint32_t)K * 2u : 0u);
-  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(X, (uint32_t)M * K * 2u);
-  const int nch = (K + DKC - 1) / DKC;
-#pragma unroll
-  for (int m = 0; m < MB; ++m) acc[m] = 0.f;
-  for (int c0 = 0; c0 < nch; c0 += SEG) {
-    uint4 wb[SEG];
-#pragma unroll
-    for (int u = 0; u < SEG; ++u) {
-      const int c = c0 + u, k = c * DKC + lane * 8;
-      wb[u] = buf_load16(wrs, (c < nch && k < K) ? k * 2 : kOutOfRange);
-    }
-    if (c0 > 0) __syncthreads();  // every wave is done with the previous x segment
-    stage_x<MB, SW * 64>(xsh, xrs, c0, nch, K, t);
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < SEG; ++u)
-#pragma unroll
-      for (int m = 0; m < MB; ++m) acc[m] = dot8(wb[u], xsh[(m * SEG + u) * 64 + lane], acc[m]);
-  }
-  wave_reduce_scatter<MB>(acc, lane);
-}
+// The tag that T values of a call with generation word w carry.
+__device__ __forceinline__ uint32_t tag_of(uint32_t w) { return (w + 1u) & kGenMask; }
 
 // T rows j0 .. j0 + 3 of one member: T[m][j] = <x[m], A[j]> for rows j < r
-// (zero otherwise), written to dst[m * ld + j] for m < M.  Wave w takes row
-// j0 + w / 4 and the chunks c with c % 4 == w % 4 of every x segment, so a
-// block of four rows costs each wave a quarter of a row; the four partial
-// sums of a row are added in chunk-class order through LDS.  Every wave of
-// the workgroup must call this; it ends with a workgroup barrier.
+// (zero otherwise).  Thread t < 4 MB (wave 0) gets the value of row
+// j0 + t / MB, m = t % MB.  Wave w takes row j0 + w / 4 and the chunks c with
+// c % 4 == w % 4 of every x segment, so a block of four rows costs each wave
+// a quarter of a row; the four partial sums of a row are added in
+// chunk-class order through LDS.  Every wave of the workgroup must call
+// this; it ends with a workgroup barrier.
 constexpr int kTRows = 4;   // rows of A per T block
 constexpr int kTSplit = SW / kTRows;
-template <int MB, bool COHERENT>
-__device__ __forceinline__ void t_rows_dot(const uint16_t* A, int r, int j0, const uint16_t* X, int M, int K,
-                                           uint4* xsh, float (*tpart)[MB], float* dst, int ld, int t, int lane,
-                                           int wave) {
+template <int MB>
+__device__ __forceinline__ float t_rows_dot(const uint16_t* A, int r, int j0, const uint16_t* X, int M, int K,
+                                            uint4* xsh, float (*tpart)[MB], int t, int lane, int wave) {
   constexpr int SEG = XSeg<MB>::SEG;
   static_assert(SEG % kTSplit == 0, "every wave takes whole chunks of each segment");
+  static_assert(kTRows * MB <= 64, "the stores stay in wave 0");
   const int j = j0 + wave / kTSplit;
   const int cls = wave % kTSplit;
   const bool ok = j < r;
@@ -674,19 +665,15 @@ __device__ __forceinline__ void t_rows_dot(const uint16_t* A, int r, int j0, con
   wave_reduce_scatter<MB>(acc, lane);
   if (reduced_writer<MB>(lane)) tpart[wave][reduced_index<MB>(lane)] = acc[0];
   __syncthreads();
+  float v = 0.f;
   if (t < kTRows * MB) {
     const int q = t / MB, m = t % MB;
-    float v = tpart[q * kTSplit][m];
+    v = tpart[q * kTSplit][m];
 #pragma unroll
     for (int c = 1; c < kTSplit; ++c) v += tpart[q * kTSplit + c][m];
-    if (m < M) {
-      if constexpr (COHERENT)
-        st_dev(&dst[m * ld + j0 + q], v);
-      else
-        dst[m * ld + j0 + q] = v;
-    }
   }
   __syncthreads();
+  return v;
 }
 
 template <int MB, int RP>
@@ -699,6 +686,35 @@ __global__ __launch_bounds__(SW * 64, 8) void gemv_fused_kernel(FusedArgs fa) {
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int bid = blockIdx.x;
   const int nTall = ga.G * fa.nT;
+  if (RP > 0 && bid == fa.total) {
+    // ---------------------------------------------- the keeper
+    // Lane q < nbk watches bucket q: one load per poll for all buckets.
+    if (wave != 0) return;
+    const int q = lane;
+    const bool mine = q < fa.nbk;
+    const uint32_t want = mine ? (uint32_t)((fa.total - q + fa.nbk - 1) / fa.nbk) : 0u;
+    uint32_t bound = ld_dev(&fa.ctl[kCtlBound]);
+    if (bound == 0u) bound = kFinalWaitBound;
+    uint64_t w = ld_dev(bucket_word(fa.ctl, mine ? q : 0));
+    uint32_t it = 0;
+    bool done;
+    while (!(done = __builtin_amdgcn_ballot_w64(mine && (uint32_t)w < want) == 0ull) && ++it < bound) {
+      __builtin_amdgcn_s_sleep(1);
+      w = ld_dev(bucket_word(fa.ctl, mine ? q : 0));
+    }
+    // every copy of the generation word is the same; past the bound the
+    // poison bit is set and stays set
+    const uint32_t gw = __builtin_amdgcn_readfirstlane((uint32_t)(w >> 32));
+    const uint32_t next = tag_of(gw) | (gw & kPoison) | (done ? 0u : kPoison);
+    if (q < kFusedBuckets) st_dev(bucket_word(fa.ctl, q), (uint64_t)next << 32);
+    return;
+  }
+  // Read the generation word and report the read (one returning atomic; its
+  // value is waited for only where it is used).
+  uint64_t gword = 0;
+  if (RP > 0 && wave == 0 && lane == 0)
+    gword = __hip_atomic_fetch_add(bucket_word(fa.ctl, bid % fa.nbk), uint64_t(1), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
   float acc[MB];
   if (bid < nTall) {
     // ---------------------------------------------- rows of A: T of one member
@@ -706,192 +722,155 @@ __global__ __launch_bounds__(SW * 64, 8) void gemv_fused_kernel(FusedArgs fa) {
     const bool on = ga.y_on[gi] != nullptr && ga.A[gi] != nullptr && ga.B[gi] != nullptr;
     if (on) {
       __shared__ float tpart[SW][MB];
-      t_rows_dot<MB, true>(ga.A[gi], r, jb * kTRows, ga.x[gi], M, K, xsh, tpart, fa.tbuf + gi * kStreamRows * TS, TS,
-                           t, lane, wave);
-      wait_vm_all();  // this thread's T values are stored
+      const float v = t_rows_dot<MB>(ga.A[gi], r, jb * kTRows, ga.x[gi], M, K, xsh, tpart, t, lane, wave);
+      if (wave == 0) {
+        // (the whole wave is active here, lane 0 holds the atomic's value)
+        const uint64_t tag = tag_of(__builtin_amdgcn_readfirstlane((uint32_t)(gword >> 32)));
+        const int q = t / MB, m = t % MB;
+        if (t < kTRows * MB && m < M)
+          st_dev(&fa.tsl[(gi * kStreamRows + m) * TS + jb * kTRows + q], (tag << 32) | __float_as_uint(v));
+      }
     }
-    __syncthreads();
-    if (t == 0) {
-      __hip_atomic_fetch_add(&fa.ctl[gi], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      wait_vm_all();  // the count has landed before this workgroup reports completion
+    return;
+  }
+  // ---------------------------------------------- rows of W
+  // Every thread requests one entry of its member's T (tagged; MB x RP <=
+  // 1024 entries, one per thread) and its row of B next to its first half
+  // segment of W; after the first x stage (which waits for all of them) each
+  // checks its tag and puts the value in LDS.  Up to 4 rows of x, the rows
+  // of W stream in segments of half the staging width (4 KB per wave), so
+  // that a thread whose entry was not published yet requests it again just
+  // before the last segment's loads, behind half of this workgroup's loads
+  // instead of all of them; the shallower queue also serves the rows of W
+  // faster.  At 8 rows the segments stay whole (2 KB per wave already).
+  constexpr int SEG = MB <= 4 ? XSeg<MB>::SEG / 2 : XSeg<MB>::SEG;
+  constexpr int RPL = (TS + 63) / 64;  // j values per lane
+  static_assert(MB * TS <= SW * 64, "one T entry per thread");
+  __shared__ float tsh[MB][TS];
+  __shared__ uint32_t gw_sh, okw[SW];
+  const int idx = bid - nTall;
+  const int gi = idx / fa.nWB, nb = idx - (idx / fa.nWB) * fa.nWB;
+  const int n = nb * 16 + wave;
+  const bool row_ok = n < N;
+  float* const yo = ga.y_off[gi];
+  float* const yn = ga.y_on[gi];
+  const bool on = RP > 0 && yn != nullptr && ga.A[gi] != nullptr && ga.B[gi] != nullptr;
+  const __amdgpu_buffer_rsrc_t wrs =
+      make_rsrc(row_ok ? ga.W[gi] + (size_t)n * K : nullptr, row_ok ? (uint32_t)K * 2u : 0u);
+  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(ga.x[gi], (uint32_t)M * K * 2u);
+  const int nch = (K + DKC - 1) / DKC;
+  // this thread's T entry: row t / TS, j = t % TS (the slots of a member are
+  // [kStreamRows][TS], so the entry is slot t)
+  const bool tent = on && t < MB * TS && t / TS < M;
+  const uint64_t* const tslot = fa.tsl + (size_t)gi * kStreamRows * TS + t;
+  // tag check of this thread's entry, value into LDS, one flag per wave;
+  // returns whether this entry is good
+  auto take_t = [&](uint64_t raw) __attribute__((always_inline)) -> bool {
+    const bool good = !tent || (uint32_t)(raw >> 32) == tag_of(gw_sh);
+    if (tent) tsh[t / TS][t % TS] = __uint_as_float((uint32_t)raw);
+    const uint64_t bad = __builtin_amdgcn_ballot_w64(!good);
+    if (lane == 0) okw[wave] = bad == 0ull ? 1u : 0u;
+    return good;
+  };
+  // every wave's flag (after a barrier); wave-uniform
+  auto all_ok = [&]() __attribute__((always_inline)) -> bool {
+    uint32_t v = (gw_sh & kPoison) == 0u ? 1u : 0u;
+#pragma unroll
+    for (int w = 0; w < SW; ++w) v &= okw[w];
+    return v != 0u;
+  };
+#pragma unroll
+  for (int m = 0; m < MB; ++m) acc[m] = 0.f;
+  float bv[RPL];
+#pragma unroll
+  for (int q = 0; q < RPL; ++q) bv[q] = 0.f;
+  uint64_t traw = 0;
+  if (tent) traw = ld_dev(tslot);
+  bool stale = false;  // this thread's entry failed its last check
+  for (int c0 = 0; c0 < nch; c0 += SEG) {
+    const bool again = c0 > 0 && c0 + SEG >= nch && stale;  // the last segment: request the entry again
+    if (again) traw = ld_dev(tslot);
+    uint4 wb[SEG];
+#pragma unroll
+    for (int u = 0; u < SEG; ++u) {
+      const int c = c0 + u, k = c * DKC + lane * 8;
+      wb[u] = buf_load16(wrs, (c < nch && k < K) ? k * 2 : kOutOfRange);
     }
-  } else {
-    // ---------------------------------------------- rows of W
-    // Wave 0 reads the member's T counter before it requests its row of W
-    // and, when the counter is complete, requests T (device-coherent loads:
-    // a handful of requests per workgroup); every wave requests its row of B
-    // next to its row of W.  After the dot products wave 0 shares T through
-    // LDS.  A workgroup that started before T was published (only the first
-    // ones, which run next to the T workgroups) polls the counter after its
-    // dot products (bounded), or forms T itself.
-    constexpr int SEG = XSeg<MB>::SEG;
-    constexpr int RPL = (TS + 63) / 64;  // j values per lane
-    __shared__ float tsh[MB][TS];
-    __shared__ uint32_t seen_sh;
-    const int idx = bid - nTall;
-    const int gi = idx / fa.nWB, nb = idx - (idx / fa.nWB) * fa.nWB;
-    const int n = nb * 16 + wave;
-    const bool row_ok = n < N;
-    float* const yo = ga.y_off[gi];
-    float* const yn = ga.y_on[gi];
-    const bool on = RP > 0 && yn != nullptr && ga.A[gi] != nullptr && ga.B[gi] != nullptr;
-    const __amdgpu_buffer_rsrc_t wrs =
-        make_rsrc(row_ok ? ga.W[gi] + (size_t)n * K : nullptr, row_ok ? (uint32_t)K * 2u : 0u);
-    const __amdgpu_buffer_rsrc_t xrs = make_rsrc(ga.x[gi], (uint32_t)M * K * 2u);
-    const int nch = (K + DKC - 1) / DKC;
-#pragma unroll
-    for (int m = 0; m < MB; ++m) acc[m] = 0.f;
-    float bv[RPL], tv[MB][RPL];
-#pragma unroll
-    for (int q = 0; q < RPL; ++q) {
-      bv[q] = 0.f;
-#pragma unroll
-      for (int mm = 0; mm < MB; ++mm) tv[mm][q] = 0.f;
-    }
-    // T of the member into tv, read by the lanes j % 64 of this wave
-    auto load_t = [&]() __attribute__((always_inline)) {
+    if (c0 == 0 && on) {
+      const __amdgpu_buffer_rsrc_t brs =
+          make_rsrc(row_ok ? ga.B[gi] + (size_t)n * r : nullptr, row_ok ? (uint32_t)r * 2u : 0u);
 #pragma unroll
       for (int q = 0; q < RPL; ++q) {
         const int jj = q * 64 + lane;
-#pragma unroll
-        for (int mm = 0; mm < MB; ++mm)
-          tv[mm][q] = (jj < TS && mm < M) ? ld_dev(&fa.tbuf[(gi * kStreamRows + mm) * TS + jj]) : 0.f;
+        bv[q] = bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(brs, jj < r ? jj * 2 : kOutOfRange, 0, 0));
       }
-    };
-    uint32_t seen = 0u;
-    if (on && wave == 0) seen = ld_dev(&fa.ctl[gi]);
-    for (int c0 = 0; c0 < nch; c0 += SEG) {
-      uint4 wb[SEG];
-#pragma unroll
-      for (int u = 0; u < SEG; ++u) {
-        const int c = c0 + u, k = c * DKC + lane * 8;
-        wb[u] = buf_load16(wrs, (c < nch && k < K) ? k * 2 : kOutOfRange);
-      }
-      if (c0 == 0 && on) {
-        const __amdgpu_buffer_rsrc_t brs =
-            make_rsrc(row_ok ? ga.B[gi] + (size_t)n * r : nullptr, row_ok ? (uint32_t)r * 2u : 0u);
-#pragma unroll
-        for (int q = 0; q < RPL; ++q) {
-          const int jj = q * 64 + lane;
-          bv[q] = bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(brs, jj < r ? jj * 2 : kOutOfRange, 0, 0));
-        }
-        if (wave == 0) {
-          if (seen >= (uint32_t)fa.nT) load_t();
-          if (lane == 0) seen_sh = seen;
-        }
-      }
-      if (c0 > 0) __syncthreads();  // every wave is done with the previous x segment
-      stage_x<MB, SW * 64>(xsh, xrs, c0, nch, K, t);
-      __syncthreads();
-#pragma unroll
-      for (int u = 0; u < SEG; ++u)
-#pragma unroll
-        for (int m = 0; m < MB; ++m) acc[m] = dot8(wb[u], xsh[(m * SEG + u) * 64 + lane], acc[m]);
     }
-    wave_reduce_scatter<MB>(acc, lane);
-    const int m = reduced_index<MB>(lane);
-    const bool writer = reduced_writer<MB>(lane) && m < M && row_ok;
-    if (writer && yo) yo[(size_t)m * N + n] = acc[0];
-    if (on) {
-      if (seen_sh < (uint32_t)fa.nT) {
-        // T was not published when this workgroup started
-        if (wave == 0) {
-          uint32_t bound = ld_dev(&fa.ctl[kCtlBound]);
-          if (bound == 0u) bound = kDefaultWaitBound;
-          uint32_t it = 0;
-          seen = ld_dev(&fa.ctl[gi]);
-          while (seen < (uint32_t)fa.nT && ++it < bound) {
-            __builtin_amdgcn_s_sleep(1);
-            seen = ld_dev(&fa.ctl[gi]);
-          }
-          if (seen >= (uint32_t)fa.nT) load_t();
-        }
-        __syncthreads();  // every wave has read seen_sh
-        if (wave == 0 && lane == 0) seen_sh = seen;
-        __syncthreads();
-        if (seen_sh < (uint32_t)fa.nT) {
-          // T formed here, block by block as the T workgroups do
-          __shared__ float tpart2[SW][MB];
-          for (int q = t; q < MB * TS; q += SW * 64) tsh[q / TS][q % TS] = 0.f;
-          for (int jb = 0; jb < fa.nT; ++jb)
-            t_rows_dot<MB, false>(ga.A[gi], r, jb * kTRows, ga.x[gi], M, K, xsh, tpart2, &tsh[0][0], TS, t, lane,
-                                  wave);
+    if (c0 > 0) __syncthreads();  // every wave is done with the previous x segment
+    stage_x<MB, SW * 64, SEG>(xsh, xrs, c0, nch, K, t);
+    if (c0 == 0 && on && t == 0) gw_sh = (uint32_t)(gword >> 32);
+    __syncthreads();
+    if (on && (c0 == 0 || __builtin_amdgcn_ballot_w64(again) != 0ull)) stale = !take_t(traw);
 #pragma unroll
-          for (int q = 0; q < RPL; ++q) {
-            const int jj = q * 64 + lane;
+    for (int u = 0; u < SEG; ++u)
 #pragma unroll
-            for (int mm = 0; mm < MB; ++mm) tv[mm][q] = jj < TS ? tsh[mm][jj] : 0.f;
-          }
-        }
-      }
-      if (seen_sh >= (uint32_t)fa.nT) {
-        // wave 0 shares the T it read
-        if (wave == 0) {
-#pragma unroll
-          for (int q = 0; q < RPL; ++q) {
-            const int jj = q * 64 + lane;
-            if (jj < TS) {
-#pragma unroll
-              for (int mm = 0; mm < MB; ++mm) tsh[mm][jj] = tv[mm][q];
-            }
-          }
-        }
-        __syncthreads();
-#pragma unroll
-        for (int q = 0; q < RPL; ++q) {
-          const int jj = q * 64 + lane;
-#pragma unroll
-          for (int mm = 0; mm < MB; ++mm) tv[mm][q] = jj < TS ? tsh[mm][jj] : 0.f;
-        }
-      }
-      // d[m] = sum_j T[m][j] B[n][j]: lane l holds j = l, l + 64
-      float part[MB];
-#pragma unroll
-      for (int mm = 0; mm < MB; ++mm) {
-        part[mm] = 0.f;
-#pragma unroll
-        for (int q = 0; q < RPL; ++q) part[mm] = fmaf(tv[mm][q], bv[q], part[mm]);
-      }
-      wave_reduce_scatter<MB>(part, lane);
-      if (writer) yn[(size_t)m * N + n] = acc[0] + ga.s[gi] * part[0];
-    } else if (writer && yn) {
-      yn[(size_t)m * N + n] = acc[0];
-    }
+      for (int m = 0; m < MB; ++m) acc[m] = dot8(wb[u], xsh[(m * SEG + u) * 64 + lane], acc[m]);
   }
-  // Completion: every workgroup but the last one dispatched adds one to its
-  // bucket (no return value, so nothing waits for it); the last one, which
-  // starts after every other has started, waits until every bucket is full
-  // (every other workgroup is past its reads of the counters) and clears the
-  // counters for the next call.  Its wait is bounded too; past the bound it
-  // clears them anyway (a workgroup that still had to read them would find
-  // its member's T counter at zero and form T itself).
-  if constexpr (RP > 0) {
-    if (fa.nT > 0 && wave == 0) {
-      if (bid != fa.total - 1) {
-        if (lane == 0)
-          __hip_atomic_fetch_add(&fa.ctl[kCtlBucket0 + (bid % fa.nbk) * kCtlLine], 1u, __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_AGENT);
-      } else {
-        // lane q < nbk watches bucket q: one load per poll for all buckets
-        const int q = lane;
-        const bool mine = q < fa.nbk;
-        const uint32_t want =
-            mine ? (uint32_t)((fa.total - q + fa.nbk - 1) / fa.nbk) - (q == bid % fa.nbk ? 1u : 0u) : 0u;
-        uint32_t it = 0;
-        while (__builtin_amdgcn_ballot_w64(mine && ld_dev(&fa.ctl[kCtlBucket0 + (mine ? q : 0) * kCtlLine]) < want) !=
-                   0ull &&
-               ++it < kFinalWaitBound)
-          __builtin_amdgcn_s_sleep(1);
-        if (lane < ga.G) st_dev(&fa.ctl[lane], 0u);
-        if (mine) st_dev(&fa.ctl[kCtlBucket0 + q * kCtlLine], 0u);
+  wave_reduce_scatter<MB>(acc, lane);
+  const int m = reduced_index<MB>(lane);
+  const bool writer = reduced_writer<MB>(lane) && m < M && row_ok;
+  if (writer && yo) yo[(size_t)m * N + n] = acc[0];
+  if (on) {
+    __syncthreads();  // every wave's flag and T entry are in LDS
+    if (!all_ok()) {
+      // T was not complete when this workgroup requested it: load it again
+      // (bounded; the decision is taken by the whole workgroup), or form it here
+      bool ready = false;
+      if ((gw_sh & kPoison) == 0u) {
+        uint32_t bound = ld_dev(&fa.ctl[kCtlBound]);
+        if (bound == 0u) bound = kDefaultWaitBound;
+        for (uint32_t it = 0; it < bound; ++it) {
+          if (it > 0) __builtin_amdgcn_s_sleep(1);
+          __syncthreads();  // every wave has read the previous flags
+          take_t(tent ? ld_dev(tslot) : uint64_t(0));
+          __syncthreads();
+          if ((ready = all_ok())) break;
+        }
+      }
+      if (!ready) {
+        // T formed here, block by block as the T workgroups do
+        __shared__ float tpart2[SW][MB];
+        __syncthreads();  // every wave is done with the flags and tsh
+        for (int q = t; q < MB * TS; q += SW * 64) tsh[q / TS][q % TS] = 0.f;
+        for (int jb = 0; jb < fa.nT; ++jb) {
+          const float v = t_rows_dot<MB>(ga.A[gi], r, jb * kTRows, ga.x[gi], M, K, xsh, tpart2, t, lane, wave);
+          const int q = t / MB, mm = t % MB;
+          if (t < kTRows * MB && mm < M) tsh[mm][jb * kTRows + q] = v;
+        }
+        __syncthreads();
       }
     }
+    // d[m] = sum_j T[m][j] B[n][j]: lane l holds j = l, l + 64
+    float part[MB];
+#pragma unroll
+    for (int mm = 0; mm < MB; ++mm) {
+      part[mm] = 0.f;
+#pragma unroll
+      for (int q = 0; q < RPL; ++q) {
+        const int jj = q * 64 + lane;
+        part[mm] = fmaf(jj < TS && mm < M ? tsh[mm][jj] : 0.f, bv[q], part[mm]);
+      }
+    }
+    wave_reduce_scatter<MB>(part, lane);
+    if (writer) yn[(size_t)m * N + n] = acc[0] + ga.s[gi] * part[0];
+  } else if (writer && yn) {
+    yn[(size_t)m * N + n] = acc[0];
   }
 }
 
 template <int MB>
 hipError_t launch_fused_mb(const FusedArgs& fa, int rp, hipStream_t stream) {
-  const dim3 grid(fa.total), block(SW * 64);
+  // the keeper runs only where there is T to publish
+  const dim3 grid(fa.total + (rp > 0 ? 1 : 0)), block(SW * 64);
   switch (rp) {
     case 0: hipLaunchKernelGGL((gemv_fused_kernel<MB, 0>), grid, block, 0, stream, fa); break;
     case 16: hipLaunchKernelGGL((gemv_fused_kernel<MB, 16>), grid, block, 0, stream, fa); break;
@@ -923,7 +902,7 @@ hipError_t launch_gemv_fused(const GroupArgs& g, void* ws, hipStream_t stream) {
   FusedArgs fa{};
   fa.ga = g;
   fa.ctl = static_cast<uint32_t*>(ws);
-  fa.tbuf = reinterpret_cast<float*>(static_cast<char*>(ws) + kFusedCtlBytes);
+  fa.tsl = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + kFusedCtlBytes);
   fa.nT = rp / kTRows;
   fa.nWB = (g.N + SW - 1) / SW;
   fa.total = g.G * (fa.nT + fa.nWB);

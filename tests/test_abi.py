@@ -330,21 +330,30 @@ def test_group_ws_rejects(kw, code):
 
 
 def test_group_ws_workspace_bytes():
-    """The control words, then the published T (G x 8 rows x padded rank fp32) up to 16 rows, or above 16
-    rows at padded rank 128 the pre-pass workspace of hydra_lora_linear_ws."""
+    """The control words and the tagged T region (a fixed size, so calls of any shape find only their own or older
+    tags there), then above 16 rows at padded rank 128 the pre-pass workspace of hydra_lora_linear_ws."""
     gb = H.hydra_lora_linear_group_workspace_bytes
     C = H.HYDRA_GROUP_WS_CONTROL_BYTES
-    assert C == 34 * 128  # a line of T counters, a line of completed buckets, 32 bucket lines
-    assert gb(4, 4, 4096, 16) == C + 4 * 8 * 16 * 4
-    assert gb(4, 6, 2048, 128) == C + 4 * 8 * 128 * 4
-    assert gb(1, 1, 10, 0) == C
-    assert gb(8, 16, 100, 9) == C + 8 * 8 * 16 * 4
-    assert gb(3, 2048, 4096, 16) == C                                         # rank <= 64 above 16 rows: no body
-    assert gb(3, 2048, 4096, 128) == C + H.hydra_lora_linear_workspace_bytes(2048, 4096, 128)
+    T = H.HYDRA_GROUP_WS_T_BYTES
+    assert C == 34 * 128  # a line with the caller's bound word, a spare line, 32 bucket lines
+    assert T == 8 * 8 * 128 * 8  # up to 8 members x 8 rows x rank 128, 64-bit tagged entries
+    for args in ((4, 4, 4096, 16), (4, 6, 2048, 128), (1, 1, 10, 0), (8, 16, 100, 9), (3, 2048, 4096, 16)):
+        assert gb(*args) == C + T, args
+    assert gb(3, 2048, 4096, 128) == C + T + H.hydra_lora_linear_workspace_bytes(2048, 4096, 128)
     out = ctypes.c_size_t(0)
     assert H.lib().hydra_lora_linear_group_workspace_bytes(9, 4, 10, 0, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
     assert H.lib().hydra_lora_linear_group_workspace_bytes(1, 4, 10, 129, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
     assert H.lib().hydra_lora_linear_group_workspace_bytes(1, 4, 10, 8, None) == H.HYDRA_ERR_NULL
+
+
+def test_header_constants_match_the_binding():
+    """Every integer #define of include/hydra.h has the same value in the Python binding."""
+    txt = open(HEADER).read()
+    pat = r"#define\s+(HYDRA_[A-Z0-9_]+)\s+\(?([0-9]+)u?(?:\s*<<\s*([0-9]+))?"
+    defs = {m[0]: int(m[1]) << int(m[2] or 0) for m in re.findall(pat, txt)}
+    assert "HYDRA_GROUP_WS_T_BYTES" in defs and "HYDRA_GROUP_WS_CONTROL_BYTES" in defs
+    for name, val in defs.items():
+        assert getattr(Bd, name) == val, name
 
 
 def _multi(x_off=P, W=P, n_on=2, xs=(P, P), As=(P, P), Bs=(P, P), ss=(2.0, 2.0), M=4, N=64, K=64, r=8,

@@ -36,6 +36,25 @@ def _call(t, ws):
     return [host(v).copy() for v in t["yo"]], [None if v is None else host(v).copy() for v in t["yn"]]
 
 
+POISON = 1 << 31
+
+
+def _ctl(ws):
+    """(bucket counts, generation word copies) of the workspace's 32 bucket lines (line 2 + q: a 64-bit word, low
+    half the count, high half the generation word)."""
+    c = host(ws[:H.HYDRA_GROUP_WS_CONTROL_BYTES]).view(np.uint32)
+    lines = [2 * 32 + 32 * q for q in range(32)]
+    return [int(c[i]) for i in lines], [int(c[i + 1]) for i in lines]
+
+
+def _assert_generation(ws, launches, poisoned=False):
+    """After a call: every count cleared and every copy of the generation word advanced to `launches`."""
+    counts, gens = _ctl(ws)
+    assert counts == [0] * 32, counts
+    want = launches | (POISON if poisoned else 0)
+    assert gens == [want] * 32, (gens[:4], want)
+
+
 def _check(cases, go, gn, want_on=None):
     want_on = want_on or [True] * len(cases)
     for i, c in enumerate(cases):
@@ -60,8 +79,8 @@ def test_group_ws_decode_matches_oracle(M, K, N, r, G, dev):
     ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
     go, gn = _call(t, ws)
     _check(cases, go, gn)
-    # the control words are zero again after the call
-    assert int(host(ws[:H.HYDRA_GROUP_WS_CONTROL_BYTES]).astype(np.int64).sum()) == 0
+    # one launch: the counts are clear again and the generation has advanced by one (no keeper at rank 0)
+    _assert_generation(ws, 1 if r else 0)
 
 
 def test_group_ws_repeated_calls_reuse_the_workspace(dev):
@@ -83,7 +102,7 @@ def test_group_ws_repeated_calls_reuse_the_workspace(dev):
         if it in (3, 6, 9):  # seed 1200 again
             for i in range(G):
                 assert np.array_equal(go[i], first[0][i]) and np.array_equal(gn[i], first[1][i])
-    assert int(host(ws[:H.HYDRA_GROUP_WS_CONTROL_BYTES]).astype(np.int64).sum()) == 0
+    _assert_generation(ws, 10)
 
 
 def test_group_ws_members_without_adapter(dev):
@@ -100,7 +119,8 @@ def test_group_ws_members_without_adapter(dev):
 
 def test_group_ws_wait_bound_fallback_same_bits(dev):
     """With the wait bound word set to one round, workgroups that find T not yet published form it themselves
-    through the same routine: the bits are those of the default bound."""
+    through the same routine: the bits are those of the default bound.  If the keeper's wait ran out too, the
+    workspace stays poisoned (every later call forms T in every workgroup, same bits) until it is zeroed."""
     import torch
     say("group_ws wait bound")
     M, K, N, r, G = 6, 4096, 2048, 128, 4
@@ -109,6 +129,7 @@ def test_group_ws_wait_bound_fallback_same_bits(dev):
     ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
     go, gn = _call(t, ws)
     _check(cases, go, gn)
+    _assert_generation(ws, 1)
     bw = 4 * H.HYDRA_GROUP_WS_BOUND_WORD
     bound = ws[bw:bw + 4].view(torch.int32)  # the caller's wait bound word (0 selects the default)
     bound.fill_(1)
@@ -117,7 +138,40 @@ def test_group_ws_wait_bound_fallback_same_bits(dev):
         assert np.array_equal(go[i], go1[i]) and np.array_equal(gn[i], gn1[i]), i
     assert int(host(ws[bw:bw + 4].view(torch.int32))[0]) == 1  # the bound word is the caller's, not reset
     bound.fill_(0)
-    assert int(host(ws[:H.HYDRA_GROUP_WS_CONTROL_BYTES]).astype(np.int64).sum()) == 0
+    poisoned = (_ctl(ws)[1][0] & POISON) != 0
+    _assert_generation(ws, 2, poisoned)
+    go2, gn2 = _call(t, ws)
+    for i in range(G):
+        assert np.array_equal(go[i], go2[i]) and np.array_equal(gn[i], gn2[i]), i
+    _assert_generation(ws, 3, poisoned)  # poison is kept
+
+
+def test_group_ws_poisoned_workspace_same_bits_until_zeroed(dev):
+    """A workspace whose generation word carries the poison bit (what a keeper leaves when its bounded wait runs
+    out, set here from the host): every call forms T in every workgroup and gives the bits of a normal call, the
+    bit stays set, and zeroing the workspace restores normal calls."""
+    import torch
+    say("group_ws poisoned")
+    M, K, N, r, G = 4, 2048, 1024, 16, 4
+    cases = [WL.gen_linear(1450 + i, M, K, N, r) for i in range(G)]
+    t = _inputs(cases, dev)
+    ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
+    go, gn = _call(t, ws)
+    _check(cases, go, gn)
+    words = ws[:H.HYDRA_GROUP_WS_CONTROL_BYTES].view(torch.int32)
+    for q in range(32):
+        words[2 * 32 + 32 * q + 1] = (1 | POISON) - (1 << 32)  # the same bits as a signed 32-bit value
+    torch.cuda.synchronize()
+    for it in range(2):
+        go1, gn1 = _call(t, ws)
+        for i in range(G):
+            assert np.array_equal(go[i], go1[i]) and np.array_equal(gn[i], gn1[i]), (it, i)
+        _assert_generation(ws, 2 + it, poisoned=True)
+    ws.zero_()
+    go2, gn2 = _call(t, ws)
+    for i in range(G):
+        assert np.array_equal(go[i], go2[i]) and np.array_equal(gn[i], gn2[i]), i
+    _assert_generation(ws, 1)
 
 
 @pytest.mark.parametrize("M,r", [(12, 16), (16, 128), (130, 16), (130, 128)])
@@ -131,7 +185,8 @@ def test_group_ws_above_decode_rows(M, r, dev):
     ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
     go, gn = _call(t, ws)
     _check(cases, go, gn)
-    assert int(host(ws[:H.HYDRA_GROUP_WS_CONTROL_BYTES]).astype(np.int64).sum()) == 0
+    # the single launch runs only at rank 128 up to 16 rows (once per row half)
+    _assert_generation(ws, 2 if (M <= 16 and r > 64) else 0)
 
 
 def test_group_ws_decode_qkvo_full(dev):
@@ -146,7 +201,7 @@ def test_group_ws_decode_qkvo_full(dev):
 
 def test_group_ws_graph_replays(dev):
     """Captured in a HIP graph and replayed three times with eager work between the replays: every replay has the
-    bits of the eager call (each call leaves the control words zero for the next)."""
+    bits of the eager call (every launch, replayed or eager, advances the workspace's generation)."""
     import torch
     say("group_ws graph")
     M, K, N, r, G = 4, 1024, 512, 16, 4
@@ -168,3 +223,4 @@ def test_group_ws_graph_replays(dev):
         torch.cuda.synchronize()
         for i in range(G):
             assert np.array_equal(host(t["yo"][i]), eo[i]) and np.array_equal(host(t["yn"][i]), en[i]), (rep, i)
+    _assert_generation(ws, 1 + 3 * 2)
