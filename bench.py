@@ -465,8 +465,16 @@ def bench_advantages(torch, H, WL, dev, iters=30):
     vals = torch.empty(M, device=dev)
     r_out, a_out, ret_out = (torch.empty(M, device=dev) for _ in range(3))
 
+    # twenty sets of hidden states in rotation (320 MB, more than the 256 MB last-level cache), so that every
+    # launch reads cold data; the extra sets are seeded N(0, 1) draws on the device, for timing only
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(4096)
+    hs = [h] + [torch.randn(M, K, generator=gen, device=dev).to(torch.bfloat16).view(torch.int16) for _ in range(19)]
+    rot = [0]
+
     def vh():
-        H.hydra_value_head(h, w, vals)
+        H.hydra_value_head(hs[rot[0] % len(hs)], w, vals)
+        rot[0] += 1
 
     def gae():
         H.hydra_ppo_advantages(kl, rw, vals, adv.n_seq, adv.seq_len, a_out, ret_out, rewards=r_out, start=adv.start,
@@ -496,17 +504,18 @@ def bench_advantages(torch, H, WL, dev, iters=30):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / iters * 1e3
 
-    vh()
+    H.hydra_value_head(h, w, vals)
     gae()
     t_vh, t_gae, t_loss = timed(vh), timed(gae), timed(loss)
+    del hs
     vh_bytes = 2.0 * M * K + 2.0 * K + 4.0 * M
     gae_bytes = 4.0 * M * 2 + 4.0 * adv.n_seq + 4.0 * M * 3
     loss_bytes = 4.0 * M * 5 + 4.0 * M * 2 + 12.0
     return dict(tokens=M, K=K, value_head_us=round(t_vh, 2), value_head_gbps=round(vh_bytes / t_vh / 1e3, 1),
                 value_head_frac_hbm=round(vh_bytes / t_vh / 1e3 / PEAK_HBM_GBPS, 4), gae_us=round(t_gae, 2),
                 gae_bytes=int(gae_bytes), ppo_loss_us=round(t_loss, 2), ppo_loss_bytes=int(loss_bytes),
-                note="average over back-to-back launches (launch gaps included); the 16 MB of hidden states stay "
-                     "in the last-level cache between iterations")
+                note="average over back-to-back launches (launch gaps included); the value head reads twenty "
+                     "rotating 16 MB sets of hidden states (cold); GAE and the losses read their few hundred KB hot")
 
 
 def bench_decode_multi(torch, H, WL, dev, iters=20, sets=3):
