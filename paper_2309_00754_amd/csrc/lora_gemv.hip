@@ -867,6 +867,138 @@ __global__ __launch_bounds__(SW * 64, 8) void gemv_fused_kernel(FusedArgs fa) {
   }
 }
 
+// ---------------------------------------------------------------- decode in one launch, small ranks
+// At padded rank 16 and up to 4 rows of x the rows of A are few (16 per
+// member: 64 KB at K = 2048, read from L2 after the first workgroup of each
+// XCD) and their registers fit beside those of W (at rank 32, or 8 rows, the
+// kernel would spill; those run the published-T kernel below), so every
+// workgroup forms T = x A^T itself: wave w streams its row of W and row w of
+// A against the same staged x, in the same segments, so the
+// A requests ride with the W requests and no workgroup waits for another.
+// T is reduced by the same butterfly as the rows of W (the same bits in every
+// workgroup) and shared through LDS.  Each segment issues its x loads first,
+// then the rows of W and A (the first also the row of B), all unconditional
+// (out-of-range offsets where there is nothing to load), so that the
+// compiler's waits count exactly the requests issued after the one they wait
+// for: waiting for x never waits for W, and the dot products wait for each
+// chunk as it arrives.
+template <int MB, int RP>
+__global__ __launch_bounds__(SW * 64, 8) void gemv_selft_kernel(GroupArgs ga) {
+  static_assert((RP == 0 || RP == 16) && MB <= 4, "rank 0 or 16, up to 4 rows");
+  constexpr int AR = RP / 16;                            // rows of A per wave
+  constexpr int TS = RP > 0 ? RP : 1;
+  constexpr int SEG = MB <= 4 ? XSeg<MB>::SEG / 2 : XSeg<MB>::SEG;
+  constexpr int XE = MB * SEG * 64;                      // staged x elements per segment
+  constexpr int XPER = (XE + SW * 64 - 1) / (SW * 64);   // ... per thread
+  __shared__ uint4 xsh[XSeg<MB>::ELEMS];
+  __shared__ float tsh[MB][TS];
+  const int M = ga.M, N = ga.N, K = ga.K, r = ga.r;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int nWB = (N + SW - 1) / SW;
+  const int gi = blockIdx.x / nWB, nb = blockIdx.x - (blockIdx.x / nWB) * nWB;
+  const int n = nb * 16 + wave;
+  const bool row_ok = n < N;
+  float* const yo = ga.y_off[gi];
+  float* const yn = ga.y_on[gi];
+  const bool on = RP > 0 && yn != nullptr && ga.A[gi] != nullptr && ga.B[gi] != nullptr;
+  const __amdgpu_buffer_rsrc_t wrs =
+      make_rsrc(row_ok ? ga.W[gi] + (size_t)n * K : nullptr, row_ok ? (uint32_t)K * 2u : 0u);
+  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(ga.x[gi], (uint32_t)M * K * 2u);
+  const __amdgpu_buffer_rsrc_t brs =
+      make_rsrc(on && row_ok ? ga.B[gi] + (size_t)n * r : nullptr, on && row_ok ? (uint32_t)r * 2u : 0u);
+  __amdgpu_buffer_rsrc_t ars[AR > 0 ? AR : 1];
+#pragma unroll
+  for (int q = 0; q < AR; ++q) {
+    const int j = wave + 16 * q;
+    const bool ok = on && j < r;
+    ars[q] = make_rsrc(ok ? ga.A[gi] + (size_t)j * K : nullptr, ok ? (uint32_t)K * 2u : 0u);
+  }
+  const int nch = (K + DKC - 1) / DKC;
+  float acc[MB], tacc[AR > 0 ? AR : 1][MB];
+#pragma unroll
+  for (int m = 0; m < MB; ++m) {
+    acc[m] = 0.f;
+#pragma unroll
+    for (int q = 0; q < AR; ++q) tacc[q][m] = 0.f;
+  }
+  uint32_t braw = 0u;  // this lane's entry of the row of B (j = lane), converted in the epilogue
+  for (int c0 = 0; c0 < nch; c0 += SEG) {
+    uint4 xv[XPER];
+#pragma unroll
+    for (int q = 0; q < XPER; ++q) {
+      const int e = t + q * SW * 64;
+      const int m = e / (SEG * 64), u = (e / 64) % SEG, l = e % 64;
+      const int c = c0 + u, k = c * DKC + l * 8;
+      xv[q] = buf_load16(xrs, (e < XE && c < nch && k < K) ? (m * K + k) * 2 : kOutOfRange);
+    }
+    asm volatile("" ::: "memory");
+    uint4 wb[SEG], ab[AR > 0 ? AR : 1][SEG];
+#pragma unroll
+    for (int u = 0; u < SEG; ++u) {
+      const int c = c0 + u, k = c * DKC + lane * 8;
+      const int off = (c < nch && k < K) ? k * 2 : kOutOfRange;
+      wb[u] = buf_load16(wrs, off);
+#pragma unroll
+      for (int q = 0; q < AR; ++q) ab[q][u] = buf_load16(ars[q], off);
+    }
+    if constexpr (RP > 0) {
+      // (every segment issues it; past the first its offset is out of range)
+      const uint32_t bnew = __builtin_amdgcn_raw_buffer_load_b16(brs, c0 == 0 && lane < r ? lane * 2 : kOutOfRange, 0, 0);
+      braw |= bnew;  // zero except in the first segment
+    }
+    asm volatile("" ::: "memory");
+    if (c0 > 0) __syncthreads();  // every wave is done with the previous x segment
+#pragma unroll
+    for (int q = 0; q < XPER; ++q) {
+      const int e = t + q * SW * 64;
+      if (e < XE) xsh[e] = xv[q];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < SEG; ++u)
+#pragma unroll
+      for (int m = 0; m < MB; ++m) {
+        const uint4 xm = xsh[(m * SEG + u) * 64 + lane];
+        acc[m] = dot8(wb[u], xm, acc[m]);
+#pragma unroll
+        for (int q = 0; q < AR; ++q) tacc[q][m] = dot8(ab[q][u], xm, tacc[q][m]);
+      }
+  }
+  wave_reduce_scatter<MB>(acc, lane);
+  const int m = reduced_index<MB>(lane);
+  const bool writer = reduced_writer<MB>(lane) && m < M && row_ok;
+  if (writer && yo) yo[(size_t)m * N + n] = acc[0];
+  if constexpr (RP > 0) {
+    if (on) {
+#pragma unroll
+      for (int q = 0; q < AR; ++q) {
+        wave_reduce_scatter<MB>(tacc[q], lane);
+        if (reduced_writer<MB>(lane)) tsh[m][wave + 16 * q] = tacc[q][0];  // T[m][j] (zero for j >= r)
+      }
+      __syncthreads();
+      // d[m] = sum_j T[m][j] B[n][j]: lane l holds j = l
+      float part[MB];
+#pragma unroll
+      for (int mm = 0; mm < MB; ++mm) part[mm] = lane < RP && mm < M ? tsh[mm][lane] * bf16_to_f32(braw) : 0.f;
+      wave_reduce_scatter<MB>(part, lane);
+      if (writer) yn[(size_t)m * N + n] = acc[0] + ga.s[gi] * part[0];
+      return;
+    }
+  }
+  if (writer && yn) yn[(size_t)m * N + n] = acc[0];
+}
+
+template <int MB>
+hipError_t launch_selft_mb(const GroupArgs& g, int rp, hipStream_t stream) {
+  const dim3 grid(g.G * ((g.N + SW - 1) / SW)), block(SW * 64);
+  if (rp == 16)
+    hipLaunchKernelGGL((gemv_selft_kernel<MB, 16>), grid, block, 0, stream, g);
+  else
+    hipLaunchKernelGGL((gemv_selft_kernel<MB, 0>), grid, block, 0, stream, g);
+  return hipGetLastError();
+}
+
 template <int MB>
 hipError_t launch_fused_mb(const FusedArgs& fa, int rp, hipStream_t stream) {
   // the keeper runs only where there is T to publish
@@ -899,6 +1031,17 @@ hipError_t launch_gemv_fused(const GroupArgs& g, void* ws, hipStream_t stream) {
   bool any_on = false;
   for (int i = 0; i < g.G; ++i) any_on = any_on || (g.y_on[i] && g.A[i] && g.B[i]);
   const int rp = any_on ? padded_rank(g.r) : 0;
+  // Up to 4 rows: rank 0 takes the plain stream of gemv_selft_kernel (26.0
+  // against 26.4 us for the four Llama-7B projections), and rank 16 with
+  // K <= 2048 forms T in every workgroup (12.4 against 13.1 us for four
+  // 2048 x 2048 projections); the workspace is not used.  At K = 4096 the rows
+  // of A, as many bytes per workgroup as its rows of W, slow the stream more
+  // than the hand-off of published T costs (34.4 against 30.6 us).
+  if (g.M <= 4 && (rp == 0 || (rp == 16 && g.K <= 2048))) {
+    if (g.M <= 1) return launch_selft_mb<1>(g, rp, stream);
+    if (g.M <= 2) return launch_selft_mb<2>(g, rp, stream);
+    return launch_selft_mb<4>(g, rp, stream);
+  }
   FusedArgs fa{};
   fa.ga = g;
   fa.ctl = static_cast<uint32_t*>(ws);
