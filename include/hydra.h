@@ -240,13 +240,46 @@ hydra_status hydra_lora_linear_group_ws(int64_t G, const uint16_t* const* x, con
  * one adapter: one read of W instead of two); larger M runs one GEMM per input.
  * Every output has the bits of the corresponding hydra_lora_linear call.
  * Above M = 16 with adapters, a padded rank above 64 (r > 64) returns
- * HYDRA_ERR_WORKSPACE before anything is launched (the workspace call
- * hydra_lora_linear_ws serves that rank).
+ * HYDRA_ERR_WORKSPACE before anything is launched (hydra_lora_linear_multi_ws
+ * serves that rank).
  */
 hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, int64_t n_on,
                                      const uint16_t* const* x_on, const uint16_t* const* A,
                                      const uint16_t* const* B, const float* s, int64_t M, int64_t N, int64_t K,
                                      int64_t r, float* y_off, float* const* y_on, void* stream);
+
+/*
+ * hydra_lora_linear_multi_workspace_bytes -- device workspace that
+ * hydra_lora_linear_multi_ws needs for M rows, N outputs and rank r (writes
+ * *bytes): the workspace of hydra_lora_linear_ws, shared by the adapters in
+ * turn.  HYDRA_ERR_NULL / HYDRA_ERR_SHAPE as hydra_lora_linear_workspace_bytes.
+ */
+hydra_status hydra_lora_linear_multi_workspace_bytes(int64_t M, int64_t N, int64_t r, size_t* bytes);
+
+/*
+ * hydra_lora_linear_multi_ws -- hydra_lora_linear_multi with a caller
+ * workspace, so that the paper's rank 128 (App. B) runs at every M.  Defined
+ * by: the same passages as hydra_lora_linear_multi.
+ *
+ *   arguments as hydra_lora_linear_multi, plus
+ *   workspace, workspace_bytes   device, 16-byte aligned, at least
+ *                         hydra_lora_linear_multi_workspace_bytes(M, N, r)
+ *                         bytes; its contents need not be anything in
+ *                         particular, and the call overwrites them.
+ * Above M = 16 with adapters at a padded rank above 64, the LoRA-off input runs
+ * as hydra_lora_linear without an adapter and each adapter's input as
+ * hydra_lora_linear_ws (the pre-pass GEMM), in turn over the workspace: every
+ * output has the bits of that call.  Otherwise the call is
+ * hydra_lora_linear_multi (the workspace is not used).  Errors as in
+ * hydra_lora_linear_multi, plus HYDRA_ERR_NULL for a NULL workspace,
+ * HYDRA_ERR_WORKSPACE when it is too small for the rank-128 case,
+ * HYDRA_ERR_ALIGN when it is not 16-byte aligned; all before any launch.
+ */
+hydra_status hydra_lora_linear_multi_ws(const uint16_t* x_off, const uint16_t* W, int64_t n_on,
+                                        const uint16_t* const* x_on, const uint16_t* const* A,
+                                        const uint16_t* const* B, const float* s, int64_t M, int64_t N, int64_t K,
+                                        int64_t r, float* y_off, float* const* y_on, void* workspace,
+                                        size_t workspace_bytes, void* stream);
 
 /*
  * hydra_score_workspace_bytes -- device workspace that hydra_score needs for

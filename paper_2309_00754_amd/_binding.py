@@ -39,6 +39,8 @@ EXPORTED = (
     "hydra_lora_linear_group_workspace_bytes",
     "hydra_lora_linear_group_ws",
     "hydra_lora_linear_multi",
+    "hydra_lora_linear_multi_workspace_bytes",
+    "hydra_lora_linear_multi_ws",
     "hydra_score_workspace_bytes",
     "hydra_score",
     "hydra_score_noalloc",
@@ -100,6 +102,11 @@ def lib() -> ctypes.CDLL:
     L.hydra_lora_linear_multi.argtypes = [_vp, _vp, _i64, _pp, _pp, _pp, ctypes.POINTER(ctypes.c_float), _i64, _i64,
                                           _i64, _i64, _vp, _pp, _vp]
     L.hydra_lora_linear_multi.restype = ctypes.c_int
+    L.hydra_lora_linear_multi_workspace_bytes.argtypes = [_i64, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]
+    L.hydra_lora_linear_multi_workspace_bytes.restype = ctypes.c_int
+    L.hydra_lora_linear_multi_ws.argtypes = [_vp, _vp, _i64, _pp, _pp, _pp, ctypes.POINTER(ctypes.c_float), _i64, _i64,
+                                             _i64, _i64, _vp, _pp, _vp, ctypes.c_size_t, _vp]
+    L.hydra_lora_linear_multi_ws.restype = ctypes.c_int
     L.hydra_score_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(ctypes.c_size_t)]
     L.hydra_score_workspace_bytes.restype = ctypes.c_int
     L.hydra_score.argtypes = [_vp, _vp, _vp, _vp, _f32, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
@@ -322,12 +329,7 @@ def hydra_lora_linear_group_ws(xs, Ws, As, Bs, ss, y_offs=None, y_ons=None, work
     _check(st, "hydra_lora_linear_group_ws")
 
 
-def hydra_lora_linear_multi(x_off, W, x_ons, As, Bs, ss, y_off=None, y_ons=None, stream=None) -> None:
-    """One W for a LoRA-off input and several LoRA-on inputs with their own adapters (see include/hydra.h).
-
-    x_off, y_off: tensors or None (together); x_ons, As, Bs, y_ons: sequences of n_on tensors (As, Bs may be
-    None or all-None when r == 0); ss: n_on scales.
-    """
+def _multi_args(x_off, W, x_ons, As, Bs, ss, y_off, y_ons):
     torch = _torch()
     bf = _bf16_types()
     n_on = len(x_ons)
@@ -351,10 +353,39 @@ def hydra_lora_linear_multi(x_off, W, x_ons, As, Bs, ss, y_off=None, y_ons=None,
         _need(Bs[a], "B", bf, (N, r))
         _need(y_ons[a], "y_on", (torch.float32,), (M, N))
     svals = (ctypes.c_float * max(n_on, 1))(*[float(v) for v in ss])
-    st = lib().hydra_lora_linear_multi(_ptr(x_off), _ptr(W), n_on, _ptr_array(x_ons), _ptr_array(As),
-                                       _ptr_array(Bs), svals if n_on else None, M, N, K, r, _ptr(y_off),
-                                       _ptr_array(y_ons), _stream_handle(stream))
+    return (_ptr(x_off), _ptr(W), n_on, _ptr_array(x_ons), _ptr_array(As), _ptr_array(Bs), svals if n_on else None, M,
+            N, K, r, _ptr(y_off), _ptr_array(y_ons))
+
+
+def hydra_lora_linear_multi(x_off, W, x_ons, As, Bs, ss, y_off=None, y_ons=None, stream=None) -> None:
+    """One W for a LoRA-off input and several LoRA-on inputs with their own adapters (see include/hydra.h).
+
+    x_off, y_off: tensors or None (together); x_ons, As, Bs, y_ons: sequences of n_on tensors (As, Bs may be
+    None or all-None when r == 0); ss: n_on scales.
+    """
+    st = lib().hydra_lora_linear_multi(*_multi_args(x_off, W, x_ons, As, Bs, ss, y_off, y_ons), _stream_handle(stream))
     _check(st, "hydra_lora_linear_multi")
+
+
+def hydra_lora_linear_multi_workspace_bytes(M: int, N: int, r: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().hydra_lora_linear_multi_workspace_bytes(int(M), int(N), int(r), ctypes.byref(out)),
+           "hydra_lora_linear_multi_workspace_bytes")
+    return int(out.value)
+
+
+def hydra_lora_linear_multi_ws(x_off, W, x_ons, As, Bs, ss, y_off=None, y_ons=None, workspace=None,
+                               stream=None) -> None:
+    """hydra_lora_linear_multi with a caller workspace (rank 128 at every M; see include/hydra.h).
+
+    workspace: a uint8 tensor of at least hydra_lora_linear_multi_workspace_bytes(M, N, r) bytes."""
+    torch = _torch()
+    if workspace is None:
+        raise ValueError("hydra_lora_linear_multi_ws needs a workspace")
+    _need(workspace, "workspace", (torch.uint8,))
+    st = lib().hydra_lora_linear_multi_ws(*_multi_args(x_off, W, x_ons, As, Bs, ss, y_off, y_ons), _ptr(workspace),
+                                          workspace.numel(), _stream_handle(stream))
+    _check(st, "hydra_lora_linear_multi_ws")
 
 
 def hydra_score_workspace_bytes(M: int, V: int) -> int:

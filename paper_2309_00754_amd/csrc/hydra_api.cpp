@@ -293,10 +293,14 @@ hydra_status hydra_lora_linear_ws(const uint16_t* x, const uint16_t* W, const ui
                                                reinterpret_cast<hipStream_t>(stream)));
 }
 
-hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, int64_t n_on,
-                                     const uint16_t* const* x_on, const uint16_t* const* A,
-                                     const uint16_t* const* B, const float* s, int64_t M, int64_t N, int64_t K,
-                                     int64_t r, float* y_off, float* const* y_on, void* stream) {
+}  // extern "C"
+
+namespace {
+// Argument checks of the multi-input linear (host only; the rank limit of the
+// plain call is checked by the caller).
+hydra_status multi_check(const uint16_t* x_off, const uint16_t* W, int64_t n_on, const uint16_t* const* x_on,
+                         const uint16_t* const* A, const uint16_t* const* B, const float* s, int64_t M, int64_t N,
+                         int64_t K, int64_t r, float* y_off, float* const* y_on) {
   if (!W) return HYDRA_ERR_NULL;
   if (n_on < 0 || n_on > HYDRA_MAX_ADAPTERS) return HYDRA_ERR_SHAPE;
   if ((x_off == nullptr) != (y_off == nullptr)) return HYDRA_ERR_NULL;
@@ -313,6 +317,18 @@ hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, i
     for (int64_t b = 0; b < a; ++b)
       if (y_on[b] == y_on[a]) return HYDRA_ERR_SHAPE;
   }
+  return HYDRA_OK;
+}
+}  // namespace
+
+extern "C" {
+
+hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, int64_t n_on,
+                                     const uint16_t* const* x_on, const uint16_t* const* A,
+                                     const uint16_t* const* B, const float* s, int64_t M, int64_t N, int64_t K,
+                                     int64_t r, float* y_off, float* const* y_on, void* stream) {
+  const hydra_status chk = multi_check(x_off, W, n_on, x_on, A, B, s, M, N, K, r, y_off, y_on);
+  if (chk != HYDRA_OK) return chk;
   // Above the decode sizes the adapters run on the dual GEMM, which holds
   // ranks up to 64 (hydra_lora_linear_ws serves rank 128 there): rejected
   // here, before the LoRA-off output is launched.
@@ -371,6 +387,37 @@ hydra_status hydra_lora_linear_multi(const uint16_t* x_off, const uint16_t* W, i
     g.s[a] = s[a];
   }
   return from_hip(hydra::launch_lora_update(g, st));
+}
+
+hydra_status hydra_lora_linear_multi_workspace_bytes(int64_t M, int64_t N, int64_t r, size_t* bytes) {
+  return hydra_lora_linear_workspace_bytes(M, N, r, bytes);
+}
+
+hydra_status hydra_lora_linear_multi_ws(const uint16_t* x_off, const uint16_t* W, int64_t n_on,
+                                        const uint16_t* const* x_on, const uint16_t* const* A,
+                                        const uint16_t* const* B, const float* s, int64_t M, int64_t N, int64_t K,
+                                        int64_t r, float* y_off, float* const* y_on, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  const hydra_status chk = multi_check(x_off, W, n_on, x_on, A, B, s, M, N, K, r, y_off, y_on);
+  if (chk != HYDRA_OK) return chk;
+  if (!workspace) return HYDRA_ERR_NULL;
+  const int rp = hydra::padded_rank(int(r));
+  const bool pre = M > kDecodeMaxRows && n_on > 0 && rp > 64;  // the adapters take the pre-pass GEMM
+  if (pre && workspace_bytes < linear_ws_bytes(M, N, rp)) return HYDRA_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return HYDRA_ERR_ALIGN;
+  if (!pre) return hydra_lora_linear_multi(x_off, W, n_on, x_on, A, B, s, M, N, K, r, y_off, y_on, stream);
+  // one GEMM per input: the LoRA-off input on the dual GEMM without adapter,
+  // each adapter's input through the pre-pass GEMM, sharing the workspace
+  if (x_off) {
+    const hydra_status e = hydra_lora_linear(x_off, W, nullptr, nullptr, 0.f, M, N, K, 0, y_off, nullptr, stream);
+    if (e != HYDRA_OK) return e;
+  }
+  for (int64_t a = 0; a < n_on; ++a) {
+    const hydra_status e = hydra_lora_linear_ws(x_on[a], W, A[a], B[a], s[a], M, N, K, r, nullptr, y_on[a], workspace,
+                                                workspace_bytes, stream);
+    if (e != HYDRA_OK) return e;
+  }
+  return HYDRA_OK;
 }
 
 hydra_status hydra_score_workspace_bytes(int64_t M, int64_t V, size_t* bytes) {

@@ -410,6 +410,52 @@ def test_lora_linear_multi_rank_above_64_rejected_before_any_launch():
     assert _multi(M=16, r=128, W=P8) == H.HYDRA_ERR_ALIGN
 
 
+def _multi_ws(ws=P + 0x10000, nbytes=None, **kw):
+    args = dict(x_off=P, W=P, n_on=2, xs=(P, P), As=(P, P), Bs=(P, P), ss=(2.0, 2.0), M=4, N=64, K=64, r=8,
+                y_off=P + 0x2000, yn=(P + 0x3000, P + 0x4000))
+    args.update(kw)
+
+    def arr(v):
+        if v is None:
+            return None
+        a = (ctypes.c_void_p * max(len(v), 1))()
+        for i, p in enumerate(v):
+            a[i] = p
+        return a
+    if nbytes is None:
+        nbytes = H.hydra_lora_linear_multi_workspace_bytes(min(max(args["M"], 1), 1 << 20), max(args["N"], 1),
+                                                           min(max(args["r"], 0), 128))
+    ss = args["ss"]
+    svals = None if ss is None else (ctypes.c_float * max(len(ss), 1))(*ss)
+    return H.lib().hydra_lora_linear_multi_ws(args["x_off"], args["W"], args["n_on"], arr(args["xs"]),
+                                              arr(args["As"]), arr(args["Bs"]), svals, args["M"], args["N"],
+                                              args["K"], args["r"], args["y_off"], arr(args["yn"]), ws, nbytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(W=None), H.HYDRA_ERR_NULL),
+    (dict(n_on=5), H.HYDRA_ERR_SHAPE),
+    (dict(yn=(P + 0x3000, P + 0x3000)), H.HYDRA_ERR_SHAPE),
+    (dict(ws=None), H.HYDRA_ERR_NULL),
+    (dict(ws=P + 8), H.HYDRA_ERR_ALIGN),
+    (dict(M=2048, r=128, nbytes=4096), H.HYDRA_ERR_WORKSPACE),   # rank 128 above 16 rows: the pre-pass workspace
+    (dict(M=2048, r=128, x_off=P8), H.HYDRA_ERR_ALIGN),
+])
+def test_lora_linear_multi_ws_rejects(kw, code):
+    """Argument and workspace errors of the workspace multi-input call, all before any HIP call (fake pointers)."""
+    assert _multi_ws(**kw) == code
+
+
+def test_lora_linear_multi_ws_workspace_bytes():
+    """The workspace of hydra_lora_linear_ws for the same M, N, r (the adapters share it in turn); a rank-128 call
+    above 16 rows accepts exactly that size (validation then fails only on the deliberate bad alignment)."""
+    for M, N, r in ((2048, 4096, 128), (130, 300, 100), (4, 64, 8)):
+        assert H.hydra_lora_linear_multi_workspace_bytes(M, N, r) == H.hydra_lora_linear_workspace_bytes(M, N, r)
+    need = H.hydra_lora_linear_multi_workspace_bytes(2048, 64, 128)
+    assert _multi_ws(M=2048, r=128, nbytes=need, W=P8) == H.HYDRA_ERR_ALIGN
+    assert _multi_ws(M=2048, r=128, nbytes=need - 1) == H.HYDRA_ERR_WORKSPACE
+
+
 def test_lora_linear_multi_adapters_unused_at_rank_zero():
     """r == 0: A and B may be NULL arrays; validation then fails only on the deliberate bad alignment."""
     assert _multi(r=0, As=None, Bs=None, W=P8) == H.HYDRA_ERR_ALIGN

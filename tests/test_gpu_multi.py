@@ -6,7 +6,7 @@ import pytest
 import paper_2309_00754_amd as H
 import workloads as WL
 from oracle import lora_linear_multi_ref
-from gpu_helpers import assert_rel, dev_bf16, host, say
+from gpu_helpers import assert_rel, dev_bf16, host, row_chunks, say
 
 pytestmark = pytest.mark.gpu
 
@@ -82,3 +82,68 @@ def test_decode_multi_full_size(dev):
     assert_rel(g_off, e_off, "y_off")
     for a in range(len(g_ons)):
         assert_rel(g_ons[a], e_ons[a], f"y_on[{a}]")
+
+
+def _run_multi_ws(c, device):
+    import torch
+    x_off = dev_bf16(c.x_off, device) if c.x_off is not None else None
+    W = dev_bf16(c.W, device)
+    xs = [dev_bf16(x, device) for x in c.x_on]
+    As = [dev_bf16(a, device) if c.r else None for a in c.A]
+    Bs = [dev_bf16(b, device) if c.r else None for b in c.B]
+    y_off = torch.full((c.M, c.N), float("nan"), device=device) if x_off is not None else None
+    y_ons = [torch.full((c.M, c.N), float("nan"), device=device) for _ in xs]
+    ws = torch.full((H.hydra_lora_linear_multi_workspace_bytes(c.M, c.N, c.r),), 0xA5, dtype=torch.uint8,
+                    device=device)
+    H.hydra_lora_linear_multi_ws(x_off, W, xs, As, Bs, c.s, y_off, y_ons, workspace=ws)
+    torch.cuda.synchronize()
+    return (None if y_off is None else host(y_off)), [host(t) for t in y_ons]
+
+
+@pytest.mark.parametrize("M,K,N,r,n_on,with_off", [
+    (130, 520, 300, 128, 2, True), (48, 264, 136, 100, 3, False), (4, 1032, 200, 128, 2, True),
+    (64, 512, 256, 16, 2, True),
+])
+def test_multi_ws_matches_oracle_and_single_calls(M, K, N, r, n_on, with_off, dev):
+    """Rank 128 above 16 rows through the pre-pass GEMM (each adapter in turn over one workspace, filled with junk
+    first): the oracle's result, and the bits of hydra_lora_linear_ws per adapter; the decode and rank-16 shapes
+    take the plain multi-input call (its bits)."""
+    import torch
+    say("multi_ws", M, K, N, r, n_on, with_off)
+    c = WL.gen_multi(900 + M * 7 + n_on, M, K, N, r, n_on, with_off, scales=(2.0, 0.5, -1.0, 1.5))
+    g_off, g_ons = _run_multi_ws(c, dev)
+    e_off, e_ons = lora_linear_multi_ref(c.x_off, c.W, c.x_on, c.A, c.B, c.s)
+    if with_off:
+        assert_rel(g_off, e_off, "y_off")
+    for a in range(n_on):
+        assert_rel(g_ons[a], e_ons[a], f"y_on[{a}]")
+    pre = M > 16 and r > 64
+    if pre:
+        W = dev_bf16(c.W, dev)
+        for a in range(n_on):
+            y = torch.full((M, N), float("nan"), device=dev)
+            ws = torch.empty(H.hydra_lora_linear_workspace_bytes(M, N, r), dtype=torch.uint8, device=dev)
+            H.hydra_lora_linear_ws(dev_bf16(c.x_on[a], dev), W, dev_bf16(c.A[a], dev), dev_bf16(c.B[a], dev), c.s[a],
+                                   None, y, workspace=ws)
+            torch.cuda.synchronize()
+            assert np.array_equal(g_ons[a], host(y)), f"y_on[{a}] differs from hydra_lora_linear_ws"
+    else:
+        p_off, p_ons = _run_multi(c, dev)
+        if with_off:
+            assert np.array_equal(g_off, p_off)
+        for a in range(n_on):
+            assert np.array_equal(g_ons[a], p_ons[a]), a
+
+
+def test_multi_ws_opt13b_full_size_every_row(dev):
+    """OPT-1.3b's q projection at the paper's rank 128 over a PPO mini-batch of 8 x 512 tokens, for the LoRA-off,
+    actor and critic passes, each with its own input: every row against the oracle."""
+    M, K, N, r = 4096, 2048, 2048, 128
+    say("multi_ws opt13b", M, K, N, r)
+    c = WL.gen_multi(990, M, K, N, r, 2, True, scales=(2.0, 2.0))
+    g_off, g_ons = _run_multi_ws(c, dev)
+    for rows in row_chunks(M):
+        e_off, e_ons = lora_linear_multi_ref(c.x_off[rows], c.W, [x[rows] for x in c.x_on], c.A, c.B, c.s)
+        assert_rel(g_off[rows], e_off, f"y_off rows {rows[0]}..")
+        for a in range(2):
+            assert_rel(g_ons[a][rows], e_ons[a], f"y_on[{a}] rows {rows[0]}..")
