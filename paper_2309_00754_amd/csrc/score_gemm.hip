@@ -270,7 +270,20 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
 #pragma unroll
     for (int ni = 0; ni < NTL; ++ni)
 #pragma unroll
-      for (int k = 0; k < 16; ++k) z[ni * 16 + k] = acc[mi][ni][k];
+      for (int k = 0; k < 16; ++k) {
+        if constexpr (DUAL) {
+          z[ni * 16 + k] = acc[mi][ni][k];
+        } else {
+          // Read from the accumulator register here.  Left to itself the
+          // compiler copies all 256 accumulators into VGPRs when the main
+          // loop ends and, with the LoRA slabs still to come, spills a
+          // quarter of them to scratch memory.  (The two-input kernel keeps
+          // the plain copy: there the forced reads make the spills worse.)
+          float v;
+          asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(acc[mi][ni][k]));
+          z[ni * 16 + k] = v;
+        }
+      }
     if constexpr (RAGGED) {
       const int lim = N - wcol0 - 4 * lh;  // offsets at or past lim are past N
 #pragma unroll
