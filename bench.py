@@ -281,7 +281,7 @@ def main():
     roof["kernel"] = {"prefill": "lora_gemm_kernel<16,false> (4 copy + 4 MFMA waves, 128x256 tiles)",
                       "score": "lora_t_part_kernel<16> + lora_t_finish_kernel<16> + score_gemm_kernel<16,false> + "
                                "score_combine_kernel",
-                      "decode": "gemv_fused_kernel<4,16> (q/k/v/o in one launch)",
+                      "decode": "gemv_split_kernel<4,16> (q/k/v/o in one launch)",
                       "advantages": "value_head_kernel + gae_kernel"}[dom]
     tr = committed_traffic(dom)
     roof["traffic"] = None if tr is None else tr["bytes_per_launch"]

@@ -155,20 +155,25 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
  */
 hydra_status hydra_lora_linear_group_workspace_bytes(int64_t G, int64_t M, int64_t N, int64_t r, size_t* bytes);
 
-/* Control area at the start of a hydra_lora_linear_group_ws workspace, its caller-owned wait-bound word, and the
- * size of the region of published T values that follows it. */
+/* Control area at the start of a hydra_lora_linear_group_ws workspace, its caller-owned wait-bound word, the size
+ * of the region of published T values that follows it, and the size of the region of published LoRA-off outputs
+ * after that. */
 #define HYDRA_GROUP_WS_CONTROL_BYTES 4352
 #define HYDRA_GROUP_WS_BOUND_WORD 8
 #define HYDRA_GROUP_WS_T_BYTES 65536
+#define HYDRA_GROUP_WS_Y_BYTES 2097152
 
 /*
  * hydra_lora_linear_group_ws -- hydra_lora_linear_group with a caller
  * workspace, which lets a decode step (M <= 8 rows, App. A Alg. 1 / Alg. 2,
  * generation step) run as a single launch: the first workgroups form
- * T = x A^T of every member once and publish it in the workspace, and the
- * workgroups that stream the rows of W add s T B^T to their own rows of y_on
- * (no second launch, no T recomputed per column block).  Defined by: the
- * same passages as hydra_lora_linear.
+ * T = x A^T of every member once and publish it in the workspace; up to
+ * padded rank 64 (when G x N x M, with M rounded up to 1, 2, 4 or 8, is at
+ * most HYDRA_GROUP_WS_Y_BYTES / 8) the workgroups that stream the rows of W
+ * publish their LoRA-off outputs there too, and workgroups at the end of the
+ * launch add s T B^T to them to form y_on; otherwise the workgroups that stream W add
+ * s T B^T to their own rows of y_on (no second launch, no T recomputed per
+ * column block).  Defined by: the same passages as hydra_lora_linear.
  *
  *   G, x, W, A, B, s, M, N, K, r, y_off, y_on   as in hydra_lora_linear_group
  *   workspace, workspace_bytes   device, 16-byte aligned, at least
@@ -177,9 +182,10 @@ hydra_status hydra_lora_linear_group_workspace_bytes(int64_t G, int64_t M, int64
  *                         allocating it; after that the library keeps its
  *                         state there (HYDRA_GROUP_WS_CONTROL_BYTES of control
  *                         words holding a call generation, then
- *                         HYDRA_GROUP_WS_T_BYTES of published T values tagged
- *                         with it), so the buffer is reused as it is and
- *                         serves calls of any shape.  To reset it, zero all of
+ *                         HYDRA_GROUP_WS_T_BYTES of published T values and
+ *                         HYDRA_GROUP_WS_Y_BYTES of published LoRA-off outputs,
+ *                         each tagged with it), so the buffer is reused as it
+ *                         is and serves calls of any shape.  To reset it, zero all of
  *                         it (the control words alone are not enough), and
  *                         zero it again before its next use here after lending
  *                         it to another entry point.  One workspace serves one
@@ -187,12 +193,13 @@ hydra_status hydra_lora_linear_group_workspace_bytes(int64_t G, int64_t M, int64
  *                         not share it.  The 32-bit word
  *                         HYDRA_GROUP_WS_BOUND_WORD of the control area is the
  *                         caller's: 0 selects the default bounds of the
- *                         launch's two waits (for T, about 10 ms; for every
- *                         workgroup to have read the generation, about 1 s);
- *                         another value bounds each to that many polls.  A
- *                         workgroup that gives up waiting for T forms it
- *                         itself, with the same bits; if the second wait runs
- *                         out, every later call forms T in every workgroup
+ *                         launch's waits (for T and for a published LoRA-off
+ *                         output, about 10 ms each; for every workgroup to
+ *                         have read the generation, about 1 s); another value
+ *                         bounds each to that many polls.  A workgroup that
+ *                         gives up waiting for T or for an output forms it
+ *                         itself, with the same bits; if the last wait runs
+ *                         out, every later call forms them where they are used
  *                         (same bits, slower) until the workspace is zeroed.
  * By rows: M <= 8 one launch; 8 < M <= 16 as hydra_lora_linear_group, but at
  * rank above 64 the two row halves each take the single launch; M > 16 as

@@ -29,6 +29,7 @@ HYDRA_SCORE_NOALLOC_MAX_BYTES = 48 << 20
 HYDRA_GROUP_WS_CONTROL_BYTES = 4352
 HYDRA_GROUP_WS_BOUND_WORD = 8
 HYDRA_GROUP_WS_T_BYTES = 65536
+HYDRA_GROUP_WS_Y_BYTES = 2097152
 
 # Every symbol include/hydra.h declares.
 EXPORTED = (

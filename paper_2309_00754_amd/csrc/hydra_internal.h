@@ -228,12 +228,15 @@ hipError_t launch_lora_update(const GroupArgs& g, hipStream_t stream);
 // The decode step of a group (M <= 8) in one launch.  ws (16-byte aligned,
 // zero before its first use): kFusedCtlBytes of control words (the kernel
 // keeps a call generation there), then kFusedTSlotBytes of tagged T slots
-// (64-bit entries, [G][kStreamRows][padded rank]), a region of fixed size so
-// that calls of any shape find only their own or older tags there.
+// (64-bit entries, [G][kStreamRows][padded rank]), then kFusedYBytes of
+// tagged LoRA-off outputs (64-bit entries, [G][N][rows padded to 1, 2, 4 or
+// 8]); both regions have a fixed size, and nothing else is ever written
+// there, so that calls of any shape find only their own or older tags.
 constexpr int kFusedBuckets = 32;
 constexpr size_t kFusedCtlBytes = size_t(2 + kFusedBuckets) * 128;
 constexpr size_t kFusedTSlotBytes = size_t(kMaxGroup) * kStreamRows * 128 * 8;
-constexpr size_t kFusedWsBytes = kFusedCtlBytes + kFusedTSlotBytes;
+constexpr size_t kFusedYBytes = size_t(2) << 20;
+constexpr size_t kFusedWsBytes = kFusedCtlBytes + kFusedTSlotBytes + kFusedYBytes;
 hipError_t launch_gemv_fused(const GroupArgs& g, void* ws, hipStream_t stream);
 hipError_t launch_score_gemm(const ScoreGemmArgs& a, hipStream_t stream);
 hipError_t launch_value_head(const ValueHeadArgs& a, hipStream_t stream);

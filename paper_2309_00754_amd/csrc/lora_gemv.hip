@@ -603,6 +603,7 @@ static_assert(kFusedCtlBytes == HYDRA_GROUP_WS_CONTROL_BYTES && kCtlBound == HYD
               "control area as documented in hydra.h");
 static_assert(kFusedCtlBytes == size_t(kCtlBucket0 / kCtlLine + kFusedBuckets) * 128, "bucket lines");
 static_assert(kFusedTSlotBytes == HYDRA_GROUP_WS_T_BYTES, "T region as documented in hydra.h");
+static_assert(kFusedYBytes == HYDRA_GROUP_WS_Y_BYTES, "y_off region as documented in hydra.h");
 constexpr uint32_t kPoison = 1u << 31;
 constexpr uint32_t kGenMask = kPoison - 1;
 constexpr uint32_t kDefaultWaitBound = 1u << 18;  // s_sleep(1) rounds (~10 ms)
@@ -676,6 +677,53 @@ __device__ __forceinline__ float t_rows_dot(const uint16_t* A, int r, int j0, co
   return v;
 }
 
+// The keeper (wave 0 of the last workgroup): lane q < nbk watches bucket q,
+// one load per poll for all buckets, until every workgroup of the call has
+// read the generation (bounded); then it writes the next generation, with
+// the poison bit if the bound ran out, and zero counts to every line.
+__device__ __forceinline__ void keeper(const FusedArgs& fa, int wave, int lane) {
+  if (wave != 0) return;
+  const int q = lane;
+  const bool mine = q < fa.nbk;
+  const uint32_t want = mine ? (uint32_t)((fa.total - q + fa.nbk - 1) / fa.nbk) : 0u;
+  uint32_t bound = ld_dev(&fa.ctl[kCtlBound]);
+  if (bound == 0u) bound = kFinalWaitBound;
+  uint64_t w = ld_dev(bucket_word(fa.ctl, mine ? q : 0));
+  uint32_t it = 0;
+  bool done;
+  while (!(done = __builtin_amdgcn_ballot_w64(mine && (uint32_t)w < want) == 0ull) && ++it < bound) {
+    __builtin_amdgcn_s_sleep(1);
+    w = ld_dev(bucket_word(fa.ctl, mine ? q : 0));
+  }
+  // every copy of the generation word is the same; past the bound the
+  // poison bit is set and stays set
+  const uint32_t gw = __builtin_amdgcn_readfirstlane((uint32_t)(w >> 32));
+  const uint32_t next = tag_of(gw) | (gw & kPoison) | (done ? 0u : kPoison);
+  if (q < kFusedBuckets) st_dev(bucket_word(fa.ctl, q), (uint64_t)next << 32);
+}
+
+// A T workgroup: rows jb * 4 .. jb * 4 + 3 of T of one member, each value
+// published with the call's tag in one 64-bit device-coherent store.  Thread
+// 0 holds the generation word its atomic returned.
+template <int MB, int RP>
+__device__ __forceinline__ void publish_t(const FusedArgs& fa, int bid, uint64_t gword, uint4* xsh, int t, int lane,
+                                          int wave) {
+  constexpr int TS = RP > 0 ? RP : 1;
+  const GroupArgs& ga = fa.ga;
+  const int gi = bid / fa.nT, jb = bid - (bid / fa.nT) * fa.nT;
+  const bool on = ga.y_on[gi] != nullptr && ga.A[gi] != nullptr && ga.B[gi] != nullptr;
+  if (!on) return;
+  __shared__ float tpart[SW][MB];
+  const float v = t_rows_dot<MB>(ga.A[gi], ga.r, jb * kTRows, ga.x[gi], ga.M, ga.K, xsh, tpart, t, lane, wave);
+  if (wave == 0) {
+    // (the whole wave is active here, lane 0 holds the atomic's value)
+    const uint64_t tag = tag_of(__builtin_amdgcn_readfirstlane((uint32_t)(gword >> 32)));
+    const int q = t / MB, m = t % MB;
+    if (t < kTRows * MB && m < ga.M)
+      st_dev(&fa.tsl[(gi * kStreamRows + m) * TS + jb * kTRows + q], (tag << 32) | __float_as_uint(v));
+  }
+}
+
 template <int MB, int RP>
 __global__ __launch_bounds__(SW * 64, 8) void gemv_fused_kernel(FusedArgs fa) {
   constexpr int TS = RP > 0 ? RP : 1;
@@ -687,26 +735,7 @@ __global__ __launch_bounds__(SW * 64, 8) void gemv_fused_kernel(FusedArgs fa) {
   const int bid = blockIdx.x;
   const int nTall = ga.G * fa.nT;
   if (RP > 0 && bid == fa.total) {
-    // ---------------------------------------------- the keeper
-    // Lane q < nbk watches bucket q: one load per poll for all buckets.
-    if (wave != 0) return;
-    const int q = lane;
-    const bool mine = q < fa.nbk;
-    const uint32_t want = mine ? (uint32_t)((fa.total - q + fa.nbk - 1) / fa.nbk) : 0u;
-    uint32_t bound = ld_dev(&fa.ctl[kCtlBound]);
-    if (bound == 0u) bound = kFinalWaitBound;
-    uint64_t w = ld_dev(bucket_word(fa.ctl, mine ? q : 0));
-    uint32_t it = 0;
-    bool done;
-    while (!(done = __builtin_amdgcn_ballot_w64(mine && (uint32_t)w < want) == 0ull) && ++it < bound) {
-      __builtin_amdgcn_s_sleep(1);
-      w = ld_dev(bucket_word(fa.ctl, mine ? q : 0));
-    }
-    // every copy of the generation word is the same; past the bound the
-    // poison bit is set and stays set
-    const uint32_t gw = __builtin_amdgcn_readfirstlane((uint32_t)(w >> 32));
-    const uint32_t next = tag_of(gw) | (gw & kPoison) | (done ? 0u : kPoison);
-    if (q < kFusedBuckets) st_dev(bucket_word(fa.ctl, q), (uint64_t)next << 32);
+    keeper(fa, wave, lane);
     return;
   }
   // Read the generation word and report the read (one returning atomic; its
@@ -717,20 +746,7 @@ __global__ __launch_bounds__(SW * 64, 8) void gemv_fused_kernel(FusedArgs fa) {
                                    __HIP_MEMORY_SCOPE_AGENT);
   float acc[MB];
   if (bid < nTall) {
-    // ---------------------------------------------- rows of A: T of one member
-    const int gi = bid / fa.nT, jb = bid - (bid / fa.nT) * fa.nT;
-    const bool on = ga.y_on[gi] != nullptr && ga.A[gi] != nullptr && ga.B[gi] != nullptr;
-    if (on) {
-      __shared__ float tpart[SW][MB];
-      const float v = t_rows_dot<MB>(ga.A[gi], r, jb * kTRows, ga.x[gi], M, K, xsh, tpart, t, lane, wave);
-      if (wave == 0) {
-        // (the whole wave is active here, lane 0 holds the atomic's value)
-        const uint64_t tag = tag_of(__builtin_amdgcn_readfirstlane((uint32_t)(gword >> 32)));
-        const int q = t / MB, m = t % MB;
-        if (t < kTRows * MB && m < M)
-          st_dev(&fa.tsl[(gi * kStreamRows + m) * TS + jb * kTRows + q], (tag << 32) | __float_as_uint(v));
-      }
-    }
+    publish_t<MB, RP>(fa, bid, gword, xsh, t, lane, wave);
     return;
   }
   // ---------------------------------------------- rows of W
@@ -989,6 +1005,278 @@ __global__ __launch_bounds__(SW * 64, 8) void gemv_selft_kernel(GroupArgs ga) {
   if (writer && yn) yn[(size_t)m * N + n] = acc[0];
 }
 
+// ---------------------------------------------------------------- decode in one launch, LoRA at the tail
+// The same three kinds of workgroup as gemv_fused_kernel, plus a fourth, but
+// no workgroup that streams W ever waits:
+//  * T workgroups (first in the grid) publish tagged T as there;
+//  * W workgroups stream their 16 rows of W exactly as gemv_selft_kernel does
+//    at rank 0 and write y_off; for a member with an adapter they also
+//    publish each value of y_off, tagged like T, in the workspace, and leave
+//    y_on alone;
+//  * update workgroups (after all W workgroups in the grid, so they start as
+//    the stream ends) each take 128 rows of one member (64 from rank 64 on,
+//    or with 8 rows of x): they load the rows of
+//    B and the published T, form d = s T B^T, wait (bounded) for the tagged
+//    y_off of their rows and write y_on = y_off + d.  Every y_off they wait
+//    for comes from a workgroup the hardware dispatched earlier.
+//  * the keeper, as there.
+// An update workgroup that finds a value missing past its bound (or a
+// poisoned generation) computes T, or its rows' y_off, itself, through the
+// same routines as the T and W workgroups, so the bits are the same.
+struct SplitArgs {
+  FusedArgs f;
+  uint64_t* ysl;  // tagged y_off [G][N][MB]: (tag << 32) | value bits
+  int nUB;        // update workgroups per member
+};
+// threads per row of an update workgroup (each takes RP / that many j) and
+// rows per update workgroup
+constexpr int upd_tpr(int mb, int rp) { return rp >= 64 || mb == 8 ? 16 : 8; }
+constexpr int upd_rows(int mb, int rp) { return SW * 64 / upd_tpr(mb, rp); }
+
+// Base products <x[m], W[n]> of the 16 rows n = nb * 16 + wave of member gi,
+// one wave per row, streamed as in gemv_selft_kernel at rank 0: each segment
+// issues its x loads first, then the row of W, all unconditional (out-of-range
+// offsets where there is nothing to load), so that waiting for x never waits
+// for W.  Returns this lane's sum after the reduce-scatter (row n, m =
+// reduced_index<MB>(lane)).  Every wave of the workgroup must call it (it has
+// workgroup barriers).  With gw_dst set, thread 0 stores the high half of
+// its gword there before the first barrier, for the whole workgroup to read.
+template <int MB>
+__device__ __forceinline__ float stream_rows(const GroupArgs& ga, int gi, int nb, uint4* xsh, int t, int lane,
+                                             int wave, uint32_t* gw_dst, uint64_t gword) {
+  constexpr int SEG = MB <= 4 ? XSeg<MB>::SEG / 2 : XSeg<MB>::SEG;
+  constexpr int XE = MB * SEG * 64;                      // staged x elements per segment
+  constexpr int XPER = (XE + SW * 64 - 1) / (SW * 64);   // ... per thread
+  const int M = ga.M, N = ga.N, K = ga.K;
+  const int n = nb * 16 + wave;
+  const bool row_ok = n < N;
+  const __amdgpu_buffer_rsrc_t wrs =
+      make_rsrc(row_ok ? ga.W[gi] + (size_t)n * K : nullptr, row_ok ? (uint32_t)K * 2u : 0u);
+  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(ga.x[gi], (uint32_t)M * K * 2u);
+  const int nch = (K + DKC - 1) / DKC;
+  float acc[MB];
+#pragma unroll
+  for (int m = 0; m < MB; ++m) acc[m] = 0.f;
+#pragma unroll 1
+  for (int c0 = 0; c0 < nch; c0 += SEG) {
+    uint4 xv[XPER];
+#pragma unroll
+    for (int q = 0; q < XPER; ++q) {
+      const int e = t + q * SW * 64;
+      const int m = e / (SEG * 64), u = (e / 64) % SEG, l = e % 64;
+      const int c = c0 + u, k = c * DKC + l * 8;
+      xv[q] = buf_load16(xrs, (e < XE && c < nch && k < K) ? (m * K + k) * 2 : kOutOfRange);
+    }
+    asm volatile("" ::: "memory");
+    uint4 wb[SEG];
+#pragma unroll
+    for (int u = 0; u < SEG; ++u) {
+      const int c = c0 + u, k = c * DKC + lane * 8;
+      wb[u] = buf_load16(wrs, (c < nch && k < K) ? k * 2 : kOutOfRange);
+    }
+    asm volatile("" ::: "memory");
+    if (c0 > 0) __syncthreads();  // every wave is done with the previous x segment
+#pragma unroll
+    for (int q = 0; q < XPER; ++q) {
+      const int e = t + q * SW * 64;
+      if (e < XE) xsh[e] = xv[q];
+    }
+    if (gw_dst && t == 0) *gw_dst = (uint32_t)(gword >> 32);  // (the same value in every segment)
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < SEG; ++u)
+#pragma unroll
+      for (int m = 0; m < MB; ++m) acc[m] = dot8(wb[u], xsh[(m * SEG + u) * 64 + lane], acc[m]);
+  }
+  wave_reduce_scatter<MB>(acc, lane);
+  return acc[0];
+}
+
+template <int MB, int RP>
+__global__ __launch_bounds__(SW * 64, 8) void gemv_split_kernel(SplitArgs sa) {
+  static_assert(RP > 0 && RP <= 64, "the split form carries a LoRA update up to rank 64");
+  constexpr int TS = RP;
+  const FusedArgs& fa = sa.f;
+  __shared__ uint4 xsh[XSeg<MB>::ELEMS];
+  __shared__ uint32_t gw_sh;
+  const GroupArgs& ga = fa.ga;
+  const int M = ga.M, N = ga.N, K = ga.K, r = ga.r;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int bid = blockIdx.x;
+  const int nTall = ga.G * fa.nT;
+  const int nWall = ga.G * fa.nWB;
+  if (bid == fa.total) {
+    keeper(fa, wave, lane);
+    return;
+  }
+  // the generation, read and reported by one returning atomic
+  uint64_t gword = 0;
+  if (wave == 0 && lane == 0)
+    gword = __hip_atomic_fetch_add(bucket_word(fa.ctl, bid % fa.nbk), uint64_t(1), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+  if (bid < nTall) {
+    publish_t<MB, RP>(fa, bid, gword, xsh, t, lane, wave);
+    return;
+  }
+  if (bid < nTall + nWall) {
+    // ---------------------------------------------- rows of W
+    const int idx = bid - nTall;
+    const int gi = idx / fa.nWB, nb = idx - (idx / fa.nWB) * fa.nWB;
+    float* const yo = ga.y_off[gi];
+    float* const yn = ga.y_on[gi];
+    const bool on = yn != nullptr && ga.A[gi] != nullptr && ga.B[gi] != nullptr;
+    const float v = stream_rows<MB>(ga, gi, nb, xsh, t, lane, wave, on ? &gw_sh : nullptr, gword);
+    const int n = nb * 16 + wave;
+    const int m = reduced_index<MB>(lane);
+    const bool writer = reduced_writer<MB>(lane) && m < M && n < N;
+    if (writer && yo) yo[(size_t)m * N + n] = v;
+    if (on) {
+      // (gw_sh was written before the stream's first barrier)
+      if (writer && (gw_sh & kPoison) == 0u)
+        st_dev(&sa.ysl[((size_t)gi * N + n) * MB + m], ((uint64_t)tag_of(gw_sh) << 32) | __float_as_uint(v));
+    } else if (writer && yn) {
+      yn[(size_t)m * N + n] = v;
+    }
+    return;
+  }
+  // ---------------------------------------------- LoRA update of y_on
+  __shared__ float tsh[MB][TS];
+  __shared__ uint32_t okw[SW];
+  const int uidx = bid - nTall - nWall;
+  const int gi = uidx / sa.nUB, ub = uidx - (uidx / sa.nUB) * sa.nUB;
+  float* const yn = ga.y_on[gi];
+  if (yn == nullptr || ga.A[gi] == nullptr || ga.B[gi] == nullptr) return;  // member without an adapter
+  constexpr int TPR = upd_tpr(MB, RP);
+  constexpr int UR = upd_rows(MB, RP);
+  constexpr int JPT = RP / TPR;  // j values per thread
+  static_assert(JPT * TPR == RP && TPR >= MB, "whole j ranges; thread q of a row writes m = q");
+  const int nl = t / TPR, q = t % TPR;
+  const int n = ub * UR + nl;
+  const bool row_ok = n < N;
+  // this thread's piece of the row of B (j = q JPT .. q JPT + JPT - 1, zero past r), requested first; one
+  // descriptor for the member's whole B (a per-row descriptor would not be wave-uniform)
+  const __amdgpu_buffer_rsrc_t brs = make_rsrc(ga.B[gi], (uint32_t)N * r * 2u);
+  uint32_t braw[JPT];
+#pragma unroll
+  for (int i = 0; i < JPT; ++i) {
+    const int j = q * JPT + i;
+    braw[i] = __builtin_amdgcn_raw_buffer_load_b16(brs, row_ok && j < r ? (n * r + j) * 2 : kOutOfRange, 0, 0);
+  }
+  // this thread's entry of T (one per thread: row t / TS, j = t % TS)
+  const bool tent = t < MB * TS && t / TS < M;
+  const uint64_t* const tslot = fa.tsl + (size_t)gi * kStreamRows * TS + t;
+  uint64_t traw = tent ? ld_dev(tslot) : 0ull;
+  // this thread's tagged y_off (thread q of a row takes m = q)
+  const bool yent = row_ok && q < MB && q < M;
+  const uint64_t* const yslot = sa.ysl + ((size_t)gi * N + n) * MB + q;
+  uint64_t yraw = yent ? ld_dev(yslot) : 0ull;
+  if (t == 0) gw_sh = (uint32_t)(gword >> 32);
+  __syncthreads();
+  const uint32_t gw = gw_sh;
+  const bool poisoned = (gw & kPoison) != 0u;
+  const uint32_t tag = tag_of(gw);
+  uint32_t bound = ld_dev(&fa.ctl[kCtlBound]);
+  if (bound == 0u) bound = kDefaultWaitBound;
+  // T into LDS: every entry tagged with this call's tag, else (bounded) again, else formed here
+  auto take_t = [&](uint64_t raw) __attribute__((always_inline)) -> bool {
+    const bool good = !tent || (uint32_t)(raw >> 32) == tag;
+    if (tent) tsh[t / TS][t % TS] = __uint_as_float((uint32_t)raw);
+    const uint64_t bad = __builtin_amdgcn_ballot_w64(!good);
+    if (lane == 0) okw[wave] = bad == 0ull ? 1u : 0u;
+    return good;
+  };
+  auto all_ok = [&]() __attribute__((always_inline)) -> bool {
+    uint32_t v = 1u;
+#pragma unroll
+    for (int w = 0; w < SW; ++w) v &= okw[w];
+    return v != 0u;
+  };
+  bool ready = false;
+  if (!poisoned) {
+    take_t(traw);
+    __syncthreads();
+    ready = all_ok();
+    for (uint32_t it = 0; !ready && it < bound; ++it) {
+      __builtin_amdgcn_s_sleep(1);
+      __syncthreads();  // every wave has read the previous flags
+      take_t(tent ? ld_dev(tslot) : 0ull);
+      __syncthreads();
+      ready = all_ok();
+    }
+  }
+  if (!ready) {
+    __shared__ float tpart[SW][MB];
+    __syncthreads();  // every wave is done with the flags and tsh
+    for (int e = t; e < MB * TS; e += SW * 64) tsh[e / TS][e % TS] = 0.f;
+    for (int jb = 0; jb < fa.nT; ++jb) {
+      const float v = t_rows_dot<MB>(ga.A[gi], r, jb * kTRows, ga.x[gi], M, K, xsh, tpart, t, lane, wave);
+      const int qq = t / MB, mm = t % MB;
+      if (t < kTRows * MB && mm < M) tsh[mm][jb * kTRows + qq] = v;
+    }
+  }
+  __syncthreads();  // T complete in LDS
+  // d[m] over this thread's j range, then summed over the row's TPR threads (butterfly: every thread of the row
+  // ends with the same bits)
+  float d[MB];
+#pragma unroll
+  for (int m = 0; m < MB; ++m) {
+    d[m] = 0.f;
+#pragma unroll
+    for (int i = 0; i < JPT; ++i) {
+      const int j = q * JPT + i;
+      d[m] = fmaf(j < TS && m < M ? tsh[m][j] : 0.f, bf16_to_f32(braw[i]), d[m]);
+    }
+  }
+#pragma unroll
+  for (int o = 1; o < TPR; o <<= 1)
+#pragma unroll
+    for (int m = 0; m < MB; ++m) d[m] += __shfl_xor(d[m], o);
+  float dq = 0.f;
+#pragma unroll
+  for (int m = 0; m < MB; ++m) dq = q == m ? d[m] : dq;
+  // the row's y_off, published by its W workgroup (bounded wait), else formed here
+  bool ygood = !yent || (!poisoned && (uint32_t)(yraw >> 32) == tag);
+  if (!poisoned)
+    for (uint32_t it = 0; !ygood && it < bound; ++it) {
+      __builtin_amdgcn_s_sleep(1);
+      yraw = ld_dev(yslot);
+      ygood = (uint32_t)(yraw >> 32) == tag;
+    }
+  const uint64_t badw = __builtin_amdgcn_ballot_w64(!ygood);
+  if (lane == 0) okw[wave] = badw == 0ull ? 1u : 0u;
+  __syncthreads();
+  const float s = ga.s[gi];
+  if (all_ok()) {
+    if (yent) yn[(size_t)q * N + n] = __uint_as_float((uint32_t)yraw) + s * dq;
+    return;
+  }
+  // some y_off did not arrive: this workgroup streams its own rows (16 per pass, the W workgroups' routine and
+  // bits) and writes every row's y_on from them
+  __shared__ float ysh[UR][MB];
+  __syncthreads();  // every wave is done with the flags
+  for (int p = 0; p < UR / 16; ++p) {
+    const int nb = (ub * UR) / 16 + p;
+    const float v = stream_rows<MB>(ga, gi, nb, xsh, t, lane, wave, nullptr, 0ull);
+    const int m = reduced_index<MB>(lane);
+    if (reduced_writer<MB>(lane)) ysh[p * 16 + wave][m] = v;
+  }
+  __syncthreads();
+  if (row_ok && q < MB && q < M) yn[(size_t)q * N + n] = ysh[nl][q] + s * dq;
+}
+
+template <int MB>
+hipError_t launch_split_mb(const SplitArgs& sa, int rp, hipStream_t stream) {
+  const dim3 grid(sa.f.total + 1), block(SW * 64);
+  switch (rp) {
+    case 16: hipLaunchKernelGGL((gemv_split_kernel<MB, 16>), grid, block, 0, stream, sa); break;
+    case 32: hipLaunchKernelGGL((gemv_split_kernel<MB, 32>), grid, block, 0, stream, sa); break;
+    case 64: hipLaunchKernelGGL((gemv_split_kernel<MB, 64>), grid, block, 0, stream, sa); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template <int MB>
 hipError_t launch_selft_mb(const GroupArgs& g, int rp, hipStream_t stream) {
   const dim3 grid(g.G * ((g.N + SW - 1) / SW)), block(SW * 64);
@@ -1048,6 +1336,26 @@ hipError_t launch_gemv_fused(const GroupArgs& g, void* ws, hipStream_t stream) {
   fa.tsl = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + kFusedCtlBytes);
   fa.nT = rp / kTRows;
   fa.nWB = (g.N + SW - 1) / SW;
+  const int mb = g.M <= 1 ? 1 : g.M <= 2 ? 2 : g.M <= 4 ? 4 : 8;
+  // Up to rank 64 the LoRA update runs at the tail of the grid and no
+  // workgroup that streams W waits: four Llama-7B projections (M = 4, K = N =
+  // 4096, r = 16) take 29.2-30.0 against 30.6-32.1 us, four 2048 x 2048 at M
+  // = 6 take 13.7-14.3 against 15.7-16.1 us.  At rank 128 the tail takes
+  // longer than the hand-off it saves (M = 4: 31.1 against 30.1 us; M = 8:
+  // 47.2 against 38.7 us), so rank 128 keeps gemv_fused_kernel.
+  if (rp > 0 && rp <= 64 && (size_t)g.G * g.N * mb * 8 <= kFusedYBytes) {
+    SplitArgs sa{};
+    sa.f = fa;
+    sa.ysl = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + kFusedCtlBytes + kFusedTSlotBytes);
+    const int ur = upd_rows(mb, rp);
+    sa.nUB = (g.N + ur - 1) / ur;
+    sa.f.total = g.G * (fa.nT + fa.nWB + sa.nUB);
+    sa.f.nbk = sa.f.total < kFusedBuckets ? sa.f.total : kFusedBuckets;
+    if (mb == 1) return launch_split_mb<1>(sa, rp, stream);
+    if (mb == 2) return launch_split_mb<2>(sa, rp, stream);
+    if (mb == 4) return launch_split_mb<4>(sa, rp, stream);
+    return launch_split_mb<8>(sa, rp, stream);
+  }
   fa.total = g.G * (fa.nT + fa.nWB);
   fa.nbk = fa.total < kFusedBuckets ? fa.total : kFusedBuckets;
   if (g.M <= 1) return launch_fused_mb<1>(fa, rp, stream);

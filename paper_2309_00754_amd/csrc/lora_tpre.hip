@@ -135,8 +135,10 @@ __device__ __forceinline__ void t_part_wide(const TpreArgs& a, int kch, int kc) 
   const int lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int l32 = lane & 31, lh = lane >> 5;
-  const int m0 = blockIdx.x * W_ROWS + wave * 32;
-  const int rows = max(0, min(32, M - m0));
+  // (made provably wave-uniform: the descriptor built from them must live in
+  // SGPRs, or every load becomes a loop over the lanes' descriptors)
+  const int m0 = __builtin_amdgcn_readfirstlane(blockIdx.x * W_ROWS + wave * 32);
+  const int rows = __builtin_amdgcn_readfirstlane(max(0, min(32, M - m0)));
   const __amdgpu_buffer_rsrc_t xrs = make_rsrc(a.x + (size_t)min(m0, M) * K, (uint32_t)rows * K * 2u);
   const __amdgpu_buffer_rsrc_t ars = make_rsrc(a.A, (uint32_t)min(a.r, RP) * K * 2u);
   f32x16_t acc[TJ];

@@ -128,13 +128,15 @@ def test_group_ws_members_without_adapter(dev):
     _check(cases, go, gn, want_on)
 
 
-def test_group_ws_wait_bound_fallback_same_bits(dev):
-    """With the wait bound word set to one round, workgroups that find T not yet published form it themselves
-    through the same routine: the bits are those of the default bound.  If the keeper's wait ran out too, the
-    workspace stays poisoned (every later call forms T in every workgroup, same bits) until it is zeroed."""
+@pytest.mark.parametrize("M,K,N,r", [(6, 4096, 2048, 128), (4, 4096, 4096, 16)])
+def test_group_ws_wait_bound_fallback_same_bits(M, K, N, r, dev):
+    """With the wait bound word set to one round, workgroups that find T (or, up to rank 64, a row's published
+    LoRA-off output) not yet there form it themselves through the same routine: the bits are those of the default
+    bound.  If the keeper's wait ran out too, the workspace stays poisoned (every later call forms them where they
+    are used, same bits) until it is zeroed."""
     import torch
-    say("group_ws wait bound")
-    M, K, N, r, G = 6, 4096, 2048, 128, 4
+    say("group_ws wait bound", M, K, N, r)
+    G = 4
     cases = [WL.gen_linear(1400 + i, M, K, N, r) for i in range(G)]
     t = _inputs(cases, dev)
     ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
