@@ -202,6 +202,23 @@ def test_group_ws_above_decode_rows(M, r, dev):
     _assert_generation(ws, 2 if (M <= 16 and r > 64) else 0)
 
 
+@pytest.mark.parametrize("N", [16000, 20000])
+def test_group_ws_output_region_limit(N, dev):
+    """Up to rank 64 the stream workgroups publish their LoRA-off outputs in a region of fixed size
+    (HYDRA_GROUP_WS_Y_BYTES, G x N x 8 rows x 8 bytes here): at N = 16000 they fit and the LoRA update runs at the
+    tail of the launch, at N = 20000 they do not and the workgroups that stream W add it themselves.  Both match the
+    oracle and advance the generation once."""
+    say("group_ws output region", N)
+    M, K, r, G = 8, 256, 16, 2
+    assert (G * N * 8 * 8 <= H.HYDRA_GROUP_WS_Y_BYTES) == (N == 16000)
+    cases = [WL.gen_linear(1650 + i, M, K, N, r) for i in range(G)]
+    t = _inputs(cases, dev)
+    ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
+    go, gn = _call(t, ws)
+    _check(cases, go, gn)
+    _assert_generation(ws, 1)
+
+
 def test_group_ws_decode_qkvo_full(dev):
     """The decode step of the Llama-7B attention projections (batch 4, 4096 x 4096, r = 16) as one call."""
     say("group_ws decode_qkvo")
