@@ -271,18 +271,13 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
     for (int ni = 0; ni < NTL; ++ni)
 #pragma unroll
       for (int k = 0; k < 16; ++k) {
-        if constexpr (DUAL) {
-          z[ni * 16 + k] = acc[mi][ni][k];
-        } else {
-          // Read from the accumulator register here.  Left to itself the
-          // compiler copies all 256 accumulators into VGPRs when the main
-          // loop ends and, with the LoRA slabs still to come, spills a
-          // quarter of them to scratch memory.  (The two-input kernel keeps
-          // the plain copy: there the forced reads make the spills worse.)
-          float v;
-          asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(acc[mi][ni][k]));
-          z[ni * 16 + k] = v;
-        }
+        // Read from the accumulator register here.  Left to itself the
+        // compiler copies all 256 accumulators into VGPRs when the main loop
+        // ends and, with the LoRA slabs still to come, spills a quarter of
+        // them to scratch memory.
+        float v;
+        asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(acc[mi][ni][k]));
+        z[ni * 16 + k] = v;
       }
     if constexpr (RAGGED) {
       const int lim = N - wcol0 - 4 * lh;  // offsets at or past lim are past N
@@ -313,15 +308,36 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
   };
 
   float st_off[MT][2], st_on[MT][2];
-  if (do_off) {
+  if constexpr (DUAL) {
+    // two inputs: an actor tile runs the LoRA slabs, then every tile takes
+    // one kind of statistics through a single call site (so that the
+    // accumulators are read in one place)
+    if constexpr (LS > 0) {
+      if (is_act) {
+#pragma unroll
+        for (int q = 0; q < LS; ++q) {
+          const int kq = nkt + q;
+          slab(IC<0>{}, sm[kq % NS], sm[(kq + 1) % NS], sm[(kq + NS - 1) % NS], kq);
+        }
+      }
+    }
+    const int pass = is_act ? 1 : 0;
+#pragma unroll
+    for (int mi = 0; mi < MT; ++mi) {
+      __builtin_amdgcn_sched_barrier(0);
+      row_stats(mi, pass, st_off[mi][0], st_off[mi][1]);
+      st_on[mi][0] = st_off[mi][0];
+      st_on[mi][1] = st_off[mi][1];
+    }
+  } else if (do_off) {
 #pragma unroll
     for (int mi = 0; mi < MT; ++mi) {
       __builtin_amdgcn_sched_barrier(0);
       row_stats(mi, 0, st_off[mi][0], st_off[mi][1]);  // LoRA off
     }
   }
-  if (!do_on) {
-    // a LoRA-off tile of two inputs: nothing more
+  if constexpr (DUAL) {
+    // done above
   } else if constexpr (LS > 0) {
     // The LoRA slabs nkt .. nkt + LS - 1 (stage (nkt + q) % NS; the last main
     // slab already read the first k-step of slab nkt into F0).
@@ -334,13 +350,6 @@ __global__ __launch_bounds__(NT, 1) void score_gemm_kernel(ScoreGemmArgs g) {
     for (int mi = 0; mi < MT; ++mi) {
       __builtin_amdgcn_sched_barrier(0);
       row_stats(mi, 1, st_on[mi][0], st_on[mi][1]);  // LoRA on
-    }
-  } else if constexpr (DUAL) {
-    // an actor tile without an adapter: its logits are the LoRA-on logits
-#pragma unroll
-    for (int mi = 0; mi < MT; ++mi) {
-      __builtin_amdgcn_sched_barrier(0);
-      row_stats(mi, 1, st_on[mi][0], st_on[mi][1]);
     }
   } else {
     // no adapter: the LoRA-on logits are the LoRA-off logits
