@@ -337,7 +337,9 @@ constexpr int UW = 16;   // waves per workgroup of the LoRA update
 // columns of y_on per workgroup (fewer at rank 128, for the registers and LDS
 // that hold the block of B)
 constexpr int update_cols(int rp) { return rp <= 64 ? 256 : 128; }
-constexpr int URW = 8;   // rows of A per wave in the T pass
+// rows of A per wave in the T pass: 8, or 4 with 8 rows of x up to rank 64
+// (8 x 8 partial sums per lane would spill)
+constexpr int upd_urw(int mb, int rp) { return mb >= 8 && rp <= 64 ? 4 : 8; }
 
 // y_on += s * T B^T with T = x A^T, for the members of the group that have an
 // adapter.  Every workgroup forms T itself: the 16 waves split A into RP / 8
@@ -358,6 +360,7 @@ template <int MB, int RP>
 __global__ __launch_bounds__(UW * 64) void lora_update_kernel(GroupArgs ga) {
   constexpr int NT = UW * 64;
   constexpr int UNB = update_cols(RP);
+  constexpr int URW = upd_urw(MB, RP);
   constexpr int GR = RP / URW;                     // row groups
   constexpr int GC = UW / GR;                      // chunk groups
   constexpr int VT = URW * MB;                     // partial sums of T per lane
