@@ -790,11 +790,44 @@ def cpu_baseline(target_s: float, host_inputs=None):
         fl += f_
         t += t_
         reps += 1
-    return dict(value=round(fl / t / 1e12, 5), unit="TFLOP/s", cores=int(threads), kind="oracle",
-                seconds=round(t, 2),
-                sample=f"float64 oracle on {reps} step(s) with the 2048-token parts cut to their first {rows} rows "
-                       f"(decode 4 x M=4 in full; prefill 7 linears and two-head scoring on {rows} rows)",
-                host_cpus=len(os.sched_getaffinity(0)))
+    out = dict(value=round(fl / t / 1e12, 5), unit="TFLOP/s", cores=int(threads), kind="oracle",
+               seconds=round(t, 2),
+               sample=f"float64 oracle on {reps} step(s) with the 2048-token parts cut to their first {rows} rows "
+                      f"(decode 4 x M=4 in full; prefill 7 linears and two-head scoring on {rows} rows)",
+               host_cpus=len(os.sched_getaffinity(0)))
+    out["single_thread"] = cpu_small_configs()
+    return out
+
+
+def cpu_small_configs():
+    """The oracle on one thread for the two small configurations: the single linear (16 x 512 -> 512, r = 8) and
+    the logits epilogue (512 x 32000 on and off); median of 3 runs after one warm-up."""
+    import oracle
+    import workloads as WL
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:  # pragma: no cover
+        return None
+    lin = WL.make("single_linear")
+    lon, loff, ids = WL.make("score_logits")
+
+    def med(fn):
+        fn()
+        ts = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            fn()
+            ts.append(time.perf_counter() - t0)
+        return float(np.median(ts))
+
+    with threadpool_limits(limits=1):
+        t_lin = med(lambda: oracle.lora_linear_ref(lin.x, lin.W, lin.A, lin.B, lin.s))
+        t_log = med(lambda: oracle.score_logits_ref(lon, loff, ids))
+    return {"threads": 1,
+            "single_linear_us": round(t_lin * 1e6, 1),
+            "single_linear_tflops": round(lin_flops(lin.M, lin.K, lin.N, lin.r) / t_lin / 1e12, 6),
+            "logits_epilogue_ms": round(t_log * 1e3, 2),
+            "logits_epilogue_tokens_per_s": round(lon.shape[0] / t_log, 1)}
 
 
 if __name__ == "__main__":
