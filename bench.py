@@ -323,10 +323,15 @@ def main():
         out["aux"] = {name: aux_fns[name](torch, H, WL, dev) for name in aux_names}
 
     if not args.no_cpu_baseline:
-        hi = None
+        hi = gout = None
         if all(k in host for k in ("decode", "prefill", "score")):
             hi = (host["decode"], host["prefill"], host["score"])
-        out["cpu_baseline"] = cpu_baseline(args.cpu_seconds, hi)
+            # the outputs of the last timed step, for the oracle's comparison on the sampled rows
+            gout = dict(decode=[(a.cpu().numpy(), b.cpu().numpy()) for a, b in zip(gyo, gyn)],
+                        prefill={n: (v[5].cpu().numpy(), v[6].cpu().numpy()) for n, v in dev_in.items()},
+                        score=dict(lp_on=lp_on.cpu().numpy(), lp_off=lp_off.cpu().numpy(), kl=kl.cpu().numpy(),
+                                   reward=reward.cpu().numpy()))
+        out["cpu_baseline"] = cpu_baseline(args.cpu_seconds, hi, gout)
 
     print(json.dumps(out), flush=True)
 
@@ -746,8 +751,19 @@ def bench_score_two_input(torch, H, WL, dev, iters=5):
                                frac_bf16_peak=round(fl1 / t1 / 1e6 / PEAK_BF16_TFLOPS, 4)))
 
 
-def cpu_baseline(target_s: float, host_inputs=None):
-    """The float64 oracle, as it stands, on a row sample of the same step (host cores)."""
+def rel_err(got, ref):
+    """max_i |g_i - o_i| / max(|o_i|, rms(o)): the error of an output relative to its own scale."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if ref.size == 0:
+        return 0.0
+    denom = np.maximum(np.abs(ref), np.sqrt(np.mean(ref * ref)))
+    return float(np.max(np.abs(got - ref) / np.where(denom == 0, 1.0, denom)))
+
+
+def cpu_baseline(target_s: float, host_inputs=None, gpu_out=None):
+    """The float64 oracle, as it stands, on a row sample of the same step (host cores); with gpu_out (the step's
+    outputs on the host), also the largest error of the GPU outputs against the oracle on the sampled rows."""
     import oracle
     import workloads as WL
 
@@ -761,17 +777,17 @@ def cpu_baseline(target_s: float, host_inputs=None):
         host_inputs = (WL.make("decode_qkvo"), WL.make("prefill_layer"), WL.make("two_head_score"))
     dec, pre, sc = host_inputs
 
+    last = {}
+
     def run(rows):
         fl = 0.0
         t0 = time.perf_counter()
-        for c in dec:
-            oracle.lora_linear_ref(c.x, c.W, c.A, c.B, c.s)
-            fl += lin_flops(c.M, c.K, c.N, c.r)
-        for c in pre:
-            oracle.lora_linear_ref(c.x[:rows], c.W, c.A, c.B, c.s)
-            fl += lin_flops(rows, c.K, c.N, c.r)
-        oracle.score_head_ref(sc.h[:rows], sc.W_lm, sc.A, sc.B, sc.s, sc.ids[:rows])
-        oracle.reward_ref(sc.h, sc.w_rm, sc.n_seq, sc.seq_len)
+        last["decode"] = [oracle.lora_linear_ref(c.x, c.W, c.A, c.B, c.s) for c in dec]
+        fl += sum(lin_flops(c.M, c.K, c.N, c.r) for c in dec)
+        last["prefill"] = {c.name: oracle.lora_linear_ref(c.x[:rows], c.W, c.A, c.B, c.s) for c in pre}
+        fl += sum(lin_flops(rows, c.K, c.N, c.r) for c in pre)
+        last["score"] = oracle.score_head_ref(sc.h[:rows], sc.W_lm, sc.A, sc.B, sc.s, sc.ids[:rows])
+        last["reward"] = oracle.reward_ref(sc.h, sc.w_rm, sc.n_seq, sc.seq_len)
         fl += lin_flops(rows, sc.K, sc.V, sc.r) + 2.0 * sc.n_seq * sc.K
         return fl, time.perf_counter() - t0
 
@@ -795,6 +811,19 @@ def cpu_baseline(target_s: float, host_inputs=None):
                sample=f"float64 oracle on {reps} step(s) with the 2048-token parts cut to their first {rows} rows "
                       f"(decode 4 x M=4 in full; prefill 7 linears and two-head scoring on {rows} rows)",
                host_cpus=len(os.sched_getaffinity(0)))
+    if gpu_out is not None:
+        # y and reward: relative to the output's scale; log-probabilities and KL: absolute (nats)
+        err = {"decode_y_rel": max(max(rel_err(g[0], o[0]), rel_err(g[1], o[1]))
+                                   for g, o in zip(gpu_out["decode"], last["decode"])),
+               "prefill_y_rel": max(max(rel_err(gpu_out["prefill"][n][0][:rows], o[0]),
+                                        rel_err(gpu_out["prefill"][n][1][:rows], o[1]))
+                                    for n, o in last["prefill"].items()),
+               "score_reward_rel": rel_err(gpu_out["score"]["reward"], last["reward"])}
+        for k in ("lp_on", "lp_off", "kl"):
+            err[f"score_{k}_abs"] = float(np.max(np.abs(gpu_out["score"][k][:rows].astype(np.float64)
+                                                        - last["score"][k])))
+        out["max_error_vs_oracle"] = {k: float(f"{v:.3e}") for k, v in err.items()}
+        out["max_error_vs_oracle"]["rows"] = rows
     out["single_thread"] = cpu_small_configs()
     return out
 
