@@ -16,6 +16,10 @@ CASES = [
     (4, 4096, 512, 16, 2, True), (4, 520, 300, 16, 1, True), (1, 64, 40, 8, 3, True), (8, 1032, 77, 32, 1, True),
     (3, 136, 33, 0, 2, False), (2, 4104, 130, 64, 4, True), (5, 256, 96, 16, 0, True), (4, 11008, 64, 16, 2, True),
     (12, 520, 300, 16, 2, True), (64, 512, 256, 16, 2, True),
+    # above 16 rows (one GEMM per input): ragged rows and columns, four adapters, rank 64, no LoRA-off input,
+    # rank 0
+    (300, 520, 300, 16, 4, True), (130, 72, 513, 64, 2, True), (200, 264, 520, 32, 3, False),
+    (257, 1024, 700, 0, 2, True),
 ]
 
 
@@ -82,6 +86,23 @@ def test_decode_multi_full_size(dev):
     assert_rel(g_off, e_off, "y_off")
     for a in range(len(g_ons)):
         assert_rel(g_ons[a], e_ons[a], f"y_on[{a}]")
+
+
+def test_prefill_multi_full_size_every_row(dev):
+    """One 4096 x 4096 projection over 2048 tokens for the LoRA-off, actor and critic passes (three inputs): every
+    row against the oracle, and the bits of the single-input calls."""
+    M, K, N, r = 2048, 4096, 4096, 16
+    say("prefill multi", M, K, N, r)
+    c = WL.gen_multi(991, M, K, N, r, 2, True, scales=(2.0, -1.0))
+    g_off, g_ons = _run_multi(c, dev)
+    e_off, e_ons = lora_linear_multi_ref(c.x_off, c.W, c.x_on, c.A, c.B, c.s)
+    assert_rel(g_off, e_off, "y_off")
+    s_off, _ = _run_single(c.x_off, c.W, None, None, 0.0, dev, want_off=True)
+    assert np.array_equal(g_off, s_off), "y_off differs from the single LoRA-off call"
+    for a in range(2):
+        assert_rel(g_ons[a], e_ons[a], f"y_on[{a}]")
+        _, s_on = _run_single(c.x_on[a], c.W, c.A[a], c.B[a], c.s[a], dev, want_off=False)
+        assert np.array_equal(g_ons[a], s_on), f"y_on[{a}] differs from the single LoRA-on call"
 
 
 def _run_multi_ws(c, device):
