@@ -833,7 +833,7 @@ def cpu_baseline(target_s: float, host_inputs=None, gpu_out=None):
             err[f"score_{k}_abs"] = float(np.max(np.abs(gpu_out["score"][k][:rows].astype(np.float64)
                                                         - last["score"][k])))
         out["max_error_vs_oracle"] = {k: float(f"{v:.3e}") for k, v in err.items()}
-        out["max_error_vs_oracle"]["rows"] = rows
+        out["max_error_vs_oracle"]["rows"] = min([rows, sc.M] + [c.M for c in pre])
     out["single_thread"] = cpu_small_configs()
     return out
 
