@@ -10,8 +10,10 @@
 //    a per-thread running (max, sum exp) and reducing it across the
 //    workgroup in a fixed tree.
 //  * score_combine_kernel: one wave per token row merges the per-column-tile
-//    partials written by the fused CLM-head GEMM in tile order, then forms
-//    lse, lp and KL; extra workgroups compute the reward head's dot products.
+//    partials written by the fused CLM-head GEMM (row maximum, then the sum
+//    of the partial sums rescaled to it, each by a fixed butterfly), then
+//    forms lse, lp and KL; extra workgroups compute the reward head's dot
+//    products.
 // The LoRA-on and LoRA-off statistics always go through the same code, so
 // equal logit rows give bit-identical results and KL == 0 exactly.
 #include "hydra_device.h"
@@ -237,7 +239,9 @@ __global__ __launch_bounds__(CB_THREADS) void score_combine_kernel(CombineArgs c
   const int t = threadIdx.x;
   const int nrow_blocks = (c.M + CB_ROWS - 1) / CB_ROWS;
   if ((int)blockIdx.x < nrow_blocks) {
-    const int row = blockIdx.x * CB_ROWS + (t >> 6);
+    // (the wave index made provably wave-uniform: the row's buffer descriptor
+    // then lives in SGPRs, with no per-lane loop around its loads)
+    const int row = blockIdx.x * CB_ROWS + __builtin_amdgcn_readfirstlane(t >> 6);
     if (row >= c.M) return;
     const int lane = t & 63;
     // token and gathered logits first: their latency overlaps the merge
@@ -248,15 +252,59 @@ __global__ __launch_bounds__(CB_THREADS) void score_combine_kernel(CombineArgs c
       z_off = c.zt[(size_t)row * 2 + 0];
       z_on = c.zt[(size_t)row * 2 + 1];
     }
-    const float4* p = c.part + (size_t)row * c.ntn;
-    float mo = -INFINITY, so = 0.f, mn = -INFINITY, sn = 0.f;
-    for (int j = lane; j < c.ntn; j += 64) {
-      const float4 q = p[j];
-      lse_merge(mo, so, q.x, q.y);
-      lse_merge(mn, sn, q.z, q.w);
+    // Two passes over the row's partials (the second from cache): the row
+    // maximum of each kind by a max butterfly, then sum_i s_i e^(m_i - max)
+    // by an add butterfly, one exponential per partial.
+    // Lane l takes partials l, l + 64, ..., four per round: the round's loads
+    // are issued together (past the row they read as zeros and are masked by
+    // selects, no branches).
+    const int ntn = c.ntn;
+    const __amdgpu_buffer_rsrc_t pr = make_rsrc(c.part + (size_t)row * ntn, (uint32_t)ntn * 16u);
+    constexpr int RJ = 4;
+    float mo = -INFINITY, mn = -INFINITY;
+    for (int j0 = lane; j0 < ntn; j0 += 64 * RJ) {
+      float4 q[RJ];
+#pragma unroll
+      for (int u = 0; u < RJ; ++u) {
+        const int j = j0 + 64 * u;
+        q[u] = __builtin_bit_cast(float4, buf_load16(pr, j < ntn ? j * 16 : kOutOfRange));
+      }
+#pragma unroll
+      for (int u = 0; u < RJ; ++u) {
+        const bool v = j0 + 64 * u < ntn;
+        mo = fmaxf(mo, v ? q[u].x : -INFINITY);
+        mn = fmaxf(mn, v ? q[u].z : -INFINITY);
+      }
     }
-    wave_merge(mn, sn);
-    wave_merge(mo, so);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      mo = fmaxf(mo, __shfl_xor(mo, off));
+      mn = fmaxf(mn, __shfl_xor(mn, off));
+    }
+    // (a partial with no columns has s = 0; an all-empty row keeps max = -inf and sum 0)
+    const bool live_o = mo != -INFINITY, live_n = mn != -INFINITY;
+    float so = 0.f, sn = 0.f;
+    for (int j0 = lane; j0 < ntn; j0 += 64 * RJ) {
+      float4 q[RJ];
+#pragma unroll
+      for (int u = 0; u < RJ; ++u) {
+        const int j = j0 + 64 * u;
+        q[u] = __builtin_bit_cast(float4, buf_load16(pr, j < ntn ? j * 16 : kOutOfRange));
+      }
+#pragma unroll
+      for (int u = 0; u < RJ; ++u) {
+        const bool v = j0 + 64 * u < ntn;
+        const float eo = __fmul_rn(q[u].y, exp_e(q[u].x - mo));
+        const float en = __fmul_rn(q[u].w, exp_e(q[u].z - mn));
+        so = (v && live_o) ? __fadd_rn(so, eo) : so;
+        sn = (v && live_n) ? __fadd_rn(sn, en) : sn;
+      }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      so = __fadd_rn(so, __shfl_xor(so, off));
+      sn = __fadd_rn(sn, __shfl_xor(sn, off));
+    }
     if (lane == 0) {
       LogitsArgs o{};
       o.lp_on = c.lp_on;
@@ -269,13 +317,61 @@ __global__ __launch_bounds__(CB_THREADS) void score_combine_kernel(CombineArgs c
     }
     return;
   }
-  // reward head: one workgroup per sequence, fixed-order fp32 dot product
+  // reward head: one workgroup per sequence, fixed-order fp32 dot product.
+  // Thread t takes the 8-element groups t, t + 256, ... of the row (K is a
+  // multiple of 8), four groups per round with every load of a round issued
+  // before its multiply-adds (16-byte loads of h; of w_rm too when it is
+  // 16-byte aligned, else 2-byte ones); groups past the row read as zeros.
   const int b = blockIdx.x - nrow_blocks;
   if (b >= c.n_seq || c.w_rm == nullptr || c.reward == nullptr) return;
   __shared__ float part[CB_THREADS];
   const uint16_t* hr = c.h + ((size_t)b * c.seq_len + c.seq_len - 1) * c.K;
+  const __amdgpu_buffer_rsrc_t hs = make_rsrc(hr, (uint32_t)c.K * 2u);
+  const __amdgpu_buffer_rsrc_t ws = make_rsrc(c.w_rm, (uint32_t)c.K * 2u);
+  const bool wvec = (reinterpret_cast<uintptr_t>(c.w_rm) & 15) == 0;
+  const int ng = c.K / 8;
+  constexpr int RG = 4;  // groups per round
   float acc = 0.f;
-  for (int k = t; k < c.K; k += CB_THREADS) acc = fmaf(bf16_to_f32(hr[k]), bf16_to_f32(c.w_rm[k]), acc);
+  auto fma8 = [&](const uint4& h8, const uint4& w8) __attribute__((always_inline)) {
+    const uint32_t hw[4] = {h8.x, h8.y, h8.z, h8.w};
+    const uint32_t ww[4] = {w8.x, w8.y, w8.z, w8.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc = fmaf(bf16_to_f32(hw[e] & 0xFFFFu), bf16_to_f32(ww[e] & 0xFFFFu), acc);
+      acc = fmaf(bf16_to_f32(hw[e] >> 16), bf16_to_f32(ww[e] >> 16), acc);
+    }
+  };
+  if (wvec) {
+    for (int g0 = t; g0 < ng; g0 += RG * CB_THREADS) {
+      uint4 hv[RG], wv[RG];
+#pragma unroll
+      for (int u = 0; u < RG; ++u) {
+        const int gi = g0 + u * CB_THREADS;
+        const int off = gi < ng ? gi * 16 : kOutOfRange;
+        hv[u] = buf_load16(hs, off);
+        wv[u] = buf_load16(ws, off);
+      }
+#pragma unroll
+      for (int u = 0; u < RG; ++u) fma8(hv[u], wv[u]);
+    }
+  } else {
+    for (int g0 = t; g0 < ng; g0 += RG * CB_THREADS) {
+      uint4 hv[RG];
+      uint32_t w16[RG][8];
+#pragma unroll
+      for (int u = 0; u < RG; ++u) {
+        const int gi = g0 + u * CB_THREADS;
+        hv[u] = buf_load16(hs, gi < ng ? gi * 16 : kOutOfRange);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          w16[u][e] = __builtin_amdgcn_raw_buffer_load_b16(ws, gi < ng ? gi * 16 + 2 * e : kOutOfRange, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < RG; ++u)
+        fma8(hv[u], make_uint4(w16[u][0] | (w16[u][1] << 16), w16[u][2] | (w16[u][3] << 16),
+                               w16[u][4] | (w16[u][5] << 16), w16[u][6] | (w16[u][7] << 16)));
+    }
+  }
   part[t] = acc;
   __syncthreads();
   for (int w = CB_THREADS / 2; w > 0; w >>= 1) {
