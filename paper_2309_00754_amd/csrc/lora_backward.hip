@@ -144,13 +144,32 @@ __device__ __forceinline__ void outer_part(const OuterArgs& a, int b) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) acc[g][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // A operands of slab ks (rows 16 g + l16 of the hi and lo planes, m0 + 8 lg .. + 7; Mp is a multiple of 32).
+  // Up to padded rank 32 they are requested a slab ahead, so that their latency overlaps the previous slab's
+  // MFMAs; at higher ranks the second set of registers would cost occupancy, and they are requested in the slab.
+  constexpr bool PF = JG <= 2;
+  uint4 ap[JG][2], an[PF ? JG : 1][2];
+  auto load_p = [&](int ks, uint4 (&d)[JG][2]) __attribute__((always_inline)) {
+    const int m0 = m_begin + ks * O_KS;
+#pragma unroll
+    for (int g = 0; g < JG; ++g) {
+      const uint16_t* p = a.PT + (size_t)(g * 16 + l16) * a.Mp + m0 + 8 * lg;
+      d[g][0] = *reinterpret_cast<const uint4*>(p);
+      d[g][1] = *reinterpret_cast<const uint4*>(p + (size_t)a.RP * a.Mp);
+    }
+  };
+  if constexpr (PF) load_p(0, ap);
   load(0);
   store(0);
   if (nks > 1) load(1);
   __syncthreads();
   for (int ks = 0; ks < nks; ++ks) {
     const int st = ks & 1;
-    const int m0 = m_begin + ks * O_KS;
+    if constexpr (PF) {
+      if (ks + 1 < nks) load_p(ks + 1, an);
+    } else {
+      load_p(ks, ap);
+    }
     // B operands: column wave * 64 + 16 s + l16, rows 8 lg .. 8 lg + 7 of the slab
     uint4 bq[4];
 #pragma unroll
@@ -162,20 +181,22 @@ __device__ __forceinline__ void outer_part(const OuterArgs& a, int b) {
       bq[s] = uint4{w[0], w[1], w[2], w[3]};
     }
 #pragma unroll
-    for (int g = 0; g < JG; ++g) {
-      // A operands: rows 16 g + l16 of the hi and lo planes, m0 + 8 lg .. + 7 (Mp is a multiple of 32)
-      const uint16_t* p = a.PT + (size_t)(g * 16 + l16) * a.Mp + m0 + 8 * lg;
-      const uint4 ahi = *reinterpret_cast<const uint4*>(p);
-      const uint4 alo = *reinterpret_cast<const uint4*>(p + (size_t)a.RP * a.Mp);
+    for (int g = 0; g < JG; ++g)
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
-        acc[g][s] = mfma16(ahi, bq[s], acc[g][s]);
-        acc[g][s] = mfma16(alo, bq[s], acc[g][s]);
+        acc[g][s] = mfma16(ap[g][0], bq[s], acc[g][s]);
+        acc[g][s] = mfma16(ap[g][1], bq[s], acc[g][s]);
       }
-    }
     if (ks + 1 < nks) {
       store(st ^ 1);  // stage st ^ 1 was last read before the previous barrier
       if (ks + 2 < nks) load(ks + 2);
+      if constexpr (PF) {
+#pragma unroll
+        for (int g = 0; g < JG; ++g) {
+          ap[g][0] = an[g][0];
+          ap[g][1] = an[g][1];
+        }
+      }
     }
     __syncthreads();
   }
