@@ -59,15 +59,20 @@ __global__ __launch_bounds__(WAVES * 64) void lora_gemv_mfma_kernel(GroupArgs ga
   // its A and B descriptors cover zero bytes, so every read of them is a zero.
   const bool has_lora = y_on != nullptr && At != nullptr && Bt != nullptr;
 
-  // B rows of this column block, zero padded to RP (read once, early).
+  // B rows of this column block, zero padded to RP: requested first, held in
+  // registers, and written to LDS only after the main loop, so that their
+  // latency overlaps the loads of W instead of preceding them.
+  constexpr int BPT = RP > 0 ? (NB * RP + WAVES * 64 - 1) / (WAVES * 64) : 1;  // B values per thread
+  uint32_t bv[BPT];
   if constexpr (RP > 0) {
     const __amdgpu_buffer_rsrc_t brs =
         make_rsrc(has_lora ? Bt + (size_t)n0 * r : nullptr, has_lora ? (uint32_t)min(NB, N - n0) * r * 2u : 0u);
-    for (int e = t; e < NB * RP; e += WAVES * 64) {
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int e = t + i * WAVES * 64;
       const int n = e / RP, j = e % RP;
-      const bool ok = j < r;
-      const uint32_t v = __builtin_amdgcn_raw_buffer_load_b16(brs, ok ? (n * r + j) * 2 : kOutOfRange, 0, 0);
-      Bs[n][j] = ok ? (uint16_t)v : (uint16_t)0;
+      const bool ok = e < NB * RP && j < r;
+      bv[i] = __builtin_amdgcn_raw_buffer_load_b16(brs, ok ? (n * r + j) * 2 : kOutOfRange, 0, 0);
     }
   }
 
@@ -110,6 +115,13 @@ __global__ __launch_bounds__(WAVES * 64) void lora_gemv_mfma_kernel(GroupArgs ga
     }
   }
 
+  if constexpr (RP > 0) {
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int e = t + i * WAVES * 64;
+      if (e < NB * RP) Bs[e / RP][e % RP] = (uint16_t)bv[i];  // (zero past r: out-of-range reads)
+    }
+  }
 #pragma unroll
   for (int j = 0; j < NACC; ++j) red[wave][j][lane] = acc[j];
   __syncthreads();
