@@ -62,6 +62,32 @@ def test_score_matches_oracle(n_seq, seq_len, K, V, r, dev):
     assert g["err"] == 0
 
 
+@pytest.mark.parametrize("K", [64, 8200])
+def test_reward_with_a_two_byte_aligned_head_weight(K, dev):
+    """The reward head's weight is only required to be 2-byte aligned: a w_rm one element into its allocation takes
+    the 2-byte-load path of the reward dot product; at K = 8200 each thread's groups run over two rounds, the last
+    with one group.  Same bits as with an aligned copy of the same weight, and the oracle's reward."""
+    import torch
+    say("reward, w_rm 2-byte aligned", K)
+    c = WL.gen_score_head(2050 + K, 3, 5, K, 300, 16)
+    h, W, A, B = (dev_bf16(a, dev) for a in (c.h, c.W_lm, c.A, c.B))
+    ids = torch.from_numpy(c.ids.astype(np.int32)).to(dev)
+    w_al = dev_bf16(c.w_rm, dev)
+    w_buf = torch.zeros(K + 1, dtype=torch.int16, device=dev)
+    w_buf[1:] = w_al
+    w_odd = w_buf[1:]
+    assert w_odd.data_ptr() % 16 == 2
+    rewards = []
+    for w in (w_al, w_odd):
+        lp = [torch.empty(c.M, device=dev) for _ in range(3)]
+        rw = torch.full((c.n_seq,), float("nan"), device=dev)
+        H.hydra_score(h, W, A, B, c.s, ids, w, c.n_seq, c.seq_len, lp[0], lp[1], lp[2], reward=rw)
+        torch.cuda.synchronize()
+        rewards.append(host(rw))
+    assert np.array_equal(rewards[0], rewards[1])
+    assert_rel(rewards[1], reward_ref(c.h, c.w_rm, c.n_seq, c.seq_len), "reward")
+
+
 def test_score_lora_off_gives_exact_zero_kl(dev):
     say("score B=0 / s=0 / r=0 -> KL == 0")
     c = WL.gen_score_head(2100, 2, 70, 256, 1500, 16)
