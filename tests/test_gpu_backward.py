@@ -18,6 +18,8 @@ BWD_SHAPES = [
     (130, 520, 304, 128), (1, 64, 40, 1), (5, 8, 8, 128), (200, 64, 256, 0), (1000, 72, 24, 16),
     # outer-product chunks of several 32-row slabs, the last one ragged, at rank 128 (eight j groups per slab)
     (1100, 8192, 4096, 128),
+    # ... and at padded rank 32 (two j groups, operands requested a slab ahead)
+    (600, 264, 520, 24),
 ]
 
 
