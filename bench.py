@@ -666,7 +666,28 @@ def bench_opt13b(torch, H, WL, dev, iters=5):
     out["layer"] = dict(M=lay[0].M, r=lay[0].r, us=round(t_layer, 2), tflops=round(fl / t_layer / 1e6, 2),
                         frac_bf16_peak=round(fl / t_layer / 1e6 / PEAK_BF16_TFLOPS, 4),
                         per_linear_us={n: round(timed([fn]), 2) for n, fn in calls})
-    del calls, xs
+    # the same layer with the three projections that read the same input (q, k, v) in one hydra_lora_linear_group_ws
+    # call: their pre-passes run together, then one GEMM each
+    groups = {}
+    for c, (_, fn) in zip(lay, calls):
+        groups.setdefault((id(c.x), c.N, c.K) if c.name in ("q", "k", "v") else c.name, []).append((c, fn))
+    gcalls = []
+    for mem in groups.values():
+        if len(mem) == 1:
+            gcalls.append(mem[0][1])
+            continue
+        cs = [c for c, _ in mem]
+        c0 = cs[0]
+        gW, gA, gB = [bf(c.W) for c in cs], [bf(c.A) for c in cs], [bf(c.B) for c in cs]
+        gyo = [torch.empty(c0.M, c0.N, device=dev) for _ in cs]
+        gyn = [torch.empty(c0.M, c0.N, device=dev) for _ in cs]
+        gws = H.hydra_lora_linear_group_workspace(len(cs), c0.M, c0.N, c0.r, dev)
+        gcalls.append(lambda x=xs[id(c0.x)], n=len(cs), gW=gW, gA=gA, gB=gB, gs=[c.s for c in cs], gyo=gyo, gyn=gyn,
+                      gws=gws: H.hydra_lora_linear_group_ws([x] * n, gW, gA, gB, gs, gyo, gyn, workspace=gws))
+    t_grp = timed(gcalls)
+    out["layer"].update(us_shared_input_grouped=round(t_grp, 2),
+                        frac_bf16_peak_shared_input_grouped=round(fl / t_grp / 1e6 / PEAK_BF16_TFLOPS, 4))
+    del calls, gcalls, groups, xs
     # scoring head
     sc = WL.make("opt13b_score_r128")
     h, Wl, A, B, w_rm = bf(sc.h), bf(sc.W_lm), bf(sc.A), bf(sc.B), bf(sc.w_rm)

@@ -204,8 +204,10 @@ hydra_status hydra_lora_linear_group_workspace_bytes(int64_t G, int64_t M, int64
  * By rows: M <= 8 one launch; 8 < M <= 16 as hydra_lora_linear_group, but at
  * rank above 64 the two row halves each take the single launch; M > 16 as
  * hydra_lora_linear_group, and at rank above 64 each member runs the pre-pass
- * GEMM of hydra_lora_linear_ws in turn over the workspace (rank 128 is
- * accepted at every M).  Errors as in hydra_lora_linear_group, plus
+ * GEMM of hydra_lora_linear_ws over a pre-pass workspace of its own (one per
+ * member, after the regions above); when every member's B has rows of exactly
+ * the padded rank and is 16-byte aligned, the members' pre-passes share one
+ * pair of launches before the GEMMs (rank 128 is accepted at every M).  Errors as in hydra_lora_linear_group, plus
  * HYDRA_ERR_NULL for a NULL workspace, HYDRA_ERR_WORKSPACE when it is too
  * small, HYDRA_ERR_ALIGN when it is not 16-byte aligned.  Results: the
  * oracle's tolerances; the bits may differ from hydra_lora_linear_group's in

@@ -173,11 +173,11 @@ hydra_status hydra_lora_linear_group(int64_t G, const uint16_t* const* x, const 
 namespace {
 // Workspace of hydra_lora_linear_group_ws: the control words and the tagged
 // T slots of the single-launch decode (a fixed size, whatever the shape),
-// then above 16 rows at padded rank 128 the pre-pass workspace of
-// hydra_lora_linear_ws (shared by the members in turn), which therefore never
-// overwrites the T slots.
-size_t group_ws_bytes(int64_t M, int64_t N, int rp) {
-  return hydra::kFusedWsBytes + (M > kDecodeMaxRows && rp > 64 ? linear_ws_bytes(M, N, rp) : 0);
+// then above 16 rows at padded rank 128 one pre-pass workspace of
+// hydra_lora_linear_ws per member, so the T slots are never overwritten and
+// the members' pre-passes can run in the same launches.
+size_t group_ws_bytes(int64_t G, int64_t M, int64_t N, int rp) {
+  return hydra::kFusedWsBytes + (M > kDecodeMaxRows && rp > 64 ? size_t(G) * linear_ws_bytes(M, N, rp) : 0);
 }
 }  // namespace
 
@@ -188,7 +188,7 @@ hydra_status hydra_lora_linear_group_workspace_bytes(int64_t G, int64_t M, int64
   if (G < 1 || G > HYDRA_MAX_GROUP || M < 1 || M > kMaxRows || N < 1 || N > kMaxCols || r < 0 ||
       r > HYDRA_MAX_RANK)
     return HYDRA_ERR_SHAPE;
-  *bytes = group_ws_bytes(M, N, hydra::padded_rank(int(r)));
+  *bytes = group_ws_bytes(G, M, N, hydra::padded_rank(int(r)));
   return HYDRA_OK;
 }
 
@@ -203,7 +203,7 @@ hydra_status hydra_lora_linear_group_ws(int64_t G, const uint16_t* const* x, con
   if (chk != HYDRA_OK) return chk;
   const int rp = any_on ? hydra::padded_rank(int(r)) : 0;
   if (!workspace) return HYDRA_ERR_NULL;
-  if (workspace_bytes < group_ws_bytes(M, N, hydra::padded_rank(int(r))))
+  if (workspace_bytes < group_ws_bytes(G, M, N, hydra::padded_rank(int(r))))
     return HYDRA_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return HYDRA_ERR_ALIGN;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
@@ -224,10 +224,18 @@ hydra_status hydra_lora_linear_group_ws(int64_t G, const uint16_t* const* x, con
     return from_hip(e != hipSuccess ? e : hydra::launch_gemv_fused(hi, workspace, st));
   }
   if (rp <= 64) return group_gemm(g, st);
-  // rank 128 above 16 rows: each member through the pre-pass GEMM, sharing the workspace body
-  uint8_t* body = static_cast<uint8_t*>(workspace) + hydra::kFusedWsBytes;
+  // rank 128 above 16 rows: each member through the pre-pass GEMM over a workspace body of its own.  When the GEMM
+  // reads every member's B as it is (rows of exactly the padded rank, 16-byte aligned), the members' pre-passes
+  // run together, in one pair of launches, before the GEMMs; otherwise each member in turn, padding its B.
+  const size_t body_bytes = linear_ws_bytes(M, N, rp);
+  uint8_t* const body0 = static_cast<uint8_t*>(workspace) + hydra::kFusedWsBytes;
+  hydra::LinearArgs la[hydra::kMaxGroup];
+  hydra::TpreArgs ta[hydra::kMaxGroup];
+  int nj = 0;
+  bool together = true;
   for (int i = 0; i < g.G; ++i) {
-    hydra::LinearArgs a{};
+    hydra::LinearArgs& a = la[i];
+    a = hydra::LinearArgs{};
     a.x = g.x[i];
     a.W = g.W[i];
     a.A = g.A[i];
@@ -239,8 +247,39 @@ hydra_status hydra_lora_linear_group_ws(int64_t G, const uint16_t* const* x, con
     a.r = g.A[i] ? g.r : 0;
     a.y_off = g.y_off[i];
     a.y_on = g.y_on[i];
+    if (a.r > 0 && a.y_on) {
+      uint8_t* body = body0 + size_t(i) * body_bytes;
+      hydra::TpreArgs& t = ta[nj++];
+      t = hydra::TpreArgs{};
+      t.x = a.x;
+      t.A = a.A;
+      t.B = a.B;
+      t.s = a.s;
+      t.M = a.M;
+      t.N = a.N;
+      t.K = a.K;
+      t.r = a.r;
+      t.ts = reinterpret_cast<uint16_t*>(body);
+      t.bp = reinterpret_cast<uint16_t*>(body + linear_bp_offset(M, rp));
+      t.part = reinterpret_cast<float*>(body + linear_part_offset(M, N, rp));
+      together = together && a.r == rp && aligned(a.B, 16);
+    }
+  }
+  if (together && nj > 1) {
+    if (hydra::launch_lora_tpre_multi(ta, nj, rp, st) != hipSuccess) return HYDRA_ERR_HIP;
+    int j = 0;
+    for (int i = 0; i < g.G; ++i) {
+      const hydra::LinearArgs& a = la[i];
+      const hipError_t e = a.r > 0 && a.y_on ? hydra::launch_lora_gemm_slabs(a, ta[j++].ts, a.B, rp, st)
+                                             : hydra::launch_lora_gemm(a, st);
+      if (e != hipSuccess) return HYDRA_ERR_HIP;
+    }
+    return HYDRA_OK;
+  }
+  for (int i = 0; i < g.G; ++i) {
+    uint8_t* body = body0 + size_t(i) * body_bytes;
     const hipError_t e = hydra::launch_lora_gemm_tpre(
-        a, reinterpret_cast<uint16_t*>(body), reinterpret_cast<uint16_t*>(body + linear_bp_offset(M, rp)),
+        la[i], reinterpret_cast<uint16_t*>(body), reinterpret_cast<uint16_t*>(body + linear_bp_offset(M, rp)),
         reinterpret_cast<float*>(body + linear_part_offset(M, N, rp)), st);
     if (e != hipSuccess) return HYDRA_ERR_HIP;
   }

@@ -93,6 +93,10 @@ hipError_t launch_lora_tpre(const TpreArgs& a, int rp, const uint16_t** bp_used,
 // Two pre-passes over the same M rows, neither with B to pad, in the same two
 // launches.
 hipError_t launch_lora_tpre2(const TpreArgs& a0, const TpreArgs& a1, int rp, hipStream_t stream);
+// Up to kMaxGroup pre-passes over the same M rows in the same two launches;
+// none may need its B padded (B null, or r == rp and B 16-byte aligned: the
+// GEMM then reads B itself), else hipErrorInvalidValue.
+hipError_t launch_lora_tpre_multi(const TpreArgs* as, int n, int rp, hipStream_t stream);
 // Padded rank: the smallest of 16, 32, 64, 128 that holds r (0 for r == 0).
 inline int padded_rank(int r) { return r == 0 ? 0 : r <= 16 ? 16 : r <= 32 ? 32 : r <= 64 ? 64 : 128; }
 

@@ -83,17 +83,30 @@ __device__ __forceinline__ void t_part(const TpreArgs& a, int kch, int kc) {
   }
 }
 
-// Up to two pre-passes over the same rows in one launch (the backward runs
-// s dy B and s x A^T together): K chunks [0, nkc0) of blockIdx.y belong to
-// a0, the rest to a1.
+// Up to kMaxGroup pre-passes over the same number of rows in one launch
+// (the backward runs s dy B and s x A^T together, a group of linears one
+// per member): job j has K chunks ybeg[j] .. ybeg[j + 1] - 1 of blockIdx.y
+// and finish blocks bbeg[j] .. bbeg[j + 1] - 1.
+struct TpreJobs {
+  TpreArgs a[kMaxGroup];
+  int kch[kMaxGroup];
+  int nkc[kMaxGroup];
+  int ybeg[kMaxGroup + 1];
+  int bbeg[kMaxGroup + 1];
+  int n;
+};
+// The job that owns item v of a prefix table (wave-uniform).
+__device__ __forceinline__ int job_of(const int* beg, int n, int v) {
+  int j = 0;
+  for (int i = 1; i < n; ++i) j = v >= beg[i] ? i : j;
+  return __builtin_amdgcn_readfirstlane(j);
+}
+
 template <int RP>
-__global__ __launch_bounds__(T_WAVES * 64) void lora_t_part_kernel(TpreArgs a0, int kch0, int nkc0, TpreArgs a1,
-                                                                   int kch1) {
+__global__ __launch_bounds__(T_WAVES * 64) void lora_t_part_kernel(TpreJobs jobs) {
   const int y = blockIdx.y;
-  if (y < nkc0)
-    t_part<RP>(a0, kch0, y);
-  else
-    t_part<RP>(a1, kch1, y - nkc0);
+  const int j = job_of(jobs.ybeg, jobs.n, y);
+  t_part<RP>(jobs.a[j], jobs.kch[j], y - jobs.ybeg[j]);
 }
 
 // Wide ranks (RP = 64, 128): a workgroup of W_WAVES waves owns W_WAVES x 32
@@ -202,13 +215,10 @@ __device__ __forceinline__ void t_part_wide(const TpreArgs& a, int kch, int kc) 
 }
 
 template <int RP>
-__global__ __launch_bounds__(W_WAVES * 64) void lora_t_part_wide_kernel(TpreArgs a0, int kch0, int nkc0,
-                                                                        TpreArgs a1, int kch1) {
+__global__ __launch_bounds__(W_WAVES * 64) void lora_t_part_wide_kernel(TpreJobs jobs) {
   const int y = blockIdx.y;
-  if (y < nkc0)
-    t_part_wide<RP>(a0, kch0, y);
-  else
-    t_part_wide<RP>(a1, kch1, y - nkc0);
+  const int j = job_of(jobs.ybeg, jobs.n, y);
+  t_part_wide<RP>(jobs.a[j], jobs.kch[j], y - jobs.ybeg[j]);
 }
 
 // s * T of element e = row * RP + j from the chunk partials (added in chunk
@@ -243,53 +253,57 @@ __device__ __forceinline__ void t_finish(const TpreArgs& a, int nkc, size_t e) {
   }
 }
 
-// Workgroups [0, tb0) finish a0, [tb0, tb0 + tb1) finish a1; those past them
-// write a0's B zero padded to RP when the GEMM cannot read B itself.
+// Workgroups [bbeg[j], bbeg[j + 1]) finish job j; those past the last job's
+// write job 0's B zero padded to RP when the GEMM cannot read B itself (a
+// single job only).
 template <int RP>
-__global__ __launch_bounds__(256) void lora_t_finish_kernel(TpreArgs a0, int nkc0, int tb0, TpreArgs a1, int nkc1,
-                                                            int tb1) {
+__global__ __launch_bounds__(256) void lora_t_finish_kernel(TpreJobs jobs) {
   const int b = blockIdx.x;
-  if (b < tb0) {
-    t_finish<RP>(a0, nkc0, (size_t)b * 256 + threadIdx.x);
+  const int nb_fin = jobs.bbeg[jobs.n];
+  if (b < nb_fin) {
+    const int j = job_of(jobs.bbeg, jobs.n, b);
+    t_finish<RP>(jobs.a[j], jobs.nkc[j], (size_t)(b - jobs.bbeg[j]) * 256 + threadIdx.x);
     return;
   }
-  if (b < tb0 + tb1) {
-    t_finish<RP>(a1, nkc1, (size_t)(b - tb0) * 256 + threadIdx.x);
-    return;
-  }
+  const TpreArgs& a0 = jobs.a[0];
   const size_t total = (size_t)a0.N * RP;
-  const size_t nb = gridDim.x - tb0 - tb1;
-  for (size_t e = (size_t)(b - tb0 - tb1) * 256 + threadIdx.x; e < total; e += nb * 256) {
+  const size_t nb = gridDim.x - nb_fin;
+  for (size_t e = (size_t)(b - nb_fin) * 256 + threadIdx.x; e < total; e += nb * 256) {
     const int n = (int)(e / RP), j = (int)(e % RP);
     a0.bp[e] = j < a0.r ? a0.B[(size_t)n * a0.r + j] : (uint16_t)0;
   }
 }
 
 template <int RP>
-hipError_t launch_rp(const TpreArgs& a0, const TpreArgs* a1, const uint16_t** bp_used, hipStream_t stream) {
+hipError_t launch_rp(const TpreArgs* as, int n, const uint16_t** bp_used, hipStream_t stream) {
   constexpr bool wide = RP >= kWideFrom;
-  int nkc0, kch0, nkc1 = 0, kch1 = 0;
-  (wide ? tpre_wide_chunks : tpre_chunks)(a0.K, nkc0, kch0);
-  if (a1) (wide ? tpre_wide_chunks : tpre_chunks)(a1->K, nkc1, kch1);
-  const TpreArgs b1 = a1 ? *a1 : TpreArgs{};
+  TpreJobs jobs{};
+  jobs.n = n;
+  jobs.ybeg[0] = 0;
+  jobs.bbeg[0] = 0;
+  for (int j = 0; j < n; ++j) {
+    jobs.a[j] = as[j];
+    (wide ? tpre_wide_chunks : tpre_chunks)(as[j].K, jobs.nkc[j], jobs.kch[j]);
+    jobs.ybeg[j + 1] = jobs.ybeg[j] + jobs.nkc[j];
+    jobs.bbeg[j + 1] = jobs.bbeg[j] + (int)(((size_t)(as[j].tT ? as[j].Mp : as[j].M) * RP + 255) / 256);
+  }
+  const int M = as[0].M;  // (every job has the same rows)
   if constexpr (wide)
-    hipLaunchKernelGGL((lora_t_part_wide_kernel<RP>), dim3((a0.M + W_ROWS - 1) / W_ROWS, nkc0 + nkc1),
-                       dim3(W_WAVES * 64), 0, stream, a0, kch0, nkc0, b1, kch1);
+    hipLaunchKernelGGL((lora_t_part_wide_kernel<RP>), dim3((M + W_ROWS - 1) / W_ROWS, jobs.ybeg[n]),
+                       dim3(W_WAVES * 64), 0, stream, jobs);
   else
-    hipLaunchKernelGGL((lora_t_part_kernel<RP>), dim3((a0.M + 15) / 16, nkc0 + nkc1), dim3(T_WAVES * 64), 0,
-                       stream, a0, kch0, nkc0, b1, kch1);
+    hipLaunchKernelGGL((lora_t_part_kernel<RP>), dim3((M + 15) / 16, jobs.ybeg[n]), dim3(T_WAVES * 64), 0, stream,
+                       jobs);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // B serves as its own padded copy when its rows already are RP bf16, 16-byte
-  // aligned; no B at all (a.B null): nothing to pad
-  const bool direct = a0.B == nullptr || (a0.r == RP && (reinterpret_cast<uintptr_t>(a0.B) & 15) == 0);
+  // aligned; no B at all (B null): nothing to pad.  Only a single job pads.
+  const TpreArgs& a0 = as[0];
+  const bool direct = n > 1 || a0.B == nullptr || (a0.r == RP && (reinterpret_cast<uintptr_t>(a0.B) & 15) == 0);
   if (bp_used) *bp_used = a0.B == nullptr ? nullptr : direct ? a0.B : a0.bp;
-  const int tb0 = (int)(((size_t)(a0.tT ? a0.Mp : a0.M) * RP + 255) / 256);
-  const int tb1 = a1 ? (int)(((size_t)(a1->tT ? a1->Mp : a1->M) * RP + 255) / 256) : 0;
   const size_t total = (size_t)a0.N * RP;
   const int bblocks = direct ? 0 : (int)((total + 255) / 256 < 2048 ? (total + 255) / 256 : 2048);
-  hipLaunchKernelGGL((lora_t_finish_kernel<RP>), dim3(tb0 + tb1 + bblocks), dim3(256), 0, stream, a0, nkc0, tb0, b1,
-                     nkc1, tb1);
+  hipLaunchKernelGGL((lora_t_finish_kernel<RP>), dim3(jobs.bbeg[n] + bblocks), dim3(256), 0, stream, jobs);
   return hipGetLastError();
 }
 
@@ -297,23 +311,34 @@ hipError_t launch_rp(const TpreArgs& a0, const TpreArgs* a1, const uint16_t** bp
 
 hipError_t launch_lora_tpre(const TpreArgs& a, int rp, const uint16_t** bp_used, hipStream_t stream) {
   switch (rp) {
-    case 16: return launch_rp<16>(a, nullptr, bp_used, stream);
-    case 32: return launch_rp<32>(a, nullptr, bp_used, stream);
-    case 64: return launch_rp<64>(a, nullptr, bp_used, stream);
-    case 128: return launch_rp<128>(a, nullptr, bp_used, stream);
+    case 16: return launch_rp<16>(&a, 1, bp_used, stream);
+    case 32: return launch_rp<32>(&a, 1, bp_used, stream);
+    case 64: return launch_rp<64>(&a, 1, bp_used, stream);
+    case 128: return launch_rp<128>(&a, 1, bp_used, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_lora_tpre_multi(const TpreArgs* as, int n, int rp, hipStream_t stream) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
+  for (int j = 0; j < n; ++j) {
+    if (as[j].M != as[0].M) return hipErrorInvalidValue;
+    // no job may need its B padded: B absent, or rows of exactly rp bf16, 16-byte aligned
+    if (as[j].B && (as[j].r != rp || (reinterpret_cast<uintptr_t>(as[j].B) & 15) != 0)) return hipErrorInvalidValue;
+  }
+  switch (rp) {
+    case 16: return launch_rp<16>(as, n, nullptr, stream);
+    case 32: return launch_rp<32>(as, n, nullptr, stream);
+    case 64: return launch_rp<64>(as, n, nullptr, stream);
+    case 128: return launch_rp<128>(as, n, nullptr, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_lora_tpre2(const TpreArgs& a0, const TpreArgs& a1, int rp, hipStream_t stream) {
-  if (a0.M != a1.M || a0.B || a1.B) return hipErrorInvalidValue;
-  switch (rp) {
-    case 16: return launch_rp<16>(a0, &a1, nullptr, stream);
-    case 32: return launch_rp<32>(a0, &a1, nullptr, stream);
-    case 64: return launch_rp<64>(a0, &a1, nullptr, stream);
-    case 128: return launch_rp<128>(a0, &a1, nullptr, stream);
-    default: return hipErrorInvalidValue;
-  }
+  if (a0.B || a1.B) return hipErrorInvalidValue;
+  const TpreArgs as[2] = {a0, a1};
+  return launch_lora_tpre_multi(as, 2, rp, stream);
 }
 
 }  // namespace hydra

@@ -331,8 +331,8 @@ def test_group_ws_rejects(kw, code):
 
 def test_group_ws_workspace_bytes():
     """The control words, the tagged T region and the tagged LoRA-off output region (fixed sizes, so calls of any
-    shape find only their own or older tags there), then above 16 rows at padded rank 128 the pre-pass workspace of
-    hydra_lora_linear_ws."""
+    shape find only their own or older tags there), then above 16 rows at padded rank 128 one pre-pass workspace of
+    hydra_lora_linear_ws per member."""
     gb = H.hydra_lora_linear_group_workspace_bytes
     C = H.HYDRA_GROUP_WS_CONTROL_BYTES
     T = H.HYDRA_GROUP_WS_T_BYTES
@@ -342,7 +342,8 @@ def test_group_ws_workspace_bytes():
     assert Y == 2 << 20  # 64-bit tagged entries of G x N x (rows padded to 1, 2, 4 or 8)
     for args in ((4, 4, 4096, 16), (4, 6, 2048, 128), (1, 1, 10, 0), (8, 16, 100, 9), (3, 2048, 4096, 16)):
         assert gb(*args) == C + T + Y, args
-    assert gb(3, 2048, 4096, 128) == C + T + Y + H.hydra_lora_linear_workspace_bytes(2048, 4096, 128)
+    for G in (1, 3, 8):
+        assert gb(G, 2048, 4096, 128) == C + T + Y + G * H.hydra_lora_linear_workspace_bytes(2048, 4096, 128)
     out = ctypes.c_size_t(0)
     assert H.lib().hydra_lora_linear_group_workspace_bytes(9, 4, 10, 0, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE
     assert H.lib().hydra_lora_linear_group_workspace_bytes(1, 4, 10, 129, ctypes.byref(out)) == H.HYDRA_ERR_SHAPE

@@ -190,7 +190,7 @@ def test_group_ws_poisoned_workspace_same_bits_until_zeroed(dev):
 @pytest.mark.parametrize("M,r", [(12, 16), (16, 128), (130, 16), (130, 128)])
 def test_group_ws_above_decode_rows(M, r, dev):
     """9..16 rows (the small-M MFMA kernel; at rank 128 two single-launch halves) and the GEMM rows (rank 128 per
-    member through the pre-pass GEMM, sharing the workspace)."""
+    member through the pre-pass GEMM, each over its own part of the workspace)."""
     say("group_ws rows", M, r)
     K, N, G = 520, 300, 3
     cases = [WL.gen_linear(1500 + 7 * M + i, M, K, N, r, s=1.0 + i) for i in range(G)]
@@ -200,6 +200,34 @@ def test_group_ws_above_decode_rows(M, r, dev):
     _check(cases, go, gn)
     # the single launch runs only at rank 128 up to 16 rows (once per row half)
     _assert_generation(ws, 2 if (M <= 16 and r > 64) else 0)
+
+
+@pytest.mark.parametrize("r,G,off", [(128, 3, None), (128, 8, None), (128, 3, 1), (100, 3, None)])
+def test_group_ws_rank128_rows_same_bits_as_linear_ws(r, G, off, dev):
+    """Above 16 rows at padded rank 128 each member has a pre-pass workspace of its own: with every B of exactly 128
+    columns the members' pre-passes share one pair of launches (also with a member without adapter), at rank 100 each
+    member pads its B in turn.  Either way every member's outputs carry the bits of hydra_lora_linear_ws on that
+    member alone (the same K chunks, summed in the same order), and match the oracle."""
+    import torch
+    say("group_ws rank-128 rows", r, G, off)
+    M, K, N = 300, 520, 264
+    want_on = [i != off for i in range(G)]
+    cases = [WL.gen_linear(1700 + 11 * G + i, M, K, N, r, s=0.5 + i) for i in range(G)]
+    t = _inputs(cases, dev, want_on)
+    ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
+    go, gn = _call(t, ws)
+    _check(cases, go, gn, want_on)
+    for i in range(G):
+        yo = torch.full((M, N), float("nan"), device=dev)
+        yn = torch.full((M, N), float("nan"), device=dev) if want_on[i] else None
+        H.hydra_lora_linear_ws(t["xs"][i], t["Ws"][i], t["As"][i], t["Bs"][i], t["ss"][i], yo, yn)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(yo), go[i]), i
+        if want_on[i]:
+            assert np.array_equal(host(yn), gn[i]), i
+    go2, gn2 = _call(t, ws)
+    for i in range(G):
+        assert np.array_equal(go[i], go2[i]) and (gn[i] is None or np.array_equal(gn[i], gn2[i])), i
 
 
 @pytest.mark.parametrize("N", [16000, 20000])
