@@ -731,13 +731,30 @@ def bench_opt13b(torch, H, WL, dev, iters=5):
     stream.wait_stream(side)
     torch.cuda.synchronize()
     t_dec = timed([graph.replay]) / len(calls)
+    # the same ten calls without LoRA (y_off alone: the stream of W the one-launch form is built on), for scale
+    nil = [None] * len(dec)
+    off_calls = [lambda Ws=Ws: H.hydra_lora_linear_group_ws([xd] * len(dec), Ws, nil, nil, [c.s for c in dec], gyo,
+                                                            nil, workspace=dws)
+                 for Ws in sets]
+    graph_off = torch.cuda.CUDAGraph()
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph_off, stream=side):
+            for fn in off_calls:
+                fn()
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    t_off = timed([graph_off.replay]) / len(off_calls)
     by = sum(lin_bytes(c.M, c.K, c.N, c.r) for c in dec)
+    by_off = sum(2 * (c.M * c.K + c.N * c.K) + 4 * c.M * c.N for c in dec)
     out["decode"] = dict(M=dec[0].M, r=dec[0].r, us=round(t_dec, 2), gbps=round(by / t_dec / 1e3, 1),
                          frac_hbm=round(by / t_dec / 1e3 / PEAK_HBM_GBPS, 4), eager_us=round(t_eager, 2),
+                         lora_off_us=round(t_off, 2), lora_off_frac_hbm=round(by_off / t_off / 1e3 / PEAK_HBM_GBPS, 4),
                          note="four 2048 x 2048 projections per call (hydra_lora_linear_group_ws, one launch), ten "
                               "weight sets rotating (336 MB); us from a HIP-graph replay of the ten calls (the "
-                              "eager calls are host-bound: eager_us)")
-    del graph
+                              "eager calls are host-bound: eager_us); lora_off_us: the same calls without adapters "
+                              "(W streamed for y_off alone)")
+    del graph, graph_off
     return out
 
 
