@@ -719,8 +719,8 @@ def bench_opt13b(torch, H, WL, dev, iters=5):
                                                         workspace=dws)
              for Ws in sets]
     t_eager = timed(calls) / len(calls)
-    # the eager calls are bound by the host at this size (~27 us of argument marshalling per call against a ~13 us
-    # kernel), so the GPU time per call comes from the same ten calls captured in a HIP graph and replayed
+    # the eager calls are bound by the host at this size (~22 us of argument checks and marshalling per call against
+    # a ~17 us kernel), so the GPU time per call comes from the same ten calls captured in a HIP graph and replayed
     graph = torch.cuda.CUDAGraph()
     side = torch.cuda.Stream()
     side.wait_stream(stream)
