@@ -601,7 +601,7 @@ struct FusedArgs {
   GroupArgs ga;
   uint32_t* ctl;   // control words (layout below)
   uint64_t* tsl;   // tagged T [G][kStreamRows][RP]: (tag << 32) | value bits
-  int nT;          // T workgroups per member (RP / 4)
+  int nT;          // T workgroups per member (RP / 8)
   int nWB;         // W workgroups per member (ceil(N / 16))
   int total;       // T and W workgroups; workgroup `total` is the keeper
   int nbk;         // count buckets in use
@@ -639,14 +639,16 @@ __device__ __forceinline__ uint64_t* bucket_word(uint32_t* ctl, int q) {
 // The tag that T values of a call with generation word w carry.
 __device__ __forceinline__ uint32_t tag_of(uint32_t w) { return (w + 1u) & kGenMask; }
 
-// T rows j0 .. j0 + 3 of one member: T[m][j] = <x[m], A[j]> for rows j < r
-// (zero otherwise).  Thread t < 4 MB (wave 0) gets the value of row
-// j0 + t / MB, m = t % MB.  Wave w takes row j0 + w / 4 and the chunks c with
-// c % 4 == w % 4 of every x segment, so a block of four rows costs each wave
-// a quarter of a row; the four partial sums of a row are added in
-// chunk-class order through LDS.  Every wave of the workgroup must call
-// this; it ends with a workgroup barrier.
-constexpr int kTRows = 4;   // rows of A per T block
+// T rows j0 .. j0 + 7 of one member: T[m][j] = <x[m], A[j]> for rows j < r
+// (zero otherwise).  Thread t < 8 MB (wave 0) gets the value of row
+// j0 + t / MB, m = t % MB.  Wave w takes row j0 + w / 2 and the chunks c with
+// c % 2 == w % 2 of every x segment, so a block of eight rows costs each wave
+// half a row; the two partial sums of a row are added in chunk-class order
+// through LDS.  (Blocks of 8 rather than 4 rows halve the T workgroups, which
+// hold resident slots without streaming W: 16.5 against 16.9 us for the four
+// 2048 x 2048 projections at 6 rows and rank 128.)  Every wave of the
+// workgroup must call this; it ends with a workgroup barrier.
+constexpr int kTRows = 8;   // rows of A per T block
 constexpr int kTSplit = SW / kTRows;
 template <int MB>
 __device__ __forceinline__ float t_rows_dot(const uint16_t* A, int r, int j0, const uint16_t* X, int M, int K,
@@ -717,7 +719,7 @@ __device__ __forceinline__ void keeper(const FusedArgs& fa, int wave, int lane) 
   if (q < kFusedBuckets) st_dev(bucket_word(fa.ctl, q), (uint64_t)next << 32);
 }
 
-// A T workgroup: rows jb * 4 .. jb * 4 + 3 of T of one member, each value
+// A T workgroup: rows jb * 8 .. jb * 8 + 7 of T of one member, each value
 // published with the call's tag in one 64-bit device-coherent store.  Thread
 // 0 holds the generation word its atomic returned.
 template <int MB, int RP>
