@@ -202,18 +202,25 @@ def test_group_ws_above_decode_rows(M, r, dev):
     _assert_generation(ws, 2 if (M <= 16 and r > 64) else 0)
 
 
-@pytest.mark.parametrize("r,G,off", [(128, 3, None), (128, 8, None), (128, 3, 1), (100, 3, None)])
-def test_group_ws_rank128_rows_same_bits_as_linear_ws(r, G, off, dev):
+@pytest.mark.parametrize("r,G,off,b2", [(128, 3, None, False), (128, 8, None, False), (128, 3, 1, False),
+                                        (100, 3, None, False), (128, 3, None, True)])
+def test_group_ws_rank128_rows_same_bits_as_linear_ws(r, G, off, b2, dev):
     """Above 16 rows at padded rank 128 each member has a pre-pass workspace of its own: with every B of exactly 128
     columns the members' pre-passes share one pair of launches (also with a member without adapter), at rank 100 each
-    member pads its B in turn.  Either way every member's outputs carry the bits of hydra_lora_linear_ws on that
+    member pads its B in turn, and so it does when one B is only 2-byte aligned (b2).  Either way every member's outputs carry the bits of hydra_lora_linear_ws on that
     member alone (the same K chunks, summed in the same order), and match the oracle."""
     import torch
-    say("group_ws rank-128 rows", r, G, off)
+    say("group_ws rank-128 rows", r, G, off, b2)
     M, K, N = 300, 520, 264
     want_on = [i != off for i in range(G)]
     cases = [WL.gen_linear(1700 + 11 * G + i, M, K, N, r, s=0.5 + i) for i in range(G)]
     t = _inputs(cases, dev, want_on)
+    if b2:
+        # member 1's B at a 2-byte offset inside a larger buffer (same values)
+        buf = torch.empty(N * r + 8, dtype=t["Bs"][1].dtype, device=dev)
+        t["Bs"][1] = buf[1:1 + N * r].view(N, r)
+        t["Bs"][1].copy_(dev_bf16(cases[1].B, dev))
+        assert t["Bs"][1].data_ptr() % 16 != 0
     ws = H.hydra_lora_linear_group_workspace(G, M, N, r, dev)
     go, gn = _call(t, ws)
     _check(cases, go, gn, want_on)
